@@ -1,0 +1,223 @@
+"""Seeded generators shaped like LLM-engine parameter search spaces.
+
+The paper tunes engine knobs of four kinds, continuous, integer, enumerated
+and boolean (Table 1), over a space of more than 1e11 points.  The real engines,
+request traces and stress tests are not available here, so every input is
+synthetic:
+
+* a configuration is a vector in [0, 1]^d, dimensions ordered
+  [continuous..., integer..., boolean...]; an integer dimension with L levels is
+  rounded to the grid k / (L - 1) (round half to even), a boolean one to
+  x >= 0.5; rounding is done in float64, the pool is then stored as float32;
+* SLO values come from smooth seeded functions (sines for the tiny case,
+  random Fourier features for the others) plus Gaussian noise, standardised
+  over the feasible observations; all objectives are minimised;
+* hidden constraints ("crashes") come from a seeded region: a half-plane for
+  the tiny case, the intersection of two random half-spaces covering 30% of
+  the space for the others;
+* observations are drawn uniformly until m feasible ones are collected; the GP
+  sees only the feasible ones, the random forest is trained on every draw with
+  label 1 = feasible, 0 = crashed (scikit-learn, the paper's own tool);
+* the forest is exported as flat node arrays: thresholds rounded DOWN to
+  float32 (so that x <= t agrees with the float64 threshold for every float32
+  x), leaf values as Q16 integers round(v * 65536).
+
+Seeds: numpy SeedSequence([MASTER_SEED, config]) spawns independent streams
+for observations, pool, objective, noise, hyperparameters, hidden region,
+forest and a spare.
+"""
+import numpy as np
+
+MASTER_SEED = 240804323
+
+# Shapes of the five workloads.  "rho" is the correlation between objectives
+# of the random-Fourier-feature functions, chosen per workload so that the
+# observed Pareto front has roughly the size the workload names (about 30
+# points for two objectives at m = 256, about 60 for three at m = 512).
+CONFIGS = {
+    1: dict(name="tiny-ei", d_cont=3, d_int=3, int_levels=16, d_bool=2, m=32, n=4096, p=1,
+            trees=16, depth=6, q=1, noise=1e-4, objective="sines", hidden="halfplane"),
+    2: dict(name="mid-ei", d_cont=4, d_int=4, int_levels=32, d_bool=2, m=128, n=262144, p=1,
+            trees=64, depth=10, q=4, noise=1e-3, objective="rff", hidden="hyperplane_pair"),
+    3: dict(name="two-objective-ehvi", d_cont=4, d_int=4, int_levels=32, d_bool=2, m=256, n=262144,
+            p=2, rho=(-0.96,), trees=64, depth=10, q=4, noise=1e-3, objective="rff",
+            hidden="hyperplane_pair"),
+    4: dict(name="three-objective-ehvi", d_cont=5, d_int=5, int_levels=64, d_bool=2, m=512,
+            n=1048576, p=3, rho=(-0.65, 0.1, -0.45), trees=128, depth=12, q=8, noise=1e-3,
+            objective="rff", hidden="hyperplane_pair"),
+    5: dict(name="kriging-believer", d_cont=5, d_int=5, int_levels=64, d_bool=2, m=512,
+            n=1048576, p=2, rho=(-0.93,), trees=128, depth=12, q=8, noise=1e-3, objective="rff",
+            hidden="hyperplane_pair", believer=True),
+}
+
+RFF_FEATURES = 256
+RFF_LENGTHSCALE = 0.5
+HIDDEN_VOLUME = 0.30
+DELTA0 = 0.5
+XI = 1e-4
+
+
+def _streams(cfg_id):
+    ss = np.random.SeedSequence([MASTER_SEED, int(cfg_id)])
+    names = ["obs", "pool", "objective", "noise", "hyper", "hidden", "forest", "spare"]
+    return {k: np.random.default_rng(s) for k, s in zip(names, ss.spawn(8))}
+
+
+def dims(c):
+    return c["d_cont"] + c["d_int"] + c["d_bool"]
+
+
+def snap(U, c):
+    """Round the integer and boolean dimensions of U (float64, in [0,1]) to their grids."""
+    X = np.array(U, dtype=np.float64, copy=True)
+    a, b = c["d_cont"], c["d_cont"] + c["d_int"]
+    L = c["int_levels"] - 1
+    X[:, a:b] = np.rint(X[:, a:b] * L) / L
+    X[:, b:] = (X[:, b:] >= 0.5).astype(np.float64)
+    return X
+
+
+def _draw(rng, count, c):
+    return snap(rng.random((count, dims(c))), c)
+
+
+class _Objectives:
+    """Seeded smooth functions on [0,1]^d returning (n, p) values."""
+
+    def __init__(self, c, rng):
+        self.c = c
+        d, p = dims(c), c["p"]
+        if c["objective"] == "sines":
+            self.w = rng.random(d)
+        else:
+            D = RFF_FEATURES
+            self.omega = rng.standard_normal((d, D)) / RFF_LENGTHSCALE
+            self.phase = rng.random(D) * 2.0 * np.pi
+            R = np.eye(p)
+            rho = c.get("rho", ())
+            pairs = [(0, 1), (0, 2), (1, 2)]
+            for (i, j), r in zip(pairs, rho):
+                R[i, j] = R[j, i] = r
+            Z = rng.standard_normal((D, p))
+            evals, evecs = np.linalg.eigh(R)
+            R_half = evecs @ np.diag(np.sqrt(np.clip(evals, 1e-12, None))) @ evecs.T
+            self.weights = Z @ R_half
+
+    def __call__(self, X):
+        if self.c["objective"] == "sines":
+            return (np.sin(6.0 * X) @ self.w)[:, None]
+        feats = np.sqrt(2.0 / RFF_FEATURES) * np.cos(X @ self.omega + self.phase)
+        return feats @ self.weights
+
+
+class _Hidden:
+    """Seeded hidden-constraint region; feasible(X) -> bool array."""
+
+    def __init__(self, c, rng):
+        self.c = c
+        if c["hidden"] == "halfplane":
+            return
+        d = dims(c)
+        self.a1 = rng.standard_normal(d)
+        self.a2 = rng.standard_normal(d)
+        U = _draw(rng, 1_000_000, c)
+        s1, s2 = U @ self.a1, U @ self.a2
+        self.b2 = float(np.median(s2))
+        hi2 = s2 > self.b2
+        lo, hi = float(s1.min()), float(s1.max())
+        for _ in range(60):
+            mid = 0.5 * (lo + hi)
+            vol = np.mean((s1 > mid) & hi2)
+            if vol > HIDDEN_VOLUME:
+                lo = mid
+            else:
+                hi = mid
+        self.b1 = 0.5 * (lo + hi)
+        self.volume = float(np.mean((s1 > self.b1) & hi2))
+
+    def __call__(self, X):
+        if self.c["hidden"] == "halfplane":
+            return X[:, 0] + X[:, 3] < 1.2
+        return ~((X @ self.a1 > self.b1) & (X @ self.a2 > self.b2))
+
+
+def export_forest(model):
+    """Flatten a fitted sklearn forest into the node arrays the scorer reads."""
+    feat, thr, left, right, leaf, off = [], [], [], [], [], [0]
+    for est in model.estimators_:
+        t = est.tree_
+        t64 = t.threshold.astype(np.float64)
+        t32 = t64.astype(np.float32)
+        up = t32.astype(np.float64) > t64
+        t32[up] = np.nextafter(t32[up], np.float32(-np.inf))
+        is_leaf = t.children_left < 0
+        feat.append(np.where(is_leaf, 0, t.feature).astype(np.int32))
+        thr.append(np.where(is_leaf, np.float32(0), t32).astype(np.float32))
+        left.append(t.children_left.astype(np.int32))
+        right.append(t.children_right.astype(np.int32))
+        leaf.append(np.where(is_leaf, np.rint(t.value[:, 0, 0] * 65536.0), 0).astype(np.int32))
+        off.append(off[-1] + t.node_count)
+    return dict(feature=np.concatenate(feat), threshold=np.concatenate(thr),
+                left=np.concatenate(left), right=np.concatenate(right),
+                leaf_q16=np.concatenate(leaf), tree_offset=np.array(off, dtype=np.int64))
+
+
+def make_pool(cfg_id, n=None):
+    """The candidate pool alone: (n, d) float32, grid-snapped."""
+    c = CONFIGS[cfg_id]
+    rng = _streams(cfg_id)["pool"]
+    n = c["n"] if n is None else int(n)
+    return _draw(rng, n, c).astype(np.float32)
+
+
+def make_workload(cfg_id, n=None, m=None, with_forest=True):
+    """Every input of one scoring pass for workload ``cfg_id``.
+
+    ``n`` / ``m`` override the pool size / number of feasible observations
+    (smaller test cases with the same recipe)."""
+    from sklearn.ensemble import RandomForestRegressor
+
+    c = dict(CONFIGS[cfg_id])
+    if m is not None:
+        c["m"] = int(m)
+    rs = _streams(cfg_id)
+    d, p = dims(c), c["p"]
+    hidden = _Hidden(c, rs["hidden"])
+    objective = _Objectives(c, rs["objective"])
+
+    draws, labels = [], []
+    feas_x = []
+    while len(feas_x) < c["m"]:
+        x = _draw(rs["obs"], 1, c)
+        ok = bool(hidden(x)[0])
+        draws.append(x[0])
+        labels.append(1.0 if ok else 0.0)
+        if ok:
+            feas_x.append(x[0])
+    X = np.array(feas_x)
+    Xall = np.array(draws)
+    yall = np.array(labels)
+    noise_sd = np.sqrt(c["noise"]) if c["objective"] == "rff" else 0.01
+    Yraw = objective(X) + noise_sd * rs["noise"].standard_normal((len(X), p))
+    Y = (Yraw - Yraw.mean(axis=0)) / Yraw.std(axis=0)
+
+    hyp = rs["hyper"]
+    lengthscale = [hyp.uniform(0.1, 1.0, size=d) for _ in range(p)]
+
+    w = dict(cfg=cfg_id, config=c, d=d, m=len(X), p=p, X=X, Y=Y, X_draws=Xall,
+             feasible_draws=yall, lengthscale=lengthscale,
+             signal_var=[1.0] * p, noise_var=[c["noise"]] * p, prior_mean=[0.0] * p,
+             delta=DELTA0, xi=XI, q=c["q"], best_y=float(Y[:, 0].min()),
+             hidden=hidden)
+    if p > 1:
+        mx, mn = Y.max(axis=0), Y.min(axis=0)
+        w["ref"] = mx + 0.1 * (mx - mn)
+    w["Xc"] = make_pool(cfg_id, n)
+    if with_forest:
+        seed = int(rs["forest"].integers(0, 2**31 - 1))
+        model = RandomForestRegressor(n_estimators=c["trees"], max_depth=c["depth"],
+                                      random_state=seed)
+        model.fit(Xall, yall)
+        w["forest"] = export_forest(model)
+        w["forest_model"] = model
+    return w
