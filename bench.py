@@ -1,0 +1,218 @@
+"""Throughput of the candidate-scoring pass on one MI355X.
+
+A step is one whole scoring pass over a resident pool (the two-objective
+workload: m = 256 observations, n = 262144 candidates, d = 10, EHVI over the
+observed front, 64-tree feasibility mask, top-4): GP posterior of both
+objectives (K*, mean, triangular product, variance), EHVI, forest mask and
+top-q, all on the device.  The host fit of the two GPs happens once before the
+timed region and is reported on its own (fit_ms).
+
+Prints one JSON line (rank 0).  Also measures the dominant kernel (the fused
+posterior) on its own with HIP events on the stream it runs on, for the
+roofline figure, and times the CPU oracle on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_FP32_MFMA_TFLOPS = 157.3
+METRIC = "candidate configs scored/sec (GP+acq+RF mask) and % roofline, m=256 n=262144"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernel-loops", type=int, default=20)
+    ap.add_argument("--only", choices=["all", "posterior", "copy"], default="all",
+                    help="posterior: only the posterior kernel loop (for profiler counters); "
+                         "copy: a plain 1 GiB device copy (counter calibration)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the scoring pass shards by candidate, see the design notes)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2408_04323_amd as S
+    from workloads import make_workload
+    from workloads.synth import CONFIGS
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+
+    if args.only == "copy":
+        a = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        a.fill_(1.0)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": a.numel() * 4, "copy_bytes_written": b.numel() * 4}))
+        return
+
+    t0 = time.time()
+    w = make_workload(args.config)
+    gen_s = time.time() - t0
+    c = CONFIGS[args.config]
+    p, n, m = w["p"], len(w["Xc"]), w["m"]
+
+    tf = time.perf_counter()
+    gps = [S.gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][j], w["signal_var"][j], w["noise_var"][j],
+                    w["prior_mean"][j], dtype="f32") for j in range(p)]
+    fit_ms = (time.perf_counter() - tf) * 1e3
+    fd = w["forest"]
+    forest = S.forest_create(fd["feature"], fd["threshold"], fd["left"], fd["right"], fd["leaf_q16"],
+                             fd["tree_offset"], w["d"])
+    Xc = torch.as_tensor(w["Xc"]).to(dev)
+    bufs = S.PoolBuffers(n, p, w["q"], S.F32, dev)
+    front, n_boxes = S.ehvi_front(w["Y"], w["ref"]) if p > 1 else (np.zeros((0, 1)), 0)
+    print(f"[bench] workload {c['name']} m={m} n={n} d={w['d']} p={p} front={len(front)} "
+          f"gen {gen_s:.1f}s fit {fit_ms:.1f}ms", file=sys.stderr, flush=True)
+
+    def step():
+        S.score_pool(gps, forest, Xc, w["q"], best_y=w["best_y"], xi=w["xi"], Y_obs=w["Y"],
+                     ref=w.get("ref"), delta=w["delta"], buffers=bufs)
+
+    def time_loop(fn, loops):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(loops):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / loops  # ms
+
+    # dominant kernel: the fused posterior of one objective, on the stream it runs on
+    def post():
+        S.posterior(gps[0], Xc, bufs.mu[0], bufs.sigma[0])
+
+    for _ in range(3):
+        post()
+    if args.only == "posterior":
+        ms = time_loop(post, args.kernel_loops)
+        print(json.dumps({"posterior_ms": ms}))
+        return
+    post_ms = time_loop(post, args.kernel_loops)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_start = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    value = n / (ms_per_step * 1e-3)
+    print(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall:.3f}s), posterior "
+          f"{post_ms:.3f} ms/objective", file=sys.stderr, flush=True)
+
+    # other kernels, for the record
+    ehvi_ms = rf_ms = topq_ms = None
+    if p > 1:
+        ehvi_ms = time_loop(lambda: S.acq_ehvi([bufs.mu[j] for j in range(p)], [bufs.sigma[j] for j in range(p)],
+                                               w["Y"], w["ref"], out=bufs.acq), args.kernel_loops)
+    rf_ms = time_loop(lambda: S.rf_feasibility(forest, Xc, w["delta"], votes=bufs.votes, mask=bufs.mask),
+                      args.kernel_loops)
+    topq_ms = time_loop(lambda: S.suggest_topq(bufs.acq, bufs.mask, w["q"]), args.kernel_loops)
+
+    flops_per_unit = m * m  # triangular product: m^2 flops per candidate per objective
+    achieved = flops_per_unit * n / (post_ms * 1e-3) / 1e12
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{c['name']}: m={m} n={n} d={w['d']} p={p} front={len(front)} boxes={n_boxes} "
+                        f"trees={c['trees']} depth={c['depth']} q={w['q']}",
+            "timed": "posterior x p + acquisition + forest mask + top-q on the device; host GP fit excluded",
+            "fit_ms": fit_ms,
+            "value_incl_fit": n / ((ms_per_step + fit_ms) * 1e-3),
+            "kernel_ms": {"posterior_per_objective": post_ms, "ehvi": ehvi_ms, "forest": rf_ms, "topq": topq_ms},
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "posterior_f32_kernel (K*, mean, L^-1 K*^T on fp32 MFMA, variance)",
+            "achieved": achieved,
+            "peak": PEAK_FP32_MFMA_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
+            "traffic": None,
+            "algorithmic_unit": f"m^2 = {flops_per_unit} flops per candidate per objective, {n} candidates "
+                                "per launch",
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, seconds):
+    """The oracle as it stands, timed on a bounded sample of the same pool."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle.acquisition import expected_improvement
+    from oracle.forest import feasibility_mask, forest_votes
+    from oracle.gp import gp_fit, gp_posterior
+    from oracle.hypervolume import ehvi, nondominated
+    from oracle.select import top_q
+
+    p = w["p"]
+    fits = [gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][j], w["signal_var"][j], w["noise_var"][j],
+                   w["prior_mean"][j]) for j in range(p)]
+    front = nondominated(w["Y"], w["ref"]) if p > 1 else None
+    T = len(w["forest"]["tree_offset"]) - 1
+    chunk = 8192
+    done = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds and done < len(w["Xc"]):
+        Xs = w["Xc"][done:done + chunk]
+        X64 = Xs.astype(np.float64)
+        mu = np.empty((len(Xs), p))
+        sd = np.empty((len(Xs), p))
+        for j in range(p):
+            mu[:, j], sd[:, j] = gp_posterior(fits[j], X64)
+        acq = expected_improvement(mu[:, 0], sd[:, 0], w["best_y"], w["xi"]) if p == 1 else \
+            ehvi(mu, sd, front, w["ref"])
+        mask = feasibility_mask(forest_votes(w["forest"], Xs), w["delta"], T)
+        top_q(acq, mask, w["q"])
+        done += len(Xs)
+    el = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": done / el, "unit": "candidates/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {done} candidates of the same pool in chunks of {chunk}, {el:.1f}s, fit excluded"}
+
+
+if __name__ == "__main__":
+    main()

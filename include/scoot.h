@@ -1,0 +1,216 @@
+/*
+ * scoot.h -- C ABI of the MI355X (gfx950) candidate-scoring library.
+ *
+ * The library scores a pool of candidate engine configurations the way the
+ * suggestion step of SCOOT (SLO-Oriented Performance Tuning for LLM Inference
+ * Engines) does: GP posterior per objective (Sec. 4.3, Eq. 4-5), acquisition
+ * (EI, Eq. 8; EHVI, Eq. 9), the random-forest hidden-constraint mask
+ * POF(x) >= Delta (Eq. 3, Sec. 4.7) and the top-q parallel pick (Sec. 4.6).
+ * Observed configurations and SLO values go in; indices of the next
+ * configurations to evaluate come out.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Every objective is MINIMISED.  The paper maximises lambda * f (Eq. 1); pass
+ *   y = -lambda * f.  The EHVI reference point is therefore an upper bound.
+ * - Arrays of candidate length n (pool, mu, sigma, scores, votes, mask, leaf
+ *   ids) and the q-sized outputs are DEVICE pointers owned by the caller.
+ *   Everything else (observations, hyperparameters, forest arrays, reference
+ *   point) is a HOST pointer, read during the call and not retained.
+ * - The candidate pool Xc is n x d float32, row-major, on the device.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Device
+ *   work is enqueued asynchronously on it; the caller synchronises.  Calls
+ *   that use one device must be issued on one stream, or the caller orders
+ *   them: library-owned scratch of a device is reused from call to call.
+ * - Handles are library-owned and not thread-safe; destroy them with the
+ *   matching *_destroy call.
+ * - Every call returns a scoot_status.  On error the outputs are undefined and
+ *   scoot_last_error() returns a message for the calling thread.  No C++
+ *   exception crosses the ABI.
+ */
+#ifndef SCOOT_H
+#define SCOOT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SCOOT_ABI_VERSION 1
+
+typedef enum scoot_dtype { SCOOT_F32 = 0, SCOOT_F64 = 1 } scoot_dtype;
+
+typedef enum scoot_status {
+  SCOOT_OK = 0,
+  SCOOT_ERR_INVALID_ARG = -1, /* bad shape, null pointer, NaN/Inf host input, q out of range */
+  SCOOT_ERR_NOT_PD = -2,      /* K + tau^2 I is not numerically positive definite */
+  SCOOT_ERR_DEVICE = -3,      /* a HIP runtime call failed; see scoot_last_error() */
+  SCOOT_ERR_UNSUPPORTED = -4, /* size beyond the limits stated below */
+  SCOOT_ERR_NO_MEMORY = -5    /* host or device allocation failed */
+} scoot_status;
+
+/* Limits of this build. */
+#define SCOOT_MAX_DIM 16        /* d: parameters per configuration */
+#define SCOOT_MAX_OBS 576       /* m: observations per GP */
+#define SCOOT_MAX_OBJECTIVES 3  /* p */
+#define SCOOT_MAX_Q 64          /* q: picks per suggestion */
+#define SCOOT_MAX_TREES 32767   /* T: trees per forest (votes fit int32) */
+
+typedef struct scoot_gp_t* scoot_gp;
+typedef struct scoot_forest_t* scoot_forest;
+
+/* Version of this header's ABI (SCOOT_ABI_VERSION). */
+int scoot_abi_version(void);
+
+/* Static text for a status code. */
+const char* scoot_status_string(int status);
+
+/* Message describing the last failing call made by this thread ("" if none). */
+const char* scoot_last_error(void);
+
+/* ---------------------------------------------------------------------------
+ * Fit (host).  Sec. 4.3, Eq. 4-5: K = k(X, X) + tau^2 I with the Matern-5/2
+ * ARD covariance k(x, x') = s2 (1 + sqrt5 r + 5 r^2 / 3) exp(-sqrt5 r),
+ * r^2 = sum_k ((x_k - x'_k) / l_k)^2; L = chol(K); alpha = K^-1 (y - c).
+ *
+ * scoot_gp_factor_host: host-only arithmetic of the fit, for inspection.
+ *   X      [m*d] observed configurations, row-major, finite.
+ *   y      [m]   observed values of one objective, finite.
+ *   lengthscale [d] > 0; signal_var s2 > 0; noise_var tau^2 >= 0;
+ *   prior_mean c (Eq. 4 has c = 0).
+ *   L      [m*m] out: lower Cholesky factor, row-major (upper part zeroed).
+ *   alpha  [m]   out.
+ *   Errors: INVALID_ARG, UNSUPPORTED (m > SCOOT_MAX_OBS, d > SCOOT_MAX_DIM),
+ *   NOT_PD.
+ *
+ * scoot_gp_fit: the same fit, then a device-resident GP state (the inverse
+ *   factor L^-1 packed for the matrix cores, scaled observations, alpha) on the
+ *   current HIP device, uploaded asynchronously on `stream`.  dt selects the
+ *   precision of scoot_posterior for this handle.  *out receives the handle.
+ * ------------------------------------------------------------------------- */
+int scoot_gp_factor_host(const double* X, const double* y, int m, int d, const double* lengthscale,
+                         double signal_var, double noise_var, double prior_mean, double* L,
+                         double* alpha);
+int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* lengthscale,
+                 double signal_var, double noise_var, double prior_mean, scoot_dtype dt,
+                 void* stream, scoot_gp* out);
+int scoot_gp_destroy(scoot_gp gp);
+
+/* ---------------------------------------------------------------------------
+ * Posterior (device).  Eq. 4 and Eq. 5 of Sec. 4.3 at every candidate:
+ *   mu[i]    = c + k(x_i, X) alpha
+ *   sigma[i] = sqrt(max(0, s2 - ||L^-1 k(X, x_i)||^2))   (latent f; tau^2 not added)
+ * Xc [n*d] float32 device (d = the fitted d); mu, sigma [n] device, float32 or
+ * float64 per the handle's dtype.  n = 0 is a no-op.  A NaN in a candidate row
+ * gives NaN mu/sigma for that candidate.
+ * Errors: INVALID_ARG (null handle/pointer, n < 0), DEVICE.
+ * ------------------------------------------------------------------------- */
+int scoot_posterior(scoot_gp gp, const float* Xc, int64_t n, void* mu, void* sigma, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Expected improvement (device), Eq. 8 of Sec. 4.4.1 mirrored to minimisation:
+ *   ei[i] = E[max(0, best_y + xi - Y_i)],  Y_i ~ N(mu[i], sigma[i]^2)
+ *         = (c - mu) Phi(u) + sigma phi(u),  c = best_y + xi, u = (c - mu) / sigma,
+ * and max(0, c - mu) where sigma = 0.  The paper fixes xi = 1e-4 (Sec. 4.5.1).
+ * mu, sigma, ei [n] device of type dt.  Errors: INVALID_ARG, DEVICE.
+ * ------------------------------------------------------------------------- */
+int scoot_acq_ei(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double best_y, double xi,
+                 void* ei, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Expected hypervolume improvement, Eq. 9 of Sec. 4.4.2 (HV of Fig. 4).
+ *
+ * scoot_ehvi_front (host): the front of Y_obs [m_obs*p] (row-major) w.r.t. ref
+ *   [p]: rows strictly below ref in every objective that no other row weakly
+ *   dominates, duplicates once, sorted lexicographically into front
+ *   [m_obs*p] (nullable); *n_front receives its size and *n_boxes (nullable)
+ *   the number of boxes the device kernel sums over.
+ *
+ * scoot_acq_ehvi (device): for every candidate,
+ *   ehvi[i] = E[HV(P + {Y_i}) - HV(P)] = sum_B prod_j (G_j(u_Bj) - G_j(l_Bj)),
+ *   G_j(c) = E[(c - Y_ij)^+], over boxes B = [l, u] partitioning the region
+ *   below ref that the front P leaves open (G(-inf) = 0).
+ *   mu, sigma: arrays of p device pointers, each [n] of type dt.  p in 1..3.
+ *   Y_obs, ref: host.  ehvi [n] device.
+ * Errors: INVALID_ARG, UNSUPPORTED (front too large for the on-chip tables),
+ * DEVICE.
+ * ------------------------------------------------------------------------- */
+int scoot_ehvi_front(const double* Y_obs, int m_obs, int p, const double* ref, double* front,
+                     int* n_front, int* n_boxes);
+int scoot_acq_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, scoot_dtype dt,
+                   const double* Y_obs, int m_obs, const double* ref, void* ehvi, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Random-forest probability of feasibility (Sec. 4.7) and the mask of Eq. 3.
+ *
+ * scoot_forest_create: n_trees regression trees as flat host arrays; tree t
+ *   owns nodes tree_offset[t] .. tree_offset[t+1]-1 (tree_offset has
+ *   n_trees+1 entries, tree_offset[0] = 0).  left/right are tree-local child
+ *   indices, -1 at a leaf (both or neither).  feature in [0, d) at internal
+ *   nodes; threshold float32; leaf_q16 = round(leaf value * 65536) at leaves,
+ *   in [0, 65536].  Every tree must be a tree rooted at its first node.  The
+ *   forest is validated, repacked (children adjacent) and uploaded
+ *   synchronously to the current device.
+ *
+ * scoot_vote_threshold (host): the smallest vote count with POF >= delta,
+ *   ceil(delta * (n_trees * 65536)) computed in double precision.
+ *
+ * scoot_rf_feasibility (device): each tree is walked from its root, left iff
+ *   x[feature] <= threshold (float32 compare; NaN goes right), to a leaf;
+ *   votes[i] = sum of the reached leaves' Q16 values (exact int32);
+ *   mask[i] = votes[i] >= scoot_vote_threshold(delta, T);
+ *   leaf_idx [n*n_trees] (nullable) = tree-local index of the reached leaf.
+ *   Xc [n*d] float32 device; votes [n] int32 device (nullable); mask [n] u8
+ *   device (nullable).  delta in [0, 1].
+ * Errors: INVALID_ARG, UNSUPPORTED, DEVICE, NO_MEMORY.
+ * ------------------------------------------------------------------------- */
+int scoot_forest_create(const int32_t* feature, const float* threshold, const int32_t* left,
+                        const int32_t* right, const int32_t* leaf_q16, const int64_t* tree_offset,
+                        int n_trees, int d, scoot_forest* out);
+int scoot_forest_destroy(scoot_forest f);
+int scoot_vote_threshold(double delta, int n_trees, int64_t* votes_min);
+int scoot_rf_feasibility(scoot_forest f, const float* Xc, int64_t n, double delta, int32_t* votes,
+                         uint8_t* mask, int32_t* leaf_idx, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Top-q parallel suggestion (Sec. 4.6): the q eligible candidates with the
+ * largest score, score descending, lowest index first on ties (-0 == +0).
+ * Eligible = mask[i] != 0 (mask nullable: all) and score[i] is not NaN.
+ * score [n] device of type dt; idx [q] int64 device; score_out [q] device of
+ * type dt (nullable); n_valid [1] int32 device (nullable) = number eligible.
+ * Fewer than q eligible: the tail of idx is -1 and of score_out NaN (the paper
+ * fills that shortfall with Sobol points, a step left to the caller).
+ * 1 <= q <= SCOOT_MAX_Q; 0 <= n < 2^31.
+ * Errors: INVALID_ARG, DEVICE, NO_MEMORY.
+ * ------------------------------------------------------------------------- */
+int scoot_suggest_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q,
+                       int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Adaptation of Delta after a batch of k evaluated suggestions (Algorithm 1,
+ * Sec. 4.7), host only.  Some result invalid: Delta = min(0.75, max(0.5,
+ * Delta + 0.05)), c = 0.  Otherwise c += k and, if c >= 5, Delta =
+ * max(0.25, Delta - 0.05), c -= 5.  Errors: INVALID_ARG (null, k < 0).
+ * ------------------------------------------------------------------------- */
+int scoot_delta_update(double* delta, int* c, int k, int any_invalid);
+
+/* ---------------------------------------------------------------------------
+ * One whole scoring pass (Sec. 4.1 steps 3-8): scoot_posterior for each of
+ * the p GPs, EI (p = 1, with best_y and xi) or EHVI (p >= 2, with Y_obs
+ * [m_obs*p] and ref [p]), scoot_rf_feasibility with delta (f nullable: every
+ * candidate feasible) and scoot_suggest_topq on the acquisition.
+ * mu, sigma: [p*n] device (objective-major) of the GPs' dtype (all equal);
+ * acq [n]; votes [n] (nullable); mask [n]; idx [q]; score_out [q] (nullable);
+ * n_valid [1] (nullable).  Errors: as the calls it makes.
+ * ------------------------------------------------------------------------- */
+int scoot_score_pool(const scoot_gp* gps, int p, scoot_forest f, const float* Xc, int64_t n,
+                     double best_y, double xi, const double* Y_obs, int m_obs, const double* ref,
+                     double delta, int q, void* mu, void* sigma, void* acq, int32_t* votes,
+                     uint8_t* mask, int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCOOT_H */

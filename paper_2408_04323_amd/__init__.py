@@ -1,0 +1,290 @@
+"""MI355X-native candidate scoring for SCOOT's suggestion step (arXiv 2408.04323).
+
+A thin Python binding over the C ABI of ``libscoot.so`` (``include/scoot.h``):
+arguments are marshalled here, every step of the scoring path runs in the
+library's HIP kernels.  Device arrays are torch tensors on the current HIP
+device; torch provides only memory and the stream.  Names follow the C calls
+without the ``scoot_`` prefix.
+"""
+import ctypes as C
+
+import numpy as np
+
+from ._native import ScootError, check, lib  # noqa: F401
+
+F32, F64 = 0, 1
+_DT = {"f32": F32, "float32": F32, "f64": F64, "float64": F64}
+
+
+def _dt(dtype):
+    if isinstance(dtype, int):
+        return dtype
+    if not isinstance(dtype, str):
+        import torch
+        return F64 if dtype == torch.float64 else F32
+    return _DT[dtype]
+
+
+def _tdtype(dt):
+    import torch
+    return torch.float32 if dt == F32 else torch.float64
+
+
+def _stream(stream):
+    if stream is not None:
+        return C.c_void_p(int(stream))
+    import torch
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dptr(t):
+    return C.c_void_p(0 if t is None else t.data_ptr())
+
+
+def _host(a, dtype):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data_as(C.POINTER(np.ctypeslib.as_ctypes_type(dtype)))
+
+
+def _require_device(t, name, dtype=None, numel=None):
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} must have {numel} elements")
+
+
+def abi_version():
+    return lib().scoot_abi_version()
+
+
+# --------------------------------------------------------------------------- fit
+def gp_factor_host(X, y, lengthscale, signal_var, noise_var, prior_mean=0.0):
+    """Host fit arithmetic: returns (L, alpha) as float64 arrays."""
+    X, pX = _host(X, np.float64)
+    y, py = _host(y, np.float64)
+    ls, pl = _host(lengthscale, np.float64)
+    m, d = X.shape
+    L = np.zeros((m, m))
+    alpha = np.zeros(m)
+    check(lib().scoot_gp_factor_host(pX, py, m, d, pl, signal_var, noise_var, prior_mean,
+                                     L.ctypes.data_as(C.POINTER(C.c_double)),
+                                     alpha.ctypes.data_as(C.POINTER(C.c_double))), "gp_factor_host")
+    return L, alpha
+
+
+class GP:
+    """Device-resident GP state of one objective (a scoot_gp handle)."""
+
+    def __init__(self, handle, m, d, dtype):
+        self._h = C.c_void_p(handle)
+        self.m, self.d, self.dtype = m, d, dtype
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if self._h and self._h.value:
+            lib().scoot_gp_destroy(self._h)
+            self._h = C.c_void_p(0)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def gp_fit(X, y, lengthscale, signal_var, noise_var, prior_mean=0.0, dtype="f32", stream=None):
+    X, pX = _host(X, np.float64)
+    y, py = _host(y, np.float64)
+    ls, pl = _host(lengthscale, np.float64)
+    m, d = X.shape
+    h = C.c_void_p(0)
+    dt = _dt(dtype)
+    check(lib().scoot_gp_fit(pX, py, m, d, pl, signal_var, noise_var, prior_mean, dt, _stream(stream),
+                             C.byref(h)), "gp_fit")
+    return GP(h.value, m, d, dt)
+
+
+# --------------------------------------------------------------------- posterior
+def posterior(gp, Xc, mu=None, sigma=None, stream=None):
+    """mu, sigma of the latent f at every row of Xc (n x d float32 device)."""
+    import torch
+    n = Xc.shape[0]
+    _require_device(Xc, "Xc", torch.float32, n * gp.d)
+    td = _tdtype(gp.dtype)
+    mu = torch.empty(n, dtype=td, device=Xc.device) if mu is None else mu
+    sigma = torch.empty(n, dtype=td, device=Xc.device) if sigma is None else sigma
+    _require_device(mu, "mu", td, n)
+    _require_device(sigma, "sigma", td, n)
+    check(lib().scoot_posterior(gp.handle, _dptr(Xc), n, _dptr(mu), _dptr(sigma), _stream(stream)),
+          "posterior")
+    return mu, sigma
+
+
+def acq_ei(mu, sigma, best_y, xi=1e-4, out=None, stream=None):
+    import torch
+    n = mu.numel()
+    dt = _dt(mu.dtype)
+    _require_device(mu, "mu")
+    _require_device(sigma, "sigma", mu.dtype, n)
+    out = torch.empty_like(mu) if out is None else out
+    _require_device(out, "out", mu.dtype, n)
+    check(lib().scoot_acq_ei(_dptr(mu), _dptr(sigma), n, dt, best_y, xi, _dptr(out), _stream(stream)),
+          "acq_ei")
+    return out
+
+
+# -------------------------------------------------------------------------- EHVI
+def ehvi_front(Y_obs, ref):
+    """Host: (front (k x p) float64, number of boxes)."""
+    r, pr = _host(ref, np.float64)
+    Y, pY = _host(np.asarray(Y_obs, dtype=np.float64).reshape(-1, len(r)), np.float64)
+    m, p = Y.shape
+    front = np.zeros((max(m, 1), p))
+    nf, nbx = C.c_int(0), C.c_int(0)
+    check(lib().scoot_ehvi_front(pY, m, p, pr, front.ctypes.data_as(C.POINTER(C.c_double)), C.byref(nf),
+                                 C.byref(nbx)), "ehvi_front")
+    return front[:nf.value].copy(), nbx.value
+
+
+def acq_ehvi(mus, sigmas, Y_obs, ref, out=None, stream=None):
+    import torch
+    p = len(mus)
+    n = mus[0].numel()
+    dt = _dt(mus[0].dtype)
+    for t in list(mus) + list(sigmas):
+        _require_device(t, "mu/sigma", mus[0].dtype, n)
+    Y, pY = _host(Y_obs, np.float64)
+    Y = Y.reshape(len(Y), p)
+    r, pr = _host(ref, np.float64)
+    out = torch.empty_like(mus[0]) if out is None else out
+    _require_device(out, "out", mus[0].dtype, n)
+    pm = (C.c_void_p * p)(*[t.data_ptr() for t in mus])
+    ps = (C.c_void_p * p)(*[t.data_ptr() for t in sigmas])
+    check(lib().scoot_acq_ehvi(pm, ps, p, n, dt, pY, Y.shape[0], pr, _dptr(out), _stream(stream)),
+          "acq_ehvi")
+    return out
+
+
+# ------------------------------------------------------------------------ forest
+class Forest:
+    """Device-resident packed forest (a scoot_forest handle)."""
+
+    def __init__(self, handle, n_trees, d):
+        self._h = C.c_void_p(handle)
+        self.n_trees, self.d = n_trees, d
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if self._h and self._h.value:
+            lib().scoot_forest_destroy(self._h)
+            self._h = C.c_void_p(0)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def forest_create(feature, threshold, left, right, leaf_q16, tree_offset, d):
+    f, pf = _host(feature, np.int32)
+    t, pt = _host(threshold, np.float32)
+    lf, pl = _host(left, np.int32)
+    rt, pr = _host(right, np.int32)
+    q, pq = _host(leaf_q16, np.int32)
+    off, po = _host(tree_offset, np.int64)
+    T = len(off) - 1
+    h = C.c_void_p(0)
+    check(lib().scoot_forest_create(pf, pt, pl, pr, pq, po, T, d, C.byref(h)), "forest_create")
+    return Forest(h.value, T, d)
+
+
+def vote_threshold(delta, n_trees):
+    v = C.c_int64(0)
+    check(lib().scoot_vote_threshold(delta, n_trees, C.byref(v)), "vote_threshold")
+    return v.value
+
+
+def rf_feasibility(forest, Xc, delta, votes=None, mask=None, leaf_idx=False, stream=None):
+    """Returns (votes int32, mask uint8, leaf ids int32 (n, T) or None)."""
+    import torch
+    n = Xc.shape[0]
+    _require_device(Xc, "Xc", torch.float32, n * forest.d)
+    votes = torch.empty(n, dtype=torch.int32, device=Xc.device) if votes is None else votes
+    mask = torch.empty(n, dtype=torch.uint8, device=Xc.device) if mask is None else mask
+    leaves = torch.empty((n, forest.n_trees), dtype=torch.int32, device=Xc.device) if leaf_idx else None
+    check(lib().scoot_rf_feasibility(forest.handle, _dptr(Xc), n, delta, _dptr(votes), _dptr(mask),
+                                     _dptr(leaves), _stream(stream)), "rf_feasibility")
+    return votes, mask, leaves
+
+
+# ------------------------------------------------------------------------ top-q
+def suggest_topq(score, mask, q, stream=None):
+    """Returns device tensors (idx int64 (q,), score (q,), n_valid int32 (1,))."""
+    import torch
+    n = score.numel()
+    _require_device(score, "score")
+    if mask is not None:
+        _require_device(mask, "mask", torch.uint8, n)
+    idx = torch.empty(q, dtype=torch.int64, device=score.device)
+    sc = torch.empty(q, dtype=score.dtype, device=score.device)
+    nv = torch.empty(1, dtype=torch.int32, device=score.device)
+    check(lib().scoot_suggest_topq(_dptr(score), _dptr(mask), n, _dt(score.dtype), q, _dptr(idx), _dptr(sc),
+                                   _dptr(nv), _stream(stream)), "suggest_topq")
+    return idx, sc, nv
+
+
+# ---------------------------------------------------------------------- Delta
+def delta_update(delta, c, k, any_invalid):
+    dd, cc = C.c_double(delta), C.c_int(c)
+    check(lib().scoot_delta_update(C.byref(dd), C.byref(cc), k, int(bool(any_invalid))), "delta_update")
+    return dd.value, cc.value
+
+
+# ------------------------------------------------------------------ whole pass
+class PoolBuffers:
+    """Device outputs of one scoring pass, allocated once and reused."""
+
+    def __init__(self, n, p, q, dtype, device):
+        import torch
+        td = _tdtype(dtype)
+        self.mu = torch.empty((p, n), dtype=td, device=device)
+        self.sigma = torch.empty((p, n), dtype=td, device=device)
+        self.acq = torch.empty(n, dtype=td, device=device)
+        self.votes = torch.empty(n, dtype=torch.int32, device=device)
+        self.mask = torch.empty(n, dtype=torch.uint8, device=device)
+        self.idx = torch.empty(q, dtype=torch.int64, device=device)
+        self.score = torch.empty(q, dtype=td, device=device)
+        self.n_valid = torch.empty(1, dtype=torch.int32, device=device)
+
+
+def score_pool(gps, forest, Xc, q, best_y=0.0, xi=1e-4, Y_obs=None, ref=None, delta=0.5, buffers=None,
+               stream=None):
+    """One whole pass: posterior per GP, EI (one GP) or EHVI, forest mask, top-q."""
+    import torch
+    p = len(gps)
+    n = Xc.shape[0]
+    _require_device(Xc, "Xc", torch.float32, n * gps[0].d)
+    b = PoolBuffers(n, p, q, gps[0].dtype, Xc.device) if buffers is None else buffers
+    hs = (C.c_void_p * p)(*[g.handle.value for g in gps])
+    if p > 1:
+        Y, pY = _host(Y_obs, np.float64)
+        r, pr = _host(ref, np.float64)
+        m_obs = Y.reshape(-1, p).shape[0]
+    else:
+        pY, pr, m_obs = None, None, 0
+    check(lib().scoot_score_pool(hs, p, forest.handle if forest is not None else None, _dptr(Xc), n, best_y, xi,
+                                 pY, m_obs, pr, delta, q, _dptr(b.mu), _dptr(b.sigma), _dptr(b.acq),
+                                 _dptr(b.votes), _dptr(b.mask), _dptr(b.idx), _dptr(b.score), _dptr(b.n_valid),
+                                 _stream(stream)), "score_pool")
+    return b

@@ -1,0 +1,67 @@
+"""ctypes loader for libscoot.so (built in-tree by ``build.py``).
+
+Loading never falls back to anything: a missing or stale library raises.
+"""
+import ctypes as C
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libscoot.so")
+
+_lib = None
+
+c_int, c_i64, c_dbl, c_vp = C.c_int, C.c_int64, C.c_double, C.c_void_p
+P_dbl, P_int, P_i64 = C.POINTER(C.c_double), C.POINTER(C.c_int), C.POINTER(C.c_int64)
+P_i32, P_f32 = C.POINTER(C.c_int32), C.POINTER(C.c_float)
+
+# name -> argtypes (every function returns int)
+SIGNATURES = {
+    "scoot_abi_version": [],
+    "scoot_status_string": [c_int],
+    "scoot_last_error": [],
+    "scoot_gp_factor_host": [P_dbl, P_dbl, c_int, c_int, P_dbl, c_dbl, c_dbl, c_dbl, P_dbl, P_dbl],
+    "scoot_gp_fit": [P_dbl, P_dbl, c_int, c_int, P_dbl, c_dbl, c_dbl, c_dbl, c_int, c_vp, C.POINTER(c_vp)],
+    "scoot_gp_destroy": [c_vp],
+    "scoot_posterior": [c_vp, c_vp, c_i64, c_vp, c_vp, c_vp],
+    "scoot_acq_ei": [c_vp, c_vp, c_i64, c_int, c_dbl, c_dbl, c_vp, c_vp],
+    "scoot_ehvi_front": [P_dbl, c_int, c_int, P_dbl, P_dbl, P_int, P_int],
+    "scoot_acq_ehvi": [C.POINTER(c_vp), C.POINTER(c_vp), c_int, c_i64, c_int, P_dbl, c_int, P_dbl, c_vp, c_vp],
+    "scoot_forest_create": [P_i32, P_f32, P_i32, P_i32, P_i32, P_i64, c_int, c_int, C.POINTER(c_vp)],
+    "scoot_forest_destroy": [c_vp],
+    "scoot_vote_threshold": [c_dbl, c_int, P_i64],
+    "scoot_rf_feasibility": [c_vp, c_vp, c_i64, c_dbl, c_vp, c_vp, c_vp, c_vp],
+    "scoot_suggest_topq": [c_vp, c_vp, c_i64, c_int, c_int, c_vp, c_vp, c_vp, c_vp],
+    "scoot_delta_update": [P_dbl, P_int, c_int, c_int],
+    "scoot_score_pool": [C.POINTER(c_vp), c_int, c_vp, c_vp, c_i64, c_dbl, c_dbl, P_dbl, c_int, P_dbl,
+                         c_dbl, c_int, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp],
+}
+RESTYPES = {"scoot_status_string": C.c_char_p, "scoot_last_error": C.c_char_p}
+
+
+class ScootError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2408_04323_amd.build.build() "
+                               "(the scoring path has no CPU fallback)")
+        L = C.CDLL(LIB_PATH)
+        for name, args in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = RESTYPES.get(name, c_int)
+        _lib = L
+    return _lib
+
+
+def check(status, what):
+    if status != 0:
+        L = lib()
+        raise ScootError(status, f"{what}: {L.scoot_status_string(status).decode()}: "
+                                 f"{L.scoot_last_error().decode()}")

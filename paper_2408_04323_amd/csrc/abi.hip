@@ -1,0 +1,460 @@
+// C ABI of the scoring library: argument checks, handles, library-owned
+// scratch, and the order of the device calls.  See include/scoot.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+struct scoot_gp_t {
+  scoot::GPDevice dev;
+  int device = 0;
+};
+struct scoot_forest_t {
+  scoot::ForestDevice dev;
+  int device = 0;
+};
+
+namespace scoot {
+
+namespace {
+thread_local std::string g_last_error;
+
+constexpr int kMaxDevices = 64;
+constexpr int kScratchSlots = 4;
+constexpr int kStagingSlots = 2;
+
+struct Staging {
+  void* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t done = nullptr;
+  bool pending = false;
+};
+struct DeviceState {
+  void* scratch[kScratchSlots] = {};
+  size_t scratch_cap[kScratchSlots] = {};
+  Staging staging[kStagingSlots];
+};
+std::mutex g_mu;
+DeviceState g_dev[kMaxDevices];
+
+int current_device() {
+  int d = 0;
+  if (hipGetDevice(&d) != hipSuccess) return -1;
+  return d;
+}
+}  // namespace
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+int fail(int status, const std::string& msg) {
+  g_last_error = msg;
+  return status;
+}
+
+void* device_scratch(size_t bytes, int slot) {
+  const int d = current_device();
+  if (d < 0 || d >= kMaxDevices || slot < 0 || slot >= kScratchSlots) return nullptr;
+  std::lock_guard<std::mutex> lk(g_mu);
+  DeviceState& st = g_dev[d];
+  if (st.scratch_cap[slot] < bytes || !st.scratch[slot]) {
+    // Grow-only.  hipFree waits for the device, so work still reading the old
+    // buffer has finished before it is released.
+    if (st.scratch[slot]) hipFree(st.scratch[slot]);
+    st.scratch[slot] = nullptr;
+    st.scratch_cap[slot] = 0;
+    size_t cap = bytes < 4096 ? 4096 : bytes + bytes / 4;
+    if (hipMalloc(&st.scratch[slot], cap) != hipSuccess) {
+      st.scratch[slot] = nullptr;
+      return nullptr;
+    }
+    st.scratch_cap[slot] = cap;
+  }
+  return st.scratch[slot];
+}
+
+int upload_async(void* dst, const void* src, size_t bytes, int slot, void* stream) {
+  const int d = current_device();
+  if (d < 0 || d >= kMaxDevices || slot < 0 || slot >= kStagingSlots)
+    return fail(SCOOT_ERR_DEVICE, "upload: no current device");
+  if (bytes == 0) return SCOOT_OK;
+  std::lock_guard<std::mutex> lk(g_mu);
+  Staging& sg = g_dev[d].staging[slot];
+  if (sg.pending) {
+    if (hipEventSynchronize(sg.done) != hipSuccess) return fail(SCOOT_ERR_DEVICE, "upload: event wait failed");
+    sg.pending = false;
+  }
+  if (!sg.done && hipEventCreateWithFlags(&sg.done, hipEventDisableTiming) != hipSuccess)
+    return fail(SCOOT_ERR_DEVICE, "upload: event creation failed");
+  if (sg.cap < bytes) {
+    if (sg.host) hipHostFree(sg.host);
+    sg.host = nullptr;
+    sg.cap = 0;
+    size_t cap = bytes < 65536 ? 65536 : bytes;
+    if (hipHostMalloc(&sg.host, cap, hipHostMallocDefault) != hipSuccess) {
+      sg.host = nullptr;
+      return fail(SCOOT_ERR_NO_MEMORY, "upload: pinned staging allocation failed");
+    }
+    sg.cap = cap;
+  }
+  std::memcpy(sg.host, src, bytes);
+  hipStream_t s = (hipStream_t)stream;
+  if (hipMemcpyAsync(dst, sg.host, bytes, hipMemcpyHostToDevice, s) != hipSuccess)
+    return fail(SCOOT_ERR_DEVICE, "upload: hipMemcpyAsync failed");
+  if (hipEventRecord(sg.done, s) != hipSuccess) return fail(SCOOT_ERR_DEVICE, "upload: event record failed");
+  sg.pending = true;
+  return SCOOT_OK;
+}
+
+}  // namespace scoot
+
+using namespace scoot;
+
+namespace {
+constexpr double kLn2 = 0.69314718055994530942;
+
+bool check_dtype(scoot_dtype dt) { return dt == SCOOT_F32 || dt == SCOOT_F64; }
+
+int device_error(const char* what, hipError_t e) {
+  return fail(SCOOT_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+}  // namespace
+
+extern "C" {
+
+int scoot_abi_version(void) { return SCOOT_ABI_VERSION; }
+
+const char* scoot_status_string(int status) {
+  switch (status) {
+    case SCOOT_OK: return "ok";
+    case SCOOT_ERR_INVALID_ARG: return "invalid argument";
+    case SCOOT_ERR_NOT_PD: return "matrix not positive definite";
+    case SCOOT_ERR_DEVICE: return "device error";
+    case SCOOT_ERR_UNSUPPORTED: return "unsupported size";
+    case SCOOT_ERR_NO_MEMORY: return "out of memory";
+    default: return "unknown status";
+  }
+}
+
+const char* scoot_last_error(void) { return g_last_error.c_str(); }
+
+int scoot_gp_factor_host(const double* X, const double* y, int m, int d, const double* lengthscale,
+                         double signal_var, double noise_var, double prior_mean, double* L, double* alpha) {
+  g_last_error.clear();
+  if (!L || !alpha) return fail(SCOOT_ERR_INVALID_ARG, "gp factor: null output");
+  try {
+    FitHost f;
+    int rc = fit_host(X, y, m, d, lengthscale, signal_var, noise_var, prior_mean, f);
+    if (rc != SCOOT_OK) return rc;
+    std::memcpy(L, f.L.data(), sizeof(double) * (size_t)m * m);
+    std::memcpy(alpha, f.alpha.data(), sizeof(double) * (size_t)m);
+    return SCOOT_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "gp factor: host allocation failed");
+  }
+}
+
+int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* lengthscale, double signal_var,
+                 double noise_var, double prior_mean, scoot_dtype dt, void* stream, scoot_gp* out) {
+  g_last_error.clear();
+  (void)stream;
+  if (!out) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: null output handle");
+  *out = nullptr;
+  if (!check_dtype(dt)) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: bad dtype");
+  try {
+    FitHost f;
+    int rc = fit_host(X, y, m, d, lengthscale, signal_var, noise_var, prior_mean, f);
+    if (rc != SCOOT_OK) return rc;
+    GPDevice g;
+    g.dt = dt;
+    g.m = m;
+    g.d = d;
+    g.m_pad = f.m_pad;
+    g.nb = f.nb;
+    g.d4 = (d + 3) / 4;
+    g.s2 = signal_var;
+    g.tau2 = noise_var;
+    g.c = prior_mean;
+    for (int k = 0; k < SCOOT_MAX_DIM; ++k) {
+      g.scale64[k] = k < d ? f.scale[k] : 0.0;
+      g.scale32[k] = (float)g.scale64[k];
+    }
+    g.coef64[0] = signal_var;
+    g.coef64[1] = signal_var * kLn2;
+    g.coef64[2] = signal_var * kLn2 * kLn2 / 3.0;
+    for (int i = 0; i < 3; ++i) g.coef32[i] = (float)g.coef64[i];
+
+    // Host image of the device buffer: [L^-1 packed][scaled observations][alpha].
+    std::vector<unsigned char> img;
+    size_t linv_bytes, xs_bytes;
+    const size_t esz = dt == SCOOT_F32 ? 4 : 8;
+    std::vector<float> l32;
+    std::vector<double> l64;
+    if (dt == SCOOT_F32) {
+      pack_linv_f32(f, l32);
+      linv_bytes = l32.size() * 4;
+    } else {
+      pack_linv_f64(f, l64);
+      linv_bytes = l64.size() * 8;
+    }
+    linv_bytes = (linv_bytes + 255) / 256 * 256;
+    xs_bytes = ((size_t)f.m_pad * kXsStride * esz + 255) / 256 * 256;
+    const size_t alpha_bytes = (size_t)f.m_pad * 8;
+    img.assign(linv_bytes + xs_bytes + alpha_bytes, 0);
+    if (dt == SCOOT_F32) std::memcpy(img.data(), l32.data(), l32.size() * 4);
+    else std::memcpy(img.data(), l64.data(), l64.size() * 8);
+    for (int i = 0; i < f.m_pad; ++i)
+      for (int k = 0; k < kXsStride; ++k) {
+        double v = 0.0;
+        if (k < d) v = i < m ? X[(size_t)i * d + k] * f.scale[k] : kPadCoord;
+        unsigned char* at = img.data() + linv_bytes + ((size_t)i * kXsStride + k) * esz;
+        if (dt == SCOOT_F32) {
+          float fv = (float)v;
+          std::memcpy(at, &fv, 4);
+        } else {
+          std::memcpy(at, &v, 8);
+        }
+      }
+    std::vector<double> apad(f.m_pad, 0.0);
+    std::memcpy(apad.data(), f.alpha.data(), sizeof(double) * m);
+    std::memcpy(img.data() + linv_bytes + xs_bytes, apad.data(), alpha_bytes);
+
+    hipError_t e = hipMalloc(&g.buf, img.size());
+    if (e != hipSuccess) return fail(SCOOT_ERR_NO_MEMORY, "gp fit: device allocation failed");
+    e = hipMemcpy(g.buf, img.data(), img.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      hipFree(g.buf);
+      return device_error("gp fit: upload", e);
+    }
+    g.linv = g.buf;
+    g.xs = (unsigned char*)g.buf + linv_bytes;
+    g.alpha = (const double*)((unsigned char*)g.buf + linv_bytes + xs_bytes);
+    scoot_gp h = new scoot_gp_t;
+    h->dev = g;
+    hipGetDevice(&h->device);
+    *out = h;
+    return SCOOT_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "gp fit: host allocation failed");
+  }
+}
+
+int scoot_gp_destroy(scoot_gp gp) {
+  g_last_error.clear();
+  if (!gp) return SCOOT_OK;
+  if (gp->dev.buf) hipFree(gp->dev.buf);
+  delete gp;
+  return SCOOT_OK;
+}
+
+int scoot_posterior(scoot_gp gp, const float* Xc, int64_t n, void* mu, void* sigma, void* stream) {
+  g_last_error.clear();
+  if (!gp) return fail(SCOOT_ERR_INVALID_ARG, "posterior: null handle");
+  if (n < 0) return fail(SCOOT_ERR_INVALID_ARG, "posterior: n < 0");
+  if (n > 0 && (!Xc || !mu || !sigma)) return fail(SCOOT_ERR_INVALID_ARG, "posterior: null pointer");
+  return launch_posterior(gp->dev, Xc, n, mu, sigma, nullptr, nullptr, stream);
+}
+
+int scoot_acq_ei(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double best_y, double xi,
+                 void* ei, void* stream) {
+  g_last_error.clear();
+  if (!check_dtype(dt) || n < 0) return fail(SCOOT_ERR_INVALID_ARG, "ei: bad dtype or n");
+  if (n > 0 && (!mu || !sigma || !ei)) return fail(SCOOT_ERR_INVALID_ARG, "ei: null pointer");
+  if (!std::isfinite(best_y) || !std::isfinite(xi)) return fail(SCOOT_ERR_INVALID_ARG, "ei: non-finite best_y/xi");
+  return launch_ei(mu, sigma, n, dt, best_y + xi, ei, stream);
+}
+
+int scoot_ehvi_front(const double* Y_obs, int m_obs, int p, const double* ref, double* front, int* n_front,
+                     int* n_boxes) {
+  g_last_error.clear();
+  if (!n_front) return fail(SCOOT_ERR_INVALID_ARG, "ehvi front: null n_front");
+  try {
+    BoxTable bt;
+    int rc = build_boxes(Y_obs, m_obs, p, ref, bt);
+    if (rc != SCOOT_OK) return rc;
+    *n_front = bt.n_front;
+    if (front && bt.n_front) std::memcpy(front, bt.front.data(), sizeof(double) * bt.front.size());
+    if (n_boxes) *n_boxes = bt.n_boxes();
+    return SCOOT_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "ehvi front: host allocation failed");
+  }
+}
+
+int scoot_acq_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, scoot_dtype dt,
+                   const double* Y_obs, int m_obs, const double* ref, void* ehvi, void* stream) {
+  g_last_error.clear();
+  if (!check_dtype(dt) || n < 0 || p < 1 || p > SCOOT_MAX_OBJECTIVES)
+    return fail(SCOOT_ERR_INVALID_ARG, "ehvi: bad dtype, n or p");
+  if (n > 0) {
+    if (!mu || !sigma || !ehvi) return fail(SCOOT_ERR_INVALID_ARG, "ehvi: null pointer");
+    for (int j = 0; j < p; ++j)
+      if (!mu[j] || !sigma[j]) return fail(SCOOT_ERR_INVALID_ARG, "ehvi: null objective pointer");
+  }
+  try {
+    BoxTable bt;
+    int rc = build_boxes(Y_obs, m_obs, p, ref, bt);
+    if (rc != SCOOT_OK) return rc;
+    return launch_ehvi(mu, sigma, p, n, dt, bt, ehvi, stream);
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "ehvi: host allocation failed");
+  }
+}
+
+int scoot_forest_create(const int32_t* feature, const float* threshold, const int32_t* left, const int32_t* right,
+                        const int32_t* leaf_q16, const int64_t* tree_offset, int n_trees, int d,
+                        scoot_forest* out) {
+  g_last_error.clear();
+  if (!out) return fail(SCOOT_ERR_INVALID_ARG, "forest: null output handle");
+  *out = nullptr;
+  try {
+    ForestHost fh;
+    int rc = pack_forest(feature, threshold, left, right, leaf_q16, tree_offset, n_trees, d, fh);
+    if (rc != SCOOT_OK) return rc;
+    ForestDevice f;
+    f.n_trees = n_trees;
+    f.d = d;
+    f.chunk_tree = fh.chunk_tree;
+    for (size_t c = 0; c + 1 < fh.chunk_tree.size(); ++c) f.chunk_first_node.push_back(fh.root[fh.chunk_tree[c]]);
+    f.chunk_first_node.push_back(fh.root[n_trees]);
+    const size_t nb = fh.nodes.size() * 4, rb = fh.root.size() * 4;
+    hipError_t e = hipMalloc(&f.nodes, nb + rb);
+    if (e != hipSuccess) return fail(SCOOT_ERR_NO_MEMORY, "forest: device allocation failed");
+    f.root = (uint32_t*)((unsigned char*)f.nodes + nb);
+    e = hipMemcpy(f.nodes, fh.nodes.data(), nb, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(f.root, fh.root.data(), rb, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      hipFree(f.nodes);
+      return device_error("forest: upload", e);
+    }
+    scoot_forest h = new scoot_forest_t;
+    h->dev = f;
+    hipGetDevice(&h->device);
+    *out = h;
+    return SCOOT_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "forest: host allocation failed");
+  }
+}
+
+int scoot_forest_destroy(scoot_forest f) {
+  g_last_error.clear();
+  if (!f) return SCOOT_OK;
+  if (f->dev.nodes) hipFree(f->dev.nodes);
+  delete f;
+  return SCOOT_OK;
+}
+
+int scoot_vote_threshold(double delta, int n_trees, int64_t* votes_min) {
+  g_last_error.clear();
+  if (!votes_min || !(delta >= 0.0 && delta <= 1.0) || n_trees < 1 || n_trees > SCOOT_MAX_TREES)
+    return fail(SCOOT_ERR_INVALID_ARG, "vote threshold: delta must be in [0,1], 1 <= T <= SCOOT_MAX_TREES");
+  *votes_min = (int64_t)std::ceil(delta * (double)((int64_t)n_trees * 65536));
+  return SCOOT_OK;
+}
+
+int scoot_rf_feasibility(scoot_forest f, const float* Xc, int64_t n, double delta, int32_t* votes, uint8_t* mask,
+                         int32_t* leaf_idx, void* stream) {
+  g_last_error.clear();
+  if (!f) return fail(SCOOT_ERR_INVALID_ARG, "rf: null forest");
+  if (n < 0 || (n > 0 && !Xc)) return fail(SCOOT_ERR_INVALID_ARG, "rf: bad n or null pool");
+  int64_t vmin = 0;
+  int rc = scoot_vote_threshold(delta, f->dev.n_trees, &vmin);
+  if (rc != SCOOT_OK) return rc;
+  return launch_forest(f->dev, Xc, n, vmin, votes, mask, leaf_idx, stream);
+}
+
+int scoot_suggest_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q, int64_t* idx,
+                       void* score_out, int32_t* n_valid, void* stream) {
+  g_last_error.clear();
+  if (!check_dtype(dt)) return fail(SCOOT_ERR_INVALID_ARG, "topq: bad dtype");
+  if (q < 1 || q > SCOOT_MAX_Q) return fail(SCOOT_ERR_INVALID_ARG, "topq: q must be in 1..SCOOT_MAX_Q");
+  if (n < 0 || n >= ((int64_t)1 << 31)) return fail(SCOOT_ERR_INVALID_ARG, "topq: n out of range");
+  if (!idx || (n > 0 && !score)) return fail(SCOOT_ERR_INVALID_ARG, "topq: null pointer");
+  return launch_topq(score, mask, n, dt, q, idx, score_out, n_valid, stream);
+}
+
+int scoot_delta_update(double* delta, int* c, int k, int any_invalid) {
+  g_last_error.clear();
+  if (!delta || !c || k < 0) return fail(SCOOT_ERR_INVALID_ARG, "delta update: null pointer or k < 0");
+  if (any_invalid) {
+    double v = *delta + 0.05;
+    if (v < 0.5) v = 0.5;
+    if (v > 0.75) v = 0.75;
+    *delta = v;
+    *c = 0;
+  } else {
+    *c += k;
+    if (*c >= 5) {
+      double v = *delta - 0.05;
+      *delta = v < 0.25 ? 0.25 : v;
+      *c -= 5;
+    }
+  }
+  return SCOOT_OK;
+}
+
+int scoot_score_pool(const scoot_gp* gps, int p, scoot_forest f, const float* Xc, int64_t n, double best_y,
+                     double xi, const double* Y_obs, int m_obs, const double* ref, double delta, int q, void* mu,
+                     void* sigma, void* acq, int32_t* votes, uint8_t* mask, int64_t* idx, void* score_out,
+                     int32_t* n_valid, void* stream) {
+  g_last_error.clear();
+  if (!gps || p < 1 || p > SCOOT_MAX_OBJECTIVES) return fail(SCOOT_ERR_INVALID_ARG, "score pool: bad p or gps");
+  for (int j = 0; j < p; ++j)
+    if (!gps[j] || gps[j]->dev.dt != gps[0]->dev.dt || gps[j]->dev.d != gps[0]->dev.d)
+      return fail(SCOOT_ERR_INVALID_ARG, "score pool: GPs must share dtype and d");
+  if (n < 0 || (n > 0 && (!Xc || !mu || !sigma || !acq || !mask))) return fail(SCOOT_ERR_INVALID_ARG, "score pool: null pointer");
+  if (!idx) return fail(SCOOT_ERR_INVALID_ARG, "score pool: null idx");
+  if (q < 1 || q > SCOOT_MAX_Q) return fail(SCOOT_ERR_INVALID_ARG, "score pool: q out of range");
+  const scoot_dtype dt = gps[0]->dev.dt;
+  const size_t esz = dt == SCOOT_F32 ? 4 : 8;
+  const void* mus[SCOOT_MAX_OBJECTIVES];
+  const void* sds[SCOOT_MAX_OBJECTIVES];
+  int rc;
+  BoxTable bt;
+  if (p > 1) {
+    try {
+      rc = build_boxes(Y_obs, m_obs, p, ref, bt);
+    } catch (const std::bad_alloc&) {
+      return fail(SCOOT_ERR_NO_MEMORY, "score pool: host allocation failed");
+    }
+    if (rc != SCOOT_OK) return rc;
+  } else if (!std::isfinite(best_y) || !std::isfinite(xi)) {
+    return fail(SCOOT_ERR_INVALID_ARG, "score pool: non-finite best_y/xi");
+  }
+  int64_t vmin = 0;
+  if (f) {
+    rc = scoot_vote_threshold(delta, f->dev.n_trees, &vmin);
+    if (rc != SCOOT_OK) return rc;
+  }
+  for (int j = 0; j < p; ++j) {
+    void* mj = (unsigned char*)mu + (size_t)j * n * esz;
+    void* sj = (unsigned char*)sigma + (size_t)j * n * esz;
+    mus[j] = mj;
+    sds[j] = sj;
+    if (p == 1) {
+      const double c = best_y + xi;
+      rc = launch_posterior(gps[j]->dev, Xc, n, mj, sj, &c, acq, stream);
+    } else {
+      rc = launch_posterior(gps[j]->dev, Xc, n, mj, sj, nullptr, nullptr, stream);
+    }
+    if (rc != SCOOT_OK) return rc;
+  }
+  if (p > 1) {
+    rc = launch_ehvi(mus, sds, p, n, dt, bt, acq, stream);
+    if (rc != SCOOT_OK) return rc;
+  }
+  if (f) {
+    rc = launch_forest(f->dev, Xc, n, vmin, votes, mask, nullptr, stream);
+  } else if (n > 0) {
+    rc = launch_fill_u8(mask, n, 1, stream);
+  }
+  if (rc != SCOOT_OK) return rc;
+  return launch_topq(acq, mask, n, dt, q, idx, score_out, n_valid, stream);
+}
+
+}  // extern "C"

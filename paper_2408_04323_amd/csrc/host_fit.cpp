@@ -1,0 +1,163 @@
+// Host side of the GP fit (Sec. 4.3, Eq. 4-5): K = k(X, X) + tau^2 I with the
+// Matern-5/2 ARD covariance, its Cholesky factor L, alpha = K^-1 (y - c), and
+// the explicit inverse factor L^-1 that the device applies to k(X, x).
+//
+// sigma^2(x) = s2 - ||L^-1 k(X, x)||^2, so the device needs L^-1 (lower
+// triangular).  Applying it as a triangular matrix product instead of a
+// substitution removes every dependency between row blocks, so all row blocks
+// of a candidate tile can run on the matrix cores at once.
+#include <cmath>
+#include <cstring>
+#include <string>
+
+#include "internal.h"
+
+namespace scoot {
+
+namespace {
+constexpr double kSqrt5 = 2.23606797749978969641;
+constexpr double kLog2e = 1.44269504088896340736;
+
+bool finite_all(const double* v, size_t n) {
+  for (size_t i = 0; i < n; ++i)
+    if (!std::isfinite(v[i])) return false;
+  return true;
+}
+}  // namespace
+
+int fit_host(const double* X, const double* y, int m, int d, const double* ls, double s2,
+             double tau2, double c, FitHost& f, const double**) {
+  if (!X || !y || !ls) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: null pointer");
+  if (m < 1 || d < 1) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: m and d must be >= 1");
+  if (d > SCOOT_MAX_DIM) return fail(SCOOT_ERR_UNSUPPORTED, "gp fit: d exceeds SCOOT_MAX_DIM");
+  if (m > SCOOT_MAX_OBS) return fail(SCOOT_ERR_UNSUPPORTED, "gp fit: m exceeds SCOOT_MAX_OBS");
+  if (!finite_all(X, (size_t)m * d) || !finite_all(y, m))
+    return fail(SCOOT_ERR_INVALID_ARG, "gp fit: non-finite observation");
+  for (int k = 0; k < d; ++k)
+    if (!(ls[k] > 0) || !std::isfinite(ls[k]))
+      return fail(SCOOT_ERR_INVALID_ARG, "gp fit: lengthscales must be finite and > 0");
+  if (!(s2 > 0) || !std::isfinite(s2) || !(tau2 >= 0) || !std::isfinite(tau2) || !std::isfinite(c))
+    return fail(SCOOT_ERR_INVALID_ARG, "gp fit: bad signal/noise variance or prior mean");
+
+  f.m = m;
+  f.d = d;
+  f.m_pad = (m + kBlk32 - 1) / kBlk32 * kBlk32;
+  f.nb = f.m_pad / kBlk32;
+  f.s2 = s2;
+  f.tau2 = tau2;
+  f.c = c;
+  f.scale.assign(d, 0.0);
+  std::vector<double> inv_ls(d);
+  for (int k = 0; k < d; ++k) {
+    inv_ls[k] = 1.0 / ls[k];
+    f.scale[k] = kSqrt5 * kLog2e / ls[k];
+  }
+
+  // K = k(X, X) + tau^2 I (lower triangle is all the factorisation reads).
+  std::vector<double> K((size_t)m * m, 0.0);
+  for (int i = 0; i < m; ++i) {
+    for (int j = 0; j <= i; ++j) {
+      double r2 = 0;
+      for (int k = 0; k < d; ++k) {
+        double t = (X[(size_t)i * d + k] - X[(size_t)j * d + k]) * inv_ls[k];
+        r2 += t * t;
+      }
+      double t = kSqrt5 * std::sqrt(r2);
+      double kv = s2 * (1.0 + t + t * t / 3.0) * std::exp(-t);
+      K[(size_t)i * m + j] = kv + (i == j ? tau2 : 0.0);
+    }
+  }
+
+  // Row-oriented Cholesky, L L^T = K.  A pivot that is not positive, or below
+  // 1e-13 of its diagonal entry, means K is not numerically positive definite.
+  f.L.assign((size_t)m * m, 0.0);
+  double* L = f.L.data();
+  for (int i = 0; i < m; ++i) {
+    const double* Li = L + (size_t)i * m;
+    for (int j = 0; j <= i; ++j) {
+      const double* Lj = L + (size_t)j * m;
+      double s = K[(size_t)i * m + j];
+      for (int k = 0; k < j; ++k) s -= Li[k] * Lj[k];
+      if (i == j) {
+        double kii = K[(size_t)i * m + i];
+        if (!(s > 1e-13 * kii)) return fail(SCOOT_ERR_NOT_PD, "gp fit: K + tau^2 I is not positive definite");
+        L[(size_t)i * m + i] = std::sqrt(s);
+      } else {
+        L[(size_t)i * m + j] = s / Lj[j];
+      }
+    }
+  }
+
+  // alpha = L^-T L^-1 (y - c).
+  std::vector<double> z(m);
+  for (int i = 0; i < m; ++i) {
+    double s = y[i] - c;
+    for (int k = 0; k < i; ++k) s -= L[(size_t)i * m + k] * z[k];
+    z[i] = s / L[(size_t)i * m + i];
+  }
+  f.alpha.assign(m, 0.0);
+  for (int i = m - 1; i >= 0; --i) {
+    double s = z[i];
+    for (int k = i + 1; k < m; ++k) s -= L[(size_t)k * m + i] * f.alpha[k];
+    f.alpha[i] = s / L[(size_t)i * m + i];
+  }
+
+  // L^-1 column by column: forward substitution of L w = e_j.
+  f.Linv.assign((size_t)m * m, 0.0);
+  std::vector<double> w(m);
+  for (int j = 0; j < m; ++j) {
+    w[j] = 1.0 / L[(size_t)j * m + j];
+    f.Linv[(size_t)j * m + j] = w[j];
+    for (int i = j + 1; i < m; ++i) {
+      const double* Li = L + (size_t)i * m;
+      double s = 0;
+      for (int k = j; k < i; ++k) s += Li[k] * w[k];
+      w[i] = -s / Li[i];
+      f.Linv[(size_t)i * m + j] = w[i];
+    }
+  }
+  return SCOOT_OK;
+}
+
+// fp32 layout.  Row block I and column block J (32 x 32, J <= I) of L^-1 feed
+// one v_mfma_f32_32x32x2f32 chain as its A operand: at step s (0..15) lane l
+// holds A[i][k] = Linv[32I + i][32J + 2s + k] with i = l % 32, k = l / 32.
+// Blocks are stored row-block by row-block, (I, 0..I), so the blocks of a row
+// are contiguous; inside a block the 16 steps are grouped in fours so a lane
+// reads its four consecutive steps as one 16-byte load:
+//   float index = ((blk * 4 + s / 4) * 64 + l) * 4 + s % 4,  blk = I(I+1)/2 + J.
+void pack_linv_f32(const FitHost& f, std::vector<float>& out) {
+  const int nb = f.nb, m = f.m;
+  out.assign((size_t)nb * (nb + 1) / 2 * 16 * 64, 0.0f);
+  for (int I = 0; I < nb; ++I)
+    for (int J = 0; J <= I; ++J) {
+      size_t blk = (size_t)I * (I + 1) / 2 + J;
+      for (int s = 0; s < 16; ++s)
+        for (int l = 0; l < 64; ++l) {
+          int r = 32 * I + (l % 32), col = 32 * J + 2 * s + l / 32;
+          double v = (r < m && col < m) ? f.Linv[(size_t)r * m + col] : 0.0;
+          out[((blk * 4 + s / 4) * 64 + l) * 4 + s % 4] = (float)v;
+        }
+    }
+}
+
+// fp64 layout, for v_mfma_f64_16x16x4f64: 16 x 16 blocks, four steps per
+// block; at step s lane l holds Linv[16I + l % 16][16J + 4s + l / 16]; steps
+// are paired so a lane reads two consecutive steps as one 16-byte load:
+//   double index = ((blk * 2 + s / 2) * 64 + l) * 2 + s % 2,  blk = I(I+1)/2 + J.
+void pack_linv_f64(const FitHost& f, std::vector<double>& out) {
+  const int nb = f.m_pad / kBlk64, m = f.m;
+  out.assign((size_t)nb * (nb + 1) / 2 * 4 * 64, 0.0);
+  for (int I = 0; I < nb; ++I)
+    for (int J = 0; J <= I; ++J) {
+      size_t blk = (size_t)I * (I + 1) / 2 + J;
+      for (int s = 0; s < 4; ++s)
+        for (int l = 0; l < 64; ++l) {
+          int r = 16 * I + (l % 16), col = 16 * J + 4 * s + l / 16;
+          double v = (r < m && col < m) ? f.Linv[(size_t)r * m + col] : 0.0;
+          out[((blk * 2 + s / 2) * 64 + l) * 2 + s % 2] = v;
+        }
+    }
+}
+
+}  // namespace scoot

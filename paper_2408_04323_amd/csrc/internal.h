@@ -1,0 +1,110 @@
+// Internal declarations shared by the host code and the kernel launchers.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "scoot.h"
+
+namespace scoot {
+
+// Rows of the inverse factor handled by one MFMA row block (fp32 path: the
+// 32x32x2 instruction) and the padded row stride of the scaled observations.
+constexpr int kBlk32 = 32;
+constexpr int kBlk64 = 16;
+constexpr int kXsStride = 16;          // floats / doubles per observation row
+constexpr double kPadCoord = 1.0e4;    // scaled coordinate of padding rows: k(x, pad) == 0
+
+void set_error(const std::string& msg);
+int fail(int status, const std::string& msg);
+
+// ---- fit (host) -----------------------------------------------------------
+struct FitHost {
+  int m = 0, d = 0, m_pad = 0, nb = 0;     // nb = m_pad / 32
+  double s2 = 1, tau2 = 0, c = 0;
+  std::vector<double> L;                   // m x m row-major lower factor
+  std::vector<double> Linv;                // m x m row-major lower inverse factor
+  std::vector<double> alpha;               // m
+  std::vector<double> scale;               // d: sqrt5 * log2(e) / l_k
+};
+
+// Validates and computes K, its Cholesky factor, alpha and L^-1 in fp64.
+int fit_host(const double* X, const double* y, int m, int d, const double* ls, double s2,
+             double tau2, double c, FitHost& out, const double** Xout = nullptr);
+
+// Packs L^-1 into matrix-core A-operand order (see the posterior kernels).
+void pack_linv_f32(const FitHost& f, std::vector<float>& out);
+void pack_linv_f64(const FitHost& f, std::vector<double>& out);
+
+// ---- EHVI boxes (host) ------------------------------------------------------
+struct BoxTable {
+  int p = 0;
+  int n_front = 0;
+  std::vector<double> front;               // n_front x p, lexicographic
+  std::vector<std::vector<double>> coord;  // per axis: [-inf, sorted unique front values..., ref]
+  std::vector<int16_t> lo, hi;             // n_boxes x p coordinate indices (lo == 0 means -inf)
+  int n_boxes() const { return p ? (int)lo.size() / p : 0; }
+};
+int build_boxes(const double* Y, int m, int p, const double* ref, BoxTable& out);
+
+// ---- forest (host) ----------------------------------------------------------
+// Packed node: word0 = flags | payload; word1 = threshold bits or Q16 value.
+//   internal: word0 = feature (bits 0..4) | (first child index << 6), children adjacent
+//   leaf    : word0 = 0x20 | (tree-local original index << 6),   word1 = Q16 value
+constexpr uint32_t kLeafFlag = 0x20u;
+struct ForestHost {
+  int n_trees = 0, d = 0;
+  std::vector<uint32_t> nodes;             // 2 words per node
+  std::vector<uint32_t> root;              // packed index of each tree's root (n_trees + 1 entries)
+  std::vector<int> chunk_tree;             // first tree of each LDS chunk (+ end)
+};
+int pack_forest(const int32_t* feature, const float* threshold, const int32_t* left,
+                const int32_t* right, const int32_t* leaf_q16, const int64_t* tree_offset,
+                int n_trees, int d, ForestHost& out);
+
+// ---- device state -----------------------------------------------------------
+struct GPDevice {
+  scoot_dtype dt = SCOOT_F32;
+  int m = 0, d = 0, m_pad = 0, nb = 0, d4 = 1;
+  double s2 = 1, tau2 = 0, c = 0;
+  void* buf = nullptr;        // one allocation holding everything below
+  const void* linv = nullptr; // packed L^-1 (float or double)
+  const void* xs = nullptr;   // m_pad x kXsStride scaled observations (float or double)
+  const double* alpha = nullptr;  // m_pad
+  float scale32[SCOOT_MAX_DIM];
+  double scale64[SCOOT_MAX_DIM];
+  float coef32[3];
+  double coef64[3];
+};
+
+struct ForestDevice {
+  int n_trees = 0, d = 0;
+  uint32_t* nodes = nullptr;
+  uint32_t* root = nullptr;
+  std::vector<int> chunk_tree;
+  std::vector<uint32_t> chunk_first_node;
+};
+
+// Library-owned scratch of the current device, grown on demand.
+void* device_scratch(size_t bytes, int slot);
+// Pinned host staging for small uploads on a stream; the previous upload of
+// the same slot is waited for before the buffer is reused.
+int upload_async(void* dst, const void* src, size_t bytes, int slot, void* stream);
+
+// ---- launchers (device) -----------------------------------------------------
+int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, void* sigma,
+                     const double* ei_c /* nullable: fused EI with c = best + xi */, void* ei,
+                     void* stream);
+int launch_ei(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double c, void* ei,
+              void* stream);
+int launch_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, scoot_dtype dt,
+                const BoxTable& boxes, void* ehvi, void* stream);
+int launch_forest(const ForestDevice& f, const float* Xc, int64_t n, int64_t vote_min,
+                  int32_t* votes, uint8_t* mask, int32_t* leaf_idx, void* stream);
+int launch_fill_u8(uint8_t* p, int64_t n, uint8_t v, void* stream);
+int launch_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q,
+                int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
+
+}  // namespace scoot

@@ -1,0 +1,386 @@
+// GP posterior over a candidate pool (Sec. 4.3, Eq. 4-5), fused:
+//
+//   K*[c, i] = k(x_c, X_i)                     Matern-5/2 ARD, generated on chip
+//   mu[c]    = c0 + sum_i K*[c, i] alpha_i      (Eq. 4)
+//   V        = L^-1 K*^T                         triangular product on matrix cores
+//   sigma[c] = sqrt(max(0, s2 - sum_i V[i, c]^2))   (Eq. 5, latent f)
+//   ei[c]    = G(best + xi)   optional fused EI epilogue (Eq. 8)
+//
+// One workgroup owns a tile of candidates (64 in fp32, 32 in fp64) and runs
+// three phases:
+//   1. generate: every wave computes K* for a share of the observation rows,
+//      for all candidates of the tile, straight into LDS in the B-operand
+//      order of the MFMA instruction; alpha is folded in on the way (mu);
+//   2. multiply: every wave takes whole row blocks I of V (a snake order keeps
+//      the triangular work balanced), accumulates sum_{J<=I} Linv[I,J] K*[J]
+//      on the matrix cores (A from the packed L^-1 in L2, B from LDS), and
+//      keeps only the squared norms of its rows;
+//   3. reduce: partial norms and means of all waves are summed per candidate.
+// K* and V never touch HBM.  L^-1 is shared by every workgroup (L2-resident).
+//
+// Covariance with folded constants: with per-dimension scale
+// w_k = sqrt5 * log2(e) / l_k, u = sqrt(sum_k (w_k (x_k - X_ik))^2) equals
+// sqrt5 r log2(e), and k = (c0 + u (c1 + u c2)) 2^-u with c0 = s2,
+// c1 = s2 ln2, c2 = s2 ln2^2 / 3.  Observations arrive pre-scaled; padding rows
+// sit at coordinate 1e4 so their covariance underflows to exactly 0, and their
+// alpha and L^-1 entries are 0.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "internal.h"
+
+namespace scoot {
+
+typedef float f4_t __attribute__((ext_vector_type(4)));
+typedef float f16_t __attribute__((ext_vector_type(16)));
+typedef double d2_t __attribute__((ext_vector_type(2)));
+typedef double d4_t __attribute__((ext_vector_type(4)));
+
+// E[(c - Y)^+] for Y ~ N(mu, sd^2), in double (epilogue only).
+__device__ inline double partial_expectation_d(double c, double mu, double sd) {
+  if (!(sd > 0)) return fmax(c - mu, 0.0);
+  double u = (c - mu) / sd;
+  return sd * (u * 0.5 * erfc(-u * 0.70710678118654752440) +
+               0.39894228040143267794 * exp(-0.5 * u * u));
+}
+
+// ---------------------------------------------------------------------------
+// fp32
+// ---------------------------------------------------------------------------
+struct Post32 {
+  int64_t n;
+  int d, nb;
+  float scale[SCOOT_MAX_DIM];
+  float c0, c1, c2;
+  double s2, prior, ei_c;
+};
+
+template <int WAVES, int D4>
+__global__ __launch_bounds__(WAVES * 64) void posterior_f32_kernel(
+    const float* __restrict__ Xc, const f4_t* __restrict__ linv, const float* __restrict__ xs,
+    const double* __restrict__ alpha, float* __restrict__ mu_out, float* __restrict__ sd_out,
+    float* __restrict__ ei_out, const Post32 a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  f4_t* ks = reinterpret_cast<f4_t*>(smem);  // [nb][2 ct][4 s4][64 lanes] float4
+  const int nb = a.nb;
+  float* sig_red = reinterpret_cast<float*>(ks + (size_t)nb * 2 * 4 * 64);  // [WAVES][2 h][64]
+  double* mu_red = reinterpret_cast<double*>(sig_red + WAVES * 2 * 64);      // [WAVES][64]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t c0 = (int64_t)blockIdx.x * 64;
+
+  // ---- phase 1: K* for candidate c0 + lane, rows of this wave's groups ----
+  int64_t cg = c0 + lane;
+  if (cg >= a.n) cg = a.n - 1;
+  float xc[4 * D4];
+#pragma unroll
+  for (int k = 0; k < 4 * D4; ++k) xc[k] = (k < a.d) ? Xc[cg * a.d + k] * a.scale[k] : 0.0f;
+
+  // Group G covers rows 32J + 8 s4 + 2t + h, t = 0..3, of block J; lane l
+  // writes them as one float4 to B-operand slot (J, ct = l/32, s4, h*32 + l%32).
+  double mu_part = 0.0;
+  const int ngroups = nb * 8;
+  for (int G = wave; G < ngroups; G += WAVES) {
+    const int J = G >> 3, s4 = (G >> 1) & 3, h = G & 1;
+    const int row0 = 32 * J + 8 * s4 + h;
+    f4_t kv;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int i = row0 + 2 * t;
+      const float* xo = xs + (size_t)i * kXsStride;
+      float acc = 0.0f;
+#pragma unroll
+      for (int k = 0; k < 4 * D4; ++k) {
+        float df = xc[k] - xo[k];
+        acc = fmaf(df, df, acc);
+      }
+      float u = __builtin_amdgcn_sqrtf(acc);
+      float e = __builtin_amdgcn_exp2f(-u);
+      float kval = fmaf(u, fmaf(u, a.c2, a.c1), a.c0) * e;
+      kv[t] = kval;
+      mu_part = fma((double)kval, alpha[i], mu_part);
+    }
+    ks[((J * 2 + (lane >> 5)) * 4 + s4) * 64 + h * 32 + (lane & 31)] = kv;
+  }
+  __syncthreads();
+
+  // ---- phase 2: row blocks of V = L^-1 K*^T on the matrix cores ----------
+  double sq0 = 0.0, sq1 = 0.0;
+  for (int base = 0; base < nb; base += 2 * WAVES) {
+#pragma unroll
+    for (int side = 0; side < 2; ++side) {
+      const int I = base + (side == 0 ? wave : 2 * WAVES - 1 - wave);
+      if (I >= nb) continue;
+      f16_t acc0 = {0}, acc1 = {0};
+      const f4_t* ap = linv + (size_t)I * (I + 1) / 2 * 4 * 64 + lane;
+      const int steps = 4 * (I + 1);  // (J, s4) pairs of this row block
+      f4_t a_cur = ap[0];
+      f4_t a_nxt = steps > 1 ? ap[64] : a_cur;
+      for (int k = 0; k < steps; ++k) {
+        f4_t a_use = a_cur;
+        a_cur = a_nxt;
+        if (k + 2 < steps) a_nxt = ap[(size_t)(k + 2) * 64];
+        const int J = k >> 2, s4 = k & 3;
+        const f4_t b0 = ks[((J * 2 + 0) * 4 + s4) * 64 + lane];
+        const f4_t b1 = ks[((J * 2 + 1) * 4 + s4) * 64 + lane];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a_use[t], b0[t], acc0, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a_use[t], b1[t], acc1, 0, 0, 0);
+        }
+      }
+      float p0 = 0.0f, p1 = 0.0f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        p0 = fmaf(acc0[r], acc0[r], p0);
+        p1 = fmaf(acc1[r], acc1[r], p1);
+      }
+      sq0 += p0;
+      sq1 += p1;
+    }
+  }
+
+  // ---- phase 3: reduce over waves and row halves, write ------------------
+  // Accumulator lane l holds column l % 32 of its tile (ct = 0 / 1).
+  const int h = lane >> 5;
+  sig_red[(wave * 2 + h) * 64 + (lane & 31)] = (float)sq0;
+  sig_red[(wave * 2 + h) * 64 + 32 + (lane & 31)] = (float)sq1;
+  mu_red[wave * 64 + lane] = mu_part;
+  __syncthreads();
+  if (tid < 64) {
+    const int64_t c = c0 + tid;
+    if (c < a.n) {
+      double ss = 0.0, mm = 0.0;
+#pragma unroll
+      for (int w = 0; w < WAVES; ++w) {
+        ss += (double)sig_red[(w * 2 + 0) * 64 + tid] + (double)sig_red[(w * 2 + 1) * 64 + tid];
+        mm += mu_red[w * 64 + tid];
+      }
+      const double sd = sqrt(fmax(a.s2 - ss, 0.0));
+      const double mu = a.prior + mm;
+      mu_out[c] = (float)mu;
+      sd_out[c] = (float)sd;
+      if (ei_out) ei_out[c] = (float)partial_expectation_d(a.ei_c, (double)(float)mu, (double)(float)sd);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp64: v_mfma_f64_16x16x4f64, 16-row blocks, tiles of 32 candidates (two
+// 16-column MFMA tiles).  B operand at step s: lane l holds
+// K*[16J + 4s + l/16][16 ct + l%16]; stored as (J, ct, s/2, lane) double2.
+// ---------------------------------------------------------------------------
+struct Post64 {
+  int64_t n;
+  int d, nb16;
+  double scale[SCOOT_MAX_DIM];
+  double c0, c1, c2;
+  double s2, prior, ei_c;
+};
+
+template <int WAVES, int D4>
+__global__ __launch_bounds__(WAVES * 64) void posterior_f64_kernel(
+    const float* __restrict__ Xc, const d2_t* __restrict__ linv, const double* __restrict__ xs,
+    const double* __restrict__ alpha, double* __restrict__ mu_out, double* __restrict__ sd_out,
+    double* __restrict__ ei_out, const Post64 a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  d2_t* ks = reinterpret_cast<d2_t*>(smem);  // [nb16][2 ct][2 s2][64] double2
+  const int nb = a.nb16;
+  double* sig_red = reinterpret_cast<double*>(ks + (size_t)nb * 2 * 2 * 64);  // [WAVES][4 g][32]
+  double* mu_red = sig_red + WAVES * 4 * 32;                                   // [WAVES][2 h][32]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t c0 = (int64_t)blockIdx.x * 32;
+
+  // ---- phase 1: lane -> candidate c0 + lane % 32, row half h = lane / 32 ----
+  const int cl = lane & 31, h = lane >> 5;
+  int64_t cg = c0 + cl;
+  if (cg >= a.n) cg = a.n - 1;
+  double xc[4 * D4];
+#pragma unroll
+  for (int k = 0; k < 4 * D4; ++k) xc[k] = (k < a.d) ? (double)Xc[cg * a.d + k] * a.scale[k] : 0.0;
+
+  // Group G = (J, s2, kk): rows 16J + 8 s2 + 4t + k, t = 0..1, k = 2 kk + h.
+  double mu_part = 0.0;
+  const int ngroups = nb * 4;
+  const int ct = cl >> 4, ncol = cl & 15;
+  for (int G = wave; G < ngroups; G += WAVES) {
+    const int J = G >> 2, s2 = (G >> 1) & 1, kk = G & 1;
+    const int k = 2 * kk + h;
+    d2_t kv;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int i = 16 * J + 8 * s2 + 4 * t + k;
+      const double* xo = xs + (size_t)i * kXsStride;
+      double acc = 0.0;
+#pragma unroll
+      for (int q = 0; q < 4 * D4; ++q) {
+        double df = xc[q] - xo[q];
+        acc = fma(df, df, acc);
+      }
+      double u = sqrt(acc);
+      double kval = fma(u, fma(u, a.c2, a.c1), a.c0) * exp2(-u);
+      kv[t] = kval;
+      mu_part = fma(kval, alpha[i], mu_part);
+    }
+    ks[((J * 2 + ct) * 2 + s2) * 64 + k * 16 + ncol] = kv;
+  }
+  __syncthreads();
+
+  // ---- phase 2 ------------------------------------------------------------
+  double sq0 = 0.0, sq1 = 0.0;
+  for (int base = 0; base < nb; base += 2 * WAVES) {
+#pragma unroll
+    for (int side = 0; side < 2; ++side) {
+      const int I = base + (side == 0 ? wave : 2 * WAVES - 1 - wave);
+      if (I >= nb) continue;
+      d4_t acc0 = {0}, acc1 = {0};
+      const d2_t* ap = linv + (size_t)I * (I + 1) / 2 * 2 * 64 + lane;
+      const int steps = 2 * (I + 1);
+      for (int k = 0; k < steps; ++k) {
+        const d2_t av = ap[(size_t)k * 64];
+        const int J = k >> 1, s2 = k & 1;
+        const d2_t b0 = ks[((J * 2 + 0) * 2 + s2) * 64 + lane];
+        const d2_t b1 = ks[((J * 2 + 1) * 2 + s2) * 64 + lane];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(av[t], b0[t], acc0, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(av[t], b1[t], acc1, 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        sq0 = fma(acc0[r], acc0[r], sq0);
+        sq1 = fma(acc1[r], acc1[r], sq1);
+      }
+    }
+  }
+
+  // ---- phase 3: accumulator lane l holds column l % 16, rows of group l/16 --
+  const int g = lane >> 4;
+  sig_red[(wave * 4 + g) * 32 + (lane & 15)] = sq0;
+  sig_red[(wave * 4 + g) * 32 + 16 + (lane & 15)] = sq1;
+  mu_red[(wave * 2 + h) * 32 + cl] = mu_part;
+  __syncthreads();
+  if (tid < 32) {
+    const int64_t c = c0 + tid;
+    if (c < a.n) {
+      double ss = 0.0, mm = 0.0;
+#pragma unroll
+      for (int w = 0; w < WAVES; ++w) {
+#pragma unroll
+        for (int gg = 0; gg < 4; ++gg) ss += sig_red[(w * 4 + gg) * 32 + tid];
+        mm += mu_red[(w * 2 + 0) * 32 + tid] + mu_red[(w * 2 + 1) * 32 + tid];
+      }
+      const double sd = sqrt(fmax(a.s2 - ss, 0.0));
+      const double mu = a.prior + mm;
+      mu_out[c] = mu;
+      sd_out[c] = sd;
+      if (ei_out) ei_out[c] = partial_expectation_d(a.ei_c, mu, sd);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+namespace {
+
+template <int WAVES, int D4>
+int run32(const GPDevice& g, const float* Xc, int64_t n, float* mu, float* sd, float* ei,
+          const Post32& a, hipStream_t s) {
+  const size_t lds = (size_t)g.nb * 2 * 4 * 64 * 16 + WAVES * 2 * 64 * 4 + WAVES * 64 * 8;
+  auto kern = posterior_f32_kernel<WAVES, D4>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    attr_set = true;
+  }
+  const int64_t grid = (n + 63) / 64;
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WAVES * 64), lds, s, Xc,
+                     (const f4_t*)g.linv, (const float*)g.xs, g.alpha, mu, sd, ei, a);
+  return SCOOT_OK;
+}
+
+template <int WAVES, int D4>
+int run64(const GPDevice& g, const float* Xc, int64_t n, double* mu, double* sd, double* ei,
+          const Post64& a, hipStream_t s) {
+  const int nb16 = g.m_pad / kBlk64;
+  const size_t lds = (size_t)nb16 * 2 * 2 * 64 * 16 + WAVES * 4 * 32 * 8 + WAVES * 2 * 32 * 8;
+  auto kern = posterior_f64_kernel<WAVES, D4>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    attr_set = true;
+  }
+  const int64_t grid = (n + 31) / 32;
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WAVES * 64), lds, s, Xc,
+                     (const d2_t*)g.linv, (const double*)g.xs, g.alpha, mu, sd, ei, a);
+  return SCOOT_OK;
+}
+
+template <typename F>
+int by_d4(int d4, F&& f) {
+  switch (d4) {
+    case 1: return f(std::integral_constant<int, 1>());
+    case 2: return f(std::integral_constant<int, 2>());
+    case 3: return f(std::integral_constant<int, 3>());
+    default: return f(std::integral_constant<int, 4>());
+  }
+}
+
+}  // namespace
+
+int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, void* sigma,
+                     const double* ei_c, void* ei, void* stream) {
+  if (n == 0) return SCOOT_OK;
+  if (n >= ((int64_t)1 << 37)) return fail(SCOOT_ERR_UNSUPPORTED, "posterior: n too large");
+  hipStream_t s = (hipStream_t)stream;
+  const bool wide = g.nb > 9;  // more than 9 row blocks: 8 waves, one workgroup per CU
+  int rc;
+  if (g.dt == SCOOT_F32) {
+    Post32 a{};
+    a.n = n;
+    a.d = g.d;
+    a.nb = g.nb;
+    for (int k = 0; k < SCOOT_MAX_DIM; ++k) a.scale[k] = g.scale32[k];
+    a.c0 = g.coef32[0];
+    a.c1 = g.coef32[1];
+    a.c2 = g.coef32[2];
+    a.s2 = g.s2;
+    a.prior = g.c;
+    a.ei_c = ei_c ? *ei_c : 0.0;
+    float* e = ei_c ? (float*)ei : nullptr;
+    rc = by_d4(g.d4, [&](auto D4) {
+      return wide ? run32<8, decltype(D4)::value>(g, Xc, n, (float*)mu, (float*)sigma, e, a, s)
+                  : run32<4, decltype(D4)::value>(g, Xc, n, (float*)mu, (float*)sigma, e, a, s);
+    });
+  } else {
+    Post64 a{};
+    a.n = n;
+    a.d = g.d;
+    a.nb16 = g.m_pad / kBlk64;
+    for (int k = 0; k < SCOOT_MAX_DIM; ++k) a.scale[k] = g.scale64[k];
+    a.c0 = g.coef64[0];
+    a.c1 = g.coef64[1];
+    a.c2 = g.coef64[2];
+    a.s2 = g.s2;
+    a.prior = g.c;
+    a.ei_c = ei_c ? *ei_c : 0.0;
+    double* e = ei_c ? (double*)ei : nullptr;
+    rc = by_d4(g.d4, [&](auto D4) {
+      return run64<4, decltype(D4)::value>(g, Xc, n, (double*)mu, (double*)sigma, e, a, s);
+    });
+  }
+  if (rc != SCOOT_OK) return rc;
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("posterior launch: ") + hipGetErrorString(err));
+  return SCOOT_OK;
+}
+
+}  // namespace scoot

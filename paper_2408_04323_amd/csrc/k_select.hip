@@ -1,0 +1,201 @@
+// Masked top-q selection (Sec. 4.6): the q eligible candidates with the
+// largest score, score descending, lowest index first on ties.
+//
+// Every candidate becomes one integer key whose unsigned order is exactly that
+// order: the score's bits mapped to an order-preserving unsigned integer
+// (after -0 -> +0), followed by the bit-inverted index.  Key 0 marks an
+// ineligible candidate (mask 0 or NaN score); no eligible key is 0.  fp32
+// scores fit score and index in one 64-bit key; fp64 scores use a pair.
+//
+// Stage 1: each workgroup walks its share of the array in chunks of 4096 keys
+// (16 per thread) and keeps a running best-q list: q rounds of a block-wide
+// argmax over the chunk plus the list.  Stage 2: one workgroup runs the same
+// selection over all stage-1 lists and writes indices, scores and the count.
+// Selection is exact integer work, so the result does not depend on the
+// grid shape or on the order in which blocks run.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "internal.h"
+
+namespace scoot {
+
+constexpr int kSelThreads = 256;
+constexpr int kSelPer = 16;  // keys per thread per chunk
+constexpr int kSelChunk = kSelThreads * kSelPer;
+constexpr int kSelMaxGrid = 1024;
+
+struct Key64 {
+  uint64_t v;
+  __device__ bool operator>(const Key64& o) const { return v > o.v; }
+  __device__ bool zero() const { return v == 0; }
+};
+struct Key128 {
+  uint64_t hi, lo;
+  __device__ bool operator>(const Key128& o) const { return hi > o.hi || (hi == o.hi && lo > o.lo); }
+  __device__ bool zero() const { return hi == 0 && lo == 0; }
+};
+
+__device__ inline Key64 make_key(float s, int64_t i, bool ok) {
+  if (!ok || s != s) return Key64{0};
+  uint32_t b = __float_as_uint(s + 0.0f);
+  b = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+  return Key64{((uint64_t)b << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i)};
+}
+__device__ inline Key128 make_key(double s, int64_t i, bool ok) {
+  if (!ok || s != s) return Key128{0, 0};
+  uint64_t b = (uint64_t)__double_as_longlong(s + 0.0);
+  b = (b & 0x8000000000000000ull) ? ~b : (b | 0x8000000000000000ull);
+  return Key128{b, ~(uint64_t)i};
+}
+__device__ inline int64_t key_index(const Key64& k) { return (int64_t)(0xFFFFFFFFu - (uint32_t)k.v); }
+__device__ inline int64_t key_index(const Key128& k) { return (int64_t)(~k.lo); }
+
+__device__ inline Key64 shfl_xor(Key64 k, int m) {
+  return Key64{(uint64_t)__shfl_xor((unsigned long long)k.v, m)};
+}
+__device__ inline Key128 shfl_xor(Key128 k, int m) {
+  return Key128{(uint64_t)__shfl_xor((unsigned long long)k.hi, m), (uint64_t)__shfl_xor((unsigned long long)k.lo, m)};
+}
+
+// q rounds of block argmax over the thread's kSelPer keys plus list[] (the
+// running best list in LDS, q entries, zero = empty).  Rewrites list[].
+template <typename K>
+__device__ void select_rounds(K (&keys)[kSelPer], K* list, K* wave_best, int q) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  K extra = tid < q ? list[tid] : K{};
+  __syncthreads();
+  for (int r = 0; r < q; ++r) {
+    K best = extra;
+#pragma unroll
+    for (int j = 0; j < kSelPer; ++j)
+      if (keys[j] > best) best = keys[j];
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+      K o = shfl_xor(best, m);
+      if (o > best) best = o;
+    }
+    if (lane == 0) wave_best[wave] = best;
+    __syncthreads();
+    K win = wave_best[0];
+#pragma unroll
+    for (int w = 1; w < kSelThreads / 64; ++w)
+      if (wave_best[w] > win) win = wave_best[w];
+    if (!win.zero()) {  // remove the winner from its owner (keys are unique)
+      if (!(extra > win) && !(win > extra)) extra = K{};
+#pragma unroll
+      for (int j = 0; j < kSelPer; ++j)
+        if (!(keys[j] > win) && !(win > keys[j])) keys[j] = K{};
+    }
+    if (tid == 0) list[r] = win;
+    __syncthreads();
+  }
+}
+
+template <typename T, typename K>
+__global__ __launch_bounds__(kSelThreads) void topq_stage1(const T* __restrict__ score,
+                                                           const uint8_t* __restrict__ mask, int64_t n,
+                                                           int q, K* __restrict__ part_keys,
+                                                           int32_t* __restrict__ part_count) {
+  __shared__ K list[SCOOT_MAX_Q];
+  __shared__ K wave_best[kSelThreads / 64];
+  __shared__ int32_t cnt[kSelThreads / 64];
+  const int tid = threadIdx.x;
+  if (tid < q) list[tid] = K{};
+  int32_t valid = 0;
+  for (int64_t base = (int64_t)blockIdx.x * kSelChunk; base < n; base += (int64_t)gridDim.x * kSelChunk) {
+    K keys[kSelPer];
+#pragma unroll
+    for (int j = 0; j < kSelPer; ++j) {
+      const int64_t i = base + (int64_t)j * kSelThreads + tid;
+      if (i < n) {
+        const bool ok = mask ? mask[i] != 0 : true;
+        keys[j] = make_key(score[i], i, ok);
+      } else {
+        keys[j] = K{};
+      }
+      valid += keys[j].zero() ? 0 : 1;
+    }
+    select_rounds<K>(keys, list, wave_best, q);
+  }
+  for (int m = 32; m >= 1; m >>= 1) valid += __shfl_xor(valid, m);
+  if ((tid & 63) == 0) cnt[tid >> 6] = valid;
+  __syncthreads();
+  if (tid < q) part_keys[(size_t)blockIdx.x * q + tid] = list[tid];
+  if (tid == 0) {
+    int32_t s = 0;
+    for (int w = 0; w < kSelThreads / 64; ++w) s += cnt[w];
+    part_count[blockIdx.x] = s;
+  }
+}
+
+template <typename T, typename K>
+__global__ __launch_bounds__(kSelThreads) void topq_stage2(const T* __restrict__ score, int n_parts, int q,
+                                                           const K* __restrict__ part_keys,
+                                                           const int32_t* __restrict__ part_count,
+                                                           int64_t* __restrict__ idx, T* __restrict__ score_out,
+                                                           int32_t* __restrict__ n_valid) {
+  __shared__ K list[SCOOT_MAX_Q];
+  __shared__ K wave_best[kSelThreads / 64];
+  const int tid = threadIdx.x;
+  if (tid < q) list[tid] = K{};
+  const int64_t total = (int64_t)n_parts * q;
+  for (int64_t base = 0; base < total; base += kSelChunk) {
+    K keys[kSelPer];
+#pragma unroll
+    for (int j = 0; j < kSelPer; ++j) {
+      const int64_t i = base + (int64_t)j * kSelThreads + tid;
+      keys[j] = i < total ? part_keys[i] : K{};
+    }
+    select_rounds<K>(keys, list, wave_best, q);
+  }
+  if (tid < q) {
+    const K k = list[tid];
+    if (k.zero()) {
+      idx[tid] = -1;
+      if (score_out) score_out[tid] = (T)NAN;
+    } else {
+      const int64_t i = key_index(k);
+      idx[tid] = i;
+      if (score_out) score_out[tid] = score[i];
+    }
+  }
+  if (tid == 0 && n_valid) {
+    int64_t s = 0;
+    for (int b = 0; b < n_parts; ++b) s += part_count[b];
+    *n_valid = (int32_t)s;
+  }
+}
+
+namespace {
+template <typename T, typename K>
+int run_topq(const T* score, const uint8_t* mask, int64_t n, int q, int64_t* idx, T* score_out,
+             int32_t* n_valid, hipStream_t s) {
+  int64_t grid = (n + kSelChunk - 1) / kSelChunk;
+  if (grid < 1) grid = 1;
+  if (grid > kSelMaxGrid) grid = kSelMaxGrid;
+  const size_t kbytes = (size_t)grid * q * sizeof(K);
+  unsigned char* ws = (unsigned char*)device_scratch(kbytes + (size_t)grid * 4, 3);
+  if (!ws) return fail(SCOOT_ERR_NO_MEMORY, "topq: scratch allocation failed");
+  K* pk = reinterpret_cast<K*>(ws);
+  int32_t* pc = reinterpret_cast<int32_t*>(ws + kbytes);
+  hipLaunchKernelGGL((topq_stage1<T, K>), dim3((unsigned)grid), dim3(kSelThreads), 0, s, score, mask, n, q,
+                     pk, pc);
+  hipLaunchKernelGGL((topq_stage2<T, K>), dim3(1), dim3(kSelThreads), 0, s, score, (int)grid, q, pk, pc, idx,
+                     score_out, n_valid);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("topq launch: ") + hipGetErrorString(err));
+  return SCOOT_OK;
+}
+}  // namespace
+
+int launch_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q, int64_t* idx,
+                void* score_out, int32_t* n_valid, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  if (dt == SCOOT_F32)
+    return run_topq<float, Key64>((const float*)score, mask, n, q, idx, (float*)score_out, n_valid, s);
+  return run_topq<double, Key128>((const double*)score, mask, n, q, idx, (double*)score_out, n_valid, s);
+}
+
+}  // namespace scoot

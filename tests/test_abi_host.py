@@ -1,0 +1,132 @@
+"""CPU tests of the C ABI: every declared symbol is exported, and the host-side
+logic (fit arithmetic, front, Delta update, vote threshold, argument checks)
+agrees with the oracle.  No device compute runs here."""
+import ctypes as C
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2408_04323_amd as S
+from paper_2408_04323_amd._native import SIGNATURES, lib
+from oracle.forest import vote_threshold as oracle_vote_threshold
+from oracle.gp import gp_fit as oracle_fit
+from oracle.hypervolume import nondominated
+from oracle.threshold import delta_update as oracle_delta
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "scoot.h")) as fh:
+        text = fh.read()
+    return sorted(set(re.findall(r"^(?:int|const char\*)\s+(scoot_\w+)\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert len(names) >= 17
+    L = lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(SIGNATURES)
+    assert S.abi_version() == 1
+
+
+def test_factor_matches_oracle():
+    rng = np.random.default_rng(1)
+    X = rng.random((40, 7))
+    y = rng.standard_normal(40)
+    ls = rng.uniform(0.2, 1.0, 7)
+    L, alpha = S.gp_factor_host(X, y, ls, 1.3, 1e-3, 0.25)
+    f = oracle_fit(X, y, ls, 1.3, 1e-3, 0.25)
+    np.testing.assert_allclose(L, f["L"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(alpha, f["alpha"], rtol=1e-10, atol=1e-10)
+
+
+def test_fit_errors():
+    X = np.zeros((3, 2))
+    with pytest.raises(S.ScootError) as e:
+        S.gp_factor_host(X, np.zeros(3), [1.0, 1.0], 1.0, 0.0)
+    assert e.value.status == -2
+    with pytest.raises(S.ScootError) as e:
+        S.gp_factor_host(np.random.rand(4, 2), np.zeros(4), [1.0, -1.0], 1.0, 1e-3)
+    assert e.value.status == -1
+    with pytest.raises(S.ScootError) as e:
+        S.gp_factor_host(np.random.rand(4, 17), np.zeros(4), np.ones(17), 1.0, 1e-3)
+    assert e.value.status == -4
+    with pytest.raises(S.ScootError) as e:
+        S.gp_factor_host(np.random.rand(577, 2), np.zeros(577), np.ones(2), 1.0, 1e-3)
+    assert e.value.status == -4
+    y = np.zeros(4)
+    y[1] = np.nan
+    with pytest.raises(S.ScootError) as e:
+        S.gp_factor_host(np.random.rand(4, 2), y, np.ones(2), 1.0, 1e-3)
+    assert e.value.status == -1
+
+
+@pytest.mark.parametrize("p", [1, 2, 3])
+def test_front_matches_oracle(p):
+    rng = np.random.default_rng(10 + p)
+    Y = rng.standard_normal((60, p))
+    if p > 1:
+        Y[:, 1] = -0.8 * Y[:, 0] + 0.3 * Y[:, 1]
+    Y = np.vstack([Y, Y[:5]])  # duplicates
+    ref = Y.max(axis=0) + 0.1
+    front, n_boxes = S.ehvi_front(Y, ref)
+    want = nondominated(Y, ref)
+    np.testing.assert_array_equal(front, want)
+    if p == 1:
+        assert n_boxes == 1
+    if p == 2:
+        assert n_boxes == len(want) + 1
+    if p == 3:
+        assert len(want) + 1 <= n_boxes <= (len(want) + 1) ** 2
+
+
+def test_front_excludes_points_not_below_ref():
+    front, nb = S.ehvi_front(np.array([[1.0, 5.0], [2.0, 2.0], [5.0, 1.0]]), np.array([4.0, 4.0]))
+    assert front.tolist() == [[2.0, 2.0]] and nb == 2
+    front, nb = S.ehvi_front(np.zeros((0, 2)), np.array([1.0, 1.0]))
+    assert len(front) == 0 and nb == 1
+
+
+def test_delta_update_matches_golden(golden_dir):
+    with open(os.path.join(golden_dir, "delta_sequences.json")) as fh:
+        g = json.load(fh)
+    for seq in g["sequences"]:
+        d, c = 0.5, 0
+        od, oc = 0.5, 0
+        for k, bad, want_d, want_c in seq["steps"]:
+            d, c = S.delta_update(d, c, k, bad)
+            od, oc = oracle_delta(od, oc, k, bad)
+            assert d == pytest.approx(want_d, abs=1e-12) and c == want_c
+            assert d == od and c == oc
+
+
+def test_vote_threshold_matches_oracle():
+    for delta in [0.0, 0.25, 0.3, 0.45, 0.5, 0.55, 0.6, 0.75, 1.0]:
+        for T in [1, 3, 16, 64, 128, 1000]:
+            assert S.vote_threshold(delta, T) == oracle_vote_threshold(delta, T)
+    with pytest.raises(S.ScootError):
+        S.vote_threshold(1.5, 4)
+
+
+def test_topq_and_forest_argument_checks():
+    L = lib()
+    idx = C.c_void_p(0)
+    assert L.scoot_suggest_topq(None, None, 10, 0, 0, idx, None, None, None) == -1   # q = 0
+    assert L.scoot_suggest_topq(None, None, 10, 0, 65, idx, None, None, None) == -1  # q > max
+    assert L.scoot_suggest_topq(None, None, -1, 0, 4, idx, None, None, None) == -1
+    # a tree whose child points back at the root is not a tree
+    with pytest.raises(S.ScootError) as e:
+        S.forest_create([0, 0, 0], [0.5, 0, 0], [1, -1, 0], [2, -1, -1], [0, 1, 1], [0, 3], 2)
+    assert e.value.status == -1
+    with pytest.raises(S.ScootError) as e:  # feature out of range
+        S.forest_create([5, 0, 0], [0.5, 0, 0], [1, -1, -1], [2, -1, -1], [0, 1, 1], [0, 3], 2)
+    assert e.value.status == -1
+    with pytest.raises(S.ScootError) as e:  # leaf value above 1.0 in Q16
+        S.forest_create([0, 0, 0], [0.5, 0, 0], [1, -1, -1], [2, -1, -1], [0, 70000, 1], [0, 3], 2)
+    assert e.value.status == -1
