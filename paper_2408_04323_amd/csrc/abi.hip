@@ -188,7 +188,7 @@ int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* l
     g.coef64[2] = signal_var * kLn2 * kLn2 / 3.0;
     for (int i = 0; i < 3; ++i) g.coef32[i] = (float)g.coef64[i];
 
-    // Host image of the device buffer: [L^-1 packed][scaled observations][alpha].
+    // Host image of the device buffer: [L^-1 packed][scaled observations][alpha][alpha as float].
     std::vector<unsigned char> img;
     size_t linv_bytes, xs_bytes;
     const size_t esz = dt == SCOOT_F32 ? 4 : 8;
@@ -204,7 +204,8 @@ int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* l
     linv_bytes = (linv_bytes + 255) / 256 * 256;
     xs_bytes = ((size_t)f.m_pad * kXsStride * esz + 255) / 256 * 256;
     const size_t alpha_bytes = (size_t)f.m_pad * 8;
-    img.assign(linv_bytes + xs_bytes + alpha_bytes, 0);
+    const size_t alpha32_bytes = ((size_t)f.m_pad * 4 + 255) / 256 * 256;
+    img.assign(linv_bytes + xs_bytes + alpha_bytes + alpha32_bytes, 0);
     if (dt == SCOOT_F32) std::memcpy(img.data(), l32.data(), l32.size() * 4);
     else std::memcpy(img.data(), l64.data(), l64.size() * 8);
     for (int i = 0; i < f.m_pad; ++i)
@@ -222,6 +223,10 @@ int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* l
     std::vector<double> apad(f.m_pad, 0.0);
     std::memcpy(apad.data(), f.alpha.data(), sizeof(double) * m);
     std::memcpy(img.data() + linv_bytes + xs_bytes, apad.data(), alpha_bytes);
+    for (int i = 0; i < f.m_pad; ++i) {
+      float av = (float)apad[i];
+      std::memcpy(img.data() + linv_bytes + xs_bytes + alpha_bytes + (size_t)i * 4, &av, 4);
+    }
 
     hipError_t e = hipMalloc(&g.buf, img.size());
     if (e != hipSuccess) return fail(SCOOT_ERR_NO_MEMORY, "gp fit: device allocation failed");
@@ -233,6 +238,7 @@ int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* l
     g.linv = g.buf;
     g.xs = (unsigned char*)g.buf + linv_bytes;
     g.alpha = (const double*)((unsigned char*)g.buf + linv_bytes + xs_bytes);
+    g.alpha32 = (const float*)((unsigned char*)g.buf + linv_bytes + xs_bytes + alpha_bytes);
     scoot_gp h = new scoot_gp_t;
     h->dev = g;
     hipGetDevice(&h->device);

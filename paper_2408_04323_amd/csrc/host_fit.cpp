@@ -119,25 +119,30 @@ int fit_host(const double* X, const double* y, int m, int d, const double* ls, d
   return SCOOT_OK;
 }
 
-// fp32 layout.  Row block I and column block J (32 x 32, J <= I) of L^-1 feed
-// one v_mfma_f32_32x32x2f32 chain as its A operand: at step s (0..15) lane l
+// fp32 layout.  Block (I, J) (32 x 32, J <= I) of L^-1 feeds a
+// v_mfma_f32_32x32x2f32 chain as its A operand: at step s (0..15) lane l
 // holds A[i][k] = Linv[32I + i][32J + 2s + k] with i = l % 32, k = l / 32.
-// Blocks are stored row-block by row-block, (I, 0..I), so the blocks of a row
-// are contiguous; inside a block the 16 steps are grouped in fours so a lane
-// reads its four consecutive steps as one 16-byte load:
-//   float index = ((blk * 4 + s / 4) * 64 + l) * 4 + s % 4,  blk = I(I+1)/2 + J.
+// Inside a block the 16 steps are grouped in fours so a lane reads four
+// consecutive steps as one 16-byte load:
+//   float index = ((blk * 4 + s / 4) * 64 + l) * 4 + s % 4.
+// Blocks are ordered the way the kernel's waves consume them: wave after wave,
+// each wave's row blocks in snake order, J = 0..I within a row block.  Two
+// zero blocks of padding follow, for the kernel's read-ahead.
 void pack_linv_f32(const FitHost& f, std::vector<float>& out) {
-  const int nb = f.nb, m = f.m;
-  out.assign((size_t)nb * (nb + 1) / 2 * 16 * 64, 0.0f);
-  for (int I = 0; I < nb; ++I)
-    for (int J = 0; J <= I; ++J) {
-      size_t blk = (size_t)I * (I + 1) / 2 + J;
-      for (int s = 0; s < 16; ++s)
-        for (int l = 0; l < 64; ++l) {
-          int r = 32 * I + (l % 32), col = 32 * J + 2 * s + l / 32;
-          double v = (r < m && col < m) ? f.Linv[(size_t)r * m + col] : 0.0;
-          out[((blk * 4 + s / 4) * 64 + l) * 4 + s % 4] = (float)v;
-        }
+  const int nb = f.nb, m = f.m, W = posterior_waves(nb);
+  out.assign(((size_t)nb * (nb + 1) / 2 + 2) * 16 * 64, 0.0f);
+  size_t blk = 0;
+  for (int w = 0; w < W; ++w)
+    for (int r = 0;; ++r) {
+      const int I = snake_row(w, r, W);
+      if (I >= nb) break;
+      for (int J = 0; J <= I; ++J, ++blk)
+        for (int s = 0; s < 16; ++s)
+          for (int l = 0; l < 64; ++l) {
+            int row = 32 * I + (l % 32), col = 32 * J + 2 * s + l / 32;
+            double v = (row < m && col < m) ? f.Linv[(size_t)row * m + col] : 0.0;
+            out[((blk * 4 + s / 4) * 64 + l) * 4 + s % 4] = (float)v;
+          }
     }
 }
 
@@ -147,7 +152,7 @@ void pack_linv_f32(const FitHost& f, std::vector<float>& out) {
 //   double index = ((blk * 2 + s / 2) * 64 + l) * 2 + s % 2,  blk = I(I+1)/2 + J.
 void pack_linv_f64(const FitHost& f, std::vector<double>& out) {
   const int nb = f.m_pad / kBlk64, m = f.m;
-  out.assign((size_t)nb * (nb + 1) / 2 * 4 * 64, 0.0);
+  out.assign(((size_t)nb * (nb + 1) / 2 + 2) * 4 * 64, 0.0);
   for (int I = 0; I < nb; ++I)
     for (int J = 0; J <= I; ++J) {
       size_t blk = (size_t)I * (I + 1) / 2 + J;

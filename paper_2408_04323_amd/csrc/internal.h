@@ -17,6 +17,33 @@ constexpr int kBlk64 = 16;
 constexpr int kXsStride = 16;          // floats / doubles per observation row
 constexpr double kPadCoord = 1.0e4;    // scaled coordinate of padding rows: k(x, pad) == 0
 
+#ifdef __HIPCC__
+#define SCOOT_HOST_DEVICE __host__ __device__
+#else
+#define SCOOT_HOST_DEVICE
+#endif
+
+// Waves per workgroup of the fp32 posterior: more than 9 row blocks of K*
+// (72 KiB of LDS per 64-candidate tile) leave room for one workgroup per CU,
+// so it gets 8 waves; otherwise two 4-wave workgroups share a CU.
+inline int posterior_waves(int nb) { return nb > 9 ? 8 : 4; }
+
+// Row blocks of wave w in the snake order that balances the triangular work
+// (row block I costs I + 1 blocks): w, 2W-1-w, 2W+w, 4W-1-w, ...  Increasing in r.
+SCOOT_HOST_DEVICE inline int snake_row(int w, int r, int W) {
+  return (r >> 1) * 2 * W + ((r & 1) ? 2 * W - 1 - w : w);
+}
+// Number of 32 x 32 blocks wave w streams through.
+SCOOT_HOST_DEVICE inline int wave_blocks(int w, int nb, int W) {
+  int total = 0;
+  for (int r = 0;; ++r) {
+    const int I = snake_row(w, r, W);
+    if (I >= nb) break;
+    total += I + 1;
+  }
+  return total;
+}
+
 void set_error(const std::string& msg);
 int fail(int status, const std::string& msg);
 
@@ -73,6 +100,7 @@ struct GPDevice {
   const void* linv = nullptr; // packed L^-1 (float or double)
   const void* xs = nullptr;   // m_pad x kXsStride scaled observations (float or double)
   const double* alpha = nullptr;  // m_pad
+  const float* alpha32 = nullptr; // m_pad, float copy
   float scale32[SCOOT_MAX_DIM];
   double scale64[SCOOT_MAX_DIM];
   float coef32[3];

@@ -174,7 +174,7 @@ int run_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, 
   static bool attr_set[4] = {false, false, false, false};
   auto launch = [&](auto kern) {
     if (!attr_set[p]) {
-      hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+      (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
       attr_set[p] = true;
     }
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kEhviThreads), lds, s, m[0], m[1], m[2], sd[0], sd[1],

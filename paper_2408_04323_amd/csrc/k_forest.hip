@@ -68,13 +68,13 @@ int launch_forest(const ForestDevice& f, const float* Xc, int64_t n, int64_t vot
     if (!votes) return fail(SCOOT_ERR_NO_MEMORY, "forest: vote scratch allocation failed");
   }
   int dev = 0, cus = 256;
-  hipGetDevice(&dev);
-  hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  (void)hipGetDevice(&dev);
+  (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   int64_t groups = (n + kForestThreads - 1) / kForestThreads;
   int64_t grid = groups < (int64_t)cus * 2 ? groups : (int64_t)cus * 2;
   static bool attr_set = false;
   if (!attr_set) {
-    hipFuncSetAttribute((const void*)forest_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    (void)hipFuncSetAttribute((const void*)forest_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     attr_set = true;
   }
   for (int ch = 0; ch < n_chunks; ++ch) {

@@ -27,6 +27,8 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <type_traits>
+#include <utility>
 
 #include "internal.h"
 
@@ -56,16 +58,116 @@ struct Post32 {
   double s2, prior, ei_c;
 };
 
-template <int WAVES, int D4>
-__global__ __launch_bounds__(WAVES * 64) void posterior_f32_kernel(
+// Candidate coordinates times the per-dimension scale (D = the exact number
+// of dimensions, so every load is unconditional and all are in flight at once).
+template <int D>
+__device__ inline void load_scaled_f32(float (&xc)[D], const float* __restrict__ row, const float* scale) {
+  float xf[D];
+#pragma unroll
+  for (int q = 0; q < D; ++q) xf[q] = row[q];
+#pragma unroll
+  for (int q = 0; q < D; ++q) xc[q] = xf[q] * scale[q];
+}
+
+// One 32 x 32 block (row block I, column block J) of L^-1 against the tile's
+// two 32-candidate halves of K*[J]: 16 MFMA steps; steps 0-7 go to the "lo"
+// accumulators and 8-15 to the "hi" ones, so four independent chains are in
+// flight (summed before squaring).
+__device__ inline void mfma_block4(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, const f4_t (&a)[4],
+                                   const f4_t* ks, int J, int lane) {
+#pragma unroll
+  for (int s4 = 0; s4 < 2; ++s4) {
+    const f4_t bl0 = ks[((J * 2 + 0) * 4 + s4) * 64 + lane];
+    const f4_t bl1 = ks[((J * 2 + 1) * 4 + s4) * 64 + lane];
+    const f4_t bh0 = ks[((J * 2 + 0) * 4 + s4 + 2) * 64 + lane];
+    const f4_t bh1 = ks[((J * 2 + 1) * 4 + s4 + 2) * 64 + lane];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      l0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4][t], bl0[t], l0, 0, 0, 0);
+      l1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4][t], bl1[t], l1, 0, 0, 0);
+      h0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4 + 2][t], bh0[t], h0, 0, 0, 0);
+      h1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4 + 2][t], bh1[t], h1, 0, 0, 0);
+    }
+  }
+}
+
+__device__ inline void load_block32(f4_t (&a)[4], const f4_t* ap, int k) {
+#pragma unroll
+  for (int s4 = 0; s4 < 4; ++s4) a[s4] = ap[(size_t)(k * 4 + s4) * 64];
+}
+
+// Completes a row block: squared norms of its V columns into sq0 / sq1.
+__device__ inline void finish_row(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, float& sq0, float& sq1) {
+  float p0 = 0.0f, p1 = 0.0f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const float v0 = l0[r] + h0[r], v1 = l1[r] + h1[r];
+    p0 = fmaf(v0, v0, p0);
+    p1 = fmaf(v1, v1, p1);
+    l0[r] = 0.0f;
+    l1[r] = 0.0f;
+    h0[r] = 0.0f;
+    h1[r] = 0.0f;
+  }
+  sq0 += p0;
+  sq1 += p1;
+}
+
+// The wave's whole stream of blocks with one block of read-ahead in two fixed
+// buffers.  The packed inverse ends with two blocks of padding, so reading
+// ahead past the last block stays in bounds.
+template <int WAVES>
+__device__ inline void wave_stream32(const f4_t* __restrict__ linv, const f4_t* ks, int nb, int wave, int lane,
+                                     float& sq0, float& sq1) {
+  int start = 0;
+  for (int w = 0; w < wave; ++w) start += wave_blocks(w, nb, WAVES);
+  const int count = wave_blocks(wave, nb, WAVES);
+  if (count == 0) return;
+  const f4_t* ap = linv + (size_t)start * 4 * 64 + lane;
+  f16_t l0 = {0}, l1 = {0}, h0 = {0}, h1 = {0};
+  // (r, I, J): row slot, row block, column block of the block being computed
+  int r = 0, I = snake_row(wave, 0, WAVES), J = 0;
+  auto advance = [&]() {
+    if (J == I) {
+      finish_row(l0, l1, h0, h1, sq0, sq1);
+      J = 0;
+      ++r;
+      I = snake_row(wave, r, WAVES);
+    } else {
+      ++J;
+    }
+  };
+  f4_t x[4], y[4];
+  load_block32(x, ap, 0);
+  int k = 0;
+  for (; k + 1 < count; k += 2) {
+    load_block32(y, ap, k + 1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_block4(l0, l1, h0, h1, x, ks, J, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    advance();
+    load_block32(x, ap, k + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_block4(l0, l1, h0, h1, y, ks, J, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    advance();
+  }
+  if (k < count) {
+    mfma_block4(l0, l1, h0, h1, x, ks, J, lane);
+    advance();
+  }
+}
+
+template <int WAVES, int D>
+__global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
     const float* __restrict__ Xc, const f4_t* __restrict__ linv, const float* __restrict__ xs,
-    const double* __restrict__ alpha, float* __restrict__ mu_out, float* __restrict__ sd_out,
+    const float* __restrict__ alpha, float* __restrict__ mu_out, float* __restrict__ sd_out,
     float* __restrict__ ei_out, const Post32 a) {
   extern __shared__ __align__(16) unsigned char smem[];
   f4_t* ks = reinterpret_cast<f4_t*>(smem);  // [nb][2 ct][4 s4][64 lanes] float4
   const int nb = a.nb;
   float* sig_red = reinterpret_cast<float*>(ks + (size_t)nb * 2 * 4 * 64);  // [WAVES][2 h][64]
-  double* mu_red = reinterpret_cast<double*>(sig_red + WAVES * 2 * 64);      // [WAVES][64]
+  float* mu_red = sig_red + WAVES * 2 * 64;                                  // [WAVES][64]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -75,13 +177,12 @@ __global__ __launch_bounds__(WAVES * 64) void posterior_f32_kernel(
   // ---- phase 1: K* for candidate c0 + lane, rows of this wave's groups ----
   int64_t cg = c0 + lane;
   if (cg >= a.n) cg = a.n - 1;
-  float xc[4 * D4];
-#pragma unroll
-  for (int k = 0; k < 4 * D4; ++k) xc[k] = (k < a.d) ? Xc[cg * a.d + k] * a.scale[k] : 0.0f;
+  float xc[D];
+  load_scaled_f32<D>(xc, Xc + cg * D, a.scale);
 
   // Group G covers rows 32J + 8 s4 + 2t + h, t = 0..3, of block J; lane l
   // writes them as one float4 to B-operand slot (J, ct = l/32, s4, h*32 + l%32).
-  double mu_part = 0.0;
+  float mu_part = 0.0f;
   const int ngroups = nb * 8;
   for (int G = wave; G < ngroups; G += WAVES) {
     const int J = G >> 3, s4 = (G >> 1) & 3, h = G & 1;
@@ -93,7 +194,7 @@ __global__ __launch_bounds__(WAVES * 64) void posterior_f32_kernel(
       const float* xo = xs + (size_t)i * kXsStride;
       float acc = 0.0f;
 #pragma unroll
-      for (int k = 0; k < 4 * D4; ++k) {
+      for (int k = 0; k < D; ++k) {
         float df = xc[k] - xo[k];
         acc = fmaf(df, df, acc);
       }
@@ -101,53 +202,21 @@ __global__ __launch_bounds__(WAVES * 64) void posterior_f32_kernel(
       float e = __builtin_amdgcn_exp2f(-u);
       float kval = fmaf(u, fmaf(u, a.c2, a.c1), a.c0) * e;
       kv[t] = kval;
-      mu_part = fma((double)kval, alpha[i], mu_part);
+      mu_part = fmaf(kval, alpha[i], mu_part);
     }
     ks[((J * 2 + (lane >> 5)) * 4 + s4) * 64 + h * 32 + (lane & 31)] = kv;
   }
   __syncthreads();
 
-  // ---- phase 2: row blocks of V = L^-1 K*^T on the matrix cores ----------
-  double sq0 = 0.0, sq1 = 0.0;
-  for (int base = 0; base < nb; base += 2 * WAVES) {
-#pragma unroll
-    for (int side = 0; side < 2; ++side) {
-      const int I = base + (side == 0 ? wave : 2 * WAVES - 1 - wave);
-      if (I >= nb) continue;
-      f16_t acc0 = {0}, acc1 = {0};
-      const f4_t* ap = linv + (size_t)I * (I + 1) / 2 * 4 * 64 + lane;
-      const int steps = 4 * (I + 1);  // (J, s4) pairs of this row block
-      f4_t a_cur = ap[0];
-      f4_t a_nxt = steps > 1 ? ap[64] : a_cur;
-      for (int k = 0; k < steps; ++k) {
-        f4_t a_use = a_cur;
-        a_cur = a_nxt;
-        if (k + 2 < steps) a_nxt = ap[(size_t)(k + 2) * 64];
-        const int J = k >> 2, s4 = k & 3;
-        const f4_t b0 = ks[((J * 2 + 0) * 4 + s4) * 64 + lane];
-        const f4_t b1 = ks[((J * 2 + 1) * 4 + s4) * 64 + lane];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a_use[t], b0[t], acc0, 0, 0, 0);
-          acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a_use[t], b1[t], acc1, 0, 0, 0);
-        }
-      }
-      float p0 = 0.0f, p1 = 0.0f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        p0 = fmaf(acc0[r], acc0[r], p0);
-        p1 = fmaf(acc1[r], acc1[r], p1);
-      }
-      sq0 += p0;
-      sq1 += p1;
-    }
-  }
+  // ---- phase 2: this wave's row blocks of V = L^-1 K*^T on the matrix cores
+  float sq0 = 0.0f, sq1 = 0.0f;
+  wave_stream32<WAVES>(linv, ks, nb, wave, lane, sq0, sq1);
 
   // ---- phase 3: reduce over waves and row halves, write ------------------
   // Accumulator lane l holds column l % 32 of its tile (ct = 0 / 1).
   const int h = lane >> 5;
-  sig_red[(wave * 2 + h) * 64 + (lane & 31)] = (float)sq0;
-  sig_red[(wave * 2 + h) * 64 + 32 + (lane & 31)] = (float)sq1;
+  sig_red[(wave * 2 + h) * 64 + (lane & 31)] = sq0;
+  sig_red[(wave * 2 + h) * 64 + 32 + (lane & 31)] = sq1;
   mu_red[wave * 64 + lane] = mu_part;
   __syncthreads();
   if (tid < 64) {
@@ -157,7 +226,7 @@ __global__ __launch_bounds__(WAVES * 64) void posterior_f32_kernel(
 #pragma unroll
       for (int w = 0; w < WAVES; ++w) {
         ss += (double)sig_red[(w * 2 + 0) * 64 + tid] + (double)sig_red[(w * 2 + 1) * 64 + tid];
-        mm += mu_red[w * 64 + tid];
+        mm += (double)mu_red[w * 64 + tid];
       }
       const double sd = sqrt(fmax(a.s2 - ss, 0.0));
       const double mu = a.prior + mm;
@@ -202,8 +271,13 @@ __global__ __launch_bounds__(WAVES * 64) void posterior_f64_kernel(
   int64_t cg = c0 + cl;
   if (cg >= a.n) cg = a.n - 1;
   double xc[4 * D4];
+  {
+    float xf[4 * D4];
 #pragma unroll
-  for (int k = 0; k < 4 * D4; ++k) xc[k] = (k < a.d) ? (double)Xc[cg * a.d + k] * a.scale[k] : 0.0;
+    for (int k = 0; k < 4 * D4; ++k) xf[k] = Xc[cg * a.d + (k < a.d ? k : a.d - 1)];
+#pragma unroll
+    for (int k = 0; k < 4 * D4; ++k) xc[k] = k < a.d ? (double)xf[k] * a.scale[k] : 0.0;
+  }
 
   // Group G = (J, s2, kk): rows 16J + 8 s2 + 4t + k, t = 0..1, k = 2 kk + h.
   double mu_part = 0.0;
@@ -291,19 +365,19 @@ __global__ __launch_bounds__(WAVES * 64) void posterior_f64_kernel(
 // ---------------------------------------------------------------------------
 namespace {
 
-template <int WAVES, int D4>
+template <int WAVES, int D>
 int run32(const GPDevice& g, const float* Xc, int64_t n, float* mu, float* sd, float* ei,
           const Post32& a, hipStream_t s) {
-  const size_t lds = (size_t)g.nb * 2 * 4 * 64 * 16 + WAVES * 2 * 64 * 4 + WAVES * 64 * 8;
-  auto kern = posterior_f32_kernel<WAVES, D4>;
+  const size_t lds = (size_t)g.nb * 2 * 4 * 64 * 16 + WAVES * 2 * 64 * 4 + WAVES * 64 * 4;
+  auto kern = posterior_f32_kernel<WAVES, D>;
   static bool attr_set = false;
   if (!attr_set) {
-    hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     attr_set = true;
   }
   const int64_t grid = (n + 63) / 64;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WAVES * 64), lds, s, Xc,
-                     (const f4_t*)g.linv, (const float*)g.xs, g.alpha, mu, sd, ei, a);
+                     (const f4_t*)g.linv, (const float*)g.xs, g.alpha32, mu, sd, ei, a);
   return SCOOT_OK;
 }
 
@@ -315,13 +389,23 @@ int run64(const GPDevice& g, const float* Xc, int64_t n, double* mu, double* sd,
   auto kern = posterior_f64_kernel<WAVES, D4>;
   static bool attr_set = false;
   if (!attr_set) {
-    hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     attr_set = true;
   }
   const int64_t grid = (n + 31) / 32;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WAVES * 64), lds, s, Xc,
                      (const d2_t*)g.linv, (const double*)g.xs, g.alpha, mu, sd, ei, a);
   return SCOOT_OK;
+}
+
+template <int D, typename F>
+int by_d_rec(int d, F&& f) {
+  if constexpr (D > SCOOT_MAX_DIM) {
+    return fail(SCOOT_ERR_UNSUPPORTED, "posterior: d exceeds SCOOT_MAX_DIM");
+  } else {
+    if (d == D) return f(std::integral_constant<int, D>());
+    return by_d_rec<D + 1>(d, std::forward<F>(f));
+  }
 }
 
 template <typename F>
@@ -341,7 +425,6 @@ int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, vo
   if (n == 0) return SCOOT_OK;
   if (n >= ((int64_t)1 << 37)) return fail(SCOOT_ERR_UNSUPPORTED, "posterior: n too large");
   hipStream_t s = (hipStream_t)stream;
-  const bool wide = g.nb > 9;  // more than 9 row blocks: 8 waves, one workgroup per CU
   int rc;
   if (g.dt == SCOOT_F32) {
     Post32 a{};
@@ -356,9 +439,9 @@ int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, vo
     a.prior = g.c;
     a.ei_c = ei_c ? *ei_c : 0.0;
     float* e = ei_c ? (float*)ei : nullptr;
-    rc = by_d4(g.d4, [&](auto D4) {
-      return wide ? run32<8, decltype(D4)::value>(g, Xc, n, (float*)mu, (float*)sigma, e, a, s)
-                  : run32<4, decltype(D4)::value>(g, Xc, n, (float*)mu, (float*)sigma, e, a, s);
+    rc = by_d_rec<1>(g.d, [&](auto Dc) {
+      return posterior_waves(g.nb) == 8 ? run32<8, decltype(Dc)::value>(g, Xc, n, (float*)mu, (float*)sigma, e, a, s)
+                                        : run32<4, decltype(Dc)::value>(g, Xc, n, (float*)mu, (float*)sigma, e, a, s);
     });
   } else {
     Post64 a{};
