@@ -5,14 +5,18 @@
 //   G(c) = sd * h(u),  u = (c - mu) / sd,  h(u) = u Phi(u) + phi(u),
 // and G(c) = max(0, c - mu) when sd = 0.  For u well below zero the two terms
 // of h cancel, so there h is taken from the continued fraction of the Mills
-// ratio: with x = -u and F_k = x + k / F_{k+1} (F_{N+1} = x),
-//   Phi(-x) = phi(x) / F_1   and   h(-x) = phi(x) / (F_1 F_2).
+// ratio (Laplace): Phi(-x) = phi(x) / F_1 with F_k = x + k / F_{k+1}, and
+// h(-x) = phi(x) (1 - x Phi(-x) / phi(x)) = phi(x) / (F_1 F_2) = phi(x) / (x F_2 + 1).
 //
 // EI  = G(best + xi).
 // EHVI = sum over boxes B = [l, u] of prod_j (G_j(u_j) - G_j(l_j)), G_j(-inf) = 0,
-// with the boxes and their coordinates built on the host.  Each thread owns a
-// candidate and tabulates G_j at every coordinate of every axis in its own
-// LDS column; the box list is read with wave-uniform (scalar) loads.
+// with the boxes and their coordinates built on the host.
+// * one or two objectives: the boxes are the column strips of the front in
+//   order of the first objective, [a_i, a_{i+1}] x [-inf, h_i]; each thread
+//   streams them, G_1 at consecutive a's carried in a register, no tables;
+// * three objectives: each thread tabulates G_j at every coordinate of every
+//   axis in its own LDS column, then sums over the box list (wave-uniform
+//   loads).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -26,12 +30,14 @@ struct Tail;
 template <>
 struct Tail<float> {
   static constexpr float kSwitch = -4.0f;
-  static constexpr int kTerms = 16;
+  static constexpr float kZero = 13.6f;  // phi(x) underflows beyond (and the convergents would overflow)
+  static constexpr int kTerms = 8;
 };
 template <>
 struct Tail<double> {
   static constexpr double kSwitch = -5.0;
-  static constexpr int kTerms = 40;
+  static constexpr double kZero = 38.6;
+  static constexpr int kTerms = 24;
 };
 
 __device__ inline float erfc_t(float v) { return erfcf(v); }
@@ -39,25 +45,34 @@ __device__ inline double erfc_t(double v) { return erfc(v); }
 __device__ inline float exp_t(float v) { return expf(v); }
 __device__ inline double exp_t(double v) { return exp(v); }
 
+// h(u) = u Phi(u) + phi(u), so that G(c) = sd * h((c - mu) / sd).
+// Tail (u < kSwitch, x = -u): with F_2 = x + 2/(x + 3/(x + 4/(...))),
+// h(-x) = phi(x) / (x F_2 + 1); F_2 = P/Q from the forward recurrence of its
+// convergents, P_k = x P_{k-1} + (k+1) P_{k-2} (same for Q), one division.
+template <typename T>
+__device__ inline T h_normal(T u) {
+  const T inv_sqrt2pi = T(0.39894228040143267794);
+  if (u >= Tail<T>::kSwitch)
+    return u * T(0.5) * erfc_t(u * T(-0.70710678118654752440)) + inv_sqrt2pi * exp_t(T(-0.5) * u * u);
+  const T x = -u;
+  if (x > Tail<T>::kZero) return T(0);
+  T pm = T(1), p0 = x, qm = T(0), q0 = T(1);
+#pragma unroll
+  for (int k = 1; k <= Tail<T>::kTerms; ++k) {
+    const T p1 = x * p0 + T(k + 1) * pm;
+    const T q1 = x * q0 + T(k + 1) * qm;
+    pm = p0;
+    p0 = p1;
+    qm = q0;
+    q0 = q1;
+  }
+  return inv_sqrt2pi * exp_t(T(-0.5) * x * x) * q0 / (x * p0 + q0);
+}
+
 template <typename T>
 __device__ inline T partial_expectation(T c, T mu, T sd) {
   if (!(sd > T(0))) return c - mu > T(0) ? c - mu : T(0);
-  const T u = (c - mu) / sd;
-  const T inv_sqrt2pi = T(0.39894228040143267794);
-  T h;
-  if (u >= Tail<T>::kSwitch) {
-    h = u * T(0.5) * erfc_t(u * T(-0.70710678118654752440)) + inv_sqrt2pi * exp_t(T(-0.5) * u * u);
-  } else {
-    const T x = -u;
-    T F = x, F2 = x;
-#pragma unroll
-    for (int k = Tail<T>::kTerms; k >= 1; --k) {
-      F = x + T(k) / F;
-      if (k == 2) F2 = F;
-    }
-    h = inv_sqrt2pi * exp_t(T(-0.5) * x * x) / (F * F2);
-  }
-  return sd * h;
+  return sd * h_normal<T>((c - mu) / sd);
 }
 
 template <typename T>
@@ -76,6 +91,32 @@ struct EhviArgs {
 };
 
 constexpr int kEhviThreads = 64;
+constexpr int kStripThreads = 256;
+
+// p <= 2: boxes in strip order; coords holds, per box, a_{i+1} (axis 0) and
+// h_i (axis 1, unused when p = 1); a_0 = -inf.
+template <typename T, int P>
+__global__ __launch_bounds__(kStripThreads) void ehvi_strip_kernel(const T* __restrict__ mu0, const T* __restrict__ mu1,
+                                                                   const T* __restrict__ sd0, const T* __restrict__ sd1,
+                                                                   const T* __restrict__ hi, int n_boxes, int64_t n,
+                                                                   T* __restrict__ out) {
+  for (int64_t c = (int64_t)blockIdx.x * kStripThreads + threadIdx.x; c < n; c += (int64_t)gridDim.x * kStripThreads) {
+    const T m0 = mu0[c], s0 = sd0[c];
+    T m1 = T(0), s1 = T(0);
+    if (P == 2) {
+      m1 = mu1[c];
+      s1 = sd1[c];
+    }
+    T g_prev = T(0), acc = T(0);
+    for (int b = 0; b < n_boxes; ++b) {
+      const T g_next = partial_expectation<T>(hi[2 * b], m0, s0);
+      const T w = P == 2 ? partial_expectation<T>(hi[2 * b + 1], m1, s1) : T(1);
+      acc += (g_next - g_prev) * w;
+      g_prev = g_next;
+    }
+    out[c] = acc;
+  }
+}
 
 // boxes: n_boxes records of 2P uint16 (P lower then P upper coordinate indices)
 template <typename T, int P>
@@ -133,6 +174,37 @@ int launch_ei(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, doub
 }
 
 namespace {
+// One or two objectives: per-box upper coordinates (a_{i+1}, h_i) in strip order.
+template <typename T>
+int run_ehvi_strip(const void* const* mu, const void* const* sigma, int p, int64_t n, const BoxTable& bt, void* out,
+                   hipStream_t s) {
+  const int nbx = bt.n_boxes();
+  std::vector<T> hi((size_t)nbx * 2, T(0));
+  for (int b = 0; b < nbx; ++b) {
+    hi[2 * b] = (T)bt.coord[0][bt.hi[(size_t)b * p]];
+    if (p == 2) hi[2 * b + 1] = (T)bt.coord[1][bt.hi[(size_t)b * p + 1]];
+  }
+  void* dev = device_scratch(hi.size() * sizeof(T), 1);
+  if (!dev) return fail(SCOOT_ERR_NO_MEMORY, "ehvi: device scratch allocation failed");
+  int rc = upload_async(dev, hi.data(), hi.size() * sizeof(T), 0, s);
+  if (rc != SCOOT_OK) return rc;
+  int64_t blocks = (n + kStripThreads - 1) / kStripThreads;
+  if (blocks > 8192) blocks = 8192;
+  const T* m0 = (const T*)mu[0];
+  const T* s0 = (const T*)sigma[0];
+  const T* m1 = (const T*)(p == 2 ? mu[1] : mu[0]);
+  const T* s1 = (const T*)(p == 2 ? sigma[1] : sigma[0]);
+  if (p == 2)
+    hipLaunchKernelGGL((ehvi_strip_kernel<T, 2>), dim3((unsigned)blocks), dim3(kStripThreads), 0, s, m0, m1, s0, s1,
+                       (const T*)dev, nbx, n, (T*)out);
+  else
+    hipLaunchKernelGGL((ehvi_strip_kernel<T, 1>), dim3((unsigned)blocks), dim3(kStripThreads), 0, s, m0, m1, s0, s1,
+                       (const T*)dev, nbx, n, (T*)out);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("ehvi launch: ") + hipGetErrorString(err));
+  return SCOOT_OK;
+}
+
 template <typename T>
 int run_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, const BoxTable& bt,
              void* out, hipStream_t s) {
@@ -180,9 +252,7 @@ int run_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, 
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kEhviThreads), lds, s, m[0], m[1], m[2], sd[0], sd[1],
                        sd[2], coords, boxes, (T*)out, a);
   };
-  if (p == 1) launch(ehvi_kernel<T, 1>);
-  else if (p == 2) launch(ehvi_kernel<T, 2>);
-  else launch(ehvi_kernel<T, 3>);
+  launch(ehvi_kernel<T, 3>);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("ehvi launch: ") + hipGetErrorString(err));
   return SCOOT_OK;
@@ -193,6 +263,9 @@ int launch_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t 
                 const BoxTable& bt, void* ehvi, void* stream) {
   if (n == 0) return SCOOT_OK;
   hipStream_t s = (hipStream_t)stream;
+  if (p <= 2)
+    return dt == SCOOT_F32 ? run_ehvi_strip<float>(mu, sigma, p, n, bt, ehvi, s)
+                           : run_ehvi_strip<double>(mu, sigma, p, n, bt, ehvi, s);
   return dt == SCOOT_F32 ? run_ehvi<float>(mu, sigma, p, n, bt, ehvi, s)
                          : run_ehvi<double>(mu, sigma, p, n, bt, ehvi, s);
 }

@@ -5,16 +5,19 @@
 // The packed trees of one chunk (at most 64 KiB, children adjacent) are
 // staged in LDS once per workgroup; each thread owns one candidate, keeps its
 // features in its own LDS column (features are indexed dynamically) and walks
-// every tree of the chunk: left iff x[f] <= threshold, a plain float32 compare
-// (NaN goes right).  Forests larger than one chunk take one launch per chunk,
+// every tree of the chunk, four trees at a time so their dependent LDS reads
+// overlap: left iff x[f] <= threshold, a plain float32 compare (NaN goes right).  Forests larger than one chunk take one launch per chunk,
 // the vote counts carried in the votes array between launches.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 
 #include "internal.h"
 
 namespace scoot {
 
-constexpr int kForestThreads = 256;
+constexpr int kForestThreads = 512;
+constexpr int kWalks = 4;
 
 struct ForestArgs {
   int64_t n;
@@ -40,17 +43,33 @@ __global__ __launch_bounds__(kForestThreads) void forest_kernel(
     if (c >= a.n) continue;
     for (int k = 0; k < a.d; ++k) xs[k * kForestThreads + tid] = Xc[c * a.d + k];
     int32_t v = a.first ? 0 : votes[c];
-    for (int t = a.t_begin; t < a.t_end; ++t) {
-      uint32_t node = root[t] - a.node_base;
-      while (true) {
-        const uint2 rec = tree[node];
-        if (rec.x & kLeafFlag) {
-          v += (int32_t)rec.y;
-          if (leaf_idx) leaf_idx[c * a.n_trees + t] = (int32_t)(rec.x >> 6);
-          break;
+    // Four walks in flight, branch-free: all node reads, then all feature
+    // reads, then the steps; a finished walk stays on its leaf.
+    for (int t0 = a.t_begin; t0 < a.t_end; t0 += kWalks) {
+      uint32_t node[kWalks];
+      bool live[kWalks];
+#pragma unroll
+      for (int q = 0; q < kWalks; ++q) {
+        live[q] = t0 + q < a.t_end;
+        node[q] = live[q] ? root[t0 + q] - a.node_base : root[t0] - a.node_base;
+      }
+      while (live[0] || live[1] || live[2] || live[3]) {
+        uint2 rec[kWalks];
+        float x[kWalks];
+#pragma unroll
+        for (int q = 0; q < kWalks; ++q) rec[q] = tree[node[q]];
+#pragma unroll
+        for (int q = 0; q < kWalks; ++q) x[q] = xs[(rec[q].x & 31u) * kForestThreads + tid];
+#pragma unroll
+        for (int q = 0; q < kWalks; ++q) {
+          const bool leaf = (rec[q].x & kLeafFlag) != 0;
+          if (leaf && live[q]) {
+            v += (int32_t)rec[q].y;
+            if (leaf_idx) leaf_idx[c * a.n_trees + t0 + q] = (int32_t)(rec[q].x >> 6);
+          }
+          live[q] = live[q] && !leaf;
+          node[q] = leaf ? node[q] : (rec[q].x >> 6) + (x[q] <= __uint_as_float(rec[q].y) ? 0u : 1u);
         }
-        const float x = xs[(rec.x & 31u) * kForestThreads + tid];
-        node = (rec.x >> 6) + (x <= __uint_as_float(rec.y) ? 0u : 1u);
       }
     }
     if (votes) votes[c] = v;
@@ -70,8 +89,14 @@ int launch_forest(const ForestDevice& f, const float* Xc, int64_t n, int64_t vot
   int dev = 0, cus = 256;
   (void)hipGetDevice(&dev);
   (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  // As many workgroups as the LDS of a CU holds (each stages the largest chunk).
+  uint32_t max_nodes = 0;
+  for (int ch = 0; ch < n_chunks; ++ch)
+    max_nodes = std::max(max_nodes, f.chunk_first_node[ch + 1] - f.chunk_first_node[ch]);
+  const size_t lds_max = (size_t)max_nodes * 8 + (size_t)f.d * kForestThreads * 4;
+  const int per_cu = std::max(1, std::min(4, (int)((160 * 1024) / lds_max)));
   int64_t groups = (n + kForestThreads - 1) / kForestThreads;
-  int64_t grid = groups < (int64_t)cus * 2 ? groups : (int64_t)cus * 2;
+  int64_t grid = std::min(groups, (int64_t)cus * per_cu);
   static bool attr_set = false;
   if (!attr_set) {
     (void)hipFuncSetAttribute((const void*)forest_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
