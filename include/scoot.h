@@ -209,6 +209,30 @@ int scoot_score_pool(const scoot_gp* gps, int p, scoot_forest f, const float* Xc
                      double delta, int q, void* mu, void* sigma, void* acq, int32_t* votes,
                      uint8_t* mask, int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Sequential Kriging-believer suggestion of q candidates, an extension of the
+ * parallel suggestion of Sec. 4.6 (the paper takes the top k at once).  Each
+ * pick maximises EHVI (Eq. 9, p = 1..3) over the feasible (Eq. 3 with delta;
+ * f nullable: all feasible), not yet picked candidates; the pick then joins
+ * the observations with its posterior mean as a fantasy value and noise
+ * tau^2: the Cholesky factor is extended by one row, V = L^-1 K*^T gains the
+ * row (k(x, x_p) - v_p^T V[:, x]) / d, sigma^2 drops by its square, the mean
+ * stays, and the front gains the fantasy.  Ties go to the lowest index.
+ *
+ * gps: p fp32 handles (fp64: UNSUPPORTED) sharing d.  Xc [n*d] device.
+ * Y_obs [m_obs*p], ref [p]: host.  workspace: device, at least the size
+ * scoot_suggest_kb_workspace returns (it holds V of every objective: about
+ * 4 (m + q) n p bytes); NULL: the library allocates and frees it in the call.
+ * picks [q], pick_acq [q] (nullable), n_picked: HOST outputs — the call
+ * synchronises `stream` after every pick.  Fewer than q feasible candidates:
+ * *n_picked < q and the tail of picks is untouched.
+ * Errors: INVALID_ARG, UNSUPPORTED, NO_MEMORY, DEVICE.
+ * ------------------------------------------------------------------------- */
+int scoot_suggest_kb_workspace(const scoot_gp* gps, int p, int64_t n, int q, uint64_t* bytes);
+int scoot_suggest_kb(const scoot_gp* gps, int p, scoot_forest f, const float* Xc, int64_t n,
+                     const double* Y_obs, int m_obs, const double* ref, double delta, int q, void* workspace,
+                     uint64_t workspace_bytes, int64_t* picks, double* pick_acq, int* n_picked, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

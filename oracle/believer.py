@@ -16,10 +16,14 @@ from .hypervolume import ehvi, nondominated
 from .select import top_q
 
 
-def kriging_believer(X, Y, hypers, Xc, mask, ref, q):
+def kriging_believer(X, Y, hypers, Xc, mask, ref, q, follow=None, record=None):
     """hypers: list over objectives of dicts with lengthscale, signal_var,
     noise_var, prior_mean.  Returns (picks (q,), per-pick EHVI (q,),
-    final mu (n, p), final sigma (n, p))."""
+    final mu (n, p), final sigma (n, p)).
+
+    ``follow``: a pick sequence to take instead of the arg max at each step
+    (to check another implementation's greedy sequence step by step);
+    ``record``: a list that receives (acq, eligible) of every step."""
     X = np.asarray(X, dtype=np.float64)
     Y = np.asarray(Y, dtype=np.float64)
     Xc64 = np.asarray(Xc, dtype=np.float64)
@@ -35,10 +39,18 @@ def kriging_believer(X, Y, hypers, Xc, mask, ref, q):
             mu[:, j], sd[:, j] = gp_posterior(fit, Xc64)
         front = nondominated(Ya, ref)
         acq = ehvi(mu, sd, front, ref)
-        idx, val, _ = top_q(acq, eligible, 1)
-        if idx[0] < 0:
-            break
-        i = int(idx[0])
+        if record is not None:
+            record.append((acq.copy(), eligible.copy()))
+        if follow is not None:
+            if len(picks) >= len(follow):
+                break
+            i = int(follow[len(picks)])
+            val = [acq[i]]
+        else:
+            idx, val, _ = top_q(acq, eligible, 1)
+            if idx[0] < 0:
+                break
+            i = int(idx[0])
         picks.append(i)
         vals.append(float(val[0]))
         eligible[i] = False

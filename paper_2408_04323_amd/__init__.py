@@ -288,3 +288,32 @@ def score_pool(gps, forest, Xc, q, best_y=0.0, xi=1e-4, Y_obs=None, ref=None, de
                                  _dptr(b.votes), _dptr(b.mask), _dptr(b.idx), _dptr(b.score), _dptr(b.n_valid),
                                  _stream(stream)), "score_pool")
     return b
+
+
+# ------------------------------------------------------------- believer picks
+def suggest_kb_workspace(gps, n, q):
+    hs = (C.c_void_p * len(gps))(*[g.handle.value for g in gps])
+    b = C.c_uint64(0)
+    check(lib().scoot_suggest_kb_workspace(hs, len(gps), n, q, C.byref(b)), "suggest_kb_workspace")
+    return b.value
+
+
+def suggest_kb(gps, forest, Xc, q, Y_obs, ref, delta=0.5, workspace=None, stream=None):
+    """Sequential Kriging-believer picks.  Returns (picks int64 (k,), EHVI at each pick (k,))."""
+    import torch
+    p = len(gps)
+    n = Xc.shape[0]
+    _require_device(Xc, "Xc", torch.float32, n * gps[0].d)
+    hs = (C.c_void_p * p)(*[g.handle.value for g in gps])
+    r, pr = _host(ref, np.float64)
+    Y, pY = _host(np.asarray(Y_obs, dtype=np.float64).reshape(-1, p), np.float64)
+    picks = np.full(q, -1, dtype=np.int64)
+    acq = np.full(q, np.nan)
+    k = C.c_int(0)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    check(lib().scoot_suggest_kb(hs, p, forest.handle if forest is not None else None, _dptr(Xc), n, pY, Y.shape[0],
+                                 pr, delta, q, _dptr(workspace), ws_bytes,
+                                 picks.ctypes.data_as(C.POINTER(C.c_int64)),
+                                 acq.ctypes.data_as(C.POINTER(C.c_double)), C.byref(k), _stream(stream)),
+          "suggest_kb")
+    return picks[:k.value], acq[:k.value]

@@ -34,6 +34,9 @@ SIGNATURES = {
     "scoot_delta_update": [P_dbl, P_int, c_int, c_int],
     "scoot_score_pool": [C.POINTER(c_vp), c_int, c_vp, c_vp, c_i64, c_dbl, c_dbl, P_dbl, c_int, P_dbl,
                          c_dbl, c_int, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp],
+    "scoot_suggest_kb_workspace": [C.POINTER(c_vp), c_int, c_i64, c_int, C.POINTER(C.c_uint64)],
+    "scoot_suggest_kb": [C.POINTER(c_vp), c_int, c_vp, c_vp, c_i64, P_dbl, c_int, P_dbl, c_dbl, c_int, c_vp,
+                         C.c_uint64, P_i64, P_dbl, P_int, c_vp],
 }
 RESTYPES = {"scoot_status_string": C.c_char_p, "scoot_last_error": C.c_char_p}
 

@@ -463,4 +463,64 @@ int scoot_score_pool(const scoot_gp* gps, int p, scoot_forest f, const float* Xc
   return launch_topq(acq, mask, n, dt, q, idx, score_out, n_valid, stream);
 }
 
+namespace {
+int kb_check(const scoot_gp* gps, int p, int64_t n, int q, const GPDevice** g) {
+  if (!gps || p < 1 || p > SCOOT_MAX_OBJECTIVES) return fail(SCOOT_ERR_INVALID_ARG, "believer: bad p or gps");
+  if (n < 1 || q < 1 || q > SCOOT_MAX_Q) return fail(SCOOT_ERR_INVALID_ARG, "believer: bad n or q");
+  for (int j = 0; j < p; ++j) {
+    if (!gps[j]) return fail(SCOOT_ERR_INVALID_ARG, "believer: null GP");
+    if (gps[j]->dev.dt != SCOOT_F32) return fail(SCOOT_ERR_UNSUPPORTED, "believer: float32 GPs only");
+    if (gps[j]->dev.d != gps[0]->dev.d) return fail(SCOOT_ERR_INVALID_ARG, "believer: GPs must share d");
+    g[j] = &gps[j]->dev;
+  }
+  return SCOOT_OK;
+}
+}  // namespace
+
+int scoot_suggest_kb_workspace(const scoot_gp* gps, int p, int64_t n, int q, uint64_t* bytes) {
+  g_last_error.clear();
+  const GPDevice* g[SCOOT_MAX_OBJECTIVES];
+  if (!bytes) return fail(SCOOT_ERR_INVALID_ARG, "believer: null bytes");
+  int rc = kb_check(gps, p, n, q, g);
+  if (rc != SCOOT_OK) return rc;
+  *bytes = kb_workspace_bytes(g, p, n, q);
+  return SCOOT_OK;
+}
+
+int scoot_suggest_kb(const scoot_gp* gps, int p, scoot_forest f, const float* Xc, int64_t n, const double* Y_obs,
+                     int m_obs, const double* ref, double delta, int q, void* workspace, uint64_t workspace_bytes,
+                     int64_t* picks, double* pick_acq, int* n_picked, void* stream) {
+  g_last_error.clear();
+  const GPDevice* g[SCOOT_MAX_OBJECTIVES];
+  int rc = kb_check(gps, p, n, q, g);
+  if (rc != SCOOT_OK) return rc;
+  if (!Xc || !picks || !n_picked || !ref || (m_obs > 0 && !Y_obs) || m_obs < 0)
+    return fail(SCOOT_ERR_INVALID_ARG, "believer: null pointer");
+  int64_t vmin = 0;
+  if (f) {
+    rc = scoot_vote_threshold(delta, f->dev.n_trees, &vmin);
+    if (rc != SCOOT_OK) return rc;
+  }
+  const size_t need = kb_workspace_bytes(g, p, n, q);
+  void* ws = workspace;
+  bool own = false;
+  if (!ws) {
+    if (hipMalloc(&ws, need) != hipSuccess) return fail(SCOOT_ERR_NO_MEMORY, "believer: workspace allocation failed");
+    own = true;
+  } else if (workspace_bytes < need) {
+    return fail(SCOOT_ERR_INVALID_ARG, "believer: workspace too small");
+  }
+  try {
+    rc = run_kriging_believer(g, p, f ? &f->dev : nullptr, vmin, Xc, n, Y_obs, m_obs, ref, q, ws, picks, pick_acq,
+                              n_picked, stream);
+  } catch (const std::bad_alloc&) {
+    rc = fail(SCOOT_ERR_NO_MEMORY, "believer: host allocation failed");
+  }
+  if (own) {
+    (void)hipStreamSynchronize((hipStream_t)stream);
+    (void)hipFree(ws);
+  }
+  return rc;
+}
+
 }  // extern "C"

@@ -122,9 +122,10 @@ void* device_scratch(size_t bytes, int slot);
 int upload_async(void* dst, const void* src, size_t bytes, int slot, void* stream);
 
 // ---- launchers (device) -----------------------------------------------------
+// v_out (nullable, fp32 handles only): V = L^-1 K*^T, m_pad rows of n floats.
 int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, void* sigma,
                      const double* ei_c /* nullable: fused EI with c = best + xi */, void* ei,
-                     void* stream);
+                     void* stream, float* v_out = nullptr);
 int launch_ei(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double c, void* ei,
               void* stream);
 int launch_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, scoot_dtype dt,
@@ -134,5 +135,11 @@ int launch_forest(const ForestDevice& f, const float* Xc, int64_t n, int64_t vot
 int launch_fill_u8(uint8_t* p, int64_t n, uint8_t v, void* stream);
 int launch_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q,
                 int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
+
+// Sequential Kriging-believer picks (fp32 GPs only).
+size_t kb_workspace_bytes(const GPDevice* const* g, int p, int64_t n, int q);
+int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f, int64_t vote_min, const float* Xc,
+                         int64_t n, const double* Y_obs, int m_obs, const double* ref, int q, void* ws,
+                         int64_t* picks, double* pick_acq, int* n_picked, void* stream);
 
 }  // namespace scoot

@@ -96,12 +96,30 @@ __device__ inline void load_block32(f4_t (&a)[4], const f4_t* ap, int k) {
   for (int s4 = 0; s4 < 4; ++s4) a[s4] = ap[(size_t)(k * 4 + s4) * 64];
 }
 
-// Completes a row block: squared norms of its V columns into sq0 / sq1.
-__device__ inline void finish_row(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, float& sq0, float& sq1) {
+// Where V goes when it is kept (the sequential believer needs it): row-major,
+// rows = observations in their order, row stride ld = number of candidates.
+struct VStore {
+  float* v;
+  int64_t ld;
+  int64_t c0;  // first candidate of the tile
+  int64_t n;
+};
+
+// Completes a row block: squared norms of its V columns into sq0 / sq1, and
+// the block itself into V when kept.  Accumulator register r of lane l holds
+// row 8 (r / 4) + 4 (l / 32) + r % 4 of the block, column l % 32.
+__device__ inline void finish_row(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, float& sq0, float& sq1,
+                                  const VStore& vs, int I, int lane) {
   float p0 = 0.0f, p1 = 0.0f;
+  const int64_t c_a = vs.c0 + (lane & 31), c_b = c_a + 32;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const float v0 = l0[r] + h0[r], v1 = l1[r] + h1[r];
+    if (vs.v) {
+      const int64_t row = 32 * I + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      if (c_a < vs.n) vs.v[row * vs.ld + c_a] = v0;
+      if (c_b < vs.n) vs.v[row * vs.ld + c_b] = v1;
+    }
     p0 = fmaf(v0, v0, p0);
     p1 = fmaf(v1, v1, p1);
     l0[r] = 0.0f;
@@ -118,7 +136,7 @@ __device__ inline void finish_row(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, fl
 // ahead past the last block stays in bounds.
 template <int WAVES>
 __device__ inline void wave_stream32(const f4_t* __restrict__ linv, const f4_t* ks, int nb, int wave, int lane,
-                                     float& sq0, float& sq1) {
+                                     float& sq0, float& sq1, const VStore& vs) {
   int start = 0;
   for (int w = 0; w < wave; ++w) start += wave_blocks(w, nb, WAVES);
   const int count = wave_blocks(wave, nb, WAVES);
@@ -129,7 +147,7 @@ __device__ inline void wave_stream32(const f4_t* __restrict__ linv, const f4_t* 
   int r = 0, I = snake_row(wave, 0, WAVES), J = 0;
   auto advance = [&]() {
     if (J == I) {
-      finish_row(l0, l1, h0, h1, sq0, sq1);
+      finish_row(l0, l1, h0, h1, sq0, sq1, vs, I, lane);
       J = 0;
       ++r;
       I = snake_row(wave, r, WAVES);
@@ -162,7 +180,7 @@ template <int WAVES, int D>
 __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
     const float* __restrict__ Xc, const f4_t* __restrict__ linv, const float* __restrict__ xs,
     const float* __restrict__ alpha, float* __restrict__ mu_out, float* __restrict__ sd_out,
-    float* __restrict__ ei_out, const Post32 a) {
+    float* __restrict__ ei_out, float* __restrict__ v_out, const Post32 a) {
   extern __shared__ __align__(16) unsigned char smem[];
   f4_t* ks = reinterpret_cast<f4_t*>(smem);  // [nb][2 ct][4 s4][64 lanes] float4
   const int nb = a.nb;
@@ -210,7 +228,8 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
 
   // ---- phase 2: this wave's row blocks of V = L^-1 K*^T on the matrix cores
   float sq0 = 0.0f, sq1 = 0.0f;
-  wave_stream32<WAVES>(linv, ks, nb, wave, lane, sq0, sq1);
+  const VStore vs{v_out, a.n, c0, a.n};
+  wave_stream32<WAVES>(linv, ks, nb, wave, lane, sq0, sq1, vs);
 
   // ---- phase 3: reduce over waves and row halves, write ------------------
   // Accumulator lane l holds column l % 32 of its tile (ct = 0 / 1).
@@ -366,7 +385,7 @@ __global__ __launch_bounds__(WAVES * 64) void posterior_f64_kernel(
 namespace {
 
 template <int WAVES, int D>
-int run32(const GPDevice& g, const float* Xc, int64_t n, float* mu, float* sd, float* ei,
+int run32(const GPDevice& g, const float* Xc, int64_t n, float* mu, float* sd, float* ei, float* v_out,
           const Post32& a, hipStream_t s) {
   const size_t lds = (size_t)g.nb * 2 * 4 * 64 * 16 + WAVES * 2 * 64 * 4 + WAVES * 64 * 4;
   auto kern = posterior_f32_kernel<WAVES, D>;
@@ -377,7 +396,7 @@ int run32(const GPDevice& g, const float* Xc, int64_t n, float* mu, float* sd, f
   }
   const int64_t grid = (n + 63) / 64;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WAVES * 64), lds, s, Xc,
-                     (const f4_t*)g.linv, (const float*)g.xs, g.alpha32, mu, sd, ei, a);
+                     (const f4_t*)g.linv, (const float*)g.xs, g.alpha32, mu, sd, ei, v_out, a);
   return SCOOT_OK;
 }
 
@@ -421,7 +440,7 @@ int by_d4(int d4, F&& f) {
 }  // namespace
 
 int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, void* sigma,
-                     const double* ei_c, void* ei, void* stream) {
+                     const double* ei_c, void* ei, void* stream, float* v_out) {
   if (n == 0) return SCOOT_OK;
   if (n >= ((int64_t)1 << 37)) return fail(SCOOT_ERR_UNSUPPORTED, "posterior: n too large");
   hipStream_t s = (hipStream_t)stream;
@@ -440,8 +459,9 @@ int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, vo
     a.ei_c = ei_c ? *ei_c : 0.0;
     float* e = ei_c ? (float*)ei : nullptr;
     rc = by_d_rec<1>(g.d, [&](auto Dc) {
-      return posterior_waves(g.nb) == 8 ? run32<8, decltype(Dc)::value>(g, Xc, n, (float*)mu, (float*)sigma, e, a, s)
-                                        : run32<4, decltype(Dc)::value>(g, Xc, n, (float*)mu, (float*)sigma, e, a, s);
+      return posterior_waves(g.nb) == 8
+                 ? run32<8, decltype(Dc)::value>(g, Xc, n, (float*)mu, (float*)sigma, e, v_out, a, s)
+                 : run32<4, decltype(Dc)::value>(g, Xc, n, (float*)mu, (float*)sigma, e, v_out, a, s);
     });
   } else {
     Post64 a{};

@@ -384,3 +384,57 @@ def test_repeat_runs_bit_identical():
     for o in outs[1:]:
         for a, c in zip(outs[0], o):
             np.testing.assert_array_equal(a, c)
+
+
+# --------------------------------------------------------------------------- believer
+def _check_believer(w, n, q, picks, acq_g, mask):
+    hyp = [dict(lengthscale=w["lengthscale"][j], signal_var=w["signal_var"][j], noise_var=w["noise_var"][j],
+                prior_mean=w["prior_mean"][j]) for j in range(w["p"])]
+    from oracle.believer import kriging_believer
+    steps = []
+    kriging_believer(w["X"], w["Y"], hyp, w["Xc"], mask, w["ref"], q, follow=picks, record=steps)
+    assert len(steps) == len(picks)
+    for j, (acq_o, elig) in enumerate(steps):
+        scale = np.max(acq_o[elig != 0])
+        tol = 1e-3 * scale
+        i = int(picks[j])
+        assert elig[i], f"step {j}: pick {i} not eligible"
+        best = np.max(acq_o[elig != 0])
+        assert acq_o[i] >= best - 2 * tol, f"step {j}: pick {i} has EHVI {acq_o[i]} below the best {best}"
+        assert abs(acq_g[j] - acq_o[i]) <= tol + 1e-3 * abs(acq_o[i]), f"step {j}: EHVI {acq_g[j]} vs {acq_o[i]}"
+        order = np.lexsort((np.arange(n), -np.where(elig != 0, acq_o, -np.inf)))
+        if acq_o[order[0]] - acq_o[order[1]] > 2 * tol:
+            assert i == order[0], f"step {j}: decided pick {order[0]} but got {i}"
+
+
+@pytest.mark.parametrize("n,m,q", [(2048 + 7, 40, 8), (16384, 200, 6)])
+def test_believer_sequence(n, m, q):
+    w = wl(5, n, m)
+    gps = [S.gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][j], w["signal_var"][j], w["noise_var"][j],
+                    w["prior_mean"][j]) for j in range(2)]
+    f = _forest(w["forest"], w["d"])
+    say("believer", n, m, q)
+    picks, acq_g = S.suggest_kb(gps, f, dev(w["Xc"]), q, w["Y"], w["ref"], delta=w["delta"])
+    torch.cuda.synchronize()
+    assert len(picks) == q and len(set(picks.tolist())) == q
+    mask = feasibility_mask(forest_votes(w["forest"], w["Xc"]), w["delta"], len(w["forest"]["tree_offset"]) - 1)
+    _check_believer(w, n, q, picks, acq_g, mask)
+
+
+def test_believer_shortfall_and_workspace():
+    w = wl(5, 300, 40)
+    gps = [S.gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][j], 1.0, w["noise_var"][j]) for j in range(2)]
+    Xc = dev(w["Xc"])
+    nbytes = S.suggest_kb_workspace(gps, 300, 4)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+    say("believer workspace", nbytes)
+    p1, a1 = S.suggest_kb(gps, None, Xc, 4, w["Y"], w["ref"], workspace=ws)
+    p2, a2 = S.suggest_kb(gps, None, Xc, 4, w["Y"], w["ref"])
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(p1, p2)
+    np.testing.assert_array_equal(a1, a2)
+    # every candidate infeasible: no pick
+    f = _forest(w["forest"], w["d"])
+    p3, _ = S.suggest_kb(gps, f, Xc, 4, w["Y"], w["ref"], delta=1.0)
+    mask = feasibility_mask(forest_votes(w["forest"], w["Xc"]), 1.0, len(w["forest"]["tree_offset"]) - 1)
+    assert len(p3) == min(4, int(mask.sum()))
