@@ -20,7 +20,7 @@ ARCH = "gfx950"
 HIP_FLAGS = ["-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-I", os.path.join(ROOT, "include"), "-I", CSRC]
-CXX_FLAGS = ["-O3", "-fPIC", "-std=c++17", "-I", os.path.join(ROOT, "include"), "-I", CSRC]
+CXX_FLAGS = ["-O3", "-fPIC", "-std=c++17", "-fopenmp-simd", "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 
 
 def _hipcc():

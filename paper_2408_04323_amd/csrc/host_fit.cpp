@@ -76,8 +76,10 @@ int fit_host(const double* X, const double* y, int m, int d, const double* ls, d
     const double* Li = L + (size_t)i * m;
     for (int j = 0; j <= i; ++j) {
       const double* Lj = L + (size_t)j * m;
-      double s = K[(size_t)i * m + j];
-      for (int k = 0; k < j; ++k) s -= Li[k] * Lj[k];
+      double dot = 0.0;
+#pragma omp simd reduction(+ : dot)
+      for (int k = 0; k < j; ++k) dot += Li[k] * Lj[k];
+      double s = K[(size_t)i * m + j] - dot;
       if (i == j) {
         double kii = K[(size_t)i * m + i];
         if (!(s > 1e-13 * kii)) return fail(SCOOT_ERR_NOT_PD, "gp fit: K + tau^2 I is not positive definite");
@@ -91,8 +93,10 @@ int fit_host(const double* X, const double* y, int m, int d, const double* ls, d
   // alpha = L^-T L^-1 (y - c).
   std::vector<double> z(m);
   for (int i = 0; i < m; ++i) {
-    double s = y[i] - c;
-    for (int k = 0; k < i; ++k) s -= L[(size_t)i * m + k] * z[k];
+    double dot = 0.0;
+#pragma omp simd reduction(+ : dot)
+    for (int k = 0; k < i; ++k) dot += L[(size_t)i * m + k] * z[k];
+    double s = y[i] - c - dot;
     z[i] = s / L[(size_t)i * m + i];
   }
   f.alpha.assign(m, 0.0);
@@ -111,6 +115,7 @@ int fit_host(const double* X, const double* y, int m, int d, const double* ls, d
     for (int i = j + 1; i < m; ++i) {
       const double* Li = L + (size_t)i * m;
       double s = 0;
+#pragma omp simd reduction(+ : s)
       for (int k = j; k < i; ++k) s += Li[k] * w[k];
       w[i] = -s / Li[i];
       f.Linv[(size_t)i * m + j] = w[i];
