@@ -50,9 +50,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-loops", type=int, default=20)
-    ap.add_argument("--only", choices=["all", "posterior", "copy"], default="all",
-                    help="posterior: only the posterior kernel loop (for profiler counters); "
-                         "copy: a plain 1 GiB device copy (counter calibration)")
+    ap.add_argument("--only", choices=["all", "posterior", "forest", "ehvi", "topq", "copy"], default="all",
+                    help="posterior / forest / ehvi / topq: only that kernel's loop (for profiler "
+                         "counters); copy: a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
 
 
@@ -129,6 +129,15 @@ def main():
     if args.only == "posterior":
         ms = time_loop(post, args.kernel_loops)
         print(json.dumps({"posterior_ms": ms}))
+        return
+    if args.only in ("forest", "ehvi", "topq"):
+        step()
+        fn = {"forest": lambda: S.rf_feasibility(forest, Xc, w["delta"], votes=bufs.votes, mask=bufs.mask),
+              "ehvi": lambda: S.acq_ehvi([bufs.mu[j] for j in range(p)], [bufs.sigma[j] for j in range(p)],
+                                         w["Y"], w["ref"], out=bufs.acq),
+              "topq": lambda: S.suggest_topq(bufs.acq, bufs.mask, w["q"])}[args.only]
+        fn()
+        print(json.dumps({args.only + "_ms": time_loop(fn, args.kernel_loops)}))
         return
     post_ms = time_loop(post, args.kernel_loops)
 

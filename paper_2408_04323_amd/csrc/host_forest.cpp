@@ -1,8 +1,9 @@
 // Host side of the random-forest feasibility mask (Sec. 4.7, Eq. 3): checks
 // the flat tree arrays and repacks every tree breadth-first so that the two
 // children of a node are adjacent (one child index per node), 8 bytes per
-// node, and groups consecutive trees into chunks that fit the on-chip memory
-// of one workgroup.
+// node (encoding in internal.h), and groups consecutive trees into chunks
+// that fit the on-chip memory of one workgroup.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <deque>
@@ -10,10 +11,6 @@
 #include "internal.h"
 
 namespace scoot {
-
-namespace {
-constexpr int kChunkNodes = 8192;  // 64 KiB of packed nodes per chunk
-}
 
 int pack_forest(const int32_t* feature, const float* threshold, const int32_t* left,
                 const int32_t* right, const int32_t* leaf_q16, const int64_t* tree_offset,
@@ -27,19 +24,22 @@ int pack_forest(const int32_t* feature, const float* threshold, const int32_t* l
   fh.n_trees = n_trees;
   fh.d = d;
 
-  // Breadth-first order of each tree, validated.
+  // Breadth-first order of each tree, validated, with its depth.
   std::vector<std::vector<int>> order(n_trees);
+  fh.depth.assign(n_trees, 0);
   for (int t = 0; t < n_trees; ++t) {
     int64_t base = tree_offset[t], size = tree_offset[t + 1] - base;
-    if (size < 1 || size > kChunkNodes) return fail(size < 1 ? SCOOT_ERR_INVALID_ARG : SCOOT_ERR_UNSUPPORTED,
-                                                    "forest: empty tree or tree larger than 8192 nodes");
-    std::vector<char> seen(size, 0);
+    if (size < 1 || size > kChunkNodes - 1)
+      return fail(size < 1 ? SCOOT_ERR_INVALID_ARG : SCOOT_ERR_UNSUPPORTED,
+                  "forest: empty tree or tree larger than 8191 nodes");
+    std::vector<int> level(size, -1);
     std::deque<int> q{0};
-    seen[0] = 1;
+    level[0] = 0;
     while (!q.empty()) {
       int u = q.front();
       q.pop_front();
       order[t].push_back(u);
+      fh.depth[t] = std::max<uint32_t>(fh.depth[t], (uint32_t)level[u]);
       int64_t g = base + u;
       int L = left[g], R = right[g];
       if (L < 0 && R < 0) {
@@ -52,69 +52,74 @@ int pack_forest(const int32_t* feature, const float* threshold, const int32_t* l
       if (feature[g] < 0 || feature[g] >= d) return fail(SCOOT_ERR_INVALID_ARG, "forest: bad feature index");
       if (std::isnan(threshold[g])) return fail(SCOOT_ERR_INVALID_ARG, "forest: NaN threshold");
       for (int c : {L, R}) {
-        if (seen[c]) return fail(SCOOT_ERR_INVALID_ARG, "forest: node reached twice (not a tree)");
-        seen[c] = 1;
+        if (level[c] >= 0) return fail(SCOOT_ERR_INVALID_ARG, "forest: node reached twice (not a tree)");
+        level[c] = level[u] + 1;
         q.push_back(c);
       }
     }
   }
 
-  // Chunks of consecutive trees, at most kChunkNodes packed nodes each.
+  // Chunks of consecutive trees: one unused node, then whole trees, at most
+  // kChunkNodes nodes in all.
   fh.chunk_tree.push_back(0);
-  int in_chunk = 0;
+  int in_chunk = 1;
   for (int t = 0; t < n_trees; ++t) {
     int sz = (int)order[t].size();
     if (in_chunk + sz > kChunkNodes) {
       fh.chunk_tree.push_back(t);
-      in_chunk = 0;
+      in_chunk = 1;
     }
     in_chunk += sz;
   }
   fh.chunk_tree.push_back(n_trees);
 
-  // Pack.  Child indices are relative to the first node of the tree's chunk.
-  size_t total = 0;
+  // Pack.  Child indices are relative to the chunk's first (unused) node.
+  size_t total = (fh.chunk_tree.size() - 1);
   for (auto& o : order) total += o.size();
   fh.nodes.assign(total * 2, 0);
+  fh.leaf_orig.assign(total, -1);
   fh.root.assign(n_trees + 1, 0);
   uint32_t next = 0;
-  size_t chunk = 0;
-  uint32_t chunk_first = 0;
-  for (int t = 0; t < n_trees; ++t) {
-    if (t == fh.chunk_tree[chunk + 1]) {
-      ++chunk;
-      chunk_first = next;
-    }
-    int64_t base = tree_offset[t];
-    std::vector<uint32_t> pos(tree_offset[t + 1] - base, 0);
-    // Positions: root first, then children pairs in breadth-first order.
-    uint32_t cursor = next;
-    pos[0] = cursor++;
-    for (int u : order[t]) {
-      int64_t g = base + u;
-      if (left[g] >= 0) {
-        pos[left[g]] = cursor++;
-        pos[right[g]] = cursor++;
+  for (size_t ch = 0; ch + 1 < fh.chunk_tree.size(); ++ch) {
+    const uint32_t chunk_first = next;
+    fh.chunk_first_node.push_back(chunk_first);
+    fh.nodes[2 * next] = 0;  // the unused node
+    fh.nodes[2 * next + 1] = kLeafNaN;
+    ++next;
+    for (int t = fh.chunk_tree[ch]; t < fh.chunk_tree[ch + 1]; ++t) {
+      int64_t base = tree_offset[t];
+      std::vector<uint32_t> pos(tree_offset[t + 1] - base, 0);
+      uint32_t cursor = next;
+      pos[0] = cursor++;
+      for (int u : order[t]) {
+        int64_t g = base + u;
+        if (left[g] >= 0) {
+          pos[left[g]] = cursor++;
+          pos[right[g]] = cursor++;
+        }
       }
-    }
-    fh.root[t] = pos[0];
-    for (int u : order[t]) {
-      int64_t g = base + u;
-      uint32_t at = pos[u];
-      if (left[g] < 0) {
-        fh.nodes[2 * at] = kLeafFlag | ((uint32_t)u << 6);
-        fh.nodes[2 * at + 1] = (uint32_t)leaf_q16[g];
-      } else {
-        uint32_t child = pos[left[g]] - chunk_first;
-        fh.nodes[2 * at] = (uint32_t)feature[g] | (child << 6);
-        uint32_t bits;
-        std::memcpy(&bits, &threshold[g], 4);
-        fh.nodes[2 * at + 1] = bits;
+      fh.root[t] = pos[0];
+      for (int u : order[t]) {
+        int64_t g = base + u;
+        uint32_t at = pos[u];
+        uint32_t rel = at - chunk_first;
+        if (left[g] < 0) {
+          fh.nodes[2 * at] = (rel - 1) << 15;
+          fh.nodes[2 * at + 1] = kLeafNaN | (uint32_t)leaf_q16[g];
+          fh.leaf_orig[at] = u;
+        } else {
+          uint32_t child = pos[left[g]] - chunk_first;
+          fh.nodes[2 * at] = (child << 15) | ((uint32_t)feature[g] << 11);
+          uint32_t bits;
+          std::memcpy(&bits, &threshold[g], 4);
+          fh.nodes[2 * at + 1] = bits;
+        }
       }
+      next = cursor;
     }
-    next = cursor;
   }
   fh.root[n_trees] = next;
+  fh.chunk_first_node.push_back(next);
   return SCOOT_OK;
 }
 

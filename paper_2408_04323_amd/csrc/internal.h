@@ -77,15 +77,25 @@ struct BoxTable {
 int build_boxes(const double* Y, int m, int p, const double* ref, BoxTable& out);
 
 // ---- forest (host) ----------------------------------------------------------
-// Packed node: word0 = flags | payload; word1 = threshold bits or Q16 value.
-//   internal: word0 = feature (bits 0..4) | (first child index << 6), children adjacent
-//   leaf    : word0 = 0x20 | (tree-local original index << 6),   word1 = Q16 value
-constexpr uint32_t kLeafFlag = 0x20u;
+// Packed node, 8 bytes: word0 = (child << 15) | (feature << 11), word1 = the
+// threshold's float32 bits.  The two children of a node are adjacent (right =
+// child + 1).  A leaf at position s stores child = s - 1 and, as threshold, a
+// quiet NaN whose payload is the leaf's Q16 value: x <= NaN is false for every
+// x, so a walk that reaches a leaf steps to s - 1 + 1 = s and stays there.
+// Every chunk starts with one unused node, so no leaf sits at position 0.
+// feature << 11 is the byte offset of that feature's column in the kernel's
+// LDS copy of the candidates (512 threads x 4 bytes per feature).
+constexpr int kForestThreadsPerBlock = 512;
+constexpr uint32_t kLeafNaN = 0x7FC00000u;
+constexpr int kChunkNodes = 8192;
 struct ForestHost {
   int n_trees = 0, d = 0;
   std::vector<uint32_t> nodes;             // 2 words per node
   std::vector<uint32_t> root;              // packed index of each tree's root (n_trees + 1 entries)
+  std::vector<uint32_t> depth;             // edges from each tree's root to its deepest leaf
+  std::vector<int32_t> leaf_orig;          // per packed node: tree-local index of a leaf, -1 otherwise
   std::vector<int> chunk_tree;             // first tree of each LDS chunk (+ end)
+  std::vector<uint32_t> chunk_first_node;  // packed index of each chunk's unused first node (+ end)
 };
 int pack_forest(const int32_t* feature, const float* threshold, const int32_t* left,
                 const int32_t* right, const int32_t* leaf_q16, const int64_t* tree_offset,
@@ -109,8 +119,10 @@ struct GPDevice {
 
 struct ForestDevice {
   int n_trees = 0, d = 0;
-  uint32_t* nodes = nullptr;
+  uint32_t* nodes = nullptr;     // one allocation: nodes | root | depth | leaf_orig
   uint32_t* root = nullptr;
+  uint32_t* depth = nullptr;
+  int32_t* leaf_orig = nullptr;
   std::vector<int> chunk_tree;
   std::vector<uint32_t> chunk_first_node;
 };

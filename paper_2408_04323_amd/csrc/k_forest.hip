@@ -5,9 +5,13 @@
 // The packed trees of one chunk (at most 64 KiB, children adjacent) are
 // staged in LDS once per workgroup; each thread owns one candidate, keeps its
 // features in its own LDS column (features are indexed dynamically) and walks
-// every tree of the chunk, four trees at a time so their dependent LDS reads
-// overlap: left iff x[f] <= threshold, a plain float32 compare (NaN goes right).  Forests larger than one chunk take one launch per chunk,
-// the vote counts carried in the votes array between launches.
+// four trees at a time.  A step is branch-free: read the node, read the
+// feature it names, go to child + (x <= threshold ? 0 : 1) (a float32
+// compare; NaN goes right).  Leaves carry a NaN threshold and point one below
+// themselves, so a walk that has arrived stays put; each group of trees runs
+// exactly as many steps as its deepest tree, then reads the leaves' values
+// from the NaN payloads.  Forests larger than one chunk take one launch per
+// chunk, the vote counts carried in the votes array between launches.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -16,8 +20,9 @@
 
 namespace scoot {
 
-constexpr int kForestThreads = 512;
+constexpr int kForestThreads = kForestThreadsPerBlock;
 constexpr int kWalks = 4;
+static_assert(kForestThreads * 4 == (1 << 11), "feature << 11 is the byte offset of a feature column");
 
 struct ForestArgs {
   int64_t n;
@@ -28,47 +33,47 @@ struct ForestArgs {
 };
 
 __global__ __launch_bounds__(kForestThreads) void forest_kernel(
-    const uint2* __restrict__ nodes, const uint32_t* __restrict__ root, const float* __restrict__ Xc,
-    int32_t* __restrict__ votes, uint8_t* __restrict__ mask, int32_t* __restrict__ leaf_idx,
-    const ForestArgs a) {
+    const uint2* __restrict__ nodes, const uint32_t* __restrict__ root, const uint32_t* __restrict__ depth,
+    const int32_t* __restrict__ leaf_orig, const float* __restrict__ Xc, int32_t* __restrict__ votes,
+    uint8_t* __restrict__ mask, int32_t* __restrict__ leaf_idx, const ForestArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint2* tree = reinterpret_cast<uint2*>(smem);
-  float* xs = reinterpret_cast<float*>(tree + a.n_nodes);  // [d][kForestThreads]
+  unsigned char* xs = smem + (size_t)a.n_nodes * 8;  // [d][kForestThreads] floats
   const int tid = threadIdx.x;
   for (uint32_t i = tid; i < a.n_nodes; i += kForestThreads) tree[i] = nodes[a.node_base + i];
   __syncthreads();
 
+  const unsigned char* my_x = xs + tid * 4;
   for (int64_t g = blockIdx.x; g * kForestThreads < a.n; g += gridDim.x) {
     const int64_t c = g * kForestThreads + tid;
     if (c >= a.n) continue;
-    for (int k = 0; k < a.d; ++k) xs[k * kForestThreads + tid] = Xc[c * a.d + k];
+    for (int k = 0; k < a.d; ++k) reinterpret_cast<float*>(xs)[k * kForestThreads + tid] = Xc[c * a.d + k];
     int32_t v = a.first ? 0 : votes[c];
-    // Four walks in flight, branch-free: all node reads, then all feature
-    // reads, then the steps; a finished walk stays on its leaf.
     for (int t0 = a.t_begin; t0 < a.t_end; t0 += kWalks) {
+      const int cnt = min(kWalks, a.t_end - t0);
       uint32_t node[kWalks];
-      bool live[kWalks];
+      uint32_t steps = 0;
 #pragma unroll
       for (int q = 0; q < kWalks; ++q) {
-        live[q] = t0 + q < a.t_end;
-        node[q] = live[q] ? root[t0 + q] - a.node_base : root[t0] - a.node_base;
+        const int t = q < cnt ? t0 + q : t0;
+        node[q] = root[t] - a.node_base;
+        steps = max(steps, depth[t]);
       }
-      while (live[0] || live[1] || live[2] || live[3]) {
+      for (uint32_t s = 0; s < steps; ++s) {
         uint2 rec[kWalks];
         float x[kWalks];
 #pragma unroll
         for (int q = 0; q < kWalks; ++q) rec[q] = tree[node[q]];
 #pragma unroll
-        for (int q = 0; q < kWalks; ++q) x[q] = xs[(rec[q].x & 31u) * kForestThreads + tid];
+        for (int q = 0; q < kWalks; ++q) x[q] = *reinterpret_cast<const float*>(my_x + (rec[q].x & 0x7800u));
 #pragma unroll
-        for (int q = 0; q < kWalks; ++q) {
-          const bool leaf = (rec[q].x & kLeafFlag) != 0;
-          if (leaf && live[q]) {
-            v += (int32_t)rec[q].y;
-            if (leaf_idx) leaf_idx[c * a.n_trees + t0 + q] = (int32_t)(rec[q].x >> 6);
-          }
-          live[q] = live[q] && !leaf;
-          node[q] = leaf ? node[q] : (rec[q].x >> 6) + (x[q] <= __uint_as_float(rec[q].y) ? 0u : 1u);
+        for (int q = 0; q < kWalks; ++q) node[q] = (rec[q].x >> 15) + (x[q] <= __uint_as_float(rec[q].y) ? 0u : 1u);
+      }
+#pragma unroll
+      for (int q = 0; q < kWalks; ++q) {
+        if (q < cnt) {
+          v += (int32_t)(tree[node[q]].y & 0x1FFFFu);
+          if (leaf_idx) leaf_idx[c * a.n_trees + t0 + q] = leaf_orig[a.node_base + node[q]];
         }
       }
     }
@@ -115,8 +120,8 @@ int launch_forest(const ForestDevice& f, const float* Xc, int64_t n, int64_t vot
     a.last = ch == n_chunks - 1;
     a.vote_min = (int32_t)vote_min;
     const size_t lds = (size_t)a.n_nodes * 8 + (size_t)f.d * kForestThreads * 4;
-    hipLaunchKernelGGL(forest_kernel, dim3((unsigned)grid), dim3(kForestThreads), lds, s,
-                       (const uint2*)f.nodes, f.root, Xc, votes, mask, leaf_idx, a);
+    hipLaunchKernelGGL(forest_kernel, dim3((unsigned)grid), dim3(kForestThreads), lds, s, (const uint2*)f.nodes,
+                       f.root, f.depth, f.leaf_orig, Xc, votes, mask, leaf_idx, a);
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("forest launch: ") + hipGetErrorString(err));
