@@ -130,17 +130,16 @@ int fit_host(const double* X, const double* y, int m, int d, const double* ls, d
 // Inside a block the 16 steps are grouped in fours so a lane reads four
 // consecutive steps as one 16-byte load:
 //   float index = ((blk * 4 + s / 4) * 64 + l) * 4 + s % 4.
-// Blocks are ordered the way the kernel's waves consume them: wave after wave,
-// each wave's row blocks in snake order, J = 0..I within a row block.  Two
-// zero blocks of padding follow, for the kernel's read-ahead.
+// Blocks are ordered the way the kernel's waves consume them: plan entry after
+// plan entry (plan_rows), J = 0..I within a row block.
 void pack_linv_f32(const FitHost& f, std::vector<float>& out) {
   const int nb = f.nb, m = f.m, W = posterior_waves(nb);
-  out.assign(((size_t)nb * (nb + 1) / 2 + 2) * 16 * 64, 0.0f);
+  const RowPlan plan = plan_rows(nb, W);
+  out.assign((size_t)nb * (nb + 1) / 2 * 16 * 64, 0.0f);
   size_t blk = 0;
-  for (int w = 0; w < W; ++w)
-    for (int r = 0;; ++r) {
-      const int I = snake_row(w, r, W);
-      if (I >= nb) break;
+  for (int e = 0; e < 8; ++e)
+    for (int r = 0; r < plan.nrows[e]; ++r) {
+      const int I = (int)((plan.rows[e] >> (kRowBits * r)) & 31);
       for (int J = 0; J <= I; ++J, ++blk)
         for (int s = 0; s < 16; ++s)
           for (int l = 0; l < 64; ++l) {

@@ -1,6 +1,7 @@
 // Internal declarations shared by the host code and the kernel launchers.
 #pragma once
 
+#include <algorithm>
 #include <cstddef>
 #include <cstdint>
 #include <string>
@@ -28,20 +29,95 @@ constexpr double kPadCoord = 1.0e4;    // scaled coordinate of padding rows: k(x
 // so it gets 8 waves; otherwise two 4-wave workgroups share a CU.
 inline int posterior_waves(int nb) { return nb > 9 ? 8 : 4; }
 
-// Row blocks of wave w in the snake order that balances the triangular work
-// (row block I costs I + 1 blocks): w, 2W-1-w, 2W+w, 4W-1-w, ...  Increasing in r.
-SCOOT_HOST_DEVICE inline int snake_row(int w, int r, int W) {
-  return (r >> 1) * 2 * W + ((r & 1) ? 2 * W - 1 - w : w);
-}
-// Number of 32 x 32 blocks wave w streams through.
-SCOOT_HOST_DEVICE inline int wave_blocks(int w, int nb, int W) {
+// Which row blocks of V each wave of the fp32 posterior owns.  Row block I
+// costs I + 1 blocks of the triangle.  Plan entry p goes to wave p of a 4-wave
+// workgroup; with 8 waves the two entries p and p + 4 share a SIMD and its
+// matrix unit.  So the rows are first split into four sets of (nearly) equal
+// cost, one per SIMD, by a depth-first search for the smallest capacity that
+// admits a packing; with 8 waves each set is then halved between its two
+// waves by an exact subset-sum split.  The packed inverse streams the blocks
+// entry by entry, each entry's rows in increasing I, blocks J = 0..I.
+constexpr int kMaxRowBlocks = SCOOT_MAX_OBS / kBlk32;
+constexpr int kRowBits = 5;  // rows of an entry packed 5 bits each, first row lowest
+struct RowPlan {
+  uint64_t rows[8];
+  int32_t nrows[8];
+  int32_t blk_start[9];  // first block of entry p in the packed stream
+};
+
+// Splits rows into two sets whose costs (I + 1) are as equal as possible.
+inline void bisect_rows(const std::vector<int>& rows, std::vector<int>& lo, std::vector<int>& hi) {
   int total = 0;
-  for (int r = 0;; ++r) {
-    const int I = snake_row(w, r, W);
-    if (I >= nb) break;
-    total += I + 1;
+  for (int I : rows) total += I + 1;
+  // reach[k][s]: some subset of the first k rows costs s
+  std::vector<std::vector<char>> reach(rows.size() + 1, std::vector<char>(total + 1, 0));
+  reach[0][0] = 1;
+  for (size_t k = 0; k < rows.size(); ++k)
+    for (int s = 0; s <= total; ++s)
+      if (reach[k][s]) {
+        reach[k + 1][s] = 1;
+        reach[k + 1][s + rows[k] + 1] = 1;
+      }
+  int best = 0;
+  for (int s = 0; s <= total / 2; ++s)
+    if (reach[rows.size()][s]) best = s;
+  lo.clear();
+  hi.clear();
+  for (size_t k = rows.size(); k-- > 0;) {
+    if (best >= rows[k] + 1 && reach[k][best - rows[k] - 1]) {
+      lo.push_back(rows[k]);
+      best -= rows[k] + 1;
+    } else {
+      hi.push_back(rows[k]);
+    }
   }
-  return total;
+}
+
+// Places rows[k..] (decreasing) into four sets of cost at most cap.
+inline bool pack_rows4(const std::vector<int>& rows, size_t k, int cap, int (&load)[4], std::vector<int> (&set)[4]) {
+  if (k == rows.size()) return true;
+  const int c = rows[k] + 1;
+  for (int b = 0; b < 4; ++b) {
+    bool same = false;  // a set with the same load was already tried
+    for (int b2 = 0; b2 < b; ++b2) same = same || load[b2] == load[b];
+    if (same || load[b] + c > cap) continue;
+    load[b] += c;
+    set[b].push_back(rows[k]);
+    if (pack_rows4(rows, k + 1, cap, load, set)) return true;
+    load[b] -= c;
+    set[b].pop_back();
+  }
+  return false;
+}
+
+inline RowPlan plan_rows(int nb, int W) {
+  std::vector<int> all;
+  for (int I = nb - 1; I >= 0; --I) all.push_back(I);
+  std::vector<int> quarter[4], entry[8];
+  for (int cap = (nb * (nb + 1) / 2 + 3) / 4;; ++cap) {
+    int load[4] = {0, 0, 0, 0};
+    for (auto& q : quarter) q.clear();
+    if (pack_rows4(all, 0, cap, load, quarter)) break;
+  }
+  if (W == 8) {
+    for (int q = 0; q < 4; ++q) bisect_rows(quarter[q], entry[q], entry[q + 4]);
+  } else {
+    for (int q = 0; q < 4; ++q) entry[q] = quarter[q];
+  }
+  RowPlan p{};
+  int b = 0;
+  for (int e = 0; e < 8; ++e) {
+    std::vector<int> r = entry[e];
+    std::sort(r.begin(), r.end());
+    p.blk_start[e] = b;
+    p.nrows[e] = (int)r.size();
+    for (size_t k = 0; k < r.size(); ++k) {
+      p.rows[e] |= (uint64_t)r[k] << (kRowBits * k);
+      b += r[k] + 1;
+    }
+  }
+  p.blk_start[8] = b;
+  return p;
 }
 
 void set_error(const std::string& msg);

@@ -26,7 +26,9 @@
 // alpha and L^-1 entries are 0.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
+#include <cstring>
 #include <type_traits>
 #include <utility>
 
@@ -56,44 +58,47 @@ struct Post32 {
   float scale[SCOOT_MAX_DIM];
   float c0, c1, c2;
   double s2, prior, ei_c;
+  RowPlan plan;  // row blocks of each wave and where they start in the packed inverse
 };
 
-// Candidate coordinates times the per-dimension scale (D = the exact number
-// of dimensions, so every load is unconditional and all are in flight at once).
+// Candidate coordinates (D = the exact number of dimensions, so every load is
+// unconditional and all are in flight at once); scaled once they have landed.
 template <int D>
-__device__ inline void load_scaled_f32(float (&xc)[D], const float* __restrict__ row, const float* scale) {
-  float xf[D];
+__device__ inline void load_coords_f32(float (&xr)[D], const float* __restrict__ row) {
 #pragma unroll
-  for (int q = 0; q < D; ++q) xf[q] = row[q];
-#pragma unroll
-  for (int q = 0; q < D; ++q) xc[q] = xf[q] * scale[q];
+  for (int q = 0; q < D; ++q) xr[q] = row[q];
 }
 
-// One 32 x 32 block (row block I, column block J) of L^-1 against the tile's
-// two 32-candidate halves of K*[J]: 16 MFMA steps; steps 0-7 go to the "lo"
-// accumulators and 8-15 to the "hi" ones, so four independent chains are in
-// flight (summed before squaring).
-__device__ inline void mfma_block4(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, const f4_t (&a)[4],
-                                   const f4_t* ks, int J, int lane) {
-#pragma unroll
-  for (int s4 = 0; s4 < 2; ++s4) {
-    const f4_t bl0 = ks[((J * 2 + 0) * 4 + s4) * 64 + lane];
-    const f4_t bl1 = ks[((J * 2 + 1) * 4 + s4) * 64 + lane];
-    const f4_t bh0 = ks[((J * 2 + 0) * 4 + s4 + 2) * 64 + lane];
-    const f4_t bh1 = ks[((J * 2 + 1) * 4 + s4 + 2) * 64 + lane];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      l0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4][t], bl0[t], l0, 0, 0, 0);
-      l1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4][t], bl1[t], l1, 0, 0, 0);
-      h0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4 + 2][t], bh0[t], h0, 0, 0, 0);
-      h1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4 + 2][t], bh1[t], h1, 0, 0, 0);
-    }
-  }
-}
-
+// Operands of one 32 x 32 block (row block I, column block J): A = four
+// 16-byte loads per lane from the packed inverse (16 steps), B = K*[J] for the
+// tile's two 32-candidate halves, eight 16-byte LDS reads per lane.
 __device__ inline void load_block32(f4_t (&a)[4], const f4_t* ap, int k) {
 #pragma unroll
   for (int s4 = 0; s4 < 4; ++s4) a[s4] = ap[(size_t)(k * 4 + s4) * 64];
+}
+__device__ inline void load_b32(f4_t (&b)[8], const f4_t* ks, int J, int lane) {
+#pragma unroll
+  for (int s4 = 0; s4 < 4; ++s4) {
+    b[2 * s4 + 0] = ks[((J * 2 + 0) * 4 + s4) * 64 + lane];
+    b[2 * s4 + 1] = ks[((J * 2 + 1) * 4 + s4) * 64 + lane];
+  }
+}
+
+// The 16 MFMA steps of a block: steps 0-7 on the "lo" accumulators, 8-15 on
+// the "hi" ones, issued round-robin so four independent chains are in flight
+// (summed before squaring).
+__device__ inline void mfma_block4(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, const f4_t (&a)[4],
+                                   const f4_t (&b)[8]) {
+#pragma unroll
+  for (int s4 = 0; s4 < 2; ++s4) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      l0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4][t], b[2 * s4 + 0][t], l0, 0, 0, 0);
+      l1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4][t], b[2 * s4 + 1][t], l1, 0, 0, 0);
+      h0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4 + 2][t], b[2 * (s4 + 2) + 0][t], h0, 0, 0, 0);
+      h1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4 + 2][t], b[2 * (s4 + 2) + 1][t], h1, 0, 0, 0);
+    }
+  }
 }
 
 // Where V goes when it is kept (the sequential believer needs it): row-major,
@@ -108,6 +113,7 @@ struct VStore {
 // Completes a row block: squared norms of its V columns into sq0 / sq1, and
 // the block itself into V when kept.  Accumulator register r of lane l holds
 // row 8 (r / 4) + 4 (l / 32) + r % 4 of the block, column l % 32.
+template <bool KEEP_V>
 __device__ inline void finish_row(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, float& sq0, float& sq1,
                                   const VStore& vs, int I, int lane) {
   float p0 = 0.0f, p1 = 0.0f;
@@ -115,7 +121,7 @@ __device__ inline void finish_row(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, fl
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const float v0 = l0[r] + h0[r], v1 = l1[r] + h1[r];
-    if (vs.v) {
+    if constexpr (KEEP_V) {
       const int64_t row = 32 * I + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       if (c_a < vs.n) vs.v[row * vs.ld + c_a] = v0;
       if (c_b < vs.n) vs.v[row * vs.ld + c_b] = v1;
@@ -131,52 +137,61 @@ __device__ inline void finish_row(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, fl
   sq1 += p1;
 }
 
-// The wave's whole stream of blocks with one block of read-ahead in two fixed
-// buffers.  The packed inverse ends with two blocks of padding, so reading
-// ahead past the last block stays in bounds.
-template <int WAVES>
-__device__ inline void wave_stream32(const f4_t* __restrict__ linv, const f4_t* ks, int nb, int wave, int lane,
-                                     float& sq0, float& sq1, const VStore& vs) {
-  int start = 0;
-  for (int w = 0; w < wave; ++w) start += wave_blocks(w, nb, WAVES);
-  const int count = wave_blocks(wave, nb, WAVES);
-  if (count == 0) return;
-  const f4_t* ap = linv + (size_t)start * 4 * 64 + lane;
+// One tile's pass over the wave's blocks, one block of read-ahead of both
+// operands in two fixed buffer sets.  The A stream is the same for every tile,
+// so its read-ahead wraps: on entry ax holds the wave's first block, and on
+// exit it holds it again for the next tile.  B (K* of this tile) is read
+// ahead only within the tile; past the last block it reads K*[0], unused.
+template <bool KEEP_V>
+__device__ inline void wave_tile32(const f4_t* __restrict__ ap, const f4_t* ks, uint64_t rows, int count,
+                                   int lane, f4_t (&ax)[4], float& sq0, float& sq1, const VStore& vs) {
   f16_t l0 = {0}, l1 = {0}, h0 = {0}, h1 = {0};
-  // (r, I, J): row slot, row block, column block of the block being computed
-  int r = 0, I = snake_row(wave, 0, WAVES), J = 0;
+  // (I, J): row block and column block of the block being computed; the
+  // wave's remaining rows sit in `rows`, kRowBits each (0 past the last).
+  int I = (int)(rows & 31), J = 0;
+  auto next_j = [&](int j, int i) { return j == i ? 0 : j + 1; };
   auto advance = [&]() {
     if (J == I) {
-      finish_row(l0, l1, h0, h1, sq0, sq1, vs, I, lane);
+      finish_row<KEEP_V>(l0, l1, h0, h1, sq0, sq1, vs, I, lane);
       J = 0;
-      ++r;
-      I = snake_row(wave, r, WAVES);
+      rows >>= kRowBits;
+      I = (int)(rows & 31);
     } else {
       ++J;
     }
   };
-  f4_t x[4], y[4];
-  load_block32(x, ap, 0);
+  f4_t ay[4], bx[8], by[8];
+  load_b32(bx, ks, 0, lane);
   int k = 0;
   for (; k + 1 < count; k += 2) {
-    load_block32(y, ap, k + 1);
+    load_block32(ay, ap, k + 1);
+    load_b32(by, ks, next_j(J, I), lane);
     __builtin_amdgcn_sched_barrier(0);
-    mfma_block4(l0, l1, h0, h1, x, ks, J, lane);
+    mfma_block4(l0, l1, h0, h1, ax, bx);
     __builtin_amdgcn_sched_barrier(0);
     advance();
-    load_block32(x, ap, k + 2);
+    load_block32(ax, ap, k + 2 < count ? k + 2 : 0);
+    load_b32(bx, ks, next_j(J, I), lane);
     __builtin_amdgcn_sched_barrier(0);
-    mfma_block4(l0, l1, h0, h1, y, ks, J, lane);
+    mfma_block4(l0, l1, h0, h1, ay, by);
     __builtin_amdgcn_sched_barrier(0);
     advance();
   }
   if (k < count) {
-    mfma_block4(l0, l1, h0, h1, x, ks, J, lane);
+    load_block32(ay, ap, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_block4(l0, l1, h0, h1, ax, bx);
+    __builtin_amdgcn_sched_barrier(0);
     advance();
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) ax[s4] = ay[s4];
   }
 }
 
-template <int WAVES, int D>
+// Persistent: workgroup g takes tiles g, g + G, g + 2G, ... (G = grid size),
+// so the inverse-factor stream and the next tile's coordinates are in flight
+// across tile boundaries.
+template <int WAVES, int D, bool KEEP_V>
 __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
     const float* __restrict__ Xc, const f4_t* __restrict__ linv, const float* __restrict__ xs,
     const float* __restrict__ alpha, float* __restrict__ mu_out, float* __restrict__ sd_out,
@@ -190,68 +205,102 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int64_t c0 = (int64_t)blockIdx.x * 64;
+  const int64_t n_tiles = (a.n + 63) >> 6;
 
-  // ---- phase 1: K* for candidate c0 + lane, rows of this wave's groups ----
-  int64_t cg = c0 + lane;
-  if (cg >= a.n) cg = a.n - 1;
-  float xc[D];
-  load_scaled_f32<D>(xc, Xc + cg * D, a.scale);
-
-  // Group G covers rows 32J + 8 s4 + 2t + h, t = 0..3, of block J; lane l
-  // writes them as one float4 to B-operand slot (J, ct = l/32, s4, h*32 + l%32).
-  float mu_part = 0.0f;
-  const int ngroups = nb * 8;
-  for (int G = wave; G < ngroups; G += WAVES) {
-    const int J = G >> 3, s4 = (G >> 1) & 3, h = G & 1;
-    const int row0 = 32 * J + 8 * s4 + h;
-    f4_t kv;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int i = row0 + 2 * t;
-      const float* xo = xs + (size_t)i * kXsStride;
-      float acc = 0.0f;
-#pragma unroll
-      for (int k = 0; k < D; ++k) {
-        float df = xc[k] - xo[k];
-        acc = fmaf(df, df, acc);
-      }
-      float u = __builtin_amdgcn_sqrtf(acc);
-      float e = __builtin_amdgcn_exp2f(-u);
-      float kval = fmaf(u, fmaf(u, a.c2, a.c1), a.c0) * e;
-      kv[t] = kval;
-      mu_part = fmaf(kval, alpha[i], mu_part);
-    }
-    ks[((J * 2 + (lane >> 5)) * 4 + s4) * 64 + h * 32 + (lane & 31)] = kv;
+  // Plan entry of this wave.  With 8 waves, entries p and p + 4 are meant to
+  // share a SIMD: each wave takes simd + 4 * (its arrival order on the SIMD),
+  // unless the workgroup did not land as two waves per SIMD; then entry =
+  // wave.  Either way every entry is taken exactly once.
+  int p = wave;
+  if constexpr (WAVES == 8) {
+    int* on_simd = reinterpret_cast<int*>(mu_red + WAVES * 64);  // [4]
+    if (tid < 4) on_simd[tid] = 0;
+    __syncthreads();
+    const int simd = (int)((__builtin_amdgcn_s_getreg((31 << 11) | 4) >> 4) & 3);  // HW_ID.SIMD_ID
+    int slot = 0;
+    if (lane == 0) slot = atomicAdd(&on_simd[simd], 1);
+    slot = __shfl(slot, 0);
+    __syncthreads();
+    if (on_simd[0] == 2 && on_simd[1] == 2 && on_simd[2] == 2 && on_simd[3] == 2) p = simd + 4 * slot;
+    p = __builtin_amdgcn_readfirstlane(p);
   }
-  __syncthreads();
+  const uint64_t rows = a.plan.rows[p];
+  const int count = a.plan.blk_start[p + 1] - a.plan.blk_start[p];
+  const f4_t* ap = linv + (size_t)a.plan.blk_start[p] * 4 * 64 + lane;
+  f4_t ax[4];
+  if (count > 0) load_block32(ax, ap, 0);
 
-  // ---- phase 2: this wave's row blocks of V = L^-1 K*^T on the matrix cores
-  float sq0 = 0.0f, sq1 = 0.0f;
-  const VStore vs{v_out, a.n, c0, a.n};
-  wave_stream32<WAVES>(linv, ks, nb, wave, lane, sq0, sq1, vs);
+  int64_t tile = blockIdx.x;
+  float xr[D];
+  load_coords_f32<D>(xr, Xc + min(tile * 64 + lane, a.n - 1) * D);
 
-  // ---- phase 3: reduce over waves and row halves, write ------------------
-  // Accumulator lane l holds column l % 32 of its tile (ct = 0 / 1).
-  const int h = lane >> 5;
-  sig_red[(wave * 2 + h) * 64 + (lane & 31)] = sq0;
-  sig_red[(wave * 2 + h) * 64 + 32 + (lane & 31)] = sq1;
-  mu_red[wave * 64 + lane] = mu_part;
-  __syncthreads();
-  if (tid < 64) {
-    const int64_t c = c0 + tid;
-    if (c < a.n) {
-      double ss = 0.0, mm = 0.0;
+  for (; tile < n_tiles; tile += gridDim.x) {
+    const int64_t c0 = tile * 64;
+    float xc[D];
 #pragma unroll
-      for (int w = 0; w < WAVES; ++w) {
-        ss += (double)sig_red[(w * 2 + 0) * 64 + tid] + (double)sig_red[(w * 2 + 1) * 64 + tid];
-        mm += (double)mu_red[w * 64 + tid];
+    for (int q = 0; q < D; ++q) xc[q] = xr[q] * a.scale[q];
+    // next tile's coordinates, in flight during this one
+    const int64_t next = tile + gridDim.x;
+    if (next < n_tiles) load_coords_f32<D>(xr, Xc + min(next * 64 + lane, a.n - 1) * D);
+
+    // ---- phase 1: K* for candidate c0 + lane, rows of this wave's groups --
+    // Group G covers rows 32J + 8 s4 + 2t + h, t = 0..3, of block J; lane l
+    // writes them as one float4 to B-operand slot (J, ct = l/32, s4, h*32 + l%32).
+    float mu_part = 0.0f;
+    const int ngroups = nb * 8;
+    for (int G = wave; G < ngroups; G += WAVES) {
+      const int J = G >> 3, s4 = (G >> 1) & 3, h = G & 1;
+      const int rbase = 32 * J + 8 * s4 + h;
+      f4_t kv;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int i = rbase + 2 * t;
+        const float* xo = xs + (size_t)i * kXsStride;
+        float acc = 0.0f;
+#pragma unroll
+        for (int k = 0; k < D; ++k) {
+          float df = xc[k] - xo[k];
+          acc = fmaf(df, df, acc);
+        }
+        float u = __builtin_amdgcn_sqrtf(acc);
+        float e = __builtin_amdgcn_exp2f(-u);
+        float kval = fmaf(u, fmaf(u, a.c2, a.c1), a.c0) * e;
+        kv[t] = kval;
+        mu_part = fmaf(kval, alpha[i], mu_part);
       }
-      const double sd = sqrt(fmax(a.s2 - ss, 0.0));
-      const double mu = a.prior + mm;
-      mu_out[c] = (float)mu;
-      sd_out[c] = (float)sd;
-      if (ei_out) ei_out[c] = (float)partial_expectation_d(a.ei_c, (double)(float)mu, (double)(float)sd);
+      ks[((J * 2 + (lane >> 5)) * 4 + s4) * 64 + h * 32 + (lane & 31)] = kv;
+    }
+    __syncthreads();
+
+    // ---- phase 2: this wave's row blocks of V = L^-1 K*^T on the matrix cores
+    float sq0 = 0.0f, sq1 = 0.0f;
+    if (count > 0) {
+      const VStore vs{v_out, a.n, c0, a.n};
+      wave_tile32<KEEP_V>(ap, ks, rows, count, lane, ax, sq0, sq1, vs);
+    }
+
+    // ---- phase 3: reduce over waves and row halves, write ----------------
+    // Accumulator lane l holds column l % 32 of its tile (ct = 0 / 1).
+    const int h = lane >> 5;
+    sig_red[(wave * 2 + h) * 64 + (lane & 31)] = sq0;
+    sig_red[(wave * 2 + h) * 64 + 32 + (lane & 31)] = sq1;
+    mu_red[wave * 64 + lane] = mu_part;
+    __syncthreads();
+    if (tid < 64) {
+      const int64_t c = c0 + tid;
+      if (c < a.n) {
+        double ss = 0.0, mm = 0.0;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) {
+          ss += (double)sig_red[(w * 2 + 0) * 64 + tid] + (double)sig_red[(w * 2 + 1) * 64 + tid];
+          mm += (double)mu_red[w * 64 + tid];
+        }
+        const double sd = sqrt(fmax(a.s2 - ss, 0.0));
+        const double mu = a.prior + mm;
+        mu_out[c] = (float)mu;
+        sd_out[c] = (float)sd;
+        if (ei_out) ei_out[c] = (float)partial_expectation_d(a.ei_c, (double)(float)mu, (double)(float)sd);
+      }
     }
   }
 }
@@ -384,17 +433,29 @@ __global__ __launch_bounds__(WAVES * 64) void posterior_f64_kernel(
 // ---------------------------------------------------------------------------
 namespace {
 
-template <int WAVES, int D>
+template <int WAVES, int D, bool KEEP_V>
 int run32(const GPDevice& g, const float* Xc, int64_t n, float* mu, float* sd, float* ei, float* v_out,
           const Post32& a, hipStream_t s) {
-  const size_t lds = (size_t)g.nb * 2 * 4 * 64 * 16 + WAVES * 2 * 64 * 4 + WAVES * 64 * 4;
-  auto kern = posterior_f32_kernel<WAVES, D>;
+  // K* tile, per-wave partial norms and means, four SIMD counters
+  const size_t lds = (size_t)g.nb * 2 * 4 * 64 * 16 + WAVES * 2 * 64 * 4 + WAVES * 64 * 4 + 16;
+  auto kern = posterior_f32_kernel<WAVES, D, KEEP_V>;
   static bool attr_set = false;
   if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) !=
+        hipSuccess)
+      return fail(SCOOT_ERR_DEVICE, "posterior: cannot raise the LDS limit of the kernel");
     attr_set = true;
   }
-  const int64_t grid = (n + 63) / 64;
+  // Persistent grid: as many workgroups as the chip holds at once, each
+  // looping over tiles.
+  int dev = 0, cus = 256, per_cu = 0;
+  (void)hipGetDevice(&dev);
+  (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)kern, WAVES * 64, lds) != hipSuccess ||
+      per_cu < 1)
+    return fail(SCOOT_ERR_DEVICE, "posterior: workgroup does not fit on a compute unit");
+  const int64_t tiles = (n + 63) / 64;
+  const int64_t grid = std::min(tiles, (int64_t)cus * per_cu);
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WAVES * 64), lds, s, Xc,
                      (const f4_t*)g.linv, (const float*)g.xs, g.alpha32, mu, sd, ei, v_out, a);
   return SCOOT_OK;
@@ -457,11 +518,18 @@ int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, vo
     a.s2 = g.s2;
     a.prior = g.c;
     a.ei_c = ei_c ? *ei_c : 0.0;
+    a.plan = plan_rows(g.nb, posterior_waves(g.nb));
+    for (int e = 0; e < 8; ++e)
+      if (a.plan.nrows[e] * kRowBits > 64) return fail(SCOOT_ERR_UNSUPPORTED, "posterior: row plan does not pack");
     float* e = ei_c ? (float*)ei : nullptr;
     rc = by_d_rec<1>(g.d, [&](auto Dc) {
-      return posterior_waves(g.nb) == 8
-                 ? run32<8, decltype(Dc)::value>(g, Xc, n, (float*)mu, (float*)sigma, e, v_out, a, s)
-                 : run32<4, decltype(Dc)::value>(g, Xc, n, (float*)mu, (float*)sigma, e, v_out, a, s);
+      constexpr int D = decltype(Dc)::value;
+      float *m32 = (float*)mu, *s32 = (float*)sigma;
+      if (posterior_waves(g.nb) == 8)
+        return v_out ? run32<8, D, true>(g, Xc, n, m32, s32, e, v_out, a, s)
+                     : run32<8, D, false>(g, Xc, n, m32, s32, e, nullptr, a, s);
+      return v_out ? run32<4, D, true>(g, Xc, n, m32, s32, e, v_out, a, s)
+                   : run32<4, D, false>(g, Xc, n, m32, s32, e, nullptr, a, s);
     });
   } else {
     Post64 a{};
