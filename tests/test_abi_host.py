@@ -130,3 +130,27 @@ def test_topq_and_forest_argument_checks():
     with pytest.raises(S.ScootError) as e:  # leaf value above 1.0 in Q16
         S.forest_create([0, 0, 0], [0.5, 0, 0], [1, -1, -1], [2, -1, -1], [0, 70000, 1], [0, 3], 2)
     assert e.value.status == -1
+
+
+def test_normal_tail_coefficients_match_their_generator():
+    """The float partial expectation uses P4(s) / Q6(s) for g(x) = 1 - x M(x);
+    the coefficients in the kernel source must be what the committed fitting
+    script produces, and the fit must meet its stated error."""
+    import importlib.util
+    here = os.path.join(os.path.dirname(S.__file__), "csrc")
+    spec = importlib.util.spec_from_file_location("gen_normal_tail", os.path.join(here, "gen_normal_tail.py"))
+    gen = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(gen)
+    x, y, p, q, err = gen.fit()
+    assert err < 2e-8
+    src = open(os.path.join(here, "k_acq.hip")).read()
+    body = src[src.index("__device__ inline float h_normal(float u)"):]
+    body = body[:body.index("\n}\n")]
+    nums = [float(v) for v in re.findall(r"([0-9]\.[0-9]{9}e[+-][0-9]{2})f", body)]
+    # Horner order: highest coefficient first, P then Q (constant 1 of Q written as 1.0f)
+    want = list(p[::-1]) + list(q[:0:-1])
+    assert len(nums) == len(want)
+    np.testing.assert_allclose(nums, want, rtol=5e-9)
+    # the float evaluation of the fit against g in double
+    g32 = gen.eval_f32(p, q, x).astype(np.float64)
+    assert np.max(np.abs(g32 - y) / y) < 1e-6
