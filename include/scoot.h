@@ -233,6 +233,58 @@ int scoot_suggest_kb(const scoot_gp* gps, int p, scoot_forest f, const float* Xc
                      const double* Y_obs, int m_obs, const double* ref, double delta, int q, void* workspace,
                      uint64_t workspace_bytes, int64_t* picks, double* pick_acq, int* n_picked, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * MACE suggestion for one objective (Sec. 4.5.1: UCB, PI and EI, their Pareto
+ * front over the candidates, k of them drawn at random; Sec. 4.6).  The
+ * objective is minimised, so with best = best_y + xi and Y ~ N(mu, sigma^2):
+ *
+ * scoot_ucb_beta (host): the paper's schedule beta_t = 2 log(t^2 pi^2 /
+ *   (6 delta)), delta = 1 / t^2, for tuning iteration t >= 1.  The paper
+ *   multiplies sigma by this beta itself (Eq. 6); GP-UCB proper uses its square
+ *   root -- the scoring calls take the multiplier as given.
+ *
+ * scoot_acq_mace (device): ucb = beta * sigma - mu (Eq. 6 for -Y), pi =
+ *   P(Y < best) (Eq. 7; 1 or 0 when sigma = 0), ei = E[(best - Y)^+] (Eq. 8).
+ *   mu, sigma, ucb, pi, ei: [n] device arrays of type dt.
+ *
+ * scoot_pareto_front3 (device): front[i] = 1 when candidate i is eligible
+ *   (mask[i] != 0, mask nullable = all; no NaN score) and no eligible
+ *   candidate scores at least as high on all of a, b, c and higher on one (all
+ *   maximised; equal score vectors do not dominate each other), else 0.
+ *   a, b, c [n] device of type dt; front [n] u8 device; n_front [1] int32
+ *   device (nullable) = number of front members.  0 <= n < 2^31.  Worst-case
+ *   work grows with the square of the number of candidates that survive a
+ *   1024-candidate tile.
+ *
+ * scoot_random_pick (device): the q flagged candidates (flags[i] != 0) with
+ *   the largest u_i, u_i = output number i (0-based) of SplitMix64 started
+ *   from seed (state advanced by 0x9E3779B97F4A7C15, Stafford's finaliser);
+ *   lower index first on equal draws.  That is a uniformly random q-subset of
+ *   the flagged set, in random order, reproducible from (seed, flags).
+ *   idx [q] int64 device (tail -1 when fewer are flagged); n_flagged [1] int32
+ *   device (nullable).  1 <= q <= SCOOT_MAX_Q; 0 <= n < 2^31.
+ *
+ * scoot_suggest_mace (device): scoot_posterior, scoot_acq_mace,
+ *   scoot_rf_feasibility with delta (f nullable: all feasible),
+ *   scoot_pareto_front3 on (ucb, pi, ei) under the mask, scoot_random_pick
+ *   of q from the front.  mu, sigma, ucb, pi, ei [n] of the GP's dtype; votes
+ *   [n] (nullable); mask, front [n] u8; idx [q]; n_front [1] (nullable).
+ *
+ * Errors: INVALID_ARG (null pointer, bad dtype, n or q out of range, non-finite
+ * best_y, xi or beta, t < 1), DEVICE, NO_MEMORY, and those of the calls made.
+ * ------------------------------------------------------------------------- */
+int scoot_ucb_beta(int t, double* beta);
+int scoot_acq_mace(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double best_y, double xi,
+                   double beta, void* ucb, void* pi, void* ei, void* stream);
+int scoot_pareto_front3(const void* a, const void* b, const void* c, const uint8_t* mask, int64_t n,
+                        scoot_dtype dt, uint8_t* front, int32_t* n_front, void* stream);
+int scoot_random_pick(const uint8_t* flags, int64_t n, uint64_t seed, int q, int64_t* idx, int32_t* n_flagged,
+                      void* stream);
+int scoot_suggest_mace(scoot_gp gp, scoot_forest f, const float* Xc, int64_t n, double best_y, double xi,
+                       double beta, double delta, uint64_t seed, int q, void* mu, void* sigma, void* ucb,
+                       void* pi, void* ei, int32_t* votes, uint8_t* mask, uint8_t* front, int64_t* idx,
+                       int32_t* n_front, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

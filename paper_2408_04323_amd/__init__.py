@@ -317,3 +317,82 @@ def suggest_kb(gps, forest, Xc, q, Y_obs, ref, delta=0.5, workspace=None, stream
                                  acq.ctypes.data_as(C.POINTER(C.c_double)), C.byref(k), _stream(stream)),
           "suggest_kb")
     return picks[:k.value], acq[:k.value]
+
+
+# ------------------------------------------------------------- MACE (one GP)
+def ucb_beta(t):
+    """beta_t of the paper's UCB schedule for tuning iteration t >= 1."""
+    b = C.c_double(0.0)
+    check(lib().scoot_ucb_beta(int(t), C.byref(b)), "ucb_beta")
+    return b.value
+
+
+def acq_mace(mu, sigma, best_y, beta, xi=1e-4, out=None, stream=None):
+    """Returns (ucb, pi, ei) device tensors; out = optional (ucb, pi, ei)."""
+    import torch
+    n = mu.numel()
+    _require_device(mu, "mu")
+    _require_device(sigma, "sigma", mu.dtype, n)
+    ucb, pi, ei = (torch.empty_like(mu) for _ in range(3)) if out is None else out
+    for t, name in ((ucb, "ucb"), (pi, "pi"), (ei, "ei")):
+        _require_device(t, name, mu.dtype, n)
+    check(lib().scoot_acq_mace(_dptr(mu), _dptr(sigma), n, _dt(mu.dtype), best_y, xi, beta, _dptr(ucb), _dptr(pi),
+                               _dptr(ei), _stream(stream)), "acq_mace")
+    return ucb, pi, ei
+
+
+def pareto_front3(a, b, c, mask=None, front=None, stream=None):
+    """Non-dominated flags (all three maximised).  Returns (front uint8 (n,), n_front int32 (1,))."""
+    import torch
+    n = a.numel()
+    _require_device(a, "a")
+    _require_device(b, "b", a.dtype, n)
+    _require_device(c, "c", a.dtype, n)
+    if mask is not None:
+        _require_device(mask, "mask", torch.uint8, n)
+    front = torch.empty(n, dtype=torch.uint8, device=a.device) if front is None else front
+    _require_device(front, "front", torch.uint8, n)
+    nf = torch.empty(1, dtype=torch.int32, device=a.device)
+    check(lib().scoot_pareto_front3(_dptr(a), _dptr(b), _dptr(c), _dptr(mask), n, _dt(a.dtype), _dptr(front),
+                                    _dptr(nf), _stream(stream)), "pareto_front3")
+    return front, nf
+
+
+def random_pick(flags, seed, q, stream=None):
+    """Seeded random q flagged candidates.  Returns (idx int64 (q,), n_flagged int32 (1,))."""
+    import torch
+    n = flags.numel()
+    _require_device(flags, "flags", torch.uint8)
+    idx = torch.empty(q, dtype=torch.int64, device=flags.device)
+    nf = torch.empty(1, dtype=torch.int32, device=flags.device)
+    check(lib().scoot_random_pick(_dptr(flags), n, C.c_uint64(seed & (2 ** 64 - 1)), q, _dptr(idx), _dptr(nf),
+                                  _stream(stream)), "random_pick")
+    return idx, nf
+
+
+class MaceBuffers:
+    """Device outputs of one MACE suggestion, allocated once and reused."""
+
+    def __init__(self, n, q, dtype, device):
+        import torch
+        td = _tdtype(dtype)
+        self.mu, self.sigma, self.ucb, self.pi, self.ei = (torch.empty(n, dtype=td, device=device) for _ in range(5))
+        self.votes = torch.empty(n, dtype=torch.int32, device=device)
+        self.mask = torch.empty(n, dtype=torch.uint8, device=device)
+        self.front = torch.empty(n, dtype=torch.uint8, device=device)
+        self.idx = torch.empty(q, dtype=torch.int64, device=device)
+        self.n_front = torch.empty(1, dtype=torch.int32, device=device)
+
+
+def suggest_mace(gp, forest, Xc, q, best_y, beta, seed, xi=1e-4, delta=0.5, buffers=None, stream=None):
+    """Posterior, (ucb, pi, ei), forest mask, their Pareto front, q drawn from it."""
+    import torch
+    n = Xc.shape[0]
+    _require_device(Xc, "Xc", torch.float32, n * gp.d)
+    b = MaceBuffers(n, q, gp.dtype, Xc.device) if buffers is None else buffers
+    check(lib().scoot_suggest_mace(gp.handle, forest.handle if forest is not None else None, _dptr(Xc), n, best_y,
+                                   xi, beta, delta, C.c_uint64(seed & (2 ** 64 - 1)), q, _dptr(b.mu),
+                                   _dptr(b.sigma), _dptr(b.ucb), _dptr(b.pi), _dptr(b.ei), _dptr(b.votes),
+                                   _dptr(b.mask), _dptr(b.front), _dptr(b.idx), _dptr(b.n_front), _stream(stream)),
+          "suggest_mace")
+    return b

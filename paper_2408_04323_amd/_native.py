@@ -37,6 +37,12 @@ SIGNATURES = {
     "scoot_suggest_kb_workspace": [C.POINTER(c_vp), c_int, c_i64, c_int, C.POINTER(C.c_uint64)],
     "scoot_suggest_kb": [C.POINTER(c_vp), c_int, c_vp, c_vp, c_i64, P_dbl, c_int, P_dbl, c_dbl, c_int, c_vp,
                          C.c_uint64, P_i64, P_dbl, P_int, c_vp],
+    "scoot_ucb_beta": [c_int, P_dbl],
+    "scoot_acq_mace": [c_vp, c_vp, c_i64, c_int, c_dbl, c_dbl, c_dbl, c_vp, c_vp, c_vp, c_vp],
+    "scoot_pareto_front3": [c_vp, c_vp, c_vp, c_vp, c_i64, c_int, c_vp, c_vp, c_vp],
+    "scoot_random_pick": [c_vp, c_i64, C.c_uint64, c_int, c_vp, c_vp, c_vp],
+    "scoot_suggest_mace": [c_vp, c_vp, c_vp, c_i64, c_dbl, c_dbl, c_dbl, c_dbl, C.c_uint64, c_int, c_vp, c_vp,
+                           c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp],
 }
 RESTYPES = {"scoot_status_string": C.c_char_p, "scoot_last_error": C.c_char_p}
 

@@ -26,7 +26,7 @@ namespace {
 thread_local std::string g_last_error;
 
 constexpr int kMaxDevices = 64;
-constexpr int kScratchSlots = 4;
+constexpr int kScratchSlots = 5;
 constexpr int kStagingSlots = 2;
 
 struct Staging {
@@ -386,6 +386,76 @@ int scoot_suggest_topq(const void* score, const uint8_t* mask, int64_t n, scoot_
   if (n < 0 || n >= ((int64_t)1 << 31)) return fail(SCOOT_ERR_INVALID_ARG, "topq: n out of range");
   if (!idx || (n > 0 && !score)) return fail(SCOOT_ERR_INVALID_ARG, "topq: null pointer");
   return launch_topq(score, mask, n, dt, q, idx, score_out, n_valid, stream);
+}
+
+int scoot_ucb_beta(int t, double* beta) {
+  g_last_error.clear();
+  if (!beta || t < 1) return fail(SCOOT_ERR_INVALID_ARG, "ucb beta: null beta or t < 1");
+  const double tt = (double)t, delta = 1.0 / (tt * tt), pi = 3.14159265358979323846;
+  *beta = 2.0 * std::log(tt * tt * pi * pi / (6.0 * delta));
+  return SCOOT_OK;
+}
+
+int scoot_acq_mace(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double best_y, double xi, double beta,
+                   void* ucb, void* pi, void* ei, void* stream) {
+  g_last_error.clear();
+  if (!check_dtype(dt) || n < 0) return fail(SCOOT_ERR_INVALID_ARG, "mace: bad dtype or n");
+  if (n > 0 && (!mu || !sigma || !ucb || !pi || !ei)) return fail(SCOOT_ERR_INVALID_ARG, "mace: null pointer");
+  if (!std::isfinite(best_y) || !std::isfinite(xi) || !std::isfinite(beta))
+    return fail(SCOOT_ERR_INVALID_ARG, "mace: non-finite best_y/xi/beta");
+  return launch_mace_scores(mu, sigma, n, dt, best_y + xi, beta, ucb, pi, ei, stream);
+}
+
+int scoot_pareto_front3(const void* a, const void* b, const void* c, const uint8_t* mask, int64_t n, scoot_dtype dt,
+                        uint8_t* front, int32_t* n_front, void* stream) {
+  g_last_error.clear();
+  if (!check_dtype(dt)) return fail(SCOOT_ERR_INVALID_ARG, "pareto: bad dtype");
+  if (n < 0 || n >= ((int64_t)1 << 31)) return fail(SCOOT_ERR_INVALID_ARG, "pareto: n out of range");
+  if (n > 0 && (!a || !b || !c || !front)) return fail(SCOOT_ERR_INVALID_ARG, "pareto: null pointer");
+  return launch_pareto_front3(a, b, c, mask, n, dt, front, n_front, stream);
+}
+
+int scoot_random_pick(const uint8_t* flags, int64_t n, uint64_t seed, int q, int64_t* idx, int32_t* n_flagged,
+                      void* stream) {
+  g_last_error.clear();
+  if (q < 1 || q > SCOOT_MAX_Q) return fail(SCOOT_ERR_INVALID_ARG, "pick: q must be in 1..SCOOT_MAX_Q");
+  if (n < 0 || n >= ((int64_t)1 << 31)) return fail(SCOOT_ERR_INVALID_ARG, "pick: n out of range");
+  if (!idx || (n > 0 && !flags)) return fail(SCOOT_ERR_INVALID_ARG, "pick: null pointer");
+  return launch_random_pick(flags, n, seed, q, idx, n_flagged, stream);
+}
+
+int scoot_suggest_mace(scoot_gp gp, scoot_forest f, const float* Xc, int64_t n, double best_y, double xi, double beta,
+                       double delta, uint64_t seed, int q, void* mu, void* sigma, void* ucb, void* pi, void* ei,
+                       int32_t* votes, uint8_t* mask, uint8_t* front, int64_t* idx, int32_t* n_front, void* stream) {
+  g_last_error.clear();
+  if (!gp) return fail(SCOOT_ERR_INVALID_ARG, "mace suggest: null GP");
+  if (n < 0 || n >= ((int64_t)1 << 31)) return fail(SCOOT_ERR_INVALID_ARG, "mace suggest: n out of range");
+  if (n > 0 && (!Xc || !mu || !sigma || !ucb || !pi || !ei || !mask || !front))
+    return fail(SCOOT_ERR_INVALID_ARG, "mace suggest: null pointer");
+  if (!idx) return fail(SCOOT_ERR_INVALID_ARG, "mace suggest: null idx");
+  if (q < 1 || q > SCOOT_MAX_Q) return fail(SCOOT_ERR_INVALID_ARG, "mace suggest: q out of range");
+  if (!std::isfinite(best_y) || !std::isfinite(xi) || !std::isfinite(beta))
+    return fail(SCOOT_ERR_INVALID_ARG, "mace suggest: non-finite best_y/xi/beta");
+  const scoot_dtype dt = gp->dev.dt;
+  int64_t vmin = 0;
+  int rc;
+  if (f) {
+    rc = scoot_vote_threshold(delta, f->dev.n_trees, &vmin);
+    if (rc != SCOOT_OK) return rc;
+  }
+  rc = launch_posterior(gp->dev, Xc, n, mu, sigma, nullptr, nullptr, stream);
+  if (rc != SCOOT_OK) return rc;
+  rc = launch_mace_scores(mu, sigma, n, dt, best_y + xi, beta, ucb, pi, ei, stream);
+  if (rc != SCOOT_OK) return rc;
+  if (f) {
+    rc = launch_forest(f->dev, Xc, n, vmin, votes, mask, nullptr, stream);
+  } else if (n > 0) {
+    rc = launch_fill_u8(mask, n, 1, stream);
+  }
+  if (rc != SCOOT_OK) return rc;
+  rc = launch_pareto_front3(ucb, pi, ei, mask, n, dt, front, nullptr, stream);
+  if (rc != SCOOT_OK) return rc;
+  return launch_random_pick(front, n, seed, q, idx, n_front, stream);
 }
 
 int scoot_delta_update(double* delta, int* c, int k, int any_invalid) {

@@ -223,6 +223,12 @@ int launch_forest(const ForestDevice& f, const float* Xc, int64_t n, int64_t vot
 int launch_fill_u8(uint8_t* p, int64_t n, uint8_t v, void* stream);
 int launch_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q,
                 int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
+int launch_random_pick(const uint8_t* flags, int64_t n, uint64_t seed, int q, int64_t* idx, int32_t* n_flagged,
+                       void* stream);
+int launch_mace_scores(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double c, double beta, void* ucb,
+                       void* pi, void* ei, void* stream);
+int launch_pareto_front3(const void* a, const void* b, const void* c, const uint8_t* mask, int64_t n, scoot_dtype dt,
+                         uint8_t* front, int32_t* n_front, void* stream);
 
 // Sequential Kriging-believer picks (fp32 GPs only).
 size_t kb_workspace_bytes(const GPDevice* const* g, int p, int64_t n, int q);

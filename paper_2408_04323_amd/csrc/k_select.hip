@@ -13,6 +13,12 @@
 // selection over all stage-1 lists and writes indices, scores and the count.
 // Selection is exact integer work, so the result does not depend on the
 // grid shape or on the order in which blocks run.
+//
+// The same two stages make the random pick of the MACE suggestion (Sec. 4.5.1,
+// Sec. 4.6): candidate i's key is (u_i, inverted index), u_i the i-th output of
+// SplitMix64 started from the caller's seed, so the pick is the q flagged
+// candidates with the largest draws -- a uniformly random q-subset of the
+// flagged set in random order.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -93,10 +99,32 @@ __device__ void select_rounds(K (&keys)[kSelPer], K* list, K* wave_best, int q) 
   }
 }
 
-template <typename T, typename K>
-__global__ __launch_bounds__(kSelThreads) void topq_stage1(const T* __restrict__ score,
-                                                           const uint8_t* __restrict__ mask, int64_t n,
-                                                           int q, K* __restrict__ part_keys,
+// Key sources for stage 1.
+template <typename T>
+struct ScoreKeys {
+  const T* __restrict__ score;
+  const uint8_t* __restrict__ mask;  // nullable
+  __device__ auto operator()(int64_t i) const { return make_key(score[i], i, mask ? mask[i] != 0 : true); }
+};
+
+// SplitMix64 (Steele, Lea and Flood, OOPSLA 2014; Stafford's finaliser):
+// output number i of the generator started from `seed`.
+__device__ inline uint64_t splitmix64(uint64_t seed, uint64_t i) {
+  uint64_t z = seed + (i + 1) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+struct DrawKeys {
+  const uint8_t* __restrict__ flags;
+  uint64_t seed;
+  __device__ Key128 operator()(int64_t i) const {
+    return flags[i] ? Key128{splitmix64(seed, (uint64_t)i), ~(uint64_t)i} : Key128{0, 0};
+  }
+};
+
+template <typename K, typename Src>
+__global__ __launch_bounds__(kSelThreads) void topq_stage1(const Src src, int64_t n, int q, K* __restrict__ part_keys,
                                                            int32_t* __restrict__ part_count) {
   __shared__ K list[SCOOT_MAX_Q];
   __shared__ K wave_best[kSelThreads / 64];
@@ -109,12 +137,7 @@ __global__ __launch_bounds__(kSelThreads) void topq_stage1(const T* __restrict__
 #pragma unroll
     for (int j = 0; j < kSelPer; ++j) {
       const int64_t i = base + (int64_t)j * kSelThreads + tid;
-      if (i < n) {
-        const bool ok = mask ? mask[i] != 0 : true;
-        keys[j] = make_key(score[i], i, ok);
-      } else {
-        keys[j] = K{};
-      }
+      keys[j] = i < n ? src(i) : K{};
       valid += keys[j].zero() ? 0 : 1;
     }
     select_rounds<K>(keys, list, wave_best, q);
@@ -169,9 +192,10 @@ __global__ __launch_bounds__(kSelThreads) void topq_stage2(const T* __restrict__
 }
 
 namespace {
-template <typename T, typename K>
-int run_topq(const T* score, const uint8_t* mask, int64_t n, int q, int64_t* idx, T* score_out,
-             int32_t* n_valid, hipStream_t s) {
+// score / score_out may be null (the random pick writes indices only).
+template <typename T, typename K, typename Src>
+int run_select(const Src& src, const T* score, int64_t n, int q, int64_t* idx, T* score_out, int32_t* n_valid,
+               hipStream_t s) {
   int64_t grid = (n + kSelChunk - 1) / kSelChunk;
   if (grid < 1) grid = 1;
   if (grid > kSelMaxGrid) grid = kSelMaxGrid;
@@ -180,8 +204,7 @@ int run_topq(const T* score, const uint8_t* mask, int64_t n, int q, int64_t* idx
   if (!ws) return fail(SCOOT_ERR_NO_MEMORY, "topq: scratch allocation failed");
   K* pk = reinterpret_cast<K*>(ws);
   int32_t* pc = reinterpret_cast<int32_t*>(ws + kbytes);
-  hipLaunchKernelGGL((topq_stage1<T, K>), dim3((unsigned)grid), dim3(kSelThreads), 0, s, score, mask, n, q,
-                     pk, pc);
+  hipLaunchKernelGGL((topq_stage1<K, Src>), dim3((unsigned)grid), dim3(kSelThreads), 0, s, src, n, q, pk, pc);
   hipLaunchKernelGGL((topq_stage2<T, K>), dim3(1), dim3(kSelThreads), 0, s, score, (int)grid, q, pk, pc, idx,
                      score_out, n_valid);
   hipError_t err = hipGetLastError();
@@ -193,9 +216,19 @@ int run_topq(const T* score, const uint8_t* mask, int64_t n, int q, int64_t* idx
 int launch_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q, int64_t* idx,
                 void* score_out, int32_t* n_valid, void* stream) {
   hipStream_t s = (hipStream_t)stream;
-  if (dt == SCOOT_F32)
-    return run_topq<float, Key64>((const float*)score, mask, n, q, idx, (float*)score_out, n_valid, s);
-  return run_topq<double, Key128>((const double*)score, mask, n, q, idx, (double*)score_out, n_valid, s);
+  if (dt == SCOOT_F32) {
+    const ScoreKeys<float> src{(const float*)score, mask};
+    return run_select<float, Key64>(src, (const float*)score, n, q, idx, (float*)score_out, n_valid, s);
+  }
+  const ScoreKeys<double> src{(const double*)score, mask};
+  return run_select<double, Key128>(src, (const double*)score, n, q, idx, (double*)score_out, n_valid, s);
+}
+
+int launch_random_pick(const uint8_t* flags, int64_t n, uint64_t seed, int q, int64_t* idx, int32_t* n_flagged,
+                       void* stream) {
+  const DrawKeys src{flags, seed};
+  return run_select<double, Key128>(src, (const double*)nullptr, n, q, idx, (double*)nullptr, n_flagged,
+                                    (hipStream_t)stream);
 }
 
 }  // namespace scoot

@@ -143,7 +143,7 @@ def test_normal_tail_coefficients_match_their_generator():
     spec.loader.exec_module(gen)
     x, y, p, q, err = gen.fit()
     assert err < 2e-8
-    src = open(os.path.join(here, "k_acq.hip")).read()
+    src = open(os.path.join(here, "normal.h")).read()
     body = src[src.index("__device__ inline float h_normal(float u)"):]
     body = body[:body.index("\n}\n")]
     nums = [float(v) for v in re.findall(r"([0-9]\.[0-9]{9}e[+-][0-9]{2})f", body)]

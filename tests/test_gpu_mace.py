@@ -1,0 +1,200 @@
+"""GPU parity of the MACE suggestion (Sec. 4.5.1; Eq. 6-8; pick of Sec. 4.6)
+against the oracle.
+
+Scores on shared inputs: |gpu - oracle| <= rtol * max(|oracle|, scale), rtol
+1e-5 (UCB, PI) and 1e-3 (EI) in float32, 1e-12 (UCB, PI) and 1e-10 (EI) in
+float64; end to end they carry the posterior's error and are judged at its bar.  The front and the pick are index
+work: bit-exact when both sides see the same score arrays; end to end (each
+side with its own scores) the device front must be exactly the front of the
+device's scores, and must agree with the oracle's front wherever the oracle's
+decision is not within the score tolerance.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import paper_2408_04323_amd as S  # noqa: E402
+from oracle.gp import gp_fit, gp_posterior  # noqa: E402
+from oracle.forest import feasibility_mask, forest_votes  # noqa: E402
+from oracle.mace import mace_scores, pareto_front_max, random_pick, ucb_beta  # noqa: E402
+from workloads import make_workload  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+TOL = {S.F32: dict(ucb=1e-5, pi=1e-5, ei=1e-3), S.F64: dict(ucb=1e-12, pi=1e-12, ei=1e-10)}
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def assert_close(got, want, rtol, scale, what):
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    bound = rtol * np.maximum(np.abs(want), scale)
+    err = np.abs(got - want)
+    bad = ~(err <= bound)
+    assert not bad.any(), f"{what}: {bad.sum()} of {len(got)} outside tolerance, worst at {np.argmax(err / bound)}"
+
+
+def dev(a, dtype=torch.float32):
+    return torch.as_tensor(np.ascontiguousarray(a)).to(dtype).to(DEV)
+
+
+def host(t):
+    return t.cpu().numpy().astype(np.float64)
+
+
+def test_ucb_beta_matches_oracle():
+    for t in (1, 2, 7, 50, 1000):
+        assert S.ucb_beta(t) == pytest.approx(ucb_beta(t), rel=1e-14)
+    with pytest.raises(S.ScootError):
+        S.ucb_beta(0)
+
+
+@pytest.mark.parametrize("dt", [S.F32, S.F64], ids=["f32", "f64"])
+def test_mace_scores_parity(dt):
+    rng = np.random.default_rng(11)
+    n = 5000 + 13
+    mu = rng.standard_normal(n) * 1.5
+    sd = np.abs(rng.standard_normal(n)) * 0.5
+    sd[:40] = 0.0
+    mu[40:60] = 0.05  # at the threshold
+    td = torch.float32 if dt == S.F32 else torch.float64
+    mu_d, sd_d = dev(mu, td), dev(sd, td)
+    best, xi, beta = 0.05 - 1e-4, 1e-4, ucb_beta(6)
+    say("mace scores", dt, n)
+    ucb, pi, ei = S.acq_mace(mu_d, sd_d, best, beta, xi=xi)
+    torch.cuda.synchronize()
+    u_o, p_o, e_o = mace_scores(host(mu_d), host(sd_d), best, xi, beta)
+    t = TOL[dt]
+    assert_close(host(ucb), u_o, t["ucb"], np.max(np.abs(u_o)), "ucb")
+    assert_close(host(pi), p_o, t["pi"], 1.0, "pi")
+    assert_close(host(ei), e_o, t["ei"], np.max(e_o), "ei")
+    # sigma = 0: a step at the threshold
+    assert np.all(host(pi)[:40] == (host(mu_d)[:40] < best + xi))
+
+
+def _scores_case(kind, n, seed):
+    rng = np.random.default_rng(seed)
+    if kind == "correlated":
+        z = rng.standard_normal((n, 3))
+        S3 = z @ np.array([[1, .8, .6], [0, .5, .4], [0, 0, .5]])
+    elif kind == "ties":
+        S3 = rng.integers(0, 6, (n, 3)).astype(float)
+    elif kind == "conflict":  # all on a plane: every point is on the front
+        S3 = rng.random((n, 3))
+        S3[:, 2] = 2.0 - S3[:, 0] - S3[:, 1]
+    else:
+        raise ValueError(kind)
+    mask = (rng.random(n) < 0.85).astype(np.uint8)
+    if n > 10:
+        S3[rng.integers(0, n, 5), 1] = np.nan
+        S3[rng.integers(0, n, max(1, n // 50))] = S3[rng.integers(0, n, max(1, n // 50))]  # duplicates
+    return S3, mask
+
+
+PARETO_CASES = [("correlated", 1), ("correlated", 5), ("correlated", 1023), ("correlated", 1024),
+                ("correlated", 1025), ("correlated", 20000 + 77), ("ties", 4096 + 3), ("ties", 9),
+                ("conflict", 3000 + 1)]
+
+
+@pytest.mark.parametrize("dt", [S.F32, S.F64], ids=["f32", "f64"])
+@pytest.mark.parametrize("kind,n", PARETO_CASES, ids=[f"{k}-{n}" for k, n in PARETO_CASES])
+def test_pareto_front_bitexact(kind, n, dt):
+    S3, mask = _scores_case(kind, n, 100 + n)
+    td = torch.float32 if dt == S.F32 else torch.float64
+    a, b, c = (dev(S3[:, j], td) for j in range(3))
+    m = dev(mask, torch.uint8)
+    say("pareto", kind, n, dt)
+    front, nf = S.pareto_front3(a, b, c, m)
+    torch.cuda.synchronize()
+    want = pareto_front_max(np.stack([host(a), host(b), host(c)], axis=1), mask)
+    np.testing.assert_array_equal(front.cpu().numpy().astype(bool), want)
+    assert int(nf.cpu()[0]) == int(want.sum())
+    # without a mask every row without a NaN is eligible
+    front2, _ = S.pareto_front3(a, b, c)
+    torch.cuda.synchronize()
+    want2 = pareto_front_max(np.stack([host(a), host(b), host(c)], axis=1))
+    np.testing.assert_array_equal(front2.cpu().numpy().astype(bool), want2)
+
+
+def test_pareto_front_empty():
+    e = torch.empty(0, device=DEV)
+    front, nf = S.pareto_front3(e, e, e)
+    torch.cuda.synchronize()
+    assert front.numel() == 0 and int(nf.cpu()[0]) == 0
+
+
+@pytest.mark.parametrize("n,density,q", [(1, 1.0, 1), (1000, 0.01, 4), (4096 + 7, 0.3, 8), (100003, 0.002, 16),
+                                         (50000, 0.5, 64), (300, 0.0, 3)])
+def test_random_pick_bitexact(n, density, q):
+    rng = np.random.default_rng(n)
+    flags = (rng.random(n) < density).astype(np.uint8)
+    for seed in (0, 12345, 2 ** 64 - 1, 0x9E3779B97F4A7C15):
+        say("pick", n, density, q, seed)
+        idx, nf = S.random_pick(dev(flags, torch.uint8), seed, q)
+        torch.cuda.synchronize()
+        want, wn = random_pick(flags, seed, q)
+        np.testing.assert_array_equal(idx.cpu().numpy(), want)
+        assert int(nf.cpu()[0]) == wn
+
+
+def _forest(fd, d):
+    return S.forest_create(fd["feature"], fd["threshold"], fd["left"], fd["right"], fd["leaf_q16"],
+                           fd["tree_offset"], d)
+
+
+@pytest.mark.parametrize("cfg,n,dt", [(1, 4096, S.F32), (1, 4096, S.F64), (2, 16384 + 9, S.F32), (2, 8192, S.F64)])
+def test_suggest_mace_end_to_end(cfg, n, dt):
+    w = make_workload(cfg, n=n)
+    fit = gp_fit(w["X"], w["Y"][:, 0], w["lengthscale"][0], w["signal_var"][0], w["noise_var"][0],
+                 w["prior_mean"][0])
+    mu_o, sd_o = gp_posterior(fit, w["Xc"])
+    votes = forest_votes(w["forest"], w["Xc"])
+    mask_o = feasibility_mask(votes, w["delta"], len(w["forest"]["tree_offset"]) - 1)
+    beta, seed, q = ucb_beta(9), 77 + cfg, max(w["q"], 4)
+    gp = S.gp_fit(w["X"], w["Y"][:, 0], w["lengthscale"][0], w["signal_var"][0], w["noise_var"][0],
+                  w["prior_mean"][0], dtype=dt)
+    f = _forest(w["forest"], w["d"])
+    say("suggest_mace", cfg, n, dt)
+    b = S.suggest_mace(gp, f, dev(w["Xc"]), q, w["best_y"], beta, seed, xi=w["xi"], delta=w["delta"])
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(b.mask.cpu().numpy(), mask_o)
+    u_o, p_o, e_o = mace_scores(mu_o, sd_o, w["best_y"], w["xi"], beta)
+    f32 = dt == S.F32
+    assert_close(host(b.mu), mu_o, 1e-4 if f32 else 1e-10, np.max(np.abs(mu_o)), "mu")
+    # End to end the scores inherit the posterior's error (mu, sigma): UCB at
+    # beta times the sigma bar; PI moves by phi(u) * du, du ~ (dmu + u dsigma) /
+    # sigma, so it gets an absolute bar; EI at the usual acquisition bar.
+    tol_u = (1e-3 if f32 else 1e-9) * max(1.0, beta) * max(1.0, np.max(np.abs(mu_o)))
+    tol_p = 1e-2 if f32 else 1e-8
+    tol_e = (1e-3 if f32 else 1e-10) * np.max(e_o)
+    assert np.all(np.abs(host(b.ucb) - u_o) <= tol_u), "ucb"
+    assert np.all(np.abs(host(b.pi) - p_o) <= tol_p), "pi"
+    assert np.all(np.abs(host(b.ei) - e_o) <= tol_e), "ei"
+    # the device front is exactly the front of the device's own scores
+    Sg = np.stack([host(b.ucb), host(b.pi), host(b.ei)], axis=1)
+    fg = b.front.cpu().numpy().astype(bool)
+    np.testing.assert_array_equal(fg, pareto_front_max(Sg, mask_o))
+    assert int(b.n_front.cpu()[0]) == int(fg.sum())
+    # and the pick is exactly the seeded draw from that front
+    want_idx, _ = random_pick(fg, seed, q)
+    np.testing.assert_array_equal(b.idx.cpu().numpy(), want_idx)
+    # Against the oracle's own front: where they disagree on candidate i, some
+    # other eligible j must sit within the tolerance of dominating i (all its
+    # scores at least i's minus twice the bar) with a deciding coordinate
+    # within twice the bar -- a near tie, not a wrong front.
+    So = np.stack([u_o, p_o, e_o], axis=1)
+    fo = pareto_front_max(So, mask_o)
+    tol = 2 * np.array([tol_u, tol_p, tol_e])
+    elig = np.flatnonzero(mask_o != 0)
+    for i in np.flatnonzero(fg != fo):
+        others = elig[elig != i]
+        d = So[others] - So[i]
+        near = (d >= -tol).all(axis=1) & (np.abs(d) <= tol).any(axis=1)
+        assert near.any(), f"front disagreement at {i} is not a near tie"
