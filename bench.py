@@ -50,6 +50,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-loops", type=int, default=20)
+    ap.add_argument("--mace", action="store_true",
+                    help="one-objective workloads: time the MACE suggestion (posterior, UCB/PI/EI, mask, "
+                         "Pareto front, seeded pick) and print its own line")
     ap.add_argument("--only", choices=["all", "posterior", "forest", "ehvi", "topq", "copy"], default="all",
                     help="posterior / forest / ehvi / topq: only that kernel's loop (for profiler "
                          "counters); copy: a plain 1 GiB device copy (counter calibration)")
@@ -85,6 +88,8 @@ def main():
 
     if args.config == 5:
         return bench_believer(args)
+    if args.mace:
+        return bench_mace(args)
     t0 = time.time()
     w = make_workload(args.config)
     gen_s = time.time() - t0
@@ -249,6 +254,68 @@ def bench_believer(args):
                       "config": {"workload": f"{c['name']}: m={w['m']} n={n} d={w['d']} p={p} q={w['q']} "
                                              f"trees={c['trees']} depth={c['depth']}",
                                  "picks": picks.tolist(), "workspace_bytes": ws.numel()}}), flush=True)
+
+
+def bench_mace(args):
+    """A one-objective workload scored the paper's SOBO way (Sec. 4.5.1): one
+    suggestion = posterior, UCB/PI/EI, forest mask, Pareto front of the three
+    scores over the pool, q drawn from it.  Reported on its own line."""
+    import torch
+
+    import paper_2408_04323_amd as S
+    from workloads import make_workload
+    from workloads.synth import CONFIGS
+
+    w = make_workload(args.config)
+    c = CONFIGS[args.config]
+    if w["p"] != 1:
+        print(f"--mace needs a one-objective workload; workload {args.config} has {w['p']}", file=sys.stderr)
+        sys.exit(2)
+    n, q = len(w["Xc"]), w["q"]
+    gp = S.gp_fit(w["X"], w["Y"][:, 0], w["lengthscale"][0], w["signal_var"][0], w["noise_var"][0],
+                  w["prior_mean"][0])
+    fd = w["forest"]
+    forest = S.forest_create(fd["feature"], fd["threshold"], fd["left"], fd["right"], fd["leaf_q16"],
+                             fd["tree_offset"], w["d"])
+    Xc = torch.as_tensor(w["Xc"]).cuda()
+    beta, seed = S.ucb_beta(w["m"] // q), 240804323
+    b = S.MaceBuffers(n, q, gp.dtype, Xc.device)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        S.suggest_mace(gp, forest, Xc, q, w["best_y"], beta, seed, xi=w["xi"], delta=w["delta"], buffers=b)
+
+    def time_loop(fn, loops):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(loops):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / loops
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ms = time_loop(step, args.steps)
+    n_front = int(b.n_front.cpu()[0])
+    kl = args.kernel_loops
+    parts = {
+        "posterior": time_loop(lambda: S.posterior(gp, Xc, b.mu, b.sigma), kl),
+        "scores": time_loop(lambda: S.acq_mace(b.mu, b.sigma, w["best_y"], beta, xi=w["xi"],
+                                               out=(b.ucb, b.pi, b.ei)), kl),
+        "forest": time_loop(lambda: S.rf_feasibility(forest, Xc, w["delta"], votes=b.votes, mask=b.mask), kl),
+        "front": time_loop(lambda: S.pareto_front3(b.ucb, b.pi, b.ei, b.mask, front=b.front), kl),
+        "pick": time_loop(lambda: S.random_pick(b.front, seed, q), kl),
+    }
+    print(json.dumps({"metric": "MACE suggestions (one objective) per second", "value": 1e3 / ms,
+                      "unit": "suggestions/s", "candidates_per_s": n / (ms * 1e-3), "ms_per_step": ms, "n_gpus": 1,
+                      "steps": args.steps, "warmup": args.warmup, "higher_is_better": True, "dtype": "f32",
+                      "data": "synthetic",
+                      "config": {"workload": f"{c['name']}: m={w['m']} n={n} d={w['d']} q={q} trees={c['trees']} "
+                                             f"depth={c['depth']} beta_t={beta:.4f} (t={w['m'] // q})",
+                                 "front_size": n_front, "picks": b.idx.cpu().tolist(), "kernel_ms": parts}}),
+          flush=True)
 
 
 def cpu_baseline(w, seconds):

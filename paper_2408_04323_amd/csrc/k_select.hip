@@ -184,10 +184,18 @@ __global__ __launch_bounds__(kSelThreads) void topq_stage2(const T* __restrict__
       if (score_out) score_out[tid] = score[i];
     }
   }
-  if (tid == 0 && n_valid) {
-    int64_t s = 0;
-    for (int b = 0; b < n_parts; ++b) s += part_count[b];
-    *n_valid = (int32_t)s;
+  if (n_valid) {  // sum of the stage-1 counts, in parallel
+    __shared__ int32_t wsum[kSelThreads / 64];
+    int32_t sum = 0;
+    for (int b = tid; b < n_parts; b += kSelThreads) sum += part_count[b];
+    for (int m = 32; m >= 1; m >>= 1) sum += __shfl_xor(sum, m);
+    if ((tid & 63) == 0) wsum[tid >> 6] = sum;
+    __syncthreads();
+    if (tid == 0) {
+      int32_t t = 0;
+      for (int w = 0; w < kSelThreads / 64; ++w) t += wsum[w];
+      *n_valid = t;
+    }
   }
 }
 

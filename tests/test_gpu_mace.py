@@ -198,3 +198,35 @@ def test_suggest_mace_end_to_end(cfg, n, dt):
         d = So[others] - So[i]
         near = (d >= -tol).all(axis=1) & (np.abs(d) <= tol).any(axis=1)
         assert near.any(), f"front disagreement at {i} is not a near tie"
+
+
+def test_full_size_mace_front_is_exact():
+    """The one-objective workload at its real size (m = 128, n = 262144):
+    the device front checked against the definition on the device's scores
+    (every member undominated by any eligible candidate, every other eligible
+    candidate dominated by a member) and the pick bit-exact."""
+    w = make_workload(2)
+    n, q = len(w["Xc"]), w["q"]
+    gp = S.gp_fit(w["X"], w["Y"][:, 0], w["lengthscale"][0], w["signal_var"][0], w["noise_var"][0],
+                  w["prior_mean"][0])
+    f = _forest(w["forest"], w["d"])
+    beta, seed = ucb_beta(w["m"] // q), 240804323
+    say("suggest_mace full size", n)
+    b = S.suggest_mace(gp, f, dev(w["Xc"]), q, w["best_y"], beta, seed, xi=w["xi"], delta=w["delta"])
+    torch.cuda.synchronize()
+    Sg = np.stack([host(b.ucb), host(b.pi), host(b.ei)], axis=1)
+    mask = b.mask.cpu().numpy() != 0
+    fg = b.front.cpu().numpy().astype(bool)
+    assert fg.any() and not (fg & ~mask).any()
+    F = Sg[fg]
+    E = Sg[mask]
+    for i in np.flatnonzero(fg):
+        assert not (((E >= Sg[i]).all(1)) & ((E > Sg[i]).any(1))).any(), f"front member {i} is dominated"
+    rest = np.flatnonzero(mask & ~fg)
+    for lo in range(0, len(rest), 4096):
+        X = Sg[rest[lo:lo + 4096]][:, None, :]
+        dom = ((F[None] >= X).all(2) & (F[None] > X).any(2)).any(1)
+        assert dom.all(), f"{(~dom).sum()} candidates outside the front are not dominated by it"
+    assert int(b.n_front.cpu()[0]) == int(fg.sum())
+    want, _ = random_pick(fg, seed, q)
+    np.testing.assert_array_equal(b.idx.cpu().numpy(), want)
