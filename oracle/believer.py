@@ -18,7 +18,7 @@ from .select import top_q
 
 def kriging_believer(X, Y, hypers, Xc, mask, ref, q, follow=None, record=None):
     """hypers: list over objectives of dicts with lengthscale, signal_var,
-    noise_var, prior_mean.  Returns (picks (q,), per-pick EHVI (q,),
+    noise_var, prior_mean (and optionally kernel, warp as in ``gp_fit``).  Returns (picks (q,), per-pick EHVI (q,),
     final mu (n, p), final sigma (n, p)).
 
     ``follow``: a pick sequence to take instead of the arg max at each step
@@ -35,7 +35,8 @@ def kriging_believer(X, Y, hypers, Xc, mask, ref, q, follow=None, record=None):
         mu = np.empty((len(Xc64), p))
         sd = np.empty((len(Xc64), p))
         for j, h in enumerate(hypers):
-            fit = gp_fit(Xa, Ya[:, j], h["lengthscale"], h["signal_var"], h["noise_var"], h["prior_mean"])
+            fit = gp_fit(Xa, Ya[:, j], h["lengthscale"], h["signal_var"], h["noise_var"], h["prior_mean"],
+                         kernel=h.get("kernel", "matern52"), warp=h.get("warp"))
             mu[:, j], sd[:, j] = gp_posterior(fit, Xc64)
         front = nondominated(Ya, ref)
         acq = ehvi(mu, sd, front, ref)

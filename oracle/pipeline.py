@@ -16,8 +16,10 @@ def score_pool(w, Xc=None):
     every intermediate (fits, mu, sigma, acq, votes, mask, idx, val, n_valid)."""
     Xc = w["Xc"] if Xc is None else Xc
     p = w["Y"].shape[1]
+    warps = w.get("warp")
     fits = [gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][j], w["signal_var"][j],
-                   w["noise_var"][j], w["prior_mean"][j]) for j in range(p)]
+                   w["noise_var"][j], w["prior_mean"][j], kernel=w.get("kernel", "matern52"),
+                   warp=None if warps is None else (warps[0][j], warps[1][j])) for j in range(p)]
     mu = np.empty((len(Xc), p))
     sigma = np.empty((len(Xc), p))
     for j, f in enumerate(fits):

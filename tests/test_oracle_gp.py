@@ -106,3 +106,56 @@ def test_not_positive_definite_raises():
     X = np.zeros((3, 2))
     with pytest.raises(np.linalg.LinAlgError):
         gp_fit(X, np.zeros(3), [1.0, 1.0], 1.0, 0.0)
+
+
+# ------------------------------------------- the paper's kernel: Matern-3/2 + warping
+from oracle.gp import kumaraswamy_warp, matern32  # noqa: E402
+
+
+def test_matern32_matches_sklearn():
+    rng = np.random.default_rng(4)
+    A, B = rng.random((7, 4)), rng.random((9, 4))
+    ls = np.array([0.2, 0.5, 1.0, 2.0])
+    ref = (ConstantKernel(0.6, "fixed") * Matern(length_scale=ls, nu=1.5))(A, B)
+    np.testing.assert_allclose(matern32(A, B, ls, 0.6), ref, rtol=1e-13, atol=0)
+
+
+def test_matern32_scalar_closed_form():
+    # r = 2: k = s2 (1 + 2 sqrt3) exp(-2 sqrt3)
+    got = matern32(np.array([[0.0]]), np.array([[1.0]]), [0.5], 2.0)[0, 0]
+    s3 = np.sqrt(3.0)
+    assert got == pytest.approx(2.0 * (1 + 2 * s3) * np.exp(-2 * s3), rel=1e-15)
+
+
+def test_kumaraswamy_hand_values_and_special_cases():
+    # a = 2, b = 3, x = 1/2: 1 - (1 - 1/4)^3 = 1 - 27/64 = 37/64
+    assert kumaraswamy_warp(np.array([[0.5]]), [2.0], [3.0])[0, 0] == pytest.approx(37 / 64, rel=1e-15)
+    x = np.linspace(0, 1, 101)[:, None]
+    np.testing.assert_allclose(kumaraswamy_warp(x, [1.0], [1.0]), x, atol=1e-15)        # identity
+    np.testing.assert_allclose(kumaraswamy_warp(x, [1.0], [2.5]), 1 - (1 - x) ** 2.5, atol=1e-15)
+    np.testing.assert_allclose(kumaraswamy_warp(x, [0.4], [1.0]), x ** 0.4, atol=1e-15)
+    w = kumaraswamy_warp(x, [0.7], [1.9])[:, 0]
+    assert w[0] == 0.0 and w[-1] == 1.0 and np.all(np.diff(w) > 0)
+    # outside the unit interval the input is clamped
+    np.testing.assert_array_equal(kumaraswamy_warp(np.array([[-0.2], [1.3]]), [2.0], [0.5])[:, 0], [0.0, 1.0])
+
+
+def test_warped_matern32_posterior_matches_sklearn_on_warped_inputs():
+    X, y, ls = _data(6, m=30, d=4)
+    rng = np.random.default_rng(7)
+    Xc = rng.random((200, 4))
+    a = np.array([0.5, 1.0, 2.0, 1.5])
+    b = np.array([2.0, 0.7, 1.0, 1.2])
+    tau2 = 1e-3
+    gpr = GaussianProcessRegressor(ConstantKernel(0.9, "fixed") * Matern(length_scale=ls, nu=1.5),
+                                   alpha=tau2, optimizer=None, normalize_y=False)
+    # by hand: 1 - (1 - x^a)^b per column
+    Xw = 1 - (1 - X ** a) ** b
+    Xcw = 1 - (1 - Xc ** a) ** b
+    mu_ref, sd_ref = gpr.fit(Xw, y).predict(Xcw, return_std=True)
+    mu, sd = gp_posterior(gp_fit(X, y, ls, 0.9, tau2, kernel="matern32", warp=(a, b)), Xc)
+    np.testing.assert_allclose(mu, mu_ref, rtol=1e-9, atol=1e-10)
+    np.testing.assert_allclose(sd, sd_ref, rtol=1e-7, atol=1e-9)
+    # the warp changes the answer (the test would pass vacuously otherwise)
+    mu0, _ = gp_posterior(gp_fit(X, y, ls, 0.9, tau2, kernel="matern32"), Xc)
+    assert np.max(np.abs(mu0 - mu)) > 1e-3
