@@ -41,6 +41,9 @@ extern "C" {
 
 typedef enum scoot_dtype { SCOOT_F32 = 0, SCOOT_F64 = 1 } scoot_dtype;
 
+/* Covariance of a GP (scoot_gp_fit_ex). */
+typedef enum scoot_kernel { SCOOT_MATERN52 = 0, SCOOT_MATERN32 = 1 } scoot_kernel;
+
 typedef enum scoot_status {
   SCOOT_OK = 0,
   SCOOT_ERR_INVALID_ARG = -1, /* bad shape, null pointer, NaN/Inf host input, q out of range */
@@ -73,6 +76,13 @@ const char* scoot_last_error(void);
  * Fit (host).  Sec. 4.3, Eq. 4-5: K = k(X, X) + tau^2 I with the Matern-5/2
  * ARD covariance k(x, x') = s2 (1 + sqrt5 r + 5 r^2 / 3) exp(-sqrt5 r),
  * r^2 = sum_k ((x_k - x'_k) / l_k)^2; L = chol(K); alpha = K^-1 (y - c).
+ * The _ex calls also take the paper's own covariance (Sec. 4.3): kernel =
+ * SCOOT_MATERN32, k = s2 (1 + sqrt3 r) exp(-sqrt3 r), and input warping:
+ * warp_a, warp_b [d] > 0 (both or neither; NULL = none) put every input
+ * dimension through the Kumaraswamy distribution function
+ * w(x) = 1 - (1 - x^a)^b, x clamped to [0, 1], before the covariance -- for
+ * the observations here and for every candidate in scoot_posterior (and the
+ * calls built on it); the forest mask still sees the raw candidates.
  *
  * scoot_gp_factor_host: host-only arithmetic of the fit, for inspection.
  *   X      [m*d] observed configurations, row-major, finite.
@@ -86,8 +96,9 @@ const char* scoot_last_error(void);
  *
  * scoot_gp_fit: the same fit, then a device-resident GP state (the inverse
  *   factor L^-1 packed for the matrix cores, scaled observations, alpha) on the
- *   current HIP device, uploaded asynchronously on `stream`.  dt selects the
- *   precision of scoot_posterior for this handle.  *out receives the handle.
+ *   current HIP device, uploaded synchronously (`stream` is not used).  dt
+ *   selects the precision of scoot_posterior for this handle.  *out receives
+ *   the handle.
  * ------------------------------------------------------------------------- */
 int scoot_gp_factor_host(const double* X, const double* y, int m, int d, const double* lengthscale,
                          double signal_var, double noise_var, double prior_mean, double* L,
@@ -95,6 +106,12 @@ int scoot_gp_factor_host(const double* X, const double* y, int m, int d, const d
 int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* lengthscale,
                  double signal_var, double noise_var, double prior_mean, scoot_dtype dt,
                  void* stream, scoot_gp* out);
+int scoot_gp_factor_host_ex(const double* X, const double* y, int m, int d, scoot_kernel kernel,
+                            const double* lengthscale, const double* warp_a, const double* warp_b,
+                            double signal_var, double noise_var, double prior_mean, double* L, double* alpha);
+int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel kernel,
+                    const double* lengthscale, const double* warp_a, const double* warp_b, double signal_var,
+                    double noise_var, double prior_mean, scoot_dtype dt, void* stream, scoot_gp* out);
 int scoot_gp_destroy(scoot_gp gp);
 
 /* ---------------------------------------------------------------------------

@@ -14,6 +14,22 @@ from ._native import ScootError, check, lib  # noqa: F401
 
 F32, F64 = 0, 1
 _DT = {"f32": F32, "float32": F32, "f64": F64, "float64": F64}
+MATERN52, MATERN32 = 0, 1
+_KERNEL = {"matern52": MATERN52, "matern32": MATERN32}
+
+
+def _kernel(kernel):
+    return kernel if isinstance(kernel, int) else _KERNEL[kernel]
+
+
+def _warp(warp_a, warp_b, d):
+    if (warp_a is None) != (warp_b is None):
+        raise ValueError("warp_a and warp_b go together")
+    if warp_a is None:
+        return None, None, None, None
+    a, pa = _host(np.asarray(warp_a, dtype=np.float64).reshape(d), np.float64)
+    b, pb = _host(np.asarray(warp_b, dtype=np.float64).reshape(d), np.float64)
+    return a, b, pa, pb
 
 
 def _dt(dtype):
@@ -62,17 +78,19 @@ def abi_version():
 
 
 # --------------------------------------------------------------------------- fit
-def gp_factor_host(X, y, lengthscale, signal_var, noise_var, prior_mean=0.0):
+def gp_factor_host(X, y, lengthscale, signal_var, noise_var, prior_mean=0.0, kernel="matern52", warp_a=None,
+                   warp_b=None):
     """Host fit arithmetic: returns (L, alpha) as float64 arrays."""
     X, pX = _host(X, np.float64)
     y, py = _host(y, np.float64)
     ls, pl = _host(lengthscale, np.float64)
     m, d = X.shape
+    a, b, pa, pb = _warp(warp_a, warp_b, d)
     L = np.zeros((m, m))
     alpha = np.zeros(m)
-    check(lib().scoot_gp_factor_host(pX, py, m, d, pl, signal_var, noise_var, prior_mean,
-                                     L.ctypes.data_as(C.POINTER(C.c_double)),
-                                     alpha.ctypes.data_as(C.POINTER(C.c_double))), "gp_factor_host")
+    check(lib().scoot_gp_factor_host_ex(pX, py, m, d, _kernel(kernel), pl, pa, pb, signal_var, noise_var, prior_mean,
+                                        L.ctypes.data_as(C.POINTER(C.c_double)),
+                                        alpha.ctypes.data_as(C.POINTER(C.c_double))), "gp_factor_host")
     return L, alpha
 
 
@@ -99,15 +117,19 @@ class GP:
             pass
 
 
-def gp_fit(X, y, lengthscale, signal_var, noise_var, prior_mean=0.0, dtype="f32", stream=None):
+def gp_fit(X, y, lengthscale, signal_var, noise_var, prior_mean=0.0, dtype="f32", stream=None, kernel="matern52",
+           warp_a=None, warp_b=None):
+    """Fit on the host, GP state on the device.  kernel: "matern52" or
+    "matern32" (the paper's); warp_a / warp_b: Kumaraswamy input warping."""
     X, pX = _host(X, np.float64)
     y, py = _host(y, np.float64)
     ls, pl = _host(lengthscale, np.float64)
     m, d = X.shape
+    a, b, pa, pb = _warp(warp_a, warp_b, d)
     h = C.c_void_p(0)
     dt = _dt(dtype)
-    check(lib().scoot_gp_fit(pX, py, m, d, pl, signal_var, noise_var, prior_mean, dt, _stream(stream),
-                             C.byref(h)), "gp_fit")
+    check(lib().scoot_gp_fit_ex(pX, py, m, d, _kernel(kernel), pl, pa, pb, signal_var, noise_var, prior_mean, dt,
+                                _stream(stream), C.byref(h)), "gp_fit")
     return GP(h.value, m, d, dt)
 
 

@@ -21,6 +21,10 @@ SIGNATURES = {
     "scoot_last_error": [],
     "scoot_gp_factor_host": [P_dbl, P_dbl, c_int, c_int, P_dbl, c_dbl, c_dbl, c_dbl, P_dbl, P_dbl],
     "scoot_gp_fit": [P_dbl, P_dbl, c_int, c_int, P_dbl, c_dbl, c_dbl, c_dbl, c_int, c_vp, C.POINTER(c_vp)],
+    "scoot_gp_factor_host_ex": [P_dbl, P_dbl, c_int, c_int, c_int, P_dbl, P_dbl, P_dbl, c_dbl, c_dbl, c_dbl,
+                                P_dbl, P_dbl],
+    "scoot_gp_fit_ex": [P_dbl, P_dbl, c_int, c_int, c_int, P_dbl, P_dbl, P_dbl, c_dbl, c_dbl, c_dbl, c_int, c_vp,
+                        C.POINTER(c_vp)],
     "scoot_gp_destroy": [c_vp],
     "scoot_posterior": [c_vp, c_vp, c_i64, c_vp, c_vp, c_vp],
     "scoot_acq_ei": [c_vp, c_vp, c_i64, c_int, c_dbl, c_dbl, c_vp, c_vp],

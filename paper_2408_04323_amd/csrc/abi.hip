@@ -26,7 +26,7 @@ namespace {
 thread_local std::string g_last_error;
 
 constexpr int kMaxDevices = 64;
-constexpr int kScratchSlots = 5;
+constexpr int kScratchSlots = 6;
 constexpr int kStagingSlots = 2;
 
 struct Staging {
@@ -142,13 +142,14 @@ const char* scoot_status_string(int status) {
 
 const char* scoot_last_error(void) { return g_last_error.c_str(); }
 
-int scoot_gp_factor_host(const double* X, const double* y, int m, int d, const double* lengthscale,
-                         double signal_var, double noise_var, double prior_mean, double* L, double* alpha) {
+int scoot_gp_factor_host_ex(const double* X, const double* y, int m, int d, scoot_kernel kernel,
+                            const double* lengthscale, const double* warp_a, const double* warp_b,
+                            double signal_var, double noise_var, double prior_mean, double* L, double* alpha) {
   g_last_error.clear();
   if (!L || !alpha) return fail(SCOOT_ERR_INVALID_ARG, "gp factor: null output");
   try {
     FitHost f;
-    int rc = fit_host(X, y, m, d, lengthscale, signal_var, noise_var, prior_mean, f);
+    int rc = fit_host(X, y, m, d, kernel, lengthscale, warp_a, warp_b, signal_var, noise_var, prior_mean, f);
     if (rc != SCOOT_OK) return rc;
     std::memcpy(L, f.L.data(), sizeof(double) * (size_t)m * m);
     std::memcpy(alpha, f.alpha.data(), sizeof(double) * (size_t)m);
@@ -158,8 +159,21 @@ int scoot_gp_factor_host(const double* X, const double* y, int m, int d, const d
   }
 }
 
+int scoot_gp_factor_host(const double* X, const double* y, int m, int d, const double* lengthscale,
+                         double signal_var, double noise_var, double prior_mean, double* L, double* alpha) {
+  return scoot_gp_factor_host_ex(X, y, m, d, SCOOT_MATERN52, lengthscale, nullptr, nullptr, signal_var, noise_var,
+                                 prior_mean, L, alpha);
+}
+
 int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* lengthscale, double signal_var,
                  double noise_var, double prior_mean, scoot_dtype dt, void* stream, scoot_gp* out) {
+  return scoot_gp_fit_ex(X, y, m, d, SCOOT_MATERN52, lengthscale, nullptr, nullptr, signal_var, noise_var,
+                         prior_mean, dt, stream, out);
+}
+
+int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* lengthscale,
+                    const double* warp_a, const double* warp_b, double signal_var, double noise_var,
+                    double prior_mean, scoot_dtype dt, void* stream, scoot_gp* out) {
   g_last_error.clear();
   (void)stream;
   if (!out) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: null output handle");
@@ -167,7 +181,7 @@ int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* l
   if (!check_dtype(dt)) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: bad dtype");
   try {
     FitHost f;
-    int rc = fit_host(X, y, m, d, lengthscale, signal_var, noise_var, prior_mean, f);
+    int rc = fit_host(X, y, m, d, kernel, lengthscale, warp_a, warp_b, signal_var, noise_var, prior_mean, f);
     if (rc != SCOOT_OK) return rc;
     GPDevice g;
     g.dt = dt;
@@ -183,10 +197,15 @@ int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* l
       g.scale64[k] = k < d ? f.scale[k] : 0.0;
       g.scale32[k] = (float)g.scale64[k];
     }
-    g.coef64[0] = signal_var;
-    g.coef64[1] = signal_var * kLn2;
-    g.coef64[2] = signal_var * kLn2 * kLn2 / 3.0;
-    for (int i = 0; i < 3; ++i) g.coef32[i] = (float)g.coef64[i];
+    for (int i = 0; i < 3; ++i) {
+      g.coef64[i] = f.coef[i];
+      g.coef32[i] = (float)f.coef[i];
+    }
+    g.warp = warp_a != nullptr;
+    for (int k = 0; k < SCOOT_MAX_DIM; ++k) {
+      g.warp_a[k] = g.warp && k < d ? warp_a[k] : 1.0;
+      g.warp_b[k] = g.warp && k < d ? warp_b[k] : 1.0;
+    }
 
     // Host image of the device buffer: [L^-1 packed][scaled observations][alpha][alpha as float].
     std::vector<unsigned char> img;
@@ -211,7 +230,7 @@ int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* l
     for (int i = 0; i < f.m_pad; ++i)
       for (int k = 0; k < kXsStride; ++k) {
         double v = 0.0;
-        if (k < d) v = i < m ? X[(size_t)i * d + k] * f.scale[k] : kPadCoord;
+        if (k < d) v = i < m ? f.Xw[(size_t)i * d + k] * f.scale[k] : kPadCoord;
         unsigned char* at = img.data() + linv_bytes + ((size_t)i * kXsStride + k) * esz;
         if (dt == SCOOT_F32) {
           float fv = (float)v;

@@ -1,6 +1,12 @@
-// Host side of the GP fit (Sec. 4.3, Eq. 4-5): K = k(X, X) + tau^2 I with the
-// Matern-5/2 ARD covariance, its Cholesky factor L, alpha = K^-1 (y - c), and
-// the explicit inverse factor L^-1 that the device applies to k(X, x).
+// Host side of the GP fit (Sec. 4.3, Eq. 4-5): K = k(X, X) + tau^2 I with a
+// Matern ARD covariance (5/2, or the paper's 3/2) on optionally warped inputs,
+// its Cholesky factor L, alpha = K^-1 (y - c), and the explicit inverse factor
+// L^-1 that the device applies to k(X, x).
+//
+// Both covariances are s2 P(u) 2^-u in u = sqrt(2 nu) r log2(e): Matern-5/2
+// has P = 1 + u ln2 + (u ln2)^2 / 3, Matern-3/2 has P = 1 + u ln2, so the
+// device evaluates (coef0 + u (coef1 + u coef2)) 2^-u with per-dimension
+// scales sqrt(2 nu) log2(e) / l_k folded into the coordinates.
 //
 // sigma^2(x) = s2 - ||L^-1 k(X, x)||^2, so the device needs L^-1 (lower
 // triangular).  Applying it as a triangular matrix product instead of a
@@ -16,7 +22,9 @@ namespace scoot {
 
 namespace {
 constexpr double kSqrt5 = 2.23606797749978969641;
+constexpr double kSqrt3 = 1.73205080756887729353;
 constexpr double kLog2e = 1.44269504088896340736;
+constexpr double kLn2 = 0.69314718055994530942;
 
 bool finite_all(const double* v, size_t n) {
   for (size_t i = 0; i < n; ++i)
@@ -25,9 +33,12 @@ bool finite_all(const double* v, size_t n) {
 }
 }  // namespace
 
-int fit_host(const double* X, const double* y, int m, int d, const double* ls, double s2,
-             double tau2, double c, FitHost& f, const double**) {
+int fit_host(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* ls,
+             const double* warp_a, const double* warp_b, double s2, double tau2, double c, FitHost& f) {
   if (!X || !y || !ls) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: null pointer");
+  if (kernel != SCOOT_MATERN52 && kernel != SCOOT_MATERN32) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: bad kernel");
+  if ((warp_a == nullptr) != (warp_b == nullptr))
+    return fail(SCOOT_ERR_INVALID_ARG, "gp fit: warp_a and warp_b go together");
   if (m < 1 || d < 1) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: m and d must be >= 1");
   if (d > SCOOT_MAX_DIM) return fail(SCOOT_ERR_UNSUPPORTED, "gp fit: d exceeds SCOOT_MAX_DIM");
   if (m > SCOOT_MAX_OBS) return fail(SCOOT_ERR_UNSUPPORTED, "gp fit: m exceeds SCOOT_MAX_OBS");
@@ -39,31 +50,50 @@ int fit_host(const double* X, const double* y, int m, int d, const double* ls, d
   if (!(s2 > 0) || !std::isfinite(s2) || !(tau2 >= 0) || !std::isfinite(tau2) || !std::isfinite(c))
     return fail(SCOOT_ERR_INVALID_ARG, "gp fit: bad signal/noise variance or prior mean");
 
+  if (warp_a)
+    for (int k = 0; k < d; ++k)
+      if (!(warp_a[k] > 0) || !(warp_b[k] > 0) || !std::isfinite(warp_a[k]) || !std::isfinite(warp_b[k]))
+        return fail(SCOOT_ERR_INVALID_ARG, "gp fit: warping parameters must be finite and > 0");
+
   f.m = m;
   f.d = d;
+  f.kernel = kernel;
   f.m_pad = (m + kBlk32 - 1) / kBlk32 * kBlk32;
   f.nb = f.m_pad / kBlk32;
   f.s2 = s2;
   f.tau2 = tau2;
   f.c = c;
+  const double root = kernel == SCOOT_MATERN52 ? kSqrt5 : kSqrt3;  // sqrt(2 nu)
+  f.coef[0] = s2;
+  f.coef[1] = s2 * kLn2;
+  f.coef[2] = kernel == SCOOT_MATERN52 ? s2 * kLn2 * kLn2 / 3.0 : 0.0;
   f.scale.assign(d, 0.0);
   std::vector<double> inv_ls(d);
   for (int k = 0; k < d; ++k) {
     inv_ls[k] = 1.0 / ls[k];
-    f.scale[k] = kSqrt5 * kLog2e / ls[k];
+    f.scale[k] = root * kLog2e / ls[k];
+  }
+  f.Xw.assign(X, X + (size_t)m * d);
+  if (warp_a) {
+    f.warp_a.assign(warp_a, warp_a + d);
+    f.warp_b.assign(warp_b, warp_b + d);
+    for (int i = 0; i < m; ++i)
+      for (int k = 0; k < d; ++k) f.Xw[(size_t)i * d + k] = kumaraswamy(X[(size_t)i * d + k], warp_a[k], warp_b[k]);
   }
 
   // K = k(X, X) + tau^2 I (lower triangle is all the factorisation reads).
   std::vector<double> K((size_t)m * m, 0.0);
+  const double* Xw = f.Xw.data();
   for (int i = 0; i < m; ++i) {
     for (int j = 0; j <= i; ++j) {
       double r2 = 0;
       for (int k = 0; k < d; ++k) {
-        double t = (X[(size_t)i * d + k] - X[(size_t)j * d + k]) * inv_ls[k];
+        double t = (Xw[(size_t)i * d + k] - Xw[(size_t)j * d + k]) * inv_ls[k];
         r2 += t * t;
       }
-      double t = kSqrt5 * std::sqrt(r2);
-      double kv = s2 * (1.0 + t + t * t / 3.0) * std::exp(-t);
+      const double t = root * std::sqrt(r2);
+      const double kv = kernel == SCOOT_MATERN52 ? s2 * (1.0 + t + t * t / 3.0) * std::exp(-t)
+                                                 : s2 * (1.0 + t) * std::exp(-t);
       K[(size_t)i * m + j] = kv + (i == j ? tau2 : 0.0);
     }
   }

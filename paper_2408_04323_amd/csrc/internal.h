@@ -2,6 +2,7 @@
 #pragma once
 
 #include <algorithm>
+#include <cmath>
 #include <cstddef>
 #include <cstdint>
 #include <string>
@@ -126,16 +127,30 @@ int fail(int status, const std::string& msg);
 // ---- fit (host) -----------------------------------------------------------
 struct FitHost {
   int m = 0, d = 0, m_pad = 0, nb = 0;     // nb = m_pad / 32
+  scoot_kernel kernel = SCOOT_MATERN52;
   double s2 = 1, tau2 = 0, c = 0;
   std::vector<double> L;                   // m x m row-major lower factor
   std::vector<double> Linv;                // m x m row-major lower inverse factor
   std::vector<double> alpha;               // m
-  std::vector<double> scale;               // d: sqrt5 * log2(e) / l_k
+  std::vector<double> scale;               // d: sqrt(2 nu) * log2(e) / l_k
+  std::vector<double> Xw;                  // m x d observations after input warping (= X without)
+  std::vector<double> warp_a, warp_b;      // d each, empty without warping
+  double coef[3] = {0, 0, 0};              // k = (coef0 + u (coef1 + u coef2)) 2^-u
 };
 
 // Validates and computes K, its Cholesky factor, alpha and L^-1 in fp64.
-int fit_host(const double* X, const double* y, int m, int d, const double* ls, double s2,
-             double tau2, double c, FitHost& out, const double** Xout = nullptr);
+// warp_a / warp_b: both null (no warping) or d positive values each.
+int fit_host(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* ls,
+             const double* warp_a, const double* warp_b, double s2, double tau2, double c, FitHost& out);
+
+// Kumaraswamy input warping of one coordinate, w = 1 - (1 - x^a)^b, x clamped
+// to [0, 1], without cancellation: ln x from log1p(x - 1) above 1/2,
+// 1 - x^a = -expm1(a ln x), w = -expm1(b ln(1 - x^a)).
+SCOOT_HOST_DEVICE inline double kumaraswamy(double x, double a, double b) {
+  x = x < 0.0 ? 0.0 : (x > 1.0 ? 1.0 : x);
+  const double lx = x > 0.5 ? log1p(x - 1.0) : log(x);
+  return -expm1(b * log(-expm1(a * lx)));
+}
 
 // Packs L^-1 into matrix-core A-operand order (see the posterior kernels).
 void pack_linv_f32(const FitHost& f, std::vector<float>& out);
@@ -191,6 +206,9 @@ struct GPDevice {
   double scale64[SCOOT_MAX_DIM];
   float coef32[3];
   double coef64[3];
+  bool warp = false;              // candidates go through kumaraswamy(x, warp_a, warp_b) first
+  double warp_a[SCOOT_MAX_DIM];
+  double warp_b[SCOOT_MAX_DIM];
 };
 
 struct ForestDevice {
@@ -211,9 +229,12 @@ int upload_async(void* dst, const void* src, size_t bytes, int slot, void* strea
 
 // ---- launchers (device) -----------------------------------------------------
 // v_out (nullable, fp32 handles only): V = L^-1 K*^T, m_pad rows of n floats.
+// With input warping (g.warp) the pool is warped first (fp32: into scratch by
+// launch_warp_pool; fp64: inside the kernel), unless xc_warped says Xc already is.
 int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, void* sigma,
                      const double* ei_c /* nullable: fused EI with c = best + xi */, void* ei,
-                     void* stream, float* v_out = nullptr);
+                     void* stream, float* v_out = nullptr, bool xc_warped = false);
+int launch_warp_pool(const GPDevice& g, const float* Xc, int64_t n, float* out, void* stream);
 int launch_ei(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double c, void* ei,
               void* stream);
 int launch_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, scoot_dtype dt,

@@ -82,7 +82,7 @@ namespace {
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
 struct KbLayout {
-  size_t v, mu, sd, acq, elig, votes, idx, score, nvalid, vp, dinv, total;
+  size_t v, mu, sd, acq, elig, votes, idx, score, nvalid, vp, dinv, xw, total;
 };
 
 KbLayout kb_layout(const GPDevice* const* g, int p, int64_t n, int q) {
@@ -110,6 +110,9 @@ KbLayout kb_layout(const GPDevice* const* g, int p, int64_t n, int q) {
   L.nvalid = take(4);
   L.vp = take((size_t)p * rows_max * 4);
   L.dinv = take((size_t)p * 4);
+  size_t xw = 0;  // the pool after each warped GP's input warping
+  for (int j = 0; j < p; ++j) xw += g[j]->warp ? align256((size_t)n * g[j]->d * 4) : 0;
+  L.xw = take(xw);
   L.total = off;
   return L;
 }
@@ -141,6 +144,19 @@ int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f,
   float* dinv = (float*)(w + L.dinv);
   int rows_max = 0;
   for (int j = 0; j < p; ++j) rows_max = std::max(rows_max, g[j]->m_pad + q);
+  // candidates as each GP sees them: warped copies kept for the whole loop
+  const float* xg[SCOOT_MAX_OBJECTIVES];
+  size_t xoff = L.xw;
+  for (int j = 0; j < p; ++j) {
+    xg[j] = Xc;
+    if (g[j]->warp) {
+      float* xw = (float*)(w + xoff);
+      xoff += align256((size_t)n * g[j]->d * 4);
+      int rc = launch_warp_pool(*g[j], Xc, n, xw, stream);
+      if (rc != SCOOT_OK) return rc;
+      xg[j] = xw;
+    }
+  }
 
   // Posterior of every objective, V kept; the feasibility mask is the initial eligibility.
   const void* mus[SCOOT_MAX_OBJECTIVES];
@@ -148,7 +164,8 @@ int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f,
   for (int j = 0; j < p; ++j) {
     mus[j] = mu + (size_t)j * n;
     sds[j] = sd + (size_t)j * n;
-    int rc = launch_posterior(*g[j], Xc, n, mu + (size_t)j * n, sd + (size_t)j * n, nullptr, nullptr, stream, V[j]);
+    int rc = launch_posterior(*g[j], xg[j], n, mu + (size_t)j * n, sd + (size_t)j * n, nullptr, nullptr, stream, V[j],
+                              true);
     if (rc != SCOOT_OK) return rc;
   }
   int rc = f ? launch_forest(*f, Xc, n, vote_min, votes, elig, nullptr, stream) : launch_fill_u8(elig, n, 1, stream);
@@ -198,7 +215,7 @@ int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f,
       a.c2 = g[j]->coef32[2];
       int64_t blocks = (n + kKbThreads - 1) / kKbThreads;
       if (blocks > 8192) blocks = 8192;
-      hipLaunchKernelGGL(kb_update_kernel, dim3((unsigned)blocks), dim3(kKbThreads), 0, s, V[j], vpj, dinv + j, Xc,
+      hipLaunchKernelGGL(kb_update_kernel, dim3((unsigned)blocks), dim3(kKbThreads), 0, s, V[j], vpj, dinv + j, xg[j],
                          sd + (size_t)j * n, a);
     }
     hipLaunchKernelGGL(kb_exclude_kernel, dim3(1), dim3(1), 0, s, elig, pick);

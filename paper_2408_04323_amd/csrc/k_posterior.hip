@@ -316,6 +316,8 @@ struct Post64 {
   double scale[SCOOT_MAX_DIM];
   double c0, c1, c2;
   double s2, prior, ei_c;
+  int warp;  // candidates through kumaraswamy(x, wa, wb) first
+  double wa[SCOOT_MAX_DIM], wb[SCOOT_MAX_DIM];
 };
 
 template <int WAVES, int D4>
@@ -344,7 +346,10 @@ __global__ __launch_bounds__(WAVES * 64) void posterior_f64_kernel(
 #pragma unroll
     for (int k = 0; k < 4 * D4; ++k) xf[k] = Xc[cg * a.d + (k < a.d ? k : a.d - 1)];
 #pragma unroll
-    for (int k = 0; k < 4 * D4; ++k) xc[k] = k < a.d ? (double)xf[k] * a.scale[k] : 0.0;
+    for (int k = 0; k < 4 * D4; ++k) {
+      const double x = a.warp && k < a.d ? kumaraswamy((double)xf[k], a.wa[k], a.wb[k]) : (double)xf[k];
+      xc[k] = k < a.d ? x * a.scale[k] : 0.0;
+    }
   }
 
   // Group G = (J, s2, kk): rows 16J + 8 s2 + 4t + k, t = 0..1, k = 2 kk + h.
@@ -429,6 +434,46 @@ __global__ __launch_bounds__(WAVES * 64) void posterior_f64_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Input warping of the pool (fp32 path): every coordinate through
+// w = 1 - (1 - x^a_k)^b_k, x clamped to [0, 1], in float and without
+// cancellation: ln x from log1p(x - 1) above 1/2 (x - 1 exact there),
+// 1 - x^a = -expm1(a ln x), w = -expm1(b ln(1 - x^a)).  Measured against
+// double: 2e-7 absolute (forming x^a first and subtracting it from 1 loses
+// up to 1.5e-4 near x = 1, where w is steep).  The fp64 path warps in double
+// inside its kernel, by the same steps.
+// ---------------------------------------------------------------------------
+struct WarpArgs {
+  float a[SCOOT_MAX_DIM], b[SCOOT_MAX_DIM];
+};
+
+__global__ __launch_bounds__(256) void warp_pool_kernel(const float* __restrict__ Xc, int64_t total, int d,
+                                                        const WarpArgs w, float* __restrict__ out) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int k = (int)(i % d);
+    const float x = fminf(fmaxf(Xc[i], 0.0f), 1.0f);
+    const float lx = x > 0.5f ? log1pf(x - 1.0f) : logf(x);
+    const float om = -expm1f(w.a[k] * lx);
+    out[i] = -expm1f(w.b[k] * logf(om));
+  }
+}
+
+int launch_warp_pool(const GPDevice& g, const float* Xc, int64_t n, float* out, void* stream) {
+  const int64_t total = n * g.d;
+  if (total == 0) return SCOOT_OK;
+  WarpArgs w{};
+  for (int k = 0; k < SCOOT_MAX_DIM; ++k) {
+    w.a[k] = (float)g.warp_a[k];
+    w.b[k] = (float)g.warp_b[k];
+  }
+  const int64_t blocks = std::min<int64_t>((total + 255) / 256, 8192);
+  hipLaunchKernelGGL(warp_pool_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, Xc, total, g.d,
+                     w, out);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("warp launch: ") + hipGetErrorString(err));
+  return SCOOT_OK;
+}
+
+// ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
 namespace {
@@ -501,11 +546,18 @@ int by_d4(int d4, F&& f) {
 }  // namespace
 
 int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, void* sigma,
-                     const double* ei_c, void* ei, void* stream, float* v_out) {
+                     const double* ei_c, void* ei, void* stream, float* v_out, bool xc_warped) {
   if (n == 0) return SCOOT_OK;
   if (n >= ((int64_t)1 << 37)) return fail(SCOOT_ERR_UNSUPPORTED, "posterior: n too large");
   hipStream_t s = (hipStream_t)stream;
   int rc;
+  if (g.dt == SCOOT_F32 && g.warp && !xc_warped) {
+    float* Xw = (float*)device_scratch((size_t)n * g.d * sizeof(float), 5);
+    if (!Xw) return fail(SCOOT_ERR_NO_MEMORY, "posterior: warped pool allocation failed");
+    rc = launch_warp_pool(g, Xc, n, Xw, stream);
+    if (rc != SCOOT_OK) return rc;
+    Xc = Xw;
+  }
   if (g.dt == SCOOT_F32) {
     Post32 a{};
     a.n = n;
@@ -535,6 +587,11 @@ int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, vo
     Post64 a{};
     a.n = n;
     a.d = g.d;
+    a.warp = g.warp && !xc_warped ? 1 : 0;
+    for (int k = 0; k < SCOOT_MAX_DIM; ++k) {
+      a.wa[k] = g.warp_a[k];
+      a.wb[k] = g.warp_b[k];
+    }
     a.nb16 = g.m_pad / kBlk64;
     for (int k = 0; k < SCOOT_MAX_DIM; ++k) a.scale[k] = g.scale64[k];
     a.c0 = g.coef64[0];

@@ -46,6 +46,26 @@ def test_factor_matches_oracle():
     np.testing.assert_allclose(alpha, f["alpha"], rtol=1e-10, atol=1e-10)
 
 
+def test_factor_matern32_warped_matches_oracle():
+    rng = np.random.default_rng(2)
+    X = rng.random((40, 7))
+    y = rng.standard_normal(40)
+    ls = rng.uniform(0.2, 1.0, 7)
+    a = np.exp(0.5 * rng.standard_normal(7))
+    b = np.exp(0.5 * rng.standard_normal(7))
+    L, alpha = S.gp_factor_host(X, y, ls, 0.8, 1e-3, -0.1, kernel="matern32", warp_a=a, warp_b=b)
+    f = oracle_fit(X, y, ls, 0.8, 1e-3, -0.1, kernel="matern32", warp=(a, b))
+    np.testing.assert_allclose(L, f["L"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(alpha, f["alpha"], rtol=1e-10, atol=1e-10)
+    # Matern-3/2 without warping, too
+    L2, _ = S.gp_factor_host(X, y, ls, 0.8, 1e-3, kernel="matern32")
+    np.testing.assert_allclose(L2, oracle_fit(X, y, ls, 0.8, 1e-3, kernel="matern32")["L"], rtol=0, atol=1e-12)
+    with pytest.raises(S.ScootError):
+        S.gp_factor_host(X, y, ls, 0.8, 1e-3, kernel="matern32", warp_a=a, warp_b=-b)
+    with pytest.raises(ValueError):
+        S.gp_factor_host(X, y, ls, 0.8, 1e-3, warp_a=a)
+
+
 def test_fit_errors():
     X = np.zeros((3, 2))
     with pytest.raises(S.ScootError) as e:

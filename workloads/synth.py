@@ -170,11 +170,14 @@ def make_pool(cfg_id, n=None):
     return _draw(rng, n, c).astype(np.float32)
 
 
-def make_workload(cfg_id, n=None, m=None, with_forest=True):
+def make_workload(cfg_id, n=None, m=None, with_forest=True, kernel="matern52", warp=False):
     """Every input of one scoring pass for workload ``cfg_id``.
 
     ``n`` / ``m`` override the pool size / number of feasible observations
-    (smaller test cases with the same recipe)."""
+    (smaller test cases with the same recipe).  ``kernel`` names the
+    covariance ("matern52" or "matern32"); ``warp`` adds per-objective,
+    per-dimension input-warping parameters (a, b), log-normal around 1
+    (sd 0.5 in the log), drawn from the spare stream."""
     from sklearn.ensemble import RandomForestRegressor
 
     c = dict(CONFIGS[cfg_id])
@@ -212,6 +215,11 @@ def make_workload(cfg_id, n=None, m=None, with_forest=True):
     if p > 1:
         mx, mn = Y.max(axis=0), Y.min(axis=0)
         w["ref"] = mx + 0.1 * (mx - mn)
+    w["kernel"] = kernel
+    if warp:
+        sp = rs["spare"]
+        w["warp"] = ([np.exp(0.5 * sp.standard_normal(d)) for _ in range(p)],
+                     [np.exp(0.5 * sp.standard_normal(d)) for _ in range(p)])
     w["Xc"] = make_pool(cfg_id, n)
     if with_forest:
         seed = int(rs["forest"].integers(0, 2**31 - 1))
