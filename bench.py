@@ -27,7 +27,7 @@ PEAK_FP32_MFMA_TFLOPS = 157.3
 # rocprofv3 FETCH_SIZE / WRITE_SIZE passes (calibrated against a plain copy:
 # FETCH_SIZE x 2.0, WRITE_SIZE x 1.0), valid only for the kernel source they
 # were taken on.
-POSTERIOR_TRAFFIC = {"source_sha1": "ca8d032279fd89590e768d797e6c079dbb920961", "bytes": 14177072}
+POSTERIOR_TRAFFIC = {"source_sha1": "35c7d48b8f1e467bcc0880520bfa984081a2e364", "bytes": 14177024}
 
 
 def posterior_traffic():
