@@ -115,6 +115,33 @@ int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel
 int scoot_gp_destroy(scoot_gp gp);
 
 /* ---------------------------------------------------------------------------
+ * Maximum-likelihood hyperparameters (host, fp64).  Sec. 4.3: SCOOT learns the
+ * noise level tau^2 by maximum likelihood; the lengthscales and the signal
+ * variance are learned with it.  theta [d + 2] = (log l_1 .. log l_d,
+ * log s2, log tau2); X, y, kernel, warp_a/warp_b and prior_mean as in
+ * scoot_gp_fit_ex.
+ *
+ * scoot_gp_nll: nll = 1/2 r^T K^-1 r + 1/2 log det K + m/2 log(2 pi) with
+ *   r = y - prior_mean, K = k_theta(X, X) + tau^2 I, and grad [d + 2]
+ *   (nullable) its gradient in theta.
+ * scoot_gp_mle: minimises nll over the box lower <= theta <= upper ([d + 2]
+ *   each; lower == upper holds a parameter fixed) from the theta given
+ *   (in/out): L-BFGS over theta = lower + (upper - lower) sigmoid(z), so every
+ *   iterate stays inside the box; stops when the gradient in z is below 1e-9,
+ *   the decrease per iteration is below 1e-13 of |nll|, no step decreases
+ *   nll, or after max_iter iterations.  nll (nullable) receives the final
+ *   value, iterations (nullable) the count.  Work per evaluation: a Cholesky
+ *   factorisation and an inverse of the m x m K (about m^3 flops).
+ * Errors: INVALID_ARG, UNSUPPORTED, NOT_PD (K not positive definite at the
+ *   start), NO_MEMORY.
+ * ------------------------------------------------------------------------- */
+int scoot_gp_nll(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+                 const double* warp_b, double prior_mean, const double* theta, double* nll, double* grad);
+int scoot_gp_mle(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+                 const double* warp_b, double prior_mean, const double* lower, const double* upper, int max_iter,
+                 double* theta, double* nll, int* iterations);
+
+/* ---------------------------------------------------------------------------
  * Posterior (device).  Eq. 4 and Eq. 5 of Sec. 4.3 at every candidate:
  *   mu[i]    = c + k(x_i, X) alpha
  *   sigma[i] = sqrt(max(0, s2 - ||L^-1 k(X, x_i)||^2))   (latent f; tau^2 not added)

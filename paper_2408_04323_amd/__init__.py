@@ -133,6 +133,37 @@ def gp_fit(X, y, lengthscale, signal_var, noise_var, prior_mean=0.0, dtype="f32"
     return GP(h.value, m, d, dt)
 
 
+# ---------------------------------------------------- maximum-likelihood fit
+def gp_nll(X, y, theta, kernel="matern52", warp_a=None, warp_b=None, prior_mean=0.0):
+    """(nll, grad) at theta = (log l_1..d, log s2, log tau2)."""
+    X, pX = _host(X, np.float64)
+    y, py = _host(y, np.float64)
+    m, d = X.shape
+    a, b, pa, pb = _warp(warp_a, warp_b, d)
+    th, pt = _host(theta, np.float64)
+    nll = C.c_double(0.0)
+    grad = np.zeros(d + 2)
+    check(lib().scoot_gp_nll(pX, py, m, d, _kernel(kernel), pa, pb, prior_mean, pt, C.byref(nll),
+                             grad.ctypes.data_as(C.POINTER(C.c_double))), "gp_nll")
+    return nll.value, grad
+
+
+def gp_mle(X, y, theta0, lower, upper, kernel="matern52", warp_a=None, warp_b=None, prior_mean=0.0, max_iter=200):
+    """Maximum-likelihood theta in [lower, upper] from theta0.  Returns (theta, nll, iterations)."""
+    X, pX = _host(X, np.float64)
+    y, py = _host(y, np.float64)
+    m, d = X.shape
+    a, b, pa, pb = _warp(warp_a, warp_b, d)
+    th = np.array(theta0, dtype=np.float64).copy()
+    lo, plo = _host(lower, np.float64)
+    hi, phi = _host(upper, np.float64)
+    nll = C.c_double(0.0)
+    it = C.c_int(0)
+    check(lib().scoot_gp_mle(pX, py, m, d, _kernel(kernel), pa, pb, prior_mean, plo, phi, max_iter,
+                             th.ctypes.data_as(C.POINTER(C.c_double)), C.byref(nll), C.byref(it)), "gp_mle")
+    return th, nll.value, it.value
+
+
 # --------------------------------------------------------------------- posterior
 def posterior(gp, Xc, mu=None, sigma=None, stream=None):
     """mu, sigma of the latent f at every row of Xc (n x d float32 device)."""

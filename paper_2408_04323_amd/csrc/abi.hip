@@ -268,6 +268,27 @@ int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel
   }
 }
 
+int scoot_gp_nll(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+                 const double* warp_b, double prior_mean, const double* theta, double* nll, double* grad) {
+  g_last_error.clear();
+  try {
+    return mle_nll(X, y, m, d, kernel, warp_a, warp_b, prior_mean, theta, nll, grad);
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "gp nll: host allocation failed");
+  }
+}
+
+int scoot_gp_mle(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+                 const double* warp_b, double prior_mean, const double* lower, const double* upper, int max_iter,
+                 double* theta, double* nll, int* iterations) {
+  g_last_error.clear();
+  try {
+    return mle_fit(X, y, m, d, kernel, warp_a, warp_b, prior_mean, lower, upper, max_iter, theta, nll, iterations);
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "gp mle: host allocation failed");
+  }
+}
+
 int scoot_gp_destroy(scoot_gp gp) {
   g_last_error.clear();
   if (!gp) return SCOOT_OK;

@@ -152,6 +152,13 @@ SCOOT_HOST_DEVICE inline double kumaraswamy(double x, double a, double b) {
   return -expm1(b * log(-expm1(a * lx)));
 }
 
+// Maximum-likelihood hyperparameters (host_mle.cpp); theta = (log l_1..d, log s2, log tau2).
+int mle_nll(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+            const double* warp_b, double c, const double* theta, double* nll, double* grad);
+int mle_fit(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+            const double* warp_b, double c, const double* lower, const double* upper, int max_iter, double* theta,
+            double* nll, int* iterations);
+
 // Packs L^-1 into matrix-core A-operand order (see the posterior kernels).
 void pack_linv_f32(const FitHost& f, std::vector<float>& out);
 void pack_linv_f64(const FitHost& f, std::vector<double>& out);

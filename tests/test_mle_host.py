@@ -1,0 +1,92 @@
+"""The library's maximum-likelihood fit (host, fp64; Sec. 4.3) against the
+oracle: NLL and gradient at given hyperparameters, and the optimum reached
+from the same start.  No device work."""
+import time
+
+import numpy as np
+import pytest
+
+import paper_2408_04323_amd as S
+from oracle.mle import fit_hyperparameters, nll_and_grad
+from workloads import make_workload
+
+
+def _case(seed, m, d):
+    rng = np.random.default_rng(seed)
+    X = rng.random((m, d))
+    y = np.sin(3 * X[:, 0]) + 0.5 * np.cos(5 * X[:, 1]) + 0.05 * rng.standard_normal(m)
+    return X, (y - y.mean()) / y.std()
+
+
+@pytest.mark.parametrize("kernel", ["matern52", "matern32"])
+@pytest.mark.parametrize("warped", [False, True])
+def test_nll_and_gradient_match_oracle(kernel, warped):
+    X, y = _case(1, 60, 5)
+    rng = np.random.default_rng(2)
+    warp = (np.exp(0.4 * rng.standard_normal(5)), np.exp(0.4 * rng.standard_normal(5))) if warped else None
+    for trial in range(3):
+        theta = np.concatenate([np.log(rng.uniform(0.1, 2.0, 5)), [np.log(rng.uniform(0.3, 3)),
+                                                                  np.log(rng.uniform(1e-4, 0.3))]])
+        nll, g = S.gp_nll(X, y, theta, kernel=kernel, warp_a=None if warp is None else warp[0],
+                          warp_b=None if warp is None else warp[1], prior_mean=0.05)
+        nll_o, g_o = nll_and_grad(theta, X, y, kernel, warp, prior_mean=0.05)
+        assert nll == pytest.approx(nll_o, rel=1e-11, abs=1e-10)
+        np.testing.assert_allclose(g, g_o, rtol=1e-8, atol=1e-8)
+
+
+@pytest.mark.parametrize("kernel", ["matern52", "matern32"])
+def test_fit_reaches_the_oracle_optimum(kernel):
+    X, y = _case(3, 50, 3)
+    theta0 = np.log(np.array([0.5, 0.5, 0.5, 1.0, 0.05]))
+    lo = np.log(np.array([0.02] * 3 + [0.05, 1e-6]))
+    hi = np.log(np.array([10.0] * 3 + [20.0, 1.0]))
+    th, f, it = S.gp_mle(X, y, theta0, lo, hi, kernel=kernel)
+    th_o, f_o = fit_hyperparameters(X, y, theta0, lo, hi, kernel)
+    assert it > 0 and np.all(th >= lo) and np.all(th <= hi)
+    assert f == pytest.approx(nll_and_grad(th, X, y, kernel)[0], rel=1e-12)
+    # The likelihood is not convex, so the two searches may end in different
+    # local minima: the library's must be at least as good as the oracle's,
+    # stationary under the oracle's gradient, and a point the oracle's
+    # optimiser does not leave.
+    assert f <= f_o + 1e-7 * max(1.0, abs(f_o))
+    _, g = nll_and_grad(th, X, y, kernel)
+    interior = (th > lo + 1e-3) & (th < hi - 1e-3)
+    assert np.all(np.abs(g[interior]) < 1e-4)
+    th_2, f_2 = fit_hyperparameters(X, y, th, lo, hi, kernel)
+    assert f_2 == pytest.approx(f, rel=1e-7, abs=1e-7)
+    np.testing.assert_allclose(th_2[interior], th[interior], rtol=0, atol=2e-3)
+
+
+def test_fixed_parameters_and_errors():
+    X, y = _case(4, 30, 2)
+    theta0 = np.log(np.array([0.5, 0.5, 1.0, 0.01]))
+    lo = np.log(np.array([0.02, 0.02, 1.0, 1e-6]))
+    hi = np.log(np.array([10.0, 10.0, 1.0, 1.0]))   # signal variance held at 1
+    th, f, _ = S.gp_mle(X, y, theta0, lo, hi)
+    assert th[2] == 0.0
+    with pytest.raises(S.ScootError):
+        S.gp_mle(X, y, theta0, hi, lo)          # lower > upper
+    with pytest.raises(S.ScootError):
+        S.gp_nll(X, y, np.array([0.0, 0.0, 0.0, np.nan]))
+    with pytest.raises(S.ScootError) as e:      # duplicate inputs and no noise: K singular
+        S.gp_nll(np.vstack([X, X[:1]]), np.concatenate([y, y[:1]]), np.array([0.0, 0.0, 0.0, -60.0]))
+    assert e.value.status == -2
+
+
+def test_fit_on_a_workload_and_its_time():
+    """The two-objective workload's first objective (m = 256, d = 10)."""
+    w = make_workload(3, n=16, with_forest=False)
+    X, y = w["X"], w["Y"][:, 0]
+    d = X.shape[1]
+    theta0 = np.concatenate([np.log(np.full(d, 0.5)), [0.0, np.log(1e-2)]])
+    lo = np.concatenate([np.log(np.full(d, 0.01)), [np.log(0.05), np.log(1e-6)]])
+    hi = np.concatenate([np.log(np.full(d, 20.0)), [np.log(20.0), np.log(1.0)]])
+    t0 = time.perf_counter()
+    th, f, it = S.gp_mle(X, y, theta0, lo, hi, max_iter=300)
+    el = time.perf_counter() - t0
+    print(f"[mle] m={len(X)} d={d}: {it} iterations, nll {f:.6f}, {el:.2f} s")
+    f0, _ = nll_and_grad(theta0, X, y)
+    assert f < f0
+    _, g = nll_and_grad(th, X, y)
+    interior = (th > lo + 1e-3) & (th < hi - 1e-3)
+    assert np.max(np.abs(g[interior])) < 1e-3
