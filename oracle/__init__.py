@@ -14,6 +14,8 @@ Tuning for LLM Inference Engines) and is written for clarity, not speed:
 * ``hypervolume`` -- hypervolume, its improvement and EHVI (Sec. 4.4.2, Eq. 9, Fig. 4)
 * ``forest``      -- random-forest probability of feasibility and the
                      POF >= Delta mask (Sec. 4.7, Eq. 3)
+* ``forest_train``-- training the feasibility forest: exhaustive regression
+                     trees on SplitMix64 bootstrap samples (Sec. 4.7)
 * ``select``      -- top-k parallel suggestion (Sec. 4.6)
 * ``threshold``   -- adaptation of Delta (Algorithm 1, Sec. 4.7)
 * ``believer``    -- sequential Kriging-believer picks (not in the paper; an
