@@ -213,6 +213,39 @@ int scoot_forest_create(const int32_t* feature, const float* threshold, const in
                         const int32_t* right, const int32_t* leaf_q16, const int64_t* tree_offset,
                         int n_trees, int d, scoot_forest* out);
 int scoot_forest_destroy(scoot_forest f);
+
+/* ---------------------------------------------------------------------------
+ * Training the feasibility forest (host; Sec. 4.7: a random forest regressor
+ * on every evaluated configuration, y = 1 ran, 0 crashed).  X [n*d] row-major,
+ * y [n], finite.  Each of the n_trees trees is grown by exhaustive search on
+ * the float32-rounded features: a node splits on the feature and threshold
+ * maximising sum_L^2 / w_L + sum_R^2 / w_R (weighted label sums and weights),
+ * threshold a/2 + b/2 between consecutive distinct values a < b (a if that
+ * rounds up to b); equal scores go to the lower feature, then the lower
+ * threshold; a node is a leaf (value: weighted mean label) at max_depth
+ * (0 .. 64), with fewer than two distinct samples, when its labels are all
+ * equal, or when no split beats the unsplit node.  bootstrap != 0: tree t
+ * trains on draws floor(u n), u = (output t n + j of SplitMix64 from seed,
+ * j = 0 .. n-1) >> 11 over 2^53, each with its multiplicity; otherwise on
+ * every draw once.  All features are considered at every split.
+ *
+ * scoot_forest_train: the trees as flat arrays, nodes in preorder (left child
+ *   first), child indices tree-local, -1 at leaves: feature (-1 at leaves),
+ *   threshold (double), left, right, value (double) [capacity];
+ *   tree_offset [n_trees + 1]; *n_nodes = the node count.  feature == NULL:
+ *   only the count is reported.
+ * scoot_forest_train_create: trains, then scoot_forest_create on the device
+ *   format (thresholds rounded down to float32, leaves round(value * 65536)
+ *   half to even).
+ * Errors: INVALID_ARG (null, non-finite input, bad sizes, capacity below the
+ *   count), UNSUPPORTED (d > SCOOT_MAX_DIM, a tree above 8191 nodes), and
+ *   those of scoot_forest_create.
+ * ------------------------------------------------------------------------- */
+int scoot_forest_train(const double* X, const double* y, int n, int d, int n_trees, int max_depth, uint64_t seed,
+                       int bootstrap, int64_t capacity, int32_t* feature, double* threshold, int32_t* left,
+                       int32_t* right, double* value, int64_t* tree_offset, int64_t* n_nodes);
+int scoot_forest_train_create(const double* X, const double* y, int n, int d, int n_trees, int max_depth,
+                              uint64_t seed, int bootstrap, scoot_forest* out);
 int scoot_vote_threshold(double delta, int n_trees, int64_t* votes_min);
 int scoot_rf_feasibility(scoot_forest f, const float* Xc, int64_t n, double delta, int32_t* votes,
                          uint8_t* mask, int32_t* leaf_idx, void* stream);

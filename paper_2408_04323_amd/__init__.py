@@ -262,6 +262,36 @@ def forest_create(feature, threshold, left, right, leaf_q16, tree_offset, d):
     return Forest(h.value, T, d)
 
 
+def forest_train(X, y, n_trees, max_depth, seed, bootstrap=True):
+    """Host training; returns the flat arrays (feature, threshold, left, right, value, tree_offset)."""
+    X, pX = _host(X, np.float64)
+    y, py = _host(y, np.float64)
+    n, d = X.shape
+    cnt = C.c_int64(0)
+    s = C.c_uint64(seed & (2 ** 64 - 1))
+    check(lib().scoot_forest_train(pX, py, n, d, n_trees, max_depth, s, int(bool(bootstrap)), 0, None, None, None,
+                                   None, None, None, C.byref(cnt)), "forest_train")
+    k = cnt.value
+    out = dict(feature=np.zeros(k, np.int32), threshold=np.zeros(k), left=np.zeros(k, np.int32),
+               right=np.zeros(k, np.int32), value=np.zeros(k), tree_offset=np.zeros(n_trees + 1, np.int64))
+    ptr = {k2: v.ctypes.data_as(C.POINTER(np.ctypeslib.as_ctypes_type(v.dtype))) for k2, v in out.items()}
+    check(lib().scoot_forest_train(pX, py, n, d, n_trees, max_depth, s, int(bool(bootstrap)), k, ptr["feature"],
+                                   ptr["threshold"], ptr["left"], ptr["right"], ptr["value"], ptr["tree_offset"],
+                                   C.byref(cnt)), "forest_train")
+    return out
+
+
+def forest_train_create(X, y, n_trees, max_depth, seed, bootstrap=True):
+    """Host training straight into a device forest handle."""
+    X, pX = _host(X, np.float64)
+    y, py = _host(y, np.float64)
+    n, d = X.shape
+    h = C.c_void_p(0)
+    check(lib().scoot_forest_train_create(pX, py, n, d, n_trees, max_depth, C.c_uint64(seed & (2 ** 64 - 1)),
+                                          int(bool(bootstrap)), C.byref(h)), "forest_train_create")
+    return Forest(h.value, n_trees, d)
+
+
 def vote_threshold(delta, n_trees):
     v = C.c_int64(0)
     check(lib().scoot_vote_threshold(delta, n_trees, C.byref(v)), "vote_threshold")

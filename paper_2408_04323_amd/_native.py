@@ -35,6 +35,9 @@ SIGNATURES = {
     "scoot_acq_ehvi": [C.POINTER(c_vp), C.POINTER(c_vp), c_int, c_i64, c_int, P_dbl, c_int, P_dbl, c_vp, c_vp],
     "scoot_forest_create": [P_i32, P_f32, P_i32, P_i32, P_i32, P_i64, c_int, c_int, C.POINTER(c_vp)],
     "scoot_forest_destroy": [c_vp],
+    "scoot_forest_train": [P_dbl, P_dbl, c_int, c_int, c_int, c_int, C.c_uint64, c_int, c_i64, P_i32, P_dbl, P_i32,
+                           P_i32, P_dbl, P_i64, P_i64],
+    "scoot_forest_train_create": [P_dbl, P_dbl, c_int, c_int, c_int, c_int, C.c_uint64, c_int, C.POINTER(c_vp)],
     "scoot_vote_threshold": [c_dbl, c_int, P_i64],
     "scoot_rf_feasibility": [c_vp, c_vp, c_i64, c_dbl, c_vp, c_vp, c_vp, c_vp],
     "scoot_suggest_topq": [c_vp, c_vp, c_i64, c_int, c_int, c_vp, c_vp, c_vp, c_vp],

@@ -391,6 +391,65 @@ int scoot_forest_create(const int32_t* feature, const float* threshold, const in
   }
 }
 
+int scoot_forest_train(const double* X, const double* y, int n, int d, int n_trees, int max_depth, uint64_t seed,
+                       int bootstrap, int64_t capacity, int32_t* feature, double* threshold, int32_t* left,
+                       int32_t* right, double* value, int64_t* tree_offset, int64_t* n_nodes) {
+  g_last_error.clear();
+  if (!n_nodes) return fail(SCOOT_ERR_INVALID_ARG, "forest train: null n_nodes");
+  try {
+    TrainedForest tf;
+    int rc = train_forest_host(X, y, n, d, n_trees, max_depth, seed, bootstrap != 0, tf);
+    if (rc != SCOOT_OK) return rc;
+    const int64_t total = (int64_t)tf.feature.size();
+    *n_nodes = total;
+    if (!feature) return SCOOT_OK;  // size query
+    if (!threshold || !left || !right || !value || !tree_offset)
+      return fail(SCOOT_ERR_INVALID_ARG, "forest train: null output array");
+    if (capacity < total) return fail(SCOOT_ERR_INVALID_ARG, "forest train: capacity below the node count");
+    std::memcpy(feature, tf.feature.data(), sizeof(int32_t) * total);
+    std::memcpy(threshold, tf.threshold.data(), sizeof(double) * total);
+    std::memcpy(left, tf.left.data(), sizeof(int32_t) * total);
+    std::memcpy(right, tf.right.data(), sizeof(int32_t) * total);
+    std::memcpy(value, tf.value.data(), sizeof(double) * total);
+    std::memcpy(tree_offset, tf.tree_offset.data(), sizeof(int64_t) * (n_trees + 1));
+    return SCOOT_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "forest train: host allocation failed");
+  }
+}
+
+int scoot_forest_train_create(const double* X, const double* y, int n, int d, int n_trees, int max_depth,
+                              uint64_t seed, int bootstrap, scoot_forest* out) {
+  g_last_error.clear();
+  if (!out) return fail(SCOOT_ERR_INVALID_ARG, "forest train: null output handle");
+  *out = nullptr;
+  try {
+    TrainedForest tf;
+    int rc = train_forest_host(X, y, n, d, n_trees, max_depth, seed, bootstrap != 0, tf);
+    if (rc != SCOOT_OK) return rc;
+    // device format: thresholds rounded down to float32 (x <= t keeps its
+    // decision for every float32 x), leaf values in Q16 (half to even)
+    const size_t total = tf.feature.size();
+    std::vector<int32_t> feat(total), q16(total, 0);
+    std::vector<float> thr(total, 0.0f);
+    for (size_t k = 0; k < total; ++k) {
+      const bool leaf = tf.left[k] < 0;
+      feat[k] = leaf ? 0 : tf.feature[k];
+      if (!leaf) {
+        float t32 = (float)tf.threshold[k];
+        if ((double)t32 > tf.threshold[k]) t32 = std::nextafter(t32, -INFINITY);
+        thr[k] = t32;
+      } else {
+        q16[k] = (int32_t)std::nearbyint(tf.value[k] * 65536.0);
+      }
+    }
+    return scoot_forest_create(feat.data(), thr.data(), tf.left.data(), tf.right.data(), q16.data(),
+                               tf.tree_offset.data(), n_trees, d, out);
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "forest train: host allocation failed");
+  }
+}
+
 int scoot_forest_destroy(scoot_forest f) {
   g_last_error.clear();
   if (!f) return SCOOT_OK;

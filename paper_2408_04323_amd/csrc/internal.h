@@ -159,6 +159,15 @@ int mle_fit(const double* X, const double* y, int m, int d, scoot_kernel kernel,
             const double* warp_b, double c, const double* lower, const double* upper, int max_iter, double* theta,
             double* nll, int* iterations);
 
+// Forest training (host_forest_train.cpp): tree-local child indices, preorder.
+struct TrainedForest {
+  std::vector<int32_t> feature, left, right;  // feature -1 at leaves
+  std::vector<double> threshold, value;       // value: the node's weighted mean label
+  std::vector<int64_t> tree_offset;           // n_trees + 1
+};
+int train_forest_host(const double* X, const double* y, int n, int d, int n_trees, int max_depth, uint64_t seed,
+                      bool bootstrap, TrainedForest& out);
+
 // Packs L^-1 into matrix-core A-operand order (see the posterior kernels).
 void pack_linv_f32(const FitHost& f, std::vector<float>& out);
 void pack_linv_f64(const FitHost& f, std::vector<double>& out);

@@ -438,3 +438,30 @@ def test_believer_shortfall_and_workspace():
     p3, _ = S.suggest_kb(gps, f, Xc, 4, w["Y"], w["ref"], delta=1.0)
     mask = feasibility_mask(forest_votes(w["forest"], w["Xc"]), 1.0, len(w["forest"]["tree_offset"]) - 1)
     assert len(p3) == min(4, int(mask.sum()))
+
+
+def _device_format(tf):
+    """Oracle-trained trees in the loader's format: thresholds rounded down to
+    float32, leaves as round-half-even Q16 (reading 10)."""
+    t64 = tf["threshold"]
+    t32 = t64.astype(np.float32)
+    up = t32.astype(np.float64) > t64
+    t32[up] = np.nextafter(t32[up], np.float32(-np.inf))
+    leaf = tf["left"] < 0
+    return dict(feature=np.where(leaf, 0, tf["feature"]).astype(np.int32), threshold=np.where(leaf, 0, t32).astype(
+        np.float32), left=tf["left"], right=tf["right"],
+        leaf_q16=np.where(leaf, np.rint(tf["value"] * 65536.0), 0).astype(np.int32), tree_offset=tf["tree_offset"])
+
+
+@pytest.mark.parametrize("cfg,T,depth", [(1, 16, 6), (2, 24, 10)])
+def test_trained_forest_votes_bitexact(cfg, T, depth):
+    from oracle.forest_train import train_forest
+    w = wl(cfg, 8192 + 11)
+    say("forest train + mask", cfg, T, depth)
+    f = S.forest_train_create(w["X_draws"], w["feasible_draws"], T, depth, seed=99)
+    votes, mask, _ = S.rf_feasibility(f, dev(w["Xc"]), w["delta"])
+    torch.cuda.synchronize()
+    fo = _device_format(train_forest(w["X_draws"], w["feasible_draws"], T, depth, seed=99))
+    want = forest_votes(fo, w["Xc"])
+    np.testing.assert_array_equal(votes.cpu().numpy(), want)
+    np.testing.assert_array_equal(mask.cpu().numpy(), feasibility_mask(want, w["delta"], T))
