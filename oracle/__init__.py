@@ -21,6 +21,8 @@ Tuning for LLM Inference Engines) and is written for clarity, not speed:
 * ``believer``    -- sequential Kriging-believer picks (not in the paper; an
                      extension of the parallel suggestion of Sec. 4.6)
 * ``mle``         -- maximum-likelihood GP hyperparameters (Sec. 4.3)
+* ``sobol``       -- candidate generation: Sobol pool on the space's grids, known
+                     constraints (Sec. 4.5.3, 4.7, Algorithm 1)
 * ``mace``        -- MACE for one objective: UCB, PI, EI (Eq. 6-8), their Pareto
                      front over the pool and a seeded random pick (Sec. 4.5.1, 4.6)
 * ``pipeline``    -- the whole scoring pass over a candidate pool

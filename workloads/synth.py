@@ -162,6 +162,24 @@ def export_forest(model):
                 leaf_q16=np.concatenate(leaf), tree_offset=np.array(off, dtype=np.int64))
 
 
+def levels(c):
+    """Per dimension: 0 continuous, 1 boolean, L >= 2 an integer grid of L levels."""
+    return [0] * c["d_cont"] + [c["int_levels"]] * c["d_int"] + [1] * c["d_bool"]
+
+
+def sobol_table(d):
+    """Primitive polynomials and initial direction numbers of the first d
+    Sobol dimensions: the Joe-Kuo table (new-joe-kuo-6.21201) as scipy ships
+    it, read with numpy's loader (no pickles).  An input of the method, like a
+    seed: both the generator and its check receive it from here."""
+    import glob
+    import os
+    import scipy
+    f = glob.glob(os.path.join(os.path.dirname(scipy.__file__), "stats", "_sobol_direction_numbers.npz"))[0]
+    z = np.load(f, allow_pickle=False)
+    return z["poly"][:d].astype(np.int64), z["vinit"][:d].astype(np.int64)
+
+
 def make_pool(cfg_id, n=None):
     """The candidate pool alone: (n, d) float32, grid-snapped."""
     c = CONFIGS[cfg_id]
