@@ -59,6 +59,8 @@ typedef enum scoot_status {
 #define SCOOT_MAX_OBJECTIVES 3  /* p */
 #define SCOOT_MAX_Q 64          /* q: picks per suggestion */
 #define SCOOT_MAX_TREES 32767   /* T: trees per forest (votes fit int32) */
+#define SCOOT_MAX_CONSTRAINTS 8 /* r: known-constraint rows */
+#define SCOOT_SOBOL_MAX_DEGREE 18 /* degree of a Sobol dimension's polynomial; vinit row stride */
 
 typedef struct scoot_gp_t* scoot_gp;
 typedef struct scoot_forest_t* scoot_forest;
@@ -285,6 +287,14 @@ int scoot_score_pool(const scoot_gp* gps, int p, scoot_forest f, const float* Xc
                      double best_y, double xi, const double* Y_obs, int m_obs, const double* ref,
                      double delta, int q, void* mu, void* sigma, void* acq, int32_t* votes,
                      uint8_t* mask, int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
+/* As scoot_score_pool, with the known-constraint mask of the pool (known [n]
+ * u8 device, nullable = every candidate admissible, e.g. from scoot_sobol_pool
+ * or scoot_known_constraints) folded into the mask: mask[i] = feasible and
+ * known[i] != 0. */
+int scoot_score_pool_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_t* known, const float* Xc,
+                        int64_t n, double best_y, double xi, const double* Y_obs, int m_obs, const double* ref,
+                        double delta, int q, void* mu, void* sigma, void* acq, int32_t* votes, uint8_t* mask,
+                        int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Sequential Kriging-believer suggestion of q candidates, an extension of the
@@ -309,6 +319,12 @@ int scoot_suggest_kb_workspace(const scoot_gp* gps, int p, int64_t n, int q, uin
 int scoot_suggest_kb(const scoot_gp* gps, int p, scoot_forest f, const float* Xc, int64_t n,
                      const double* Y_obs, int m_obs, const double* ref, double delta, int q, void* workspace,
                      uint64_t workspace_bytes, int64_t* picks, double* pick_acq, int* n_picked, void* stream);
+/* As scoot_suggest_kb; known [n] u8 device (nullable) restricts the
+ * eligible candidates to the admissible ones, as in scoot_score_pool_ex. */
+int scoot_suggest_kb_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_t* known, const float* Xc,
+                        int64_t n, const double* Y_obs, int m_obs, const double* ref, double delta, int q,
+                        void* workspace, uint64_t workspace_bytes, int64_t* picks, double* pick_acq, int* n_picked,
+                        void* stream);
 
 /* ---------------------------------------------------------------------------
  * MACE suggestion for one objective (Sec. 4.5.1: UCB, PI and EI, their Pareto
@@ -361,6 +377,53 @@ int scoot_suggest_mace(scoot_gp gp, scoot_forest f, const float* Xc, int64_t n, 
                        double beta, double delta, uint64_t seed, int q, void* mu, void* sigma, void* ucb,
                        void* pi, void* ei, int32_t* votes, uint8_t* mask, uint8_t* front, int64_t* idx,
                        int32_t* n_front, void* stream);
+/* As scoot_suggest_mace; known [n] u8 device (nullable) is ANDed into the
+ * mask, as in scoot_score_pool_ex. */
+int scoot_suggest_mace_ex(scoot_gp gp, scoot_forest f, const uint8_t* known, const float* Xc, int64_t n,
+                          double best_y, double xi, double beta, double delta, uint64_t seed, int q, void* mu,
+                          void* sigma, void* ucb, void* pi, void* ei, int32_t* votes, uint8_t* mask,
+                          uint8_t* front, int64_t* idx, int32_t* n_front, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Candidate generation and known constraints (Sec. 4.5.3: the optimiser's
+ * space is pruned by constraints known in advance, listed per engine in the
+ * appendix; Sec. 4.7: a shortfall of suggestions is filled with Sobol points;
+ * Sec. 4.1 and Algorithm 1: the first observations are Sobol points).
+ *
+ * scoot_sobol_pool (device): rows i = 0..n-1 of Xc [n*d] float32 are Sobol
+ *   points skip + i (Bratley-Fox direction numbers, Gray-code order, 32-bit:
+ *   coordinate j of point t is the XOR of V_j[k] over the set bits k of
+ *   t ^ (t >> 1), over 2^32) rounded to the space's grids: levels[j] = 0
+ *   continuous, 1 boolean (1 when the coordinate is >= 1/2), L >= 2 the grid
+ *   k / (L - 1) (rint in double, half to even), then stored as float32.
+ *   Dimension j is given by poly[j], the primitive polynomial over GF(2) as
+ *   the integer whose bit t is the coefficient of x^t (1 = degree 0, the van
+ *   der Corput sequence), and its initial direction numbers m_1..m_s (s the
+ *   degree) in vinit[j * SCOOT_SOBOL_MAX_DEGREE + 0 .. s-1], each odd and
+ *   below 2^k (e.g. the Joe-Kuo table; the rest of the row is not read).
+ *   known [n] u8 device (nullable) = the admissibility of each row under the
+ *   constraints (A, b, r) as scoot_known_constraints defines it, computed in
+ *   the same pass.  poly, vinit, levels, A, b: host.  1 <= d <=
+ *   SCOOT_MAX_DIM, 0 <= r <= SCOOT_MAX_CONSTRAINTS, skip >= 0, n >= 0,
+ *   skip + n <= 2^32.
+ *
+ * scoot_known_constraints (device): known[i] = 1 when every row r of the
+ *   linear constraints holds for row i of Xc [n*d] float32: sum over k = 0..d-1
+ *   in order of A[r*d + k] * x_k, in double, each product and each partial sum
+ *   rounded on its own, <= b[r]; else 0 (NaN inputs: 0).  A [r*d] and b [r]
+ *   host, finite A, b not NaN.  Every rule the paper lists is such a row over
+ *   the normalised knobs: an order between two knobs (x_a - x_b <= 0), "not
+ *   both" booleans (x_a + x_b <= 1), "a implies b" (x_a - x_b <= 0), a bound
+ *   that holds unless a boolean is set (big-M: c - x_a - M x_b <= 0).
+ *
+ * Errors: INVALID_ARG (null pointer, d out of range, negative level, bad
+ * polynomial or initial number, non-finite A, NaN b, bad skip/n), UNSUPPORTED
+ * (r or the polynomial degree beyond the limits), DEVICE.
+ * ------------------------------------------------------------------------- */
+int scoot_sobol_pool(const uint32_t* poly, const uint32_t* vinit, int d, const int32_t* levels, int64_t skip,
+                     int64_t n, const double* A, const double* b, int r, float* Xc, uint8_t* known, void* stream);
+int scoot_known_constraints(const float* Xc, int64_t n, int d, const double* A, const double* b, int r,
+                            uint8_t* known, void* stream);
 
 #ifdef __cplusplus
 }

@@ -1,8 +1,8 @@
 """Candidate generation: a Sobol quasi-Monte Carlo pool with the search
 space's grids, and the known constraints (Sec. 4.5.3: the solver's space is
 pruned by known constraints; Sec. 4.7: a shortfall of suggestions is filled
-with Sobol points; Algorithm 1: the initial observations are a uniform
-sample).
+with Sobol points; Sec. 4.1 and Algorithm 1: the first observations are
+Sobol points).
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 

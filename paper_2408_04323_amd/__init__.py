@@ -352,12 +352,15 @@ class PoolBuffers:
 
 
 def score_pool(gps, forest, Xc, q, best_y=0.0, xi=1e-4, Y_obs=None, ref=None, delta=0.5, buffers=None,
-               stream=None):
-    """One whole pass: posterior per GP, EI (one GP) or EHVI, forest mask, top-q."""
+               stream=None, known=None):
+    """One whole pass: posterior per GP, EI (one GP) or EHVI, forest mask
+    (ANDed with the known-constraint mask ``known`` when given), top-q."""
     import torch
     p = len(gps)
     n = Xc.shape[0]
     _require_device(Xc, "Xc", torch.float32, n * gps[0].d)
+    if known is not None:
+        _require_device(known, "known", torch.uint8, n)
     b = PoolBuffers(n, p, q, gps[0].dtype, Xc.device) if buffers is None else buffers
     hs = (C.c_void_p * p)(*[g.handle.value for g in gps])
     if p > 1:
@@ -366,8 +369,8 @@ def score_pool(gps, forest, Xc, q, best_y=0.0, xi=1e-4, Y_obs=None, ref=None, de
         m_obs = Y.reshape(-1, p).shape[0]
     else:
         pY, pr, m_obs = None, None, 0
-    check(lib().scoot_score_pool(hs, p, forest.handle if forest is not None else None, _dptr(Xc), n, best_y, xi,
-                                 pY, m_obs, pr, delta, q, _dptr(b.mu), _dptr(b.sigma), _dptr(b.acq),
+    check(lib().scoot_score_pool_ex(hs, p, forest.handle if forest is not None else None, _dptr(known), _dptr(Xc),
+                                    n, best_y, xi, pY, m_obs, pr, delta, q, _dptr(b.mu), _dptr(b.sigma), _dptr(b.acq),
                                  _dptr(b.votes), _dptr(b.mask), _dptr(b.idx), _dptr(b.score), _dptr(b.n_valid),
                                  _stream(stream)), "score_pool")
     return b
@@ -381,12 +384,16 @@ def suggest_kb_workspace(gps, n, q):
     return b.value
 
 
-def suggest_kb(gps, forest, Xc, q, Y_obs, ref, delta=0.5, workspace=None, stream=None):
-    """Sequential Kriging-believer picks.  Returns (picks int64 (k,), EHVI at each pick (k,))."""
+def suggest_kb(gps, forest, Xc, q, Y_obs, ref, delta=0.5, workspace=None, stream=None, known=None):
+    """Sequential Kriging-believer picks among the feasible (and, with
+    ``known``, admissible) candidates.  Returns (picks int64 (k,), EHVI at
+    each pick (k,))."""
     import torch
     p = len(gps)
     n = Xc.shape[0]
     _require_device(Xc, "Xc", torch.float32, n * gps[0].d)
+    if known is not None:
+        _require_device(known, "known", torch.uint8, n)
     hs = (C.c_void_p * p)(*[g.handle.value for g in gps])
     r, pr = _host(ref, np.float64)
     Y, pY = _host(np.asarray(Y_obs, dtype=np.float64).reshape(-1, p), np.float64)
@@ -394,7 +401,8 @@ def suggest_kb(gps, forest, Xc, q, Y_obs, ref, delta=0.5, workspace=None, stream
     acq = np.full(q, np.nan)
     k = C.c_int(0)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    check(lib().scoot_suggest_kb(hs, p, forest.handle if forest is not None else None, _dptr(Xc), n, pY, Y.shape[0],
+    check(lib().scoot_suggest_kb_ex(hs, p, forest.handle if forest is not None else None, _dptr(known), _dptr(Xc), n,
+                                    pY, Y.shape[0],
                                  pr, delta, q, _dptr(workspace), ws_bytes,
                                  picks.ctypes.data_as(C.POINTER(C.c_int64)),
                                  acq.ctypes.data_as(C.POINTER(C.c_double)), C.byref(k), _stream(stream)),
@@ -467,15 +475,89 @@ class MaceBuffers:
         self.n_front = torch.empty(1, dtype=torch.int32, device=device)
 
 
-def suggest_mace(gp, forest, Xc, q, best_y, beta, seed, xi=1e-4, delta=0.5, buffers=None, stream=None):
-    """Posterior, (ucb, pi, ei), forest mask, their Pareto front, q drawn from it."""
+def suggest_mace(gp, forest, Xc, q, best_y, beta, seed, xi=1e-4, delta=0.5, buffers=None, stream=None,
+                 known=None):
+    """Posterior, (ucb, pi, ei), forest mask (ANDed with ``known`` when
+    given), their Pareto front, q drawn from it."""
     import torch
     n = Xc.shape[0]
     _require_device(Xc, "Xc", torch.float32, n * gp.d)
+    if known is not None:
+        _require_device(known, "known", torch.uint8, n)
     b = MaceBuffers(n, q, gp.dtype, Xc.device) if buffers is None else buffers
-    check(lib().scoot_suggest_mace(gp.handle, forest.handle if forest is not None else None, _dptr(Xc), n, best_y,
-                                   xi, beta, delta, C.c_uint64(seed & (2 ** 64 - 1)), q, _dptr(b.mu),
+    check(lib().scoot_suggest_mace_ex(gp.handle, forest.handle if forest is not None else None, _dptr(known),
+                                      _dptr(Xc), n, best_y, xi, beta, delta, C.c_uint64(seed & (2 ** 64 - 1)), q, _dptr(b.mu),
                                    _dptr(b.sigma), _dptr(b.ucb), _dptr(b.pi), _dptr(b.ei), _dptr(b.votes),
                                    _dptr(b.mask), _dptr(b.front), _dptr(b.idx), _dptr(b.n_front), _stream(stream)),
           "suggest_mace")
     return b
+
+
+# ------------------------------------------------------- candidate generation
+SOBOL_MAX_DEGREE = 18
+
+
+def _sobol_inputs(poly, vinit, levels):
+    poly = np.ascontiguousarray(np.asarray(poly, dtype=np.int64).ravel())
+    d = poly.size
+    if np.any(poly < 1) or np.any(poly >= 2 ** 32):
+        raise ValueError("sobol: polynomials must be positive 32-bit integers")
+    vi = np.zeros((d, SOBOL_MAX_DEGREE), dtype=np.uint32)
+    v = np.asarray(vinit, dtype=np.int64).reshape(d, -1)
+    k = min(v.shape[1], SOBOL_MAX_DEGREE)
+    if np.any(v[:, :k] < 0) or np.any(v[:, :k] >= 2 ** 32):
+        raise ValueError("sobol: initial direction numbers must be 32-bit")
+    vi[:, :k] = v[:, :k]
+    lv = np.ascontiguousarray(np.asarray(levels, dtype=np.int32).ravel())
+    if lv.size != d:
+        raise ValueError("sobol: one level count per dimension")
+    return np.ascontiguousarray(poly.astype(np.uint32)), vi, lv, d
+
+
+def _constraint_inputs(A, b, d):
+    if A is None:
+        return None, None, 0
+    A = np.ascontiguousarray(np.asarray(A, dtype=np.float64).reshape(-1, d))
+    b = np.ascontiguousarray(np.asarray(b, dtype=np.float64).ravel())
+    if b.size != A.shape[0]:
+        raise ValueError("known constraints: one bound per row")
+    return A, b, A.shape[0]
+
+
+def sobol_pool(poly, vinit, levels, n, skip=0, A=None, b=None, device="cuda", out=None, known=None,
+               with_known=None, stream=None):
+    """Sobol points skip .. skip + n - 1 on the grids ``levels`` as a float32
+    (n, d) device tensor, and (when constraints A x <= b are given, or
+    with_known) their admissibility mask.  Returns (Xc, known or None)."""
+    import torch
+    pu, vi, lv, d = _sobol_inputs(poly, vinit, levels)
+    A, bb, r = _constraint_inputs(A, b, d)
+    Xc = torch.empty((n, d), dtype=torch.float32, device=device) if out is None else out
+    _require_device(Xc, "Xc", torch.float32, n * d)
+    if with_known is None:
+        with_known = r > 0 or known is not None
+    if with_known and known is None:
+        known = torch.empty(n, dtype=torch.uint8, device=Xc.device)
+    if known is not None:
+        _require_device(known, "known", torch.uint8, n)
+    pA = A.ctypes.data_as(C.POINTER(C.c_double)) if r else None
+    pb = bb.ctypes.data_as(C.POINTER(C.c_double)) if r else None
+    check(lib().scoot_sobol_pool(pu.ctypes.data_as(C.POINTER(C.c_uint32)), vi.ctypes.data_as(C.POINTER(C.c_uint32)),
+                                 d, lv.ctypes.data_as(C.POINTER(C.c_int32)), int(skip), int(n), pA, pb, r, _dptr(Xc),
+                                 _dptr(known), _stream(stream)), "sobol_pool")
+    return Xc, known
+
+
+def known_constraints(Xc, A, b, out=None, stream=None):
+    """uint8 (n,) device mask: 1 where every row of A x <= b holds."""
+    import torch
+    n, d = Xc.shape
+    _require_device(Xc, "Xc", torch.float32, n * d)
+    A, bb, r = _constraint_inputs(A, b, d)
+    known = torch.empty(n, dtype=torch.uint8, device=Xc.device) if out is None else out
+    _require_device(known, "known", torch.uint8, n)
+    pA = A.ctypes.data_as(C.POINTER(C.c_double)) if r else None
+    pb = bb.ctypes.data_as(C.POINTER(C.c_double)) if r else None
+    check(lib().scoot_known_constraints(_dptr(Xc), n, d, pA, pb, r, _dptr(known), _stream(stream)),
+          "known_constraints")
+    return known

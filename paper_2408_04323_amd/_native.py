@@ -12,7 +12,7 @@ _lib = None
 
 c_int, c_i64, c_dbl, c_vp = C.c_int, C.c_int64, C.c_double, C.c_void_p
 P_dbl, P_int, P_i64 = C.POINTER(C.c_double), C.POINTER(C.c_int), C.POINTER(C.c_int64)
-P_i32, P_f32 = C.POINTER(C.c_int32), C.POINTER(C.c_float)
+P_i32, P_f32, P_u32 = C.POINTER(C.c_int32), C.POINTER(C.c_float), C.POINTER(C.c_uint32)
 
 # name -> argtypes (every function returns int)
 SIGNATURES = {
@@ -53,6 +53,14 @@ SIGNATURES = {
     "scoot_random_pick": [c_vp, c_i64, C.c_uint64, c_int, c_vp, c_vp, c_vp],
     "scoot_suggest_mace": [c_vp, c_vp, c_vp, c_i64, c_dbl, c_dbl, c_dbl, c_dbl, C.c_uint64, c_int, c_vp, c_vp,
                            c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp],
+    "scoot_score_pool_ex": [C.POINTER(c_vp), c_int, c_vp, c_vp, c_vp, c_i64, c_dbl, c_dbl, P_dbl, c_int, P_dbl,
+                            c_dbl, c_int, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp],
+    "scoot_suggest_kb_ex": [C.POINTER(c_vp), c_int, c_vp, c_vp, c_vp, c_i64, P_dbl, c_int, P_dbl, c_dbl, c_int, c_vp,
+                            C.c_uint64, P_i64, P_dbl, P_int, c_vp],
+    "scoot_suggest_mace_ex": [c_vp, c_vp, c_vp, c_vp, c_i64, c_dbl, c_dbl, c_dbl, c_dbl, C.c_uint64, c_int, c_vp,
+                              c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp],
+    "scoot_sobol_pool": [P_u32, P_u32, c_int, P_i32, c_i64, c_i64, P_dbl, P_dbl, c_int, c_vp, c_vp, c_vp],
+    "scoot_known_constraints": [c_vp, c_i64, c_int, P_dbl, P_dbl, c_int, c_vp, c_vp],
 }
 RESTYPES = {"scoot_status_string": C.c_char_p, "scoot_last_error": C.c_char_p}
 

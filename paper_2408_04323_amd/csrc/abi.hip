@@ -526,6 +526,14 @@ int scoot_random_pick(const uint8_t* flags, int64_t n, uint64_t seed, int q, int
 int scoot_suggest_mace(scoot_gp gp, scoot_forest f, const float* Xc, int64_t n, double best_y, double xi, double beta,
                        double delta, uint64_t seed, int q, void* mu, void* sigma, void* ucb, void* pi, void* ei,
                        int32_t* votes, uint8_t* mask, uint8_t* front, int64_t* idx, int32_t* n_front, void* stream) {
+  return scoot_suggest_mace_ex(gp, f, nullptr, Xc, n, best_y, xi, beta, delta, seed, q, mu, sigma, ucb, pi, ei, votes,
+                               mask, front, idx, n_front, stream);
+}
+
+int scoot_suggest_mace_ex(scoot_gp gp, scoot_forest f, const uint8_t* known, const float* Xc, int64_t n,
+                          double best_y, double xi, double beta, double delta, uint64_t seed, int q, void* mu,
+                          void* sigma, void* ucb, void* pi, void* ei, int32_t* votes, uint8_t* mask, uint8_t* front,
+                          int64_t* idx, int32_t* n_front, void* stream) {
   g_last_error.clear();
   if (!gp) return fail(SCOOT_ERR_INVALID_ARG, "mace suggest: null GP");
   if (n < 0 || n >= ((int64_t)1 << 31)) return fail(SCOOT_ERR_INVALID_ARG, "mace suggest: n out of range");
@@ -546,15 +554,24 @@ int scoot_suggest_mace(scoot_gp gp, scoot_forest f, const float* Xc, int64_t n, 
   if (rc != SCOOT_OK) return rc;
   rc = launch_mace_scores(mu, sigma, n, dt, best_y + xi, beta, ucb, pi, ei, stream);
   if (rc != SCOOT_OK) return rc;
-  if (f) {
-    rc = launch_forest(f->dev, Xc, n, vmin, votes, mask, nullptr, stream);
-  } else if (n > 0) {
-    rc = launch_fill_u8(mask, n, 1, stream);
-  }
+  rc = f ? launch_forest(f->dev, Xc, n, vmin, votes, mask, nullptr, stream, known)
+         : launch_mask_init(mask, known, n, stream);
   if (rc != SCOOT_OK) return rc;
   rc = launch_pareto_front3(ucb, pi, ei, mask, n, dt, front, nullptr, stream);
   if (rc != SCOOT_OK) return rc;
   return launch_random_pick(front, n, seed, q, idx, n_front, stream);
+}
+
+int scoot_sobol_pool(const uint32_t* poly, const uint32_t* vinit, int d, const int32_t* levels, int64_t skip, int64_t n,
+                     const double* A, const double* b, int r, float* Xc, uint8_t* known, void* stream) {
+  g_last_error.clear();
+  return launch_sobol_pool(poly, vinit, d, levels, skip, n, A, b, r, Xc, known, stream);
+}
+
+int scoot_known_constraints(const float* Xc, int64_t n, int d, const double* A, const double* b, int r,
+                            uint8_t* known, void* stream) {
+  g_last_error.clear();
+  return launch_known_constraints(Xc, n, d, A, b, r, known, stream);
 }
 
 int scoot_delta_update(double* delta, int* c, int k, int any_invalid) {
@@ -581,6 +598,14 @@ int scoot_score_pool(const scoot_gp* gps, int p, scoot_forest f, const float* Xc
                      double xi, const double* Y_obs, int m_obs, const double* ref, double delta, int q, void* mu,
                      void* sigma, void* acq, int32_t* votes, uint8_t* mask, int64_t* idx, void* score_out,
                      int32_t* n_valid, void* stream) {
+  return scoot_score_pool_ex(gps, p, f, nullptr, Xc, n, best_y, xi, Y_obs, m_obs, ref, delta, q, mu, sigma, acq, votes,
+                             mask, idx, score_out, n_valid, stream);
+}
+
+int scoot_score_pool_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_t* known, const float* Xc, int64_t n,
+                        double best_y, double xi, const double* Y_obs, int m_obs, const double* ref, double delta,
+                        int q, void* mu, void* sigma, void* acq, int32_t* votes, uint8_t* mask, int64_t* idx,
+                        void* score_out, int32_t* n_valid, void* stream) {
   g_last_error.clear();
   if (!gps || p < 1 || p > SCOOT_MAX_OBJECTIVES) return fail(SCOOT_ERR_INVALID_ARG, "score pool: bad p or gps");
   for (int j = 0; j < p; ++j)
@@ -627,11 +652,8 @@ int scoot_score_pool(const scoot_gp* gps, int p, scoot_forest f, const float* Xc
     rc = launch_ehvi(mus, sds, p, n, dt, bt, acq, stream);
     if (rc != SCOOT_OK) return rc;
   }
-  if (f) {
-    rc = launch_forest(f->dev, Xc, n, vmin, votes, mask, nullptr, stream);
-  } else if (n > 0) {
-    rc = launch_fill_u8(mask, n, 1, stream);
-  }
+  rc = f ? launch_forest(f->dev, Xc, n, vmin, votes, mask, nullptr, stream, known)
+         : launch_mask_init(mask, known, n, stream);
   if (rc != SCOOT_OK) return rc;
   return launch_topq(acq, mask, n, dt, q, idx, score_out, n_valid, stream);
 }
@@ -663,6 +685,13 @@ int scoot_suggest_kb_workspace(const scoot_gp* gps, int p, int64_t n, int q, uin
 int scoot_suggest_kb(const scoot_gp* gps, int p, scoot_forest f, const float* Xc, int64_t n, const double* Y_obs,
                      int m_obs, const double* ref, double delta, int q, void* workspace, uint64_t workspace_bytes,
                      int64_t* picks, double* pick_acq, int* n_picked, void* stream) {
+  return scoot_suggest_kb_ex(gps, p, f, nullptr, Xc, n, Y_obs, m_obs, ref, delta, q, workspace, workspace_bytes, picks,
+                             pick_acq, n_picked, stream);
+}
+
+int scoot_suggest_kb_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_t* known, const float* Xc, int64_t n,
+                        const double* Y_obs, int m_obs, const double* ref, double delta, int q, void* workspace,
+                        uint64_t workspace_bytes, int64_t* picks, double* pick_acq, int* n_picked, void* stream) {
   g_last_error.clear();
   const GPDevice* g[SCOOT_MAX_OBJECTIVES];
   int rc = kb_check(gps, p, n, q, g);
@@ -684,7 +713,7 @@ int scoot_suggest_kb(const scoot_gp* gps, int p, scoot_forest f, const float* Xc
     return fail(SCOOT_ERR_INVALID_ARG, "believer: workspace too small");
   }
   try {
-    rc = run_kriging_believer(g, p, f ? &f->dev : nullptr, vmin, Xc, n, Y_obs, m_obs, ref, q, ws, picks, pick_acq,
+    rc = run_kriging_believer(g, p, f ? &f->dev : nullptr, known, vmin, Xc, n, Y_obs, m_obs, ref, q, ws, picks, pick_acq,
                               n_picked, stream);
   } catch (const std::bad_alloc&) {
     rc = fail(SCOOT_ERR_NO_MEMORY, "believer: host allocation failed");

@@ -255,9 +255,16 @@ int launch_ei(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, doub
               void* stream);
 int launch_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, scoot_dtype dt,
                 const BoxTable& boxes, void* ehvi, void* stream);
+// mask[c] = votes >= vote_min and (known nullable) known[c] != 0.
 int launch_forest(const ForestDevice& f, const float* Xc, int64_t n, int64_t vote_min,
-                  int32_t* votes, uint8_t* mask, int32_t* leaf_idx, void* stream);
-int launch_fill_u8(uint8_t* p, int64_t n, uint8_t v, void* stream);
+                  int32_t* votes, uint8_t* mask, int32_t* leaf_idx, void* stream,
+                  const uint8_t* known = nullptr);
+// mask[i] = known ? (known[i] != 0) : 1.
+int launch_mask_init(uint8_t* mask, const uint8_t* known, int64_t n, void* stream);
+int launch_sobol_pool(const uint32_t* poly, const uint32_t* vinit, int d, const int32_t* levels, int64_t skip,
+                      int64_t n, const double* A, const double* b, int r, float* Xc, uint8_t* known, void* stream);
+int launch_known_constraints(const float* Xc, int64_t n, int d, const double* A, const double* b, int r,
+                             uint8_t* known, void* stream);
 int launch_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q,
                 int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
 int launch_random_pick(const uint8_t* flags, int64_t n, uint64_t seed, int q, int64_t* idx, int32_t* n_flagged,
@@ -269,8 +276,8 @@ int launch_pareto_front3(const void* a, const void* b, const void* c, const uint
 
 // Sequential Kriging-believer picks (fp32 GPs only).
 size_t kb_workspace_bytes(const GPDevice* const* g, int p, int64_t n, int q);
-int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f, int64_t vote_min, const float* Xc,
-                         int64_t n, const double* Y_obs, int m_obs, const double* ref, int q, void* ws,
+int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f, const uint8_t* known,
+                         int64_t vote_min, const float* Xc, int64_t n, const double* Y_obs, int m_obs, const double* ref, int q, void* ws,
                          int64_t* picks, double* pick_acq, int* n_picked, void* stream);
 
 }  // namespace scoot

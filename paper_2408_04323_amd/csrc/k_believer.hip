@@ -120,9 +120,9 @@ KbLayout kb_layout(const GPDevice* const* g, int p, int64_t n, int q) {
 
 size_t kb_workspace_bytes(const GPDevice* const* g, int p, int64_t n, int q) { return kb_layout(g, p, n, q).total; }
 
-int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f, int64_t vote_min, const float* Xc,
-                         int64_t n, const double* Y_obs, int m_obs, const double* ref, int q, void* ws,
-                         int64_t* picks, double* pick_acq, int* n_picked, void* stream) {
+int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f, const uint8_t* known,
+                         int64_t vote_min, const float* Xc, int64_t n, const double* Y_obs, int m_obs,
+                         const double* ref, int q, void* ws, int64_t* picks, double* pick_acq, int* n_picked, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   const KbLayout L = kb_layout(g, p, n, q);
   unsigned char* w = (unsigned char*)ws;
@@ -168,7 +168,8 @@ int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f,
                               true);
     if (rc != SCOOT_OK) return rc;
   }
-  int rc = f ? launch_forest(*f, Xc, n, vote_min, votes, elig, nullptr, stream) : launch_fill_u8(elig, n, 1, stream);
+  int rc = f ? launch_forest(*f, Xc, n, vote_min, votes, elig, nullptr, stream, known)
+             : launch_mask_init(elig, known, n, stream);
   if (rc != SCOOT_OK) return rc;
 
   std::vector<double> Yaug(Y_obs, Y_obs + (size_t)m_obs * p);

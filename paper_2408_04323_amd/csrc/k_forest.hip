@@ -35,7 +35,8 @@ struct ForestArgs {
 __global__ __launch_bounds__(kForestThreads) void forest_kernel(
     const uint2* __restrict__ nodes, const uint32_t* __restrict__ root, const uint32_t* __restrict__ depth,
     const int32_t* __restrict__ leaf_orig, const float* __restrict__ Xc, int32_t* __restrict__ votes,
-    uint8_t* __restrict__ mask, int32_t* __restrict__ leaf_idx, const ForestArgs a) {
+    uint8_t* __restrict__ mask, int32_t* __restrict__ leaf_idx, const uint8_t* __restrict__ known,
+    const ForestArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   uint2* tree = reinterpret_cast<uint2*>(smem);
   unsigned char* xs = smem + (size_t)a.n_nodes * 8;  // [d][kForestThreads] floats
@@ -78,12 +79,12 @@ __global__ __launch_bounds__(kForestThreads) void forest_kernel(
       }
     }
     if (votes) votes[c] = v;
-    if (a.last && mask) mask[c] = v >= a.vote_min ? 1 : 0;
+    if (a.last && mask) mask[c] = v >= a.vote_min && (!known || known[c] != 0) ? 1 : 0;
   }
 }
 
 int launch_forest(const ForestDevice& f, const float* Xc, int64_t n, int64_t vote_min, int32_t* votes,
-                  uint8_t* mask, int32_t* leaf_idx, void* stream) {
+                  uint8_t* mask, int32_t* leaf_idx, void* stream, const uint8_t* known) {
   if (n == 0) return SCOOT_OK;
   hipStream_t s = (hipStream_t)stream;
   const int n_chunks = (int)f.chunk_tree.size() - 1;
@@ -121,29 +122,10 @@ int launch_forest(const ForestDevice& f, const float* Xc, int64_t n, int64_t vot
     a.vote_min = (int32_t)vote_min;
     const size_t lds = (size_t)a.n_nodes * 8 + (size_t)f.d * kForestThreads * 4;
     hipLaunchKernelGGL(forest_kernel, dim3((unsigned)grid), dim3(kForestThreads), lds, s, (const uint2*)f.nodes,
-                       f.root, f.depth, f.leaf_orig, Xc, votes, mask, leaf_idx, a);
+                       f.root, f.depth, f.leaf_orig, Xc, votes, mask, leaf_idx, known, a);
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("forest launch: ") + hipGetErrorString(err));
-  return SCOOT_OK;
-}
-
-}  // namespace scoot
-
-namespace scoot {
-
-__global__ void fill_u8_kernel(uint8_t* __restrict__ p, int64_t n, uint8_t v) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-    p[i] = v;
-}
-
-int launch_fill_u8(uint8_t* p, int64_t n, uint8_t v, void* stream) {
-  if (n == 0) return SCOOT_OK;
-  int64_t blocks = (n + 255) / 256;
-  if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(fill_u8_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, p, n, v);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("fill launch: ") + hipGetErrorString(err));
   return SCOOT_OK;
 }
 

@@ -174,3 +174,49 @@ def test_normal_tail_coefficients_match_their_generator():
     # the float evaluation of the fit against g in double
     g32 = gen.eval_f32(p, q, x).astype(np.float64)
     assert np.max(np.abs(g32 - y) / y) < 1e-6
+
+
+def test_sobol_and_known_constraint_argument_checks():
+    """Validation happens on the host before any launch (n = 0 launches nothing)."""
+    L = lib()
+    U32 = C.c_uint32 * 2
+    vin = (C.c_uint32 * 36)()
+    vin[18] = 1                                       # dim 1: x + 1, m_1 = 1
+    lv = (C.c_int32 * 2)(0, 5)
+
+    def call(poly=(1, 3), levels=lv, d=2, skip=0, n=0, A=None, b=None, r=0, v=vin):
+        return L.scoot_sobol_pool(U32(*poly), v, d, levels, skip, n, A, b, r, None, None, None)
+
+    assert call() == 0
+    assert call(poly=(1, 2)) == -1                   # no constant term
+    assert call(poly=(1, 0)) == -1
+    assert call(poly=(1, 1 << 20 | 1)) == -4          # degree 20 > 18
+    bad = (C.c_uint32 * 36)()
+    bad[18] = 2                                       # m_1 must be odd
+    assert call(v=bad) == -1
+    bad[18] = 3                                       # and below 2^1
+    assert call(v=bad) == -1
+    assert call(levels=(C.c_int32 * 2)(0, -1)) == -1
+    assert call(d=0) == -1 and call(d=17) == -1
+    assert call(skip=-1) == -1 and call(n=-1) == -1
+    assert call(skip=1 << 32, n=0) == 0 and call(skip=(1 << 32) + 1, n=0) == -1   # skip + n <= 2^32
+    assert call(n=10) == -1                           # null Xc
+    A = (C.c_double * 18)(*([1.0] * 18))
+    b = (C.c_double * 9)(*([1.0] * 9))
+    assert call(A=A, b=b, r=9) == -4                  # r > SCOOT_MAX_CONSTRAINTS
+    assert call(A=None, b=b, r=1) == -1
+    assert call(A=A, b=b, r=-1) == -4
+    A[1] = float("inf")
+    assert call(A=A, b=b, r=1) == -1
+    A[1] = 1.0
+    b[0] = float("nan")
+    assert call(A=A, b=b, r=1) == -1
+    b[0] = float("inf")                               # an always-true row is fine
+    assert call(A=A, b=b, r=1) == 0
+    K = L.scoot_known_constraints
+    assert K(None, 0, 2, A, b, 1, None, None) == 0
+    assert K(None, 5, 2, A, b, 1, None, None) == -1
+    assert K(None, 0, 0, A, b, 1, None, None) == -1
+    assert K(None, 0, 2, A, b, 9, None, None) == -4
+    with pytest.raises(ValueError):
+        S.sobol_pool([1, 3], [[0], [1]], [0], 4)      # one level per dimension

@@ -66,3 +66,33 @@ def test_known_constraints():
     b = np.array([1.0, -0.1])      # x0 + x1 <= 1 and x0 >= 0.1
     np.testing.assert_array_equal(known_constraints_mask(X, A, b), [1, 0, 1])   # 0.5 + 0.5 <= 1 holds
     assert known_constraints_mask(X, np.zeros((0, 2)), np.zeros(0)).tolist() == [1, 1, 1]
+
+
+def test_known_constraints_encode_the_engine_rules():
+    """The linear rows of the vLLM-like space decide exactly what the engine's
+    rules, checked in engine units, decide -- on a Sobol pool of the space,
+    where the integer knobs meet their boundaries (equal token and sequence
+    limits, tokens exactly at the model length) many times."""
+    from workloads import sobol_table, vllm_decode, vllm_space
+    sp = vllm_space()
+    poly, vinit = sobol_table(sp["d"])
+    X = sobol_pool(poly, vinit, sp["levels"], 4096)
+    # add hand-made boundary rows: tokens == seqs, tokens == 4096 without chunking, both booleans
+    span = 8128.0
+    extra = np.array(X[:6], dtype=np.float64)
+    extra[0, 1] = extra[0, 2] = (4096 - 64) / span
+    extra[0, 5] = extra[0, 6] = 0.0
+    extra[1, 1], extra[1, 2] = (1000 - 64) / span, (999 - 64) / span
+    extra[2, 2], extra[2, 5], extra[2, 6] = (4095 - 64) / span, 0.0, 0.0
+    extra[3, 2], extra[3, 1], extra[3, 5], extra[3, 6] = (4095 - 64) / span, 0.0, 1.0, 0.0
+    extra[4, 5] = extra[4, 6] = 1.0
+    extra[5, 1], extra[5, 2], extra[5, 5], extra[5, 6] = 0.0, 1.0, 1.0, 0.0
+    X = np.vstack([X, extra.astype(np.float32)])
+    got = known_constraints_mask(X, sp["A"], sp["b"])
+    v = vllm_decode(X.astype(np.float64))
+    tok, seqs = v["max-num-batched-tokens"], v["max-num-seqs"]
+    chunk, prefix = v["enable-chunked-prefill"], v["enable-prefix-caching"]
+    want = (tok >= seqs) & ~(chunk & prefix) & (chunk | (tok >= 4096))
+    np.testing.assert_array_equal(got, want.astype(np.uint8))
+    assert list(got[-6:]) == [1, 0, 0, 1, 0, 1]
+    assert np.sum(tok == seqs) > 0 and 0.2 < got.mean() < 0.8

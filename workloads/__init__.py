@@ -6,4 +6,5 @@ arrays, Delta, the reference point, the best observed value.  It holds none of
 the scoring arithmetic (no GP, acquisition, hypervolume, forest walk or
 selection), and both the product path and the oracle read what it produces.
 """
-from .synth import CONFIGS, MASTER_SEED, make_workload, make_pool  # noqa: F401
+from .synth import (CONFIGS, MASTER_SEED, levels, make_pool, make_workload, sobol_table,  # noqa: F401
+                    space_constraints, vllm_decode, vllm_space)

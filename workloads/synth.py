@@ -180,6 +180,81 @@ def sobol_table(d):
     return z["poly"][:d].astype(np.int64), z["vinit"][:d].astype(np.int64)
 
 
+# A vLLM-like space of nine knobs (the paper's Table 1) with the engine's
+# known constraints (the paper's appendix), on 4 GPUs and a model whose
+# maximum length is 4096 tokens.  Knob k takes x_k in [0, 1]; an integer knob
+# with range [lo, hi] is the grid of L = hi - lo + 1 levels, value
+# lo + (hi - lo) x; the block-size enumeration {8, 16, 32} is a 3-level grid
+# over its indices; booleans are 0 / 1.
+VLLM_KNOBS = [  # name, kind, lo, hi
+    ("tensor-parallel", "int", 1, 4),
+    ("max-num-seqs", "int", 64, 8192),
+    ("max-num-batched-tokens", "int", 64, 8192),
+    ("block-size", "enum", (8, 16, 32), None),
+    ("scheduler-delay-factor", "float", 0.0, 2.0),
+    ("enable-chunked-prefill", "bool", None, None),
+    ("enable-prefix-caching", "bool", None, None),
+    ("disable-custom-all-reduce", "bool", None, None),
+    ("use-v2-block-manager", "bool", None, None),
+]
+VLLM_MAX_MODEL_LEN = 4096
+
+
+def vllm_space():
+    """levels, and the known constraints as rows A x <= b over the normalised
+    knobs.  Integer inequalities get half a grid step of slack so that the
+    float32 rounding of the grid points cannot flip a boundary case:
+
+    * max-num-batched-tokens >= max-num-seqs:  x_seqs - x_tokens <= 0.5 / 8128
+    * not (chunked prefill and prefix caching):  x_chunk + x_prefix <= 1
+    * no chunked prefill => max-num-batched-tokens >= max model length:
+      (4096 - 64 - 0.5) / 8128 - x_tokens - 2 x_chunk <= 0  (big-M, M = 2)
+    """
+    fixed = {"enum": 3, "float": 0, "bool": 1}
+    levels = [hi - lo + 1 if kind == "int" else fixed[kind] for _, kind, lo, hi in VLLM_KNOBS]
+    d = len(VLLM_KNOBS)
+    A = np.zeros((3, d))
+    b = np.zeros(3)
+    span = 8192 - 64
+    A[0, 1], A[0, 2], b[0] = 1.0, -1.0, 0.5 / span
+    A[1, 5], A[1, 6], b[1] = 1.0, 1.0, 1.0
+    A[2, 2], A[2, 5], b[2] = -1.0, -2.0, -(VLLM_MAX_MODEL_LEN - 64 - 0.5) / span
+    return dict(levels=levels, A=A, b=b, d=d)
+
+
+def space_constraints(c):
+    """Known constraints of the same three shapes as the engine rules, on the
+    synthetic spaces: the first integer knob at most the second (half a grid
+    step of slack), not both booleans, and the third integer knob in the upper
+    half unless the first boolean is set (big-M, M = 2)."""
+    d = dims(c)
+    i0 = c["d_cont"]
+    b0 = c["d_cont"] + c["d_int"]
+    A = np.zeros((3, d))
+    b = np.zeros(3)
+    A[0, i0], A[0, i0 + 1], b[0] = 1.0, -1.0, 0.5 / (c["int_levels"] - 1)
+    A[1, b0], A[1, b0 + 1], b[1] = 1.0, 1.0, 1.0
+    A[2, i0 + 2], A[2, b0], b[2] = -1.0, -2.0, -0.5
+    return A, b
+
+
+def vllm_decode(X):
+    """Engine values of normalised configurations (float64 in, list of dicts' columns out)."""
+    X = np.asarray(X, dtype=np.float64)
+    cols = {}
+    for k, (name, kind, lo, hi) in enumerate(VLLM_KNOBS):
+        x = X[:, k]
+        if kind == "int":
+            cols[name] = lo + np.rint(x * (hi - lo)).astype(np.int64)
+        elif kind == "enum":
+            cols[name] = np.asarray(lo)[np.rint(x * (len(lo) - 1)).astype(np.int64)]
+        elif kind == "float":
+            cols[name] = lo + (hi - lo) * x
+        else:
+            cols[name] = x >= 0.5
+    return cols
+
+
 def make_pool(cfg_id, n=None):
     """The candidate pool alone: (n, d) float32, grid-snapped."""
     c = CONFIGS[cfg_id]
