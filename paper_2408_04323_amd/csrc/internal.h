@@ -215,7 +215,8 @@ struct GPDevice {
   double s2 = 1, tau2 = 0, c = 0;
   void* buf = nullptr;        // one allocation holding everything below
   const void* linv = nullptr; // packed L^-1 (float or double)
-  const void* xs = nullptr;   // m_pad x kXsStride scaled observations (float or double)
+  const void* xs = nullptr;   // m_pad x kXsStride scaled observations (float or double); fp32 rows
+                              // hold (float)alpha_i in column d when d < kXsStride
   const double* alpha = nullptr;  // m_pad
   const float* alpha32 = nullptr; // m_pad, float copy
   float scale32[SCOOT_MAX_DIM];

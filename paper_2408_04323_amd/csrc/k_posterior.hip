@@ -86,19 +86,28 @@ __device__ inline void load_b32(f4_t (&b)[8], const f4_t* ks, int J, int lane) {
 
 // The 16 MFMA steps of a block: steps 0-7 on the "lo" accumulators, 8-15 on
 // the "hi" ones, issued round-robin so four independent chains are in flight
-// (summed before squaring).
+// (summed before squaring).  FIRST (the row's block J = 0) starts every chain
+// from zero instead of from the accumulators, so they need no clearing.
+template <bool FIRST>
 __device__ inline void mfma_block4(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, const f4_t (&a)[4],
                                    const f4_t (&b)[8]) {
+  const f16_t zero = {0};
 #pragma unroll
   for (int s4 = 0; s4 < 2; ++s4) {
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      l0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4][t], b[2 * s4 + 0][t], l0, 0, 0, 0);
-      l1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4][t], b[2 * s4 + 1][t], l1, 0, 0, 0);
-      h0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4 + 2][t], b[2 * (s4 + 2) + 0][t], h0, 0, 0, 0);
-      h1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4 + 2][t], b[2 * (s4 + 2) + 1][t], h1, 0, 0, 0);
+      const bool z = FIRST && s4 == 0 && t == 0;
+      l0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4][t], b[2 * s4 + 0][t], z ? zero : l0, 0, 0, 0);
+      l1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4][t], b[2 * s4 + 1][t], z ? zero : l1, 0, 0, 0);
+      h0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4 + 2][t], b[2 * (s4 + 2) + 0][t], z ? zero : h0, 0, 0, 0);
+      h1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4 + 2][t], b[2 * (s4 + 2) + 1][t], z ? zero : h1, 0, 0, 0);
     }
   }
+}
+__device__ inline void mfma_block4_at(int J, f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, const f4_t (&a)[4],
+                                      const f4_t (&b)[8]) {
+  if (J == 0) mfma_block4<true>(l0, l1, h0, h1, a, b);
+  else mfma_block4<false>(l0, l1, h0, h1, a, b);
 }
 
 // Where V goes when it is kept (the sequential believer needs it): row-major,
@@ -111,7 +120,8 @@ struct VStore {
 };
 
 // Completes a row block: squared norms of its V columns into sq0 / sq1, and
-// the block itself into V when kept.  Accumulator register r of lane l holds
+// the block itself into V when kept.  The accumulators are left as they are
+// (the next row's first block overwrites them).  Accumulator register r of lane l holds
 // row 8 (r / 4) + 4 (l / 32) + r % 4 of the block, column l % 32.
 template <bool KEEP_V>
 __device__ inline void finish_row(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, float& sq0, float& sq1,
@@ -128,10 +138,6 @@ __device__ inline void finish_row(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, fl
     }
     p0 = fmaf(v0, v0, p0);
     p1 = fmaf(v1, v1, p1);
-    l0[r] = 0.0f;
-    l1[r] = 0.0f;
-    h0[r] = 0.0f;
-    h1[r] = 0.0f;
   }
   sq0 += p0;
   sq1 += p1;
@@ -145,7 +151,9 @@ __device__ inline void finish_row(f16_t& l0, f16_t& l1, f16_t& h0, f16_t& h1, fl
 template <bool KEEP_V>
 __device__ inline void wave_tile32(const f4_t* __restrict__ ap, const f4_t* ks, uint64_t rows, int count,
                                    int lane, f4_t (&ax)[4], float& sq0, float& sq1, const VStore& vs) {
-  f16_t l0 = {0}, l1 = {0}, h0 = {0}, h1 = {0};
+  // every row starts at J = 0, whose block writes the accumulators without
+  // reading them: no clearing needed, only a defined (frozen) initial value
+  f16_t l0 = __builtin_nondeterministic_value(l0), l1 = l0, h0 = l0, h1 = l0;
   // (I, J): row block and column block of the block being computed; the
   // wave's remaining rows sit in `rows`, kRowBits each (0 past the last).
   int I = (int)(rows & 31), J = 0;
@@ -167,20 +175,20 @@ __device__ inline void wave_tile32(const f4_t* __restrict__ ap, const f4_t* ks, 
     load_block32(ay, ap, k + 1);
     load_b32(by, ks, next_j(J, I), lane);
     __builtin_amdgcn_sched_barrier(0);
-    mfma_block4(l0, l1, h0, h1, ax, bx);
+    mfma_block4_at(J, l0, l1, h0, h1, ax, bx);
     __builtin_amdgcn_sched_barrier(0);
     advance();
     load_block32(ax, ap, k + 2 < count ? k + 2 : 0);
     load_b32(bx, ks, next_j(J, I), lane);
     __builtin_amdgcn_sched_barrier(0);
-    mfma_block4(l0, l1, h0, h1, ay, by);
+    mfma_block4_at(J, l0, l1, h0, h1, ay, by);
     __builtin_amdgcn_sched_barrier(0);
     advance();
   }
   if (k < count) {
     load_block32(ay, ap, 0);
     __builtin_amdgcn_sched_barrier(0);
-    mfma_block4(l0, l1, h0, h1, ax, bx);
+    mfma_block4_at(J, l0, l1, h0, h1, ax, bx);
     __builtin_amdgcn_sched_barrier(0);
     advance();
 #pragma unroll
@@ -206,6 +214,9 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int64_t n_tiles = (a.n + 63) >> 6;
+  static_assert(WAVES % 2 == 0, "phase 1 relies on an even wave count");
+  // float4 loads per observation row: the D coordinates and, below 16, alpha
+  constexpr int kRowVec = D < kXsStride ? (D + 1 + 3) / 4 : kXsStride / 4;
 
   // Plan entry of this wave.  With 8 waves, entries p and p + 4 are meant to
   // share a SIMD: each wave takes simd + 4 * (its arrival order on the SIMD),
@@ -244,31 +255,43 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
     if (next < n_tiles) load_coords_f32<D>(xr, Xc + min(next * 64 + lane, a.n - 1) * D);
 
     // ---- phase 1: K* for candidate c0 + lane, rows of this wave's groups --
-    // Group G covers rows 32J + 8 s4 + 2t + h, t = 0..3, of block J; lane l
-    // writes them as one float4 to B-operand slot (J, ct = l/32, s4, h*32 + l%32).
+    // Group G = 8J + 2 s4 + h covers rows 32J + 8 s4 + h + 2t = 4G - 3h + 2t,
+    // t = 0..3, of block J; lane l writes them as one float4 to B-operand slot
+    // (J, ct = l/32, s4, h*32 + l%32).  WAVES is even, so h = wave & 1 for all
+    // of a wave's groups and its rows advance by 4 WAVES per group: one
+    // running row pointer, the four rows at fixed offsets from it.
     float mu_part = 0.0f;
     const int ngroups = nb * 8;
-    for (int G = wave; G < ngroups; G += WAVES) {
-      const int J = G >> 3, s4 = (G >> 1) & 3, h = G & 1;
-      const int rbase = 32 * J + 8 * s4 + h;
+    const int hw = wave & 1;
+    const float* xg = xs + (size_t)(4 * wave - 3 * hw) * kXsStride;
+    for (int G = wave; G < ngroups; G += WAVES, xg += 4 * WAVES * kXsStride) {
+      const int J = G >> 3, s4 = (G >> 1) & 3;
       f4_t kv;
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const int i = rbase + 2 * t;
-        const float* xo = xs + (size_t)i * kXsStride;
+        const float* xo = xg + 2 * t * kXsStride;
+        float xv[kRowVec * 4];
+#pragma unroll
+        for (int r = 0; r < kRowVec; ++r) {
+          const f4_t v4 = reinterpret_cast<const f4_t*>(xo)[r];
+#pragma unroll
+          for (int c = 0; c < 4; ++c) xv[4 * r + c] = v4[c];
+        }
         float acc = 0.0f;
 #pragma unroll
         for (int k = 0; k < D; ++k) {
-          float df = xc[k] - xo[k];
+          float df = xc[k] - xv[k];
           acc = fmaf(df, df, acc);
         }
         float u = __builtin_amdgcn_sqrtf(acc);
         float e = __builtin_amdgcn_exp2f(-u);
         float kval = fmaf(u, fmaf(u, a.c2, a.c1), a.c0) * e;
         kv[t] = kval;
-        mu_part = fmaf(kval, alpha[i], mu_part);
+        // alpha_i rides in column D of the row when there is room
+        const float al = D < kXsStride ? xv[D < kXsStride ? D : 0] : alpha[4 * G - 3 * hw + 2 * t];
+        mu_part = fmaf(kval, al, mu_part);
       }
-      ks[((J * 2 + (lane >> 5)) * 4 + s4) * 64 + h * 32 + (lane & 31)] = kv;
+      ks[((J * 2 + (lane >> 5)) * 4 + s4) * 64 + hw * 32 + (lane & 31)] = kv;
     }
     __syncthreads();
 
