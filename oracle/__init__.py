@@ -26,6 +26,8 @@ Tuning for LLM Inference Engines) and is written for clarity, not speed:
 * ``mace``        -- MACE for one objective: UCB, PI, EI (Eq. 6-8), their Pareto
                      front over the pool and a seeded random pick (Sec. 4.5.1, 4.6)
 * ``pipeline``    -- the whole scoring pass over a candidate pool
+* ``suggest``     -- the suggestion step of Algorithm 1 end to end: learn,
+                     train, generate, score, pick, fill
 
 Conventions (the readings of the paper this oracle takes):
 

@@ -116,3 +116,20 @@ def predict(forest, X):
                     else forest["right"][base + k]
             out[i] += forest["value"][base + k]
     return out / T
+
+
+def voting_format(tf):
+    """A trained forest in the form the vote count reads (reading 10 of the
+    design notes): each float64 threshold t becomes the largest float32 not
+    above t, so a float32 feature x goes left exactly when x <= t; each leaf
+    value v becomes round(v * 2^16), ties to even."""
+    t64 = np.asarray(tf["threshold"], dtype=np.float64)
+    t32 = t64.astype(np.float32)
+    above = t32.astype(np.float64) > t64
+    t32[above] = np.nextafter(t32[above], np.float32(-np.inf))
+    leaf = np.asarray(tf["left"]) < 0
+    return dict(feature=np.where(leaf, 0, tf["feature"]).astype(np.int32),
+                threshold=np.where(leaf, np.float32(0), t32).astype(np.float32),
+                left=np.asarray(tf["left"], np.int32), right=np.asarray(tf["right"], np.int32),
+                leaf_q16=np.where(leaf, np.rint(np.asarray(tf["value"]) * 65536.0), 0).astype(np.int32),
+                tree_offset=np.asarray(tf["tree_offset"], np.int64))
