@@ -425,6 +425,100 @@ int scoot_sobol_pool(const uint32_t* poly, const uint32_t* vinit, int d, const i
 int scoot_known_constraints(const float* Xc, int64_t n, int d, const double* A, const double* b, int r,
                             uint8_t* known, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * The suggestion step, end to end (Algorithm 1, SUGGEST(k, O, RF, Delta); the
+ * workflow of Sec. 4.1, steps 3-6): observed configurations and SLO values
+ * in, k configurations to evaluate next out.  Host call; the device work runs
+ * on `stream` and the call returns after it has finished.
+ *
+ * scoot_space: the search space.  levels [d] as in scoot_sobol_pool (0
+ *   continuous, 1 boolean, L >= 2 a grid of L levels on [0, 1]); the Sobol
+ *   direction tables sobol_poly [d] and sobol_vinit [d * SCOOT_SOBOL_MAX_DEGREE]
+ *   as in scoot_sobol_pool; the known constraints A [r*d], b [r] (Sec. 4.5.3;
+ *   r = 0: none, A and b may be NULL).
+ *
+ * scoot_suggest_opts: k (1 .. SCOOT_MAX_Q) configurations wanted; delta the
+ *   POF threshold (Eq. 3, Algorithm 1); pool_size candidates (1 .. 2^31 - 1)
+ *   starting at Sobol index pool_skip are scored (the solver's search);
+ *   kernel and dtype of the GPs; warp_a, warp_b [p*d] (nullable, both or
+ *   neither) fixed Kumaraswamy warps per objective; theta_lower,
+ *   theta_upper, theta_start [p*(d+2)] (each nullable) the box and start of
+ *   the maximum-likelihood search per objective in scoot_gp_mle's
+ *   parameters, defaults: lengthscales [0.01, 10] from 0.5, signal variance
+ *   [0.05, 20] from 1, noise variance [1e-6, 1] from 1e-3 (lower == upper
+ *   fixes a parameter; all fixed skips the search); mle_max_iter (<= 0:
+ *   200); n_trees (1 .. SCOOT_MAX_TREES), max_depth, forest_seed, bootstrap
+ *   of the forest (scoot_forest_train); xi (Eq. 7-8); t >= 1 the tuning
+ *   iteration of the UCB schedule and pick_seed of the random pick (one
+ *   objective: MACE); ref [p] (nullable: worst valid observation + 10% of the
+ *   range) the EHVI reference point in the caller's units (several
+ *   objectives).
+ *
+ * scoot_suggest: X_obs [n_obs*d] observed configurations (finite), Y_obs
+ *   [n_obs*p] their objective values (minimised; read only where valid),
+ *   valid [n_obs] 1 = the engine ran, 0 = it crashed (Sec. 4.7).  Steps:
+ *   1. each objective's valid values are standardised (mean 0, standard
+ *      deviation 1; a constant column keeps scale 1);
+ *   2. per objective, hyperparameters by scoot_gp_mle from theta_start, then
+ *      the GP by scoot_gp_fit_ex on the valid observations (prior mean 0);
+ *   3. the forest by scoot_forest_train on every observation, label valid;
+ *   4. the pool by scoot_sobol_pool with the known-constraint mask;
+ *   5. one objective: scoot_suggest_mace_ex (best = the smallest valid
+ *      standardised value, beta from scoot_ucb_beta(t)); several:
+ *      scoot_score_pool_ex (EHVI over the valid standardised values, the
+ *      reference point standardised alike), both under POF >= delta and the
+ *      known constraints;
+ *   6. a shortfall is filled with pool points in Sobol order that satisfy the
+ *      known constraints and were not picked (Sec. 4.7, last paragraph); with
+ *      no valid observation every suggestion comes from this fill (the
+ *      initial design of Algorithm 1 is a call with n_obs = 0).
+ *   x_out [k*d] host receives the configurations (the float32 pool points,
+ *   widened), source [k] host (nullable) 0 = picked by the acquisition,
+ *   1 = Sobol fill, theta_out [p*(d+2)] host (nullable) the hyperparameters
+ *   used, *n_out the number written (below k only when the pool holds too
+ *   few admissible points).  Library scratch on the current device holds the
+ *   pool and the scores between calls.
+ * Errors: INVALID_ARG (null pointer, bad sizes, non-finite input, p out of
+ *   range, t < 1), UNSUPPORTED, NOT_PD, DEVICE, NO_MEMORY, and those of the
+ *   calls made.
+ * ------------------------------------------------------------------------- */
+typedef struct scoot_space {
+  int d;
+  const int32_t* levels;
+  const uint32_t* sobol_poly;
+  const uint32_t* sobol_vinit;
+  const double* A;
+  const double* b;
+  int r;
+} scoot_space;
+
+typedef struct scoot_suggest_opts {
+  int k;
+  double delta;
+  int64_t pool_size;
+  int64_t pool_skip;
+  int kernel; /* scoot_kernel */
+  int dtype;  /* scoot_dtype */
+  const double* warp_a;
+  const double* warp_b;
+  const double* theta_lower;
+  const double* theta_upper;
+  const double* theta_start;
+  int mle_max_iter;
+  int n_trees;
+  int max_depth;
+  uint64_t forest_seed;
+  int bootstrap;
+  double xi;
+  int t;
+  uint64_t pick_seed;
+  const double* ref;
+} scoot_suggest_opts;
+
+int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid, int n_obs, int p,
+                  const scoot_space* space, const scoot_suggest_opts* opts, double* x_out, int32_t* source,
+                  double* theta_out, int* n_out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

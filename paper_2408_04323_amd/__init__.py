@@ -561,3 +561,70 @@ def known_constraints(Xc, A, b, out=None, stream=None):
     check(lib().scoot_known_constraints(_dptr(Xc), n, d, pA, pb, r, _dptr(known), _stream(stream)),
           "known_constraints")
     return known
+
+
+# ------------------------------------------------------ the suggestion step
+class _Space(C.Structure):
+    _fields_ = [("d", C.c_int), ("levels", C.POINTER(C.c_int32)), ("sobol_poly", C.POINTER(C.c_uint32)),
+                ("sobol_vinit", C.POINTER(C.c_uint32)), ("A", C.POINTER(C.c_double)),
+                ("b", C.POINTER(C.c_double)), ("r", C.c_int)]
+
+
+class _SuggestOpts(C.Structure):
+    _fields_ = [("k", C.c_int), ("delta", C.c_double), ("pool_size", C.c_int64), ("pool_skip", C.c_int64),
+                ("kernel", C.c_int), ("dtype", C.c_int), ("warp_a", C.POINTER(C.c_double)),
+                ("warp_b", C.POINTER(C.c_double)), ("theta_lower", C.POINTER(C.c_double)),
+                ("theta_upper", C.POINTER(C.c_double)), ("theta_start", C.POINTER(C.c_double)),
+                ("mle_max_iter", C.c_int), ("n_trees", C.c_int), ("max_depth", C.c_int),
+                ("forest_seed", C.c_uint64), ("bootstrap", C.c_int), ("xi", C.c_double), ("t", C.c_int),
+                ("pick_seed", C.c_uint64), ("ref", C.POINTER(C.c_double))]
+
+
+def suggest(X_obs, Y_obs, valid, space, k, delta=0.5, pool_size=262144, pool_skip=0, kernel="matern52",
+            dtype="f32", warp_a=None, warp_b=None, theta_lower=None, theta_upper=None, theta_start=None,
+            mle_max_iter=0, n_trees=64, max_depth=10, forest_seed=0, bootstrap=True, xi=1e-4, t=1, pick_seed=0,
+            ref=None, stream=None):
+    """One SUGGEST of Algorithm 1 (scoot_suggest).  ``space`` is a dict with
+    ``levels``, ``poly``, ``vinit`` and optionally ``A``, ``b`` (known
+    constraints).  X_obs (n_obs, d), Y_obs (n_obs, p) minimised, valid (n_obs,)
+    host arrays; per-objective options (warps (p, d), theta bounds (p, d + 2))
+    host arrays.  Returns (x (n_out, d) float64, source (n_out,) int32,
+    theta (p, d + 2) float64)."""
+    pu, vi, lv, d = _sobol_inputs(space["poly"], space["vinit"], space["levels"])
+    A, bb, r = _constraint_inputs(space.get("A"), space.get("b"), d)
+    X = np.ascontiguousarray(np.asarray(X_obs, dtype=np.float64).reshape(-1, d))
+    n_obs = X.shape[0]
+    Y = np.asarray(Y_obs, dtype=np.float64)
+    p = Y.shape[1] if Y.ndim == 2 else 1
+    Y = np.ascontiguousarray(Y.reshape(n_obs, p))
+    ok = np.ascontiguousarray(np.asarray(valid).reshape(n_obs) != 0, dtype=np.uint8)
+    keep = []  # host buffers referenced by the structures during the call
+
+    def arr(a, shape):
+        if a is None:
+            return None
+        h, ptr = _host(np.asarray(a, dtype=np.float64).reshape(shape), np.float64)
+        keep.append(h)
+        return ptr
+
+    sp = _Space(d, lv.ctypes.data_as(C.POINTER(C.c_int32)), pu.ctypes.data_as(C.POINTER(C.c_uint32)),
+                vi.ctypes.data_as(C.POINTER(C.c_uint32)),
+                A.ctypes.data_as(C.POINTER(C.c_double)) if r else None,
+                bb.ctypes.data_as(C.POINTER(C.c_double)) if r else None, r)
+    if (warp_a is None) != (warp_b is None):
+        raise ValueError("warp_a and warp_b go together")
+    op = _SuggestOpts(int(k), float(delta), int(pool_size), int(pool_skip), _kernel(kernel), _dt(dtype),
+                      arr(warp_a, (p, d)), arr(warp_b, (p, d)), arr(theta_lower, (p, d + 2)),
+                      arr(theta_upper, (p, d + 2)), arr(theta_start, (p, d + 2)), int(mle_max_iter), int(n_trees),
+                      int(max_depth), int(forest_seed), int(bool(bootstrap)), float(xi), int(t), int(pick_seed),
+                      arr(ref, (p,)))
+    x = np.zeros((k, d), dtype=np.float64)
+    src = np.zeros(k, dtype=np.int32)
+    theta = np.zeros((p, d + 2), dtype=np.float64)
+    n_out = C.c_int(0)
+    check(lib().scoot_suggest(X.ctypes.data_as(C.POINTER(C.c_double)), Y.ctypes.data_as(C.POINTER(C.c_double)),
+                              ok.ctypes.data_as(C.POINTER(C.c_uint8)), n_obs, p, C.byref(sp), C.byref(op),
+                              x.ctypes.data_as(C.POINTER(C.c_double)), src.ctypes.data_as(C.POINTER(C.c_int32)),
+                              theta.ctypes.data_as(C.POINTER(C.c_double)), C.byref(n_out), _stream(stream)),
+          "suggest")
+    return x[:n_out.value], src[:n_out.value], theta

@@ -61,6 +61,8 @@ SIGNATURES = {
                               c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp],
     "scoot_sobol_pool": [P_u32, P_u32, c_int, P_i32, c_i64, c_i64, P_dbl, P_dbl, c_int, c_vp, c_vp, c_vp],
     "scoot_known_constraints": [c_vp, c_i64, c_int, P_dbl, P_dbl, c_int, c_vp, c_vp],
+    "scoot_suggest": [P_dbl, P_dbl, C.POINTER(C.c_uint8), c_int, c_int, c_vp, c_vp, P_dbl, P_i32, P_dbl, P_int,
+                      c_vp],
 }
 RESTYPES = {"scoot_status_string": C.c_char_p, "scoot_last_error": C.c_char_p}
 

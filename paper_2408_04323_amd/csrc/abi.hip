@@ -26,7 +26,7 @@ namespace {
 thread_local std::string g_last_error;
 
 constexpr int kMaxDevices = 64;
-constexpr int kScratchSlots = 6;
+constexpr int kScratchSlots = 7;  // used: 1 boxes, 2 votes, 3 top-q, 4 MACE front, 5 warped pool, 6 suggestion step
 constexpr int kStagingSlots = 2;
 
 struct Staging {

@@ -1,0 +1,278 @@
+// The suggestion step end to end (Algorithm 1's SUGGEST; Sec. 4.1 steps
+// 3-6): standardise the valid observations, learn each objective's GP
+// hyperparameters by maximum likelihood (Sec. 4.3), fit the GPs, train the
+// feasibility forest on every observation (Sec. 4.7), generate the Sobol pool
+// with its known-constraint mask (Sec. 4.5.3), score it -- MACE for one
+// objective (Sec. 4.5.1), EHVI top-k for several (Sec. 4.5.2) -- under
+// POF >= Delta (Eq. 3), and fill a shortfall with admissible Sobol points
+// (Sec. 4.7, last paragraph).  Built on the library's own entry points; the
+// pool and every score stay on the device, only k indices come back.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+namespace scoot {
+namespace {
+
+constexpr double kDefaultLo[3] = {0.01, 0.05, 1e-6};   // lengthscale, signal var, noise var
+constexpr double kDefaultHi[3] = {10.0, 20.0, 1.0};
+constexpr double kDefaultStart[3] = {0.5, 1.0, 1e-3};
+constexpr int kDefaultMleIter = 200;
+
+size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+// Box and start of objective j's likelihood search: the caller's, else the defaults.
+void theta_box(const scoot_suggest_opts& o, int j, int d, double* lo, double* hi, double* th) {
+  const int nt = d + 2;
+  for (int t = 0; t < nt; ++t) {
+    const int kind = t < d ? 0 : t - d + 1;
+    lo[t] = o.theta_lower ? o.theta_lower[(size_t)j * nt + t] : std::log(kDefaultLo[kind]);
+    hi[t] = o.theta_upper ? o.theta_upper[(size_t)j * nt + t] : std::log(kDefaultHi[kind]);
+    th[t] = o.theta_start ? o.theta_start[(size_t)j * nt + t] : std::log(kDefaultStart[kind]);
+    th[t] = std::fmin(std::fmax(th[t], lo[t]), hi[t]);
+  }
+}
+
+// Releases the handles a call creates, whatever path it leaves by.
+struct Handles {
+  std::vector<scoot_gp> gps;
+  scoot_forest forest = nullptr;
+  ~Handles() {
+    for (scoot_gp g : gps) scoot_gp_destroy(g);
+    if (forest) scoot_forest_destroy(forest);
+  }
+};
+
+bool finite_all(const double* v, size_t n) {
+  for (size_t i = 0; i < n; ++i)
+    if (!std::isfinite(v[i])) return false;
+  return true;
+}
+
+int check_space(const scoot_space* sp) {
+  if (!sp) return fail(SCOOT_ERR_INVALID_ARG, "suggest: null space");
+  if (sp->d < 1 || sp->d > SCOOT_MAX_DIM) return fail(SCOOT_ERR_INVALID_ARG, "suggest: d out of range");
+  if (!sp->levels || !sp->sobol_poly || !sp->sobol_vinit) return fail(SCOOT_ERR_INVALID_ARG, "suggest: null space table");
+  if (sp->r < 0) return fail(SCOOT_ERR_INVALID_ARG, "suggest: r < 0");
+  if (sp->r > 0 && (!sp->A || !sp->b)) return fail(SCOOT_ERR_INVALID_ARG, "suggest: null constraint rows");
+  return SCOOT_OK;
+}
+
+int check_opts(const scoot_suggest_opts* o, int p, int d) {
+  if (!o) return fail(SCOOT_ERR_INVALID_ARG, "suggest: null opts");
+  if (o->k < 1 || o->k > SCOOT_MAX_Q) return fail(SCOOT_ERR_INVALID_ARG, "suggest: k out of range");
+  if (!(o->delta >= 0.0 && o->delta <= 1.0)) return fail(SCOOT_ERR_INVALID_ARG, "suggest: delta outside [0, 1]");
+  if (o->pool_size < 1 || o->pool_size >= ((int64_t)1 << 31))
+    return fail(SCOOT_ERR_INVALID_ARG, "suggest: pool_size out of range");
+  if (o->pool_skip < 0) return fail(SCOOT_ERR_INVALID_ARG, "suggest: pool_skip < 0");
+  if (o->kernel != SCOOT_MATERN52 && o->kernel != SCOOT_MATERN32)
+    return fail(SCOOT_ERR_INVALID_ARG, "suggest: unknown kernel");
+  if (o->dtype != SCOOT_F32 && o->dtype != SCOOT_F64) return fail(SCOOT_ERR_INVALID_ARG, "suggest: unknown dtype");
+  if ((o->warp_a == nullptr) != (o->warp_b == nullptr))
+    return fail(SCOOT_ERR_INVALID_ARG, "suggest: warp_a and warp_b go together");
+  if (o->n_trees < 1 || o->n_trees > SCOOT_MAX_TREES) return fail(SCOOT_ERR_INVALID_ARG, "suggest: n_trees out of range");
+  if (o->max_depth < 0) return fail(SCOOT_ERR_INVALID_ARG, "suggest: max_depth < 0");
+  if (!std::isfinite(o->xi)) return fail(SCOOT_ERR_INVALID_ARG, "suggest: non-finite xi");
+  if (p == 1 && o->t < 1) return fail(SCOOT_ERR_INVALID_ARG, "suggest: t < 1");
+  const size_t nt = (size_t)p * (d + 2);
+  for (const double* v : {o->theta_lower, o->theta_upper, o->theta_start})
+    if (v && !finite_all(v, nt)) return fail(SCOOT_ERR_INVALID_ARG, "suggest: non-finite hyperparameter bound");
+  if (o->ref && !finite_all(o->ref, (size_t)p)) return fail(SCOOT_ERR_INVALID_ARG, "suggest: non-finite ref");
+  for (int j = 0; j < p; ++j) {
+    double lo[SCOOT_MAX_DIM + 2], hi[SCOOT_MAX_DIM + 2], th[SCOOT_MAX_DIM + 2];
+    theta_box(*o, j, d, lo, hi, th);
+    for (int t = 0; t < d + 2; ++t)
+      if (!(lo[t] <= hi[t])) return fail(SCOOT_ERR_INVALID_ARG, "suggest: theta_lower above theta_upper");
+  }
+  return SCOOT_OK;
+}
+
+}  // namespace
+}  // namespace scoot
+
+using namespace scoot;
+
+int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid, int n_obs, int p,
+                  const scoot_space* space, const scoot_suggest_opts* opts, double* x_out, int32_t* source,
+                  double* theta_out, int* n_out, void* stream) {
+  set_error("");
+  int rc = check_space(space);
+  if (rc != SCOOT_OK) return rc;
+  const int d = space->d;
+  if (p < 1 || p > SCOOT_MAX_OBJECTIVES) return fail(SCOOT_ERR_INVALID_ARG, "suggest: p out of range");
+  rc = check_opts(opts, p, d);
+  if (rc != SCOOT_OK) return rc;
+  if (n_obs < 0 || (n_obs > 0 && (!X_obs || !Y_obs || !valid)))
+    return fail(SCOOT_ERR_INVALID_ARG, "suggest: bad observations");
+  if (!x_out || !n_out) return fail(SCOOT_ERR_INVALID_ARG, "suggest: null output");
+  if (!finite_all(X_obs, (size_t)n_obs * d)) return fail(SCOOT_ERR_INVALID_ARG, "suggest: non-finite X_obs");
+  const scoot_suggest_opts& o = *opts;
+  const int k = o.k;
+  const int64_t n = o.pool_size;
+  hipStream_t s = (hipStream_t)stream;
+  try {
+    // ---- 1. valid observations, standardised per objective -------------
+    std::vector<int> rows;
+    for (int i = 0; i < n_obs; ++i)
+      if (valid[i]) rows.push_back(i);
+    const int m = (int)rows.size();
+    if (m > SCOOT_MAX_OBS) return fail(SCOOT_ERR_UNSUPPORTED, "suggest: more valid observations than SCOOT_MAX_OBS");
+    std::vector<double> Xv((size_t)m * d), Yv((size_t)m * p), mean(p, 0.0), scale(p, 1.0);
+    for (int r = 0; r < m; ++r) {
+      std::memcpy(&Xv[(size_t)r * d], X_obs + (size_t)rows[r] * d, sizeof(double) * d);
+      for (int j = 0; j < p; ++j) Yv[(size_t)r * p + j] = Y_obs[(size_t)rows[r] * p + j];
+    }
+    if (!finite_all(Yv.data(), Yv.size())) return fail(SCOOT_ERR_INVALID_ARG, "suggest: non-finite valid Y_obs");
+    for (int j = 0; j < p && m > 0; ++j) {
+      double sum = 0.0;
+      for (int r = 0; r < m; ++r) sum += Yv[(size_t)r * p + j];
+      mean[j] = sum / m;
+      double ss = 0.0;
+      for (int r = 0; r < m; ++r) {
+        const double e = Yv[(size_t)r * p + j] - mean[j];
+        ss += e * e;
+      }
+      const double sd = std::sqrt(ss / m);
+      scale[j] = sd > 0.0 ? sd : 1.0;
+      for (int r = 0; r < m; ++r) Yv[(size_t)r * p + j] = (Yv[(size_t)r * p + j] - mean[j]) / scale[j];
+    }
+
+    // ---- device scratch: pool, known mask, every score of the pass -------
+    const size_t esz = o.dtype == SCOOT_F32 ? 4 : 8;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+      const size_t at = off;
+      off += align256(bytes);
+      return at;
+    };
+    const size_t o_xc = take((size_t)n * d * 4), o_known = take((size_t)n), o_mu = take((size_t)p * n * esz),
+                 o_sd = take((size_t)p * n * esz), o_s1 = take((size_t)n * esz), o_s2 = take((size_t)n * esz),
+                 o_s3 = take((size_t)n * esz), o_votes = take((size_t)n * 4), o_mask = take((size_t)n),
+                 o_front = take((size_t)n), o_idx = take((size_t)k * 8), o_cnt = take(16), o_sc = take((size_t)k * 8);
+    unsigned char* ws = (unsigned char*)device_scratch(off, 6);
+    if (!ws) return fail(SCOOT_ERR_NO_MEMORY, "suggest: scratch allocation failed");
+    float* Xc = (float*)(ws + o_xc);
+    uint8_t* known = ws + o_known;
+    int64_t* idx_dev = (int64_t*)(ws + o_idx);
+
+    // ---- 4. pool and known constraints ---------------------------------
+    rc = scoot_sobol_pool(space->sobol_poly, space->sobol_vinit, d, space->levels, o.pool_skip, n, space->A,
+                          space->b, space->r, Xc, known, stream);
+    if (rc != SCOOT_OK) return rc;
+
+    std::vector<int64_t> picked;
+    Handles h;
+    if (m > 0) {
+      // ---- 2. hyperparameters and GPs ----------------------------------
+      const int nt = d + 2;
+      std::vector<double> theta((size_t)p * nt);
+      for (int j = 0; j < p; ++j) {
+        double lo[SCOOT_MAX_DIM + 2], hi[SCOOT_MAX_DIM + 2], th[SCOOT_MAX_DIM + 2];
+        theta_box(o, j, d, lo, hi, th);
+        bool all_fixed = true;
+        for (int t = 0; t < nt; ++t) all_fixed = all_fixed && lo[t] == hi[t];
+        std::vector<double> yj(m);
+        for (int r = 0; r < m; ++r) yj[r] = Yv[(size_t)r * p + j];
+        const double* wa = o.warp_a ? o.warp_a + (size_t)j * d : nullptr;
+        const double* wb = o.warp_b ? o.warp_b + (size_t)j * d : nullptr;
+        if (!all_fixed) {
+          rc = scoot_gp_mle(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, wa, wb, 0.0, lo, hi,
+                            o.mle_max_iter > 0 ? o.mle_max_iter : kDefaultMleIter, th, nullptr, nullptr);
+          if (rc != SCOOT_OK) return rc;
+        }
+        std::memcpy(&theta[(size_t)j * nt], th, sizeof(double) * nt);
+        double ell[SCOOT_MAX_DIM];
+        for (int t = 0; t < d; ++t) ell[t] = std::exp(th[t]);
+        scoot_gp g = nullptr;
+        rc = scoot_gp_fit_ex(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, ell, wa, wb, std::exp(th[d]),
+                             std::exp(th[d + 1]), 0.0, (scoot_dtype)o.dtype, stream, &g);
+        if (rc != SCOOT_OK) return rc;
+        h.gps.push_back(g);
+      }
+      if (theta_out) std::memcpy(theta_out, theta.data(), sizeof(double) * theta.size());
+
+      // ---- 3. feasibility forest on every observation ---------------------
+      std::vector<double> label(n_obs);
+      for (int i = 0; i < n_obs; ++i) label[i] = valid[i] ? 1.0 : 0.0;
+      rc = scoot_forest_train_create(X_obs, label.data(), n_obs, d, o.n_trees, o.max_depth, o.forest_seed,
+                                     o.bootstrap, &h.forest);
+      if (rc != SCOOT_OK) return rc;
+
+      // ---- 5. score the pool and pick ----------------------------------
+      void* mu = ws + o_mu;
+      void* sd = ws + o_sd;
+      int32_t* votes = (int32_t*)(ws + o_votes);
+      uint8_t* mask = ws + o_mask;
+      int32_t* cnt = (int32_t*)(ws + o_cnt);
+      if (p == 1) {
+        double best = Yv[0];
+        for (int r = 1; r < m; ++r) best = std::fmin(best, Yv[r]);
+        double beta = 0.0;
+        rc = scoot_ucb_beta(o.t, &beta);
+        if (rc != SCOOT_OK) return rc;
+        rc = scoot_suggest_mace_ex(h.gps[0], h.forest, known, Xc, n, best, o.xi, beta, o.delta, o.pick_seed, k, mu,
+                                   sd, ws + o_s1, ws + o_s2, ws + o_s3, votes, mask, ws + o_front, idx_dev, cnt,
+                                   stream);
+      } else {
+        double ref[SCOOT_MAX_OBJECTIVES];
+        for (int j = 0; j < p; ++j) {
+          if (o.ref) {
+            ref[j] = (o.ref[j] - mean[j]) / scale[j];
+          } else {
+            double lo = Yv[j], hi = Yv[j];
+            for (int r = 1; r < m; ++r) {
+              lo = std::fmin(lo, Yv[(size_t)r * p + j]);
+              hi = std::fmax(hi, Yv[(size_t)r * p + j]);
+            }
+            ref[j] = hi + 0.1 * (hi - lo);
+          }
+        }
+        rc = scoot_score_pool_ex(h.gps.data(), p, h.forest, known, Xc, n, 0.0, 0.0, Yv.data(), m, ref, o.delta, k,
+                                 mu, sd, ws + o_s1, votes, mask, idx_dev, ws + o_sc, cnt, stream);
+      }
+      if (rc != SCOOT_OK) return rc;
+      int64_t idx_host[SCOOT_MAX_Q];
+      if (hipMemcpyAsync(idx_host, idx_dev, sizeof(int64_t) * k, hipMemcpyDeviceToHost, s) != hipSuccess ||
+          hipStreamSynchronize(s) != hipSuccess)
+        return fail(SCOOT_ERR_DEVICE, "suggest: reading the picks back failed");
+      for (int r = 0; r < k; ++r)
+        if (idx_host[r] >= 0) picked.push_back(idx_host[r]);
+    } else if (theta_out) {
+      for (size_t t = 0; t < (size_t)p * (d + 2); ++t) theta_out[t] = NAN;
+    }
+    const int n_solver = (int)picked.size();
+
+    // ---- 6. Sobol fill ----------------------------------------------------
+    if ((int)picked.size() < k) {
+      std::vector<uint8_t> kh((size_t)n);
+      if (hipMemcpyAsync(kh.data(), known, (size_t)n, hipMemcpyDeviceToHost, s) != hipSuccess ||
+          hipStreamSynchronize(s) != hipSuccess)
+        return fail(SCOOT_ERR_DEVICE, "suggest: reading the known mask back failed");
+      std::vector<uint8_t> taken((size_t)n, 0);
+      for (int64_t i : picked) taken[(size_t)i] = 1;
+      for (int64_t i = 0; i < n && (int)picked.size() < k; ++i)
+        if (kh[(size_t)i] && !taken[(size_t)i]) picked.push_back(i);
+    }
+
+    // ---- outputs -----------------------------------------------------------
+    std::vector<float> row((size_t)d);
+    for (size_t r = 0; r < picked.size(); ++r) {
+      if (hipMemcpyAsync(row.data(), Xc + (size_t)picked[r] * d, sizeof(float) * d, hipMemcpyDeviceToHost, s) !=
+              hipSuccess ||
+          hipStreamSynchronize(s) != hipSuccess)
+        return fail(SCOOT_ERR_DEVICE, "suggest: reading a configuration back failed");
+      for (int t = 0; t < d; ++t) x_out[r * d + t] = (double)row[t];
+      if (source) source[r] = (int)r < n_solver ? 0 : 1;
+    }
+    *n_out = (int)picked.size();
+    return SCOOT_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "suggest: host allocation failed");
+  }
+}

@@ -220,3 +220,27 @@ def test_sobol_and_known_constraint_argument_checks():
     assert K(None, 0, 2, A, b, 9, None, None) == -4
     with pytest.raises(ValueError):
         S.sobol_pool([1, 3], [[0], [1]], [0], 4)      # one level per dimension
+
+
+def test_suggest_argument_checks():
+    """scoot_suggest rejects bad arguments before any device work."""
+    from tests.suggest_cases import observations, space
+    sp = space()
+    X, Y, v = observations(6, p=2)
+    bad = [dict(k=0), dict(k=65), dict(k=2, delta=1.5), dict(k=2, delta=-0.1), dict(k=2, pool_size=0),
+           dict(k=2, pool_size=2 ** 31), dict(k=2, pool_skip=-1), dict(k=2, kernel=7), dict(k=2, dtype=5),
+           dict(k=2, n_trees=0), dict(k=2, max_depth=-1), dict(k=2, xi=float("nan")),
+           dict(k=2, ref=[0.0, float("inf")]),
+           dict(k=2, theta_lower=np.zeros((2, 6)), theta_upper=-np.ones((2, 6)))]
+    for kw in bad:
+        with pytest.raises(S.ScootError) as e:
+            S.suggest(X, Y, v, sp, stream=0, **kw)
+        assert e.value.status == -1, kw
+    with pytest.raises(ValueError):  # warps go in pairs
+        S.suggest(X, Y, v, sp, k=2, warp_a=np.ones((2, 4)), stream=0)
+    with pytest.raises(S.ScootError):  # t < 1 with one objective
+        S.suggest(X, Y[:, :1], v, sp, k=2, t=0, stream=0)
+    with pytest.raises(S.ScootError):  # non-finite observation
+        Xn = X.copy()
+        Xn[0, 0] = np.nan
+        S.suggest(Xn, Y, v, sp, k=2, stream=0)
