@@ -27,7 +27,7 @@ PEAK_FP32_MFMA_TFLOPS = 157.3
 # rocprofv3 FETCH_SIZE / WRITE_SIZE passes (calibrated against a plain copy:
 # FETCH_SIZE x 2.0, WRITE_SIZE x 1.0), valid only for the kernel source they
 # were taken on.
-POSTERIOR_TRAFFIC = {"source_sha1": "35c7d48b8f1e467bcc0880520bfa984081a2e364", "bytes": 14177024}
+POSTERIOR_TRAFFIC = {"source_sha1": "b33d99cea65ed4840fa129a5a7f042ac568d71fb", "bytes": 14156244}
 
 
 def posterior_traffic():
@@ -56,6 +56,10 @@ def parse():
     ap.add_argument("--mace", action="store_true",
                     help="one-objective workloads: time the MACE suggestion (posterior, UCB/PI/EI, mask, "
                          "Pareto front, seeded pick) and print its own line")
+    ap.add_argument("--suggest", action="store_true",
+                    help="time the whole suggestion step (scoot_suggest: hyperparameter search, forest "
+                         "training, Sobol pool with known constraints, scoring, pick) on the workload's "
+                         "observations and print its own line")
     ap.add_argument("--only", choices=["all", "posterior", "forest", "ehvi", "topq", "copy"], default="all",
                     help="posterior / forest / ehvi / topq: only that kernel's loop (for profiler "
                          "counters); copy: a plain 1 GiB device copy (counter calibration)")
@@ -89,6 +93,8 @@ def main():
         print(json.dumps({"copy_bytes_read": a.numel() * 4, "copy_bytes_written": b.numel() * 4}))
         return
 
+    if args.suggest:
+        return bench_suggest(args)
     if args.config == 5:
         return bench_believer(args)
     if args.mace:
@@ -326,6 +332,72 @@ def bench_mace(args):
                                              f"depth={c['depth']} beta_t={beta:.4f} (t={w['m'] // q})",
                                  "front_size": n_front, "picks": b.idx.cpu().tolist(), "kernel_ms": parts}}),
           flush=True)
+
+
+def bench_suggest(args):
+    """One SUGGEST of Algorithm 1 on the workload's observations (every draw,
+    crashed ones included), the pool as large as the workload's, k = its q.
+    Wall time per call (host steps included), and the parts timed on their
+    own: hyperparameter search per objective, forest training, pool
+    generation, scoring pass."""
+    import numpy as np
+    import torch
+
+    import paper_2408_04323_amd as S
+    from workloads import make_workload
+    from workloads.synth import CONFIGS, levels, sobol_table, space_constraints
+
+    c = CONFIGS[args.config]
+    w = make_workload(args.config, with_forest=False)
+    d, p, n, k = w["d"], w["p"], len(w["Xc"]), w["q"]
+    X_obs, valid = w["X_draws"], w["feasible_draws"].astype(np.uint8)
+    Y_obs = np.zeros((len(X_obs), p))
+    Y_obs[valid != 0] = w["Y"]
+    poly, vinit = sobol_table(d)
+    A, b = space_constraints(c)
+    space = dict(levels=levels(c), poly=poly, vinit=vinit, A=A, b=b)
+    kw = dict(k=k, delta=w["delta"], pool_size=n, n_trees=c["trees"], max_depth=c["depth"], t=max(1, w["m"] // k))
+
+    def call():
+        out = S.suggest(X_obs, Y_obs, valid, space, **kw)
+        torch.cuda.synchronize()
+        return out
+
+    for _ in range(args.warmup):
+        x, src, theta = call()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        x, src, theta = call()
+    ms = (time.perf_counter() - t0) / args.steps * 1e3
+
+    parts = {}
+    ok = valid != 0
+    Ys = (Y_obs[ok] - Y_obs[ok].mean(0)) / Y_obs[ok].std(0)
+    lo = np.log(np.array([0.01] * d + [0.05, 1e-6]))
+    hi = np.log(np.array([10.0] * d + [20.0, 1.0]))
+    th0 = np.log(np.array([0.5] * d + [1.0, 1e-3]))
+    t0 = time.perf_counter()
+    iters = [S.gp_mle(X_obs[ok], Ys[:, j], th0, lo, hi)[2] for j in range(p)]
+    parts["mle_all_objectives"] = (time.perf_counter() - t0) * 1e3
+    t0 = time.perf_counter()
+    S.forest_train_create(X_obs, valid.astype(np.float64), c["trees"], c["depth"], seed=0)
+    parts["forest_train"] = (time.perf_counter() - t0) * 1e3
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    S.sobol_pool(poly, vinit, levels(c), n, A=A, b=b)
+    e0.record(stream)
+    for _ in range(10):
+        S.sobol_pool(poly, vinit, levels(c), n, A=A, b=b)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    parts["sobol_pool"] = e0.elapsed_time(e1) / 10
+    print(json.dumps({"metric": "suggestions (whole SUGGEST step) per second", "value": 1e3 / ms,
+                      "unit": "suggestions/s", "ms_per_step": ms, "n_gpus": 1, "steps": args.steps,
+                      "warmup": args.warmup, "higher_is_better": True, "dtype": "f32", "data": "synthetic",
+                      "config": {"workload": f"{c['name']}: {len(X_obs)} observations ({int(ok.sum())} valid) "
+                                             f"d={d} p={p} pool={n} k={k} trees={c['trees']} depth={c['depth']}",
+                                 "parts_ms": parts, "mle_iterations": iters,
+                                 "sources": src.tolist()}}), flush=True)
 
 
 def cpu_baseline(w, seconds):
