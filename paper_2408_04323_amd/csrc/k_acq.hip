@@ -11,9 +11,15 @@
 // * one or two objectives: the boxes are the column strips of the front in
 //   order of the first objective, [a_i, a_{i+1}] x [-inf, h_i]; each thread
 //   streams them, G_1 at consecutive a's carried in a register, no tables;
-// * three objectives: each thread tabulates G_j at every coordinate of every
-//   axis in its own LDS column, then sums over the box list (wave-uniform
-//   loads).
+// * three objectives: the boxes are columns [a_i, a_{i+1}] of the first axis,
+//   each cut along the second axis into consecutive ranges [b_j, b_k] over
+//   which the open region is [-inf, h] on the third.  Per column the EHVI
+//   term is (G_0(a_{i+1}) - G_0(a_i)) * sum over its boxes of
+//   (G_1(b_k) - G_1(b_j)) * G_2(h): each thread tabulates G_1 and G_2 at
+//   their axes' coordinates in its own LDS column, evaluates G_0 once per
+//   column, carries G_1 from one box to the next (the ranges are
+//   consecutive), so a box costs two table reads, a subtraction and an fma;
+//   the box records (k, h) arrive through wave-uniform loads.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -32,13 +38,6 @@ __global__ __launch_bounds__(256) void ei_kernel(const T* __restrict__ mu, const
     out[i] = partial_expectation<T>(c, mu[i], si, reciprocal(si));
   }
 }
-
-struct EhviArgs {
-  int64_t n;
-  int n_boxes;
-  int n_coord[SCOOT_MAX_OBJECTIVES];
-  int coord_off[SCOOT_MAX_OBJECTIVES];
-};
 
 constexpr int kEhviThreads = 64;
 constexpr int kStripThreads = 256;
@@ -69,40 +68,57 @@ __global__ __launch_bounds__(kStripThreads) void ehvi_strip_kernel(const T* __re
   }
 }
 
-// boxes: n_boxes records of 2P uint16 (P lower then P upper coordinate indices)
-template <typename T, int P>
-__global__ __launch_bounds__(kEhviThreads) void ehvi_kernel(
+// Three objectives.  coords: axis 0 (n0 values), then axis 1 (n1), then
+// axis 2 (n2), each starting at -inf.  rec[b] = k | (n1 + h) << 16: the LDS
+// rows of G_1(b_k) and G_2(c_h) for box b; col_end[i] = one past the last box
+// of column i (i = 0 .. n0 - 2); the boxes of a column start at j = 0.  The
+// records arrive through wave-uniform (scalar) loads, four boxes per load in
+// the unrolled loop.
+struct Ehvi3Args {
+  int64_t n;
+  int n0, n1, n2;
+};
+
+template <typename T>
+__global__ __launch_bounds__(kEhviThreads) void ehvi3_kernel(
     const T* __restrict__ mu0, const T* __restrict__ mu1, const T* __restrict__ mu2,
     const T* __restrict__ sd0, const T* __restrict__ sd1, const T* __restrict__ sd2,
-    const T* __restrict__ coords, const uint16_t* __restrict__ boxes, T* __restrict__ out,
-    const EhviArgs a) {
+    const T* __restrict__ coords, const uint32_t* __restrict__ rec, const uint32_t* __restrict__ col_end,
+    T* __restrict__ out, const Ehvi3Args a) {
   extern __shared__ __align__(16) unsigned char smem[];
-  T* g = reinterpret_cast<T*>(smem);  // [sum_j n_coord[j]][kEhviThreads]
+  T* g = reinterpret_cast<T*>(smem);  // [n1 + n2][kEhviThreads]: G_1 then G_2
   const int tid = threadIdx.x;
   int64_t c = (int64_t)blockIdx.x * kEhviThreads + tid;
   const bool live = c < a.n;
   if (!live) c = a.n - 1;
-  const T* mus[3] = {mu0, mu1, mu2};
-  const T* sds[3] = {sd0, sd1, sd2};
-#pragma unroll
-  for (int j = 0; j < P; ++j) {
-    const T m = mus[j][c], s = sds[j][c], r = reciprocal(s);
-    T* gj = g + (size_t)a.coord_off[j] * kEhviThreads;
-    gj[tid] = T(0);  // coordinate 0 is -inf
-    for (int q = 1; q < a.n_coord[j]; ++q)
-      gj[(size_t)q * kEhviThreads + tid] = partial_expectation<T>(coords[a.coord_off[j] + q], m, s, r);
-  }
+  const T m0 = mu0[c], s0 = sd0[c], r0 = reciprocal(s0);
+  const T m1 = mu1[c], s1 = sd1[c], r1 = reciprocal(s1);
+  const T m2 = mu2[c], s2 = sd2[c], r2 = reciprocal(s2);
+  const T* c0 = coords;
+  const T* c1 = coords + a.n0;
+  const T* c2 = c1 + a.n1;
+  g[tid] = T(0);  // -inf
+  for (int q = 1; q < a.n1; ++q) g[q * kEhviThreads + tid] = partial_expectation<T>(c1[q], m1, s1, r1);
+  g[a.n1 * kEhviThreads + tid] = T(0);
+  for (int q = 1; q < a.n2; ++q)
+    g[(a.n1 + q) * kEhviThreads + tid] = partial_expectation<T>(c2[q], m2, s2, r2);
   // Each thread reads only its own column: no barrier needed.
-  T acc = T(0);
-  for (int b = 0; b < a.n_boxes; ++b) {
-    const uint16_t* bx = boxes + (size_t)b * 2 * P;
-    T prod = T(1);
-#pragma unroll
-    for (int j = 0; j < P; ++j) {
-      const T* gj = g + (size_t)a.coord_off[j] * kEhviThreads;
-      prod *= gj[(size_t)bx[P + j] * kEhviThreads + tid] - gj[(size_t)bx[j] * kEhviThreads + tid];
+  T acc = T(0), g0_prev = T(0);
+  int b = 0;
+  for (int i = 0; i + 1 < a.n0; ++i) {
+    const T g0 = partial_expectation<T>(c0[i + 1], m0, s0, r0);
+    const int end = (int)col_end[i];
+    T col = T(0), g1_prev = T(0);
+#pragma unroll 4
+    for (; b < end; ++b) {
+      const uint32_t r = rec[b];
+      const T g1 = g[(r & 0xFFFFu) * kEhviThreads + tid];
+      const T g2 = g[(r >> 16) * kEhviThreads + tid];
+      col += (g1 - g1_prev) * g2;
+      g1_prev = g1;
     }
-    acc += prod;
+    acc += (g0 - g0_prev) * col;
+    g0_prev = g0;
   }
   if (live) out[c] = acc;
 }
@@ -157,53 +173,61 @@ int run_ehvi_strip(const void* const* mu, const void* const* sigma, int p, int64
 }
 
 template <typename T>
-int run_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, const BoxTable& bt,
-             void* out, hipStream_t s) {
-  // Device blob: coordinates (T), then box indices (uint16), uploaded through
-  // pinned staging on the stream.
-  EhviArgs a{};
+int run_ehvi3(const void* const* mu, const void* const* sigma, int64_t n, const BoxTable& bt, void* out,
+              hipStream_t s) {
+  Ehvi3Args a{};
   a.n = n;
-  a.n_boxes = bt.n_boxes();
-  int total = 0;
-  for (int j = 0; j < p; ++j) {
-    a.coord_off[j] = total;
-    a.n_coord[j] = (int)bt.coord[j].size();
-    total += a.n_coord[j];
-  }
-  const size_t lds = (size_t)total * kEhviThreads * sizeof(T);
-  if (lds > 160 * 1024) return fail(SCOOT_ERR_UNSUPPORTED, "ehvi: front too large for the on-chip tables");
-  const size_t coord_bytes = ((size_t)total * sizeof(T) + 15) / 16 * 16;
-  const size_t box_bytes = (size_t)a.n_boxes * 2 * p * sizeof(uint16_t);
-  std::vector<unsigned char> blob(coord_bytes + box_bytes, 0);
+  a.n0 = (int)bt.coord[0].size();
+  a.n1 = (int)bt.coord[1].size();
+  a.n2 = (int)bt.coord[2].size();
+  const size_t lds = (size_t)(a.n1 + a.n2) * kEhviThreads * sizeof(T);
+  if (lds > 160 * 1024 || a.n1 + a.n2 > 0xFFFF)
+    return fail(SCOOT_ERR_UNSUPPORTED, "ehvi: front too large for the on-chip tables");
+  // Device blob: coordinates (T), box records, column ends (uint32).
+  const int nb = bt.n_boxes();
+  const int ncol = a.n0 - 1;
+  const size_t coord_bytes = ((size_t)(a.n0 + a.n1 + a.n2) * sizeof(T) + 15) / 16 * 16;
+  const size_t rec_bytes = ((size_t)nb * 4 + 15) / 16 * 16;
+  std::vector<unsigned char> blob(coord_bytes + rec_bytes + (size_t)ncol * 4, 0);
   T* cc = reinterpret_cast<T*>(blob.data());
-  for (int j = 0; j < p; ++j)
-    for (int q = 0; q < a.n_coord[j]; ++q) cc[a.coord_off[j] + q] = (T)bt.coord[j][q];
-  uint16_t* bb = reinterpret_cast<uint16_t*>(blob.data() + coord_bytes);
-  for (int b = 0; b < a.n_boxes; ++b)
-    for (int j = 0; j < p; ++j) {
-      bb[b * 2 * p + j] = (uint16_t)bt.lo[(size_t)b * p + j];
-      bb[b * 2 * p + p + j] = (uint16_t)bt.hi[(size_t)b * p + j];
+  for (int j = 0, at = 0; j < 3; ++j)
+    for (double v : bt.coord[j]) cc[at++] = (T)v;
+  uint32_t* rr = reinterpret_cast<uint32_t*>(blob.data() + coord_bytes);
+  uint32_t* ce = reinterpret_cast<uint32_t*>(blob.data() + coord_bytes + rec_bytes);
+  // The boxes come column by column, each column's ranges consecutive from
+  // j = 0, the last axis from -inf (build_boxes); anything else is refused.
+  int col = 0, j_next = 0;
+  for (int b = 0; b < nb; ++b) {
+    const int16_t* lo = &bt.lo[(size_t)b * 3];
+    const int16_t* hi = &bt.hi[(size_t)b * 3];
+    if (lo[0] != col) {
+      if (lo[0] != col + 1 || j_next != a.n1 - 1) return fail(SCOOT_ERR_DEVICE, "ehvi: unexpected box layout");
+      ce[col++] = (uint32_t)b;
+      j_next = 0;
     }
+    if (hi[0] != lo[0] + 1 || lo[1] != j_next || hi[1] <= lo[1] || lo[2] != 0 || hi[2] < 1 || hi[2] >= a.n2)
+      return fail(SCOOT_ERR_DEVICE, "ehvi: unexpected box layout");
+    rr[b] = (uint32_t)hi[1] | (uint32_t)(a.n1 + hi[2]) << 16;
+    j_next = hi[1];
+  }
+  if (nb == 0 || col != ncol - 1 || j_next != a.n1 - 1) return fail(SCOOT_ERR_DEVICE, "ehvi: unexpected box layout");
+  ce[col] = (uint32_t)nb;
   void* dev = device_scratch(blob.size(), 1);
   if (!dev) return fail(SCOOT_ERR_NO_MEMORY, "ehvi: device scratch allocation failed");
   int rc = upload_async(dev, blob.data(), blob.size(), 0, s);
   if (rc != SCOOT_OK) return rc;
   const T* coords = reinterpret_cast<const T*>(dev);
-  const uint16_t* boxes = reinterpret_cast<const uint16_t*>((const unsigned char*)dev + coord_bytes);
-  const T* m[3] = {(const T*)mu[0], (const T*)(p > 1 ? mu[1] : mu[0]), (const T*)(p > 2 ? mu[2] : mu[0])};
-  const T* sd[3] = {(const T*)sigma[0], (const T*)(p > 1 ? sigma[1] : sigma[0]),
-                    (const T*)(p > 2 ? sigma[2] : sigma[0])};
+  const uint32_t* recs = reinterpret_cast<const uint32_t*>((const unsigned char*)dev + coord_bytes);
+  const uint32_t* col_end = reinterpret_cast<const uint32_t*>((const unsigned char*)dev + coord_bytes + rec_bytes);
   const unsigned grid = (unsigned)((n + kEhviThreads - 1) / kEhviThreads);
-  static bool attr_set[4] = {false, false, false, false};
-  auto launch = [&](auto kern) {
-    if (!attr_set[p]) {
-      (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-      attr_set[p] = true;
-    }
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(kEhviThreads), lds, s, m[0], m[1], m[2], sd[0], sd[1],
-                       sd[2], coords, boxes, (T*)out, a);
-  };
-  launch(ehvi_kernel<T, 3>);
+  static bool attr_set = false;
+  if (!attr_set) {
+    (void)hipFuncSetAttribute((const void*)ehvi3_kernel<T>, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(ehvi3_kernel<T>, dim3(grid), dim3(kEhviThreads), lds, s, (const T*)mu[0], (const T*)mu[1],
+                     (const T*)mu[2], (const T*)sigma[0], (const T*)sigma[1], (const T*)sigma[2], coords, recs,
+                     col_end, (T*)out, a);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("ehvi launch: ") + hipGetErrorString(err));
   return SCOOT_OK;
@@ -217,8 +241,8 @@ int launch_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t 
   if (p <= 2)
     return dt == SCOOT_F32 ? run_ehvi_strip<float>(mu, sigma, p, n, bt, ehvi, s)
                            : run_ehvi_strip<double>(mu, sigma, p, n, bt, ehvi, s);
-  return dt == SCOOT_F32 ? run_ehvi<float>(mu, sigma, p, n, bt, ehvi, s)
-                         : run_ehvi<double>(mu, sigma, p, n, bt, ehvi, s);
+  return dt == SCOOT_F32 ? run_ehvi3<float>(mu, sigma, n, bt, ehvi, s)
+                         : run_ehvi3<double>(mu, sigma, n, bt, ehvi, s);
 }
 
 }  // namespace scoot
