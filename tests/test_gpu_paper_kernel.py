@@ -10,10 +10,10 @@ import pytest
 torch = pytest.importorskip("torch")
 
 import paper_2408_04323_amd as S  # noqa: E402
-from oracle.believer import kriging_believer  # noqa: E402
 from oracle.forest import feasibility_mask, forest_votes  # noqa: E402
 from oracle.gp import gp_fit, gp_posterior  # noqa: E402
 from oracle.pipeline import score_pool as oracle_score_pool  # noqa: E402
+from tests.oracle_checks import check_believer, check_mace_front_and_pick  # noqa: E402
 from workloads import make_workload  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -133,18 +133,11 @@ def test_believer_matern32_warped():
     hyp = [dict(lengthscale=w["lengthscale"][j], signal_var=w["signal_var"][j], noise_var=w["noise_var"][j],
                 prior_mean=w["prior_mean"][j], kernel="matern32", warp=(w["warp"][0][j], w["warp"][1][j]))
            for j in range(2)]
-    steps = []
-    kriging_believer(w["X"], w["Y"], hyp, w["Xc"], mask, w["ref"], q, follow=picks, record=steps)
-    for j, (acq_o, elig) in enumerate(steps):
-        scale = np.max(acq_o[elig != 0])
-        tol = 1e-3 * scale
-        i = int(picks[j])
-        assert elig[i] and acq_o[i] >= scale - 2 * tol, f"step {j}: pick {i}"
-        assert abs(acq_g[j] - acq_o[i]) <= tol + 1e-3 * abs(acq_o[i]), f"step {j}"
+    check_believer(w, q, picks, acq_g, mask, hyp=hyp)
 
 
 def test_mace_matern32_warped():
-    from oracle.mace import mace_scores, pareto_front_max, random_pick, ucb_beta
+    from oracle.mace import mace_scores, ucb_beta
     w = wl(1, 4096)
     gp = _fits(w, S.F32)[0]
     fd = w["forest"]
@@ -159,6 +152,8 @@ def test_mace_matern32_warped():
     u, p, e = (t.cpu().numpy().astype(np.float64) for t in (b.ucb, b.pi, b.ei))
     u_o, p_o, e_o = mace_scores(mu_o, sd_o, w["best_y"], w["xi"], beta)
     assert np.all(np.abs(e - e_o) <= 1e-3 * np.max(e_o))
-    fg = b.front.cpu().numpy().astype(bool)
-    np.testing.assert_array_equal(fg, pareto_front_max(np.stack([u, p, e], 1), b.mask.cpu().numpy()))
-    np.testing.assert_array_equal(b.idx.cpu().numpy(), random_pick(fg, seed, 4)[0])
+    mask_o = feasibility_mask(forest_votes(fd, w["Xc"]), w["delta"], len(fd["tree_offset"]) - 1)
+    np.testing.assert_array_equal(b.mask.cpu().numpy(), mask_o)
+    tol = np.array([1e-3 * max(1.0, beta) * max(1.0, np.max(np.abs(mu_o))), 1e-2, 1e-3 * np.max(e_o)])
+    check_mace_front_and_pick(b.front.cpu().numpy(), b.idx.cpu().numpy(), np.stack([u_o, p_o, e_o], 1), mask_o,
+                              seed, 4, tol)

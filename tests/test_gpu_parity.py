@@ -21,6 +21,7 @@ from oracle.gp import gp_fit, gp_posterior  # noqa: E402
 from oracle.hypervolume import ehvi as oracle_ehvi, nondominated  # noqa: E402
 from oracle.pipeline import score_pool as oracle_score_pool  # noqa: E402
 from oracle.select import top_q  # noqa: E402
+from tests.oracle_checks import check_believer, check_topq  # noqa: E402
 from workloads import make_workload  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -42,6 +43,11 @@ def assert_close(got, want, rtol, scale, what):
     bad = ~(err <= bound)
     assert not bad.any(), (f"{what}: {bad.sum()} of {len(got)} outside tolerance; worst "
                            f"{np.max(err / np.maximum(bound, 1e-300)):.3g}x bound at {np.argmax(err / bound)}")
+
+
+def as_held(a, dtype):
+    """A seeded input as the device holds it (rounded on the host)."""
+    return np.asarray(a).astype(np.float32 if dtype == torch.float32 else np.float64).astype(np.float64)
 
 
 def dev(a, dtype=torch.float32):
@@ -155,12 +161,9 @@ def test_ei_parity(dt):
     sd[100:200] = 1e-6
     mu[200:300] = 40.0  # deep in the tail
     best = -0.7
-    want = expected_improvement(mu, sd, best, 1e-4)
     td = torch.float32 if dt == S.F32 else torch.float64
     mu_t, sd_t = dev(mu, td), dev(sd, td)
-    mu_c = mu_t.double().cpu().numpy()
-    sd_c = sd_t.double().cpu().numpy()
-    want = expected_improvement(mu_c, sd_c, best, 1e-4)
+    want = expected_improvement(as_held(mu, td), as_held(sd, td), best, 1e-4)
     say("ei", dt)
     got = S.acq_ei(mu_t, sd_t, best, 1e-4)
     torch.cuda.synchronize()
@@ -192,13 +195,37 @@ def test_ehvi_parity_shared_inputs(p, size, dt):
     td = torch.float32 if dt == S.F32 else torch.float64
     mus = [dev(mu[:, j], td) for j in range(p)]
     sds = [dev(sd[:, j], td) for j in range(p)]
-    mu_c = np.stack([t.double().cpu().numpy() for t in mus], 1)
-    sd_c = np.stack([t.double().cpu().numpy() for t in sds], 1)
+    mu_c, sd_c = as_held(mu, td), as_held(sd, td)
     want = oracle_ehvi(mu_c, sd_c, nondominated(Y, ref) if len(Y) else np.zeros((0, p)), ref)
     say("ehvi", p, size, dt)
     got = S.acq_ehvi(mus, sds, Y, ref)
     torch.cuda.synchronize()
     assert_close(got.cpu().numpy(), want, TOL[dt]["acq"], max(np.max(want), 1e-300), f"ehvi p={p}")
+
+
+@pytest.mark.parametrize("dt", [S.F32, S.F64], ids=["f32", "f64"])
+def test_ehvi3_parity_tied_coordinates(dt):
+    """Three objectives whose front shares coordinate values on every axis
+    (values on a quarter grid): merged axis coordinates, boxes spanning
+    several of them, candidates exactly on box edges."""
+    rng = np.random.default_rng(77)
+    Y = np.round(rng.standard_normal((40, 3)) * 4) / 4
+    Y[:, 2] = np.round((-0.6 * Y[:, 0] - 0.5 * Y[:, 1] + 0.3 * rng.standard_normal(40)) * 4) / 4
+    ref = Y.max(axis=0) + 0.5
+    n = 4096 + 3
+    mu = np.round(rng.standard_normal((n, 3)) * 4) / 4
+    sd = np.abs(rng.standard_normal((n, 3))) * 0.3
+    sd[:64] = 0.0
+    td = torch.float32 if dt == S.F32 else torch.float64
+    mus = [dev(mu[:, j], td) for j in range(3)]
+    sds = [dev(sd[:, j], td) for j in range(3)]
+    mu_c, sd_c = as_held(mu, td), as_held(sd, td)
+    P = nondominated(Y, ref)
+    want = oracle_ehvi(mu_c, sd_c, P, ref)
+    say("ehvi3 tied coordinates", dt, len(P))
+    got = S.acq_ehvi(mus, sds, Y, ref)
+    torch.cuda.synchronize()
+    assert_close(got.cpu().numpy(), want, TOL[dt]["acq"], np.max(want), "ehvi p=3 ties")
 
 
 @pytest.mark.parametrize("cfg", [3, 4])
@@ -211,8 +238,7 @@ def test_ehvi_parity_workload_front(cfg):
     sd = rng.uniform(0.01, 1.0, (2048, p))
     mus = [dev(mu[:, j]) for j in range(p)]
     sds = [dev(sd[:, j]) for j in range(p)]
-    mu_c = np.stack([t.double().cpu().numpy() for t in mus], 1)
-    sd_c = np.stack([t.double().cpu().numpy() for t in sds], 1)
+    mu_c, sd_c = as_held(mu, torch.float32), as_held(sd, torch.float32)
     want = oracle_ehvi(mu_c, sd_c, P, w["ref"])
     say("ehvi workload front", cfg, len(P))
     got = S.acq_ehvi(mus, sds, w["Y"], w["ref"])
@@ -336,8 +362,11 @@ def test_score_pool_end_to_end(cfg, n, dt):
 
 
 def test_full_size_two_objective_pool():
-    """The measured workload at its real size (m = 256, n = 262144, two objectives):
-    sampled outputs against the oracle one by one, integer outputs everywhere."""
+    """The measured workload at its real size (m = 256, n = 262144, two
+    objectives), in the launch configuration the bench times: mu, sigma and
+    EHVI on a sample against the oracle one by one, votes and mask everywhere,
+    and the top-q picks against the oracle's ranking of the whole pool (exact
+    where the oracle's cut is clear, within the bar at a near tie)."""
     w = wl(3, None)
     n = len(w["Xc"])
     gps = [S.gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][j], 1.0, w["noise_var"][j], dtype=S.F32)
@@ -347,27 +376,25 @@ def test_full_size_two_objective_pool():
     Xd = dev(w["Xc"])
     b = S.score_pool(gps, f, Xd, w["q"], Y_obs=w["Y"], ref=w["ref"], delta=w["delta"])
     torch.cuda.synchronize()
-    rng = np.random.default_rng(0)
-    sample = np.unique(np.concatenate([rng.integers(0, n, 1500), np.arange(n - 64, n), b.idx.cpu().numpy()]))
-    Xs = w["Xc"][sample].astype(np.float64)
-    mu_o = np.empty((len(sample), 2))
-    sd_o = np.empty((len(sample), 2))
+    mu_o = np.empty((n, 2))
+    sd_o = np.empty((n, 2))
+    X64 = w["Xc"].astype(np.float64)
     for j in range(2):
         fit = gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][j], 1.0, w["noise_var"][j])
-        mu_o[:, j], sd_o[:, j] = gp_posterior(fit, Xs)
-        assert_close(b.mu[j].cpu().numpy()[sample], mu_o[:, j], 1e-4, np.max(np.abs(mu_o[:, j])), f"mu{j}")
-        assert_close(b.sigma[j].cpu().numpy()[sample], sd_o[:, j], 1e-3, 1.0, f"sigma{j}")
+        mu_o[:, j], sd_o[:, j] = gp_posterior(fit, X64)
+    rng = np.random.default_rng(0)
+    sample = np.unique(np.concatenate([rng.integers(0, n, 20000), np.arange(n - 64, n)]))
+    for j in range(2):
+        assert_close(b.mu[j].cpu().numpy()[sample], mu_o[sample, j], 1e-4, np.max(np.abs(mu_o[:, j])), f"mu{j}")
+        assert_close(b.sigma[j].cpu().numpy()[sample], sd_o[sample, j], 1e-3, 1.0, f"sigma{j}")
     e_o = oracle_ehvi(mu_o, sd_o, nondominated(w["Y"], w["ref"]), w["ref"])
     acq = b.acq.cpu().numpy()
-    assert_close(acq[sample], e_o, 1e-3, np.max(e_o), "ehvi")
+    assert_close(acq[sample], e_o[sample], 1e-3, np.max(e_o), "ehvi")
     v_o = forest_votes(w["forest"], w["Xc"])
     np.testing.assert_array_equal(b.votes.cpu().numpy(), v_o)
     mask_o = feasibility_mask(v_o, w["delta"], 64)
     np.testing.assert_array_equal(b.mask.cpu().numpy(), mask_o)
-    # top-q of the GPU scores is exactly the oracle selection on those scores
-    want_idx, _, want_nv = top_q(acq, mask_o, w["q"])
-    assert b.idx.cpu().numpy().tolist() == want_idx.tolist()
-    assert int(b.n_valid.cpu()[0]) == want_nv
+    check_topq(b.idx.cpu().numpy(), b.n_valid.cpu()[0], e_o, mask_o, w["q"], 1e-3)
 
 
 def test_repeat_runs_bit_identical():
@@ -387,26 +414,6 @@ def test_repeat_runs_bit_identical():
 
 
 # --------------------------------------------------------------------------- believer
-def _check_believer(w, n, q, picks, acq_g, mask):
-    hyp = [dict(lengthscale=w["lengthscale"][j], signal_var=w["signal_var"][j], noise_var=w["noise_var"][j],
-                prior_mean=w["prior_mean"][j]) for j in range(w["p"])]
-    from oracle.believer import kriging_believer
-    steps = []
-    kriging_believer(w["X"], w["Y"], hyp, w["Xc"], mask, w["ref"], q, follow=picks, record=steps)
-    assert len(steps) == len(picks)
-    for j, (acq_o, elig) in enumerate(steps):
-        scale = np.max(acq_o[elig != 0])
-        tol = 1e-3 * scale
-        i = int(picks[j])
-        assert elig[i], f"step {j}: pick {i} not eligible"
-        best = np.max(acq_o[elig != 0])
-        assert acq_o[i] >= best - 2 * tol, f"step {j}: pick {i} has EHVI {acq_o[i]} below the best {best}"
-        assert abs(acq_g[j] - acq_o[i]) <= tol + 1e-3 * abs(acq_o[i]), f"step {j}: EHVI {acq_g[j]} vs {acq_o[i]}"
-        order = np.lexsort((np.arange(n), -np.where(elig != 0, acq_o, -np.inf)))
-        if acq_o[order[0]] - acq_o[order[1]] > 2 * tol:
-            assert i == order[0], f"step {j}: decided pick {order[0]} but got {i}"
-
-
 @pytest.mark.parametrize("n,m,q", [(2048 + 7, 40, 8), (16384, 200, 6)])
 def test_believer_sequence(n, m, q):
     w = wl(5, n, m)
@@ -418,7 +425,7 @@ def test_believer_sequence(n, m, q):
     torch.cuda.synchronize()
     assert len(picks) == q and len(set(picks.tolist())) == q
     mask = feasibility_mask(forest_votes(w["forest"], w["Xc"]), w["delta"], len(w["forest"]["tree_offset"]) - 1)
-    _check_believer(w, n, q, picks, acq_g, mask)
+    check_believer(w, q, picks, acq_g, mask)
 
 
 def test_believer_shortfall_and_workspace():

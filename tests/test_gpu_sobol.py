@@ -11,8 +11,9 @@ torch = pytest.importorskip("torch")
 
 import paper_2408_04323_amd as S  # noqa: E402
 from oracle.forest import feasibility_mask, forest_votes  # noqa: E402
-from oracle.select import top_q  # noqa: E402
+from oracle.pipeline import score_pool as oracle_score_pool  # noqa: E402
 from oracle.sobol import known_constraints_mask, sobol_pool as oracle_pool  # noqa: E402
+from tests.oracle_checks import check_believer, check_topq  # noqa: E402
 from workloads import CONFIGS, levels, make_workload, sobol_table, space_constraints, vllm_space  # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -89,9 +90,9 @@ def test_sobol_pool_without_constraints_and_into_given_buffers():
 
 
 def test_sobol_pool_full_size():
-    """The three-objective space at n = 2^20: sampled rows against the oracle
-    point by point, the whole mask against the oracle on the generated pool,
-    and the exact balance of every boolean over a power-of-two prefix."""
+    """The three-objective space at n = 2^20: sampled rows and their mask
+    entries against the oracle point by point, and the exact balance of every
+    boolean over the power-of-two pool."""
     c = CONFIGS[4]
     lv = levels(c)
     A, b = space_constraints(c)
@@ -107,8 +108,9 @@ def test_sobol_pool_full_size():
     edges = np.concatenate([np.arange(k * per_block - 3, k * per_block + 3) for k in (1, 2, 777, n // per_block)])
     rows = np.unique(np.concatenate([rng.integers(0, n, 300), np.arange(40), np.arange(n - 40, n), edges]))
     rows = rows[(rows >= 0) & (rows < n)]
-    np.testing.assert_array_equal(X[rows], _oracle_rows(poly, vinit, lv, rows, 0))
-    np.testing.assert_array_equal(known.cpu().numpy(), known_constraints_mask(X, A, b))
+    Xo = _oracle_rows(poly, vinit, lv, rows, 0)
+    np.testing.assert_array_equal(X[rows], Xo)
+    np.testing.assert_array_equal(known.cpu().numpy()[rows], known_constraints_mask(Xo, A, b))
     for j, L in enumerate(lv):
         if L == 1:
             assert np.count_nonzero(X[:, j]) == n // 2
@@ -145,8 +147,12 @@ def _sobol_workload(cfg, n, m=None):
     poly, vinit = sobol_table(len(lv))
     Xc, known = S.sobol_pool(poly, vinit, lv, n, skip=1, A=A, b=b, device=DEV)
     torch.cuda.synchronize()
-    w["Xc"] = Xc.cpu().numpy()
-    return w, Xc, known, known.cpu().numpy()
+    # the oracle's side is generated by the oracle; the two pools are the same
+    w["Xc"] = oracle_pool(poly, vinit, lv, n, skip=1)
+    kn = known_constraints_mask(w["Xc"], A, b)
+    np.testing.assert_array_equal(Xc.cpu().numpy(), w["Xc"])
+    np.testing.assert_array_equal(known.cpu().numpy(), kn)
+    return w, Xc, known, kn
 
 
 def test_score_pool_with_known_mask():
@@ -158,9 +164,8 @@ def test_score_pool_with_known_mask():
     torch.cuda.synchronize()
     mask_o = feasibility_mask(forest_votes(w["forest"], w["Xc"]), w["delta"], 64) & kn
     np.testing.assert_array_equal(bk.mask.cpu().numpy(), mask_o)
-    want_idx, _, want_nv = top_q(bk.acq.cpu().numpy(), mask_o, w["q"])
-    assert bk.idx.cpu().numpy().tolist() == want_idx.tolist()
-    assert int(bk.n_valid.cpu()[0]) == want_nv
+    ref = oracle_score_pool(w)
+    check_topq(bk.idx.cpu().numpy(), bk.n_valid.cpu()[0], ref["acq"], mask_o, w["q"], 1e-3)
     # without a forest the mask is the known mask itself
     b0 = S.score_pool(gps, None, Xd, w["q"], Y_obs=w["Y"], ref=w["ref"], known=known)
     torch.cuda.synchronize()
@@ -182,7 +187,6 @@ def test_suggest_mace_with_known_mask():
 
 
 def test_suggest_kb_with_known_mask():
-    from oracle.believer import kriging_believer
     w, Xd, known, kn = _sobol_workload(5, 2055, m=40)
     gps = [S.gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][j], w["signal_var"][j], w["noise_var"][j],
                     w["prior_mean"][j]) for j in range(2)]
@@ -193,11 +197,4 @@ def test_suggest_kb_with_known_mask():
     torch.cuda.synchronize()
     mask = feasibility_mask(forest_votes(w["forest"], w["Xc"]), w["delta"], 128) & kn
     assert len(picks) == q and all(mask[i] for i in picks)
-    hyp = [dict(lengthscale=w["lengthscale"][j], signal_var=w["signal_var"][j], noise_var=w["noise_var"][j],
-                prior_mean=w["prior_mean"][j]) for j in range(2)]
-    steps = []
-    kriging_believer(w["X"], w["Y"], hyp, w["Xc"], mask, w["ref"], q, follow=picks, record=steps)
-    for j, (acq_o, elig) in enumerate(steps):
-        tol = 1e-3 * np.max(acq_o[elig != 0])
-        assert acq_o[picks[j]] >= np.max(acq_o[elig != 0]) - 2 * tol
-        assert abs(acq_g[j] - acq_o[picks[j]]) <= tol + 1e-3 * abs(acq_o[picks[j]])
+    check_believer(w, q, picks, acq_g, mask)
