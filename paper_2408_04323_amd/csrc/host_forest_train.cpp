@@ -106,34 +106,42 @@ int train_forest_host(const double* X, const double* y, int n, int d, int n_tree
   }
   for (int i = 0; i < n; ++i)
     if (!std::isfinite(y[i])) return fail(SCOOT_ERR_INVALID_ARG, "forest train: non-finite label");
+  // Trees are independent: each is grown on its own (tree t by chunk
+  // t mod the chunk count) and the forest is put together in tree order.
+  std::vector<TrainedForest> trees(n_trees);
+  const int n_chunks = std::min(n_trees, 64);
+  parallel_chunks(n_chunks, [&](int c) {
+    std::vector<double> w(n);
+    for (int t = c; t < n_trees; t += n_chunks) {
+      if (bootstrap) {
+        std::fill(w.begin(), w.end(), 0.0);
+        for (int j = 0; j < n; ++j) {
+          const uint64_t r = splitmix64_host(seed, (uint64_t)t * (uint64_t)n + (uint64_t)j);
+          const double u = (double)(r >> 11) * (1.0 / 9007199254740992.0);
+          w[(int)(u * n)] += 1.0;
+        }
+      } else {
+        std::fill(w.begin(), w.end(), 1.0);
+      }
+      std::vector<int> idx;
+      for (int i = 0; i < n; ++i)
+        if (w[i] > 0) idx.push_back(i);
+      Grower g{X32, y, w, n, d, max_depth, trees[t], {}};
+      g.grow(idx, 0);  // node indices come out tree-local
+    }
+  });
   out = TrainedForest();
   out.tree_offset.push_back(0);
-  std::vector<double> w(n);
   for (int t = 0; t < n_trees; ++t) {
-    if (bootstrap) {
-      std::fill(w.begin(), w.end(), 0.0);
-      for (int j = 0; j < n; ++j) {
-        const uint64_t r = splitmix64_host(seed, (uint64_t)t * (uint64_t)n + (uint64_t)j);
-        const double u = (double)(r >> 11) * (1.0 / 9007199254740992.0);
-        w[(int)(u * n)] += 1.0;
-      }
-    } else {
-      std::fill(w.begin(), w.end(), 1.0);
-    }
-    std::vector<int> idx;
-    for (int i = 0; i < n; ++i)
-      if (w[i] > 0) idx.push_back(i);
-    const int base = (int)out.feature.size();
-    Grower g{X32, y, w, n, d, max_depth, out, {}};
-    g.grow(idx, 0);
-    // tree-local child indices
-    for (size_t k = base; k < out.feature.size(); ++k) {
-      if (out.left[k] >= 0) out.left[k] -= base;
-      if (out.right[k] >= 0) out.right[k] -= base;
-    }
-    out.tree_offset.push_back((int64_t)out.feature.size());
-    if (out.feature.size() - base > (size_t)kChunkNodes - 1)
+    const TrainedForest& tr = trees[t];
+    if (tr.feature.size() > (size_t)kChunkNodes - 1)
       return fail(SCOOT_ERR_UNSUPPORTED, "forest train: a tree has more than 8191 nodes (lower max_depth)");
+    out.feature.insert(out.feature.end(), tr.feature.begin(), tr.feature.end());
+    out.threshold.insert(out.threshold.end(), tr.threshold.begin(), tr.threshold.end());
+    out.left.insert(out.left.end(), tr.left.begin(), tr.left.end());
+    out.right.insert(out.right.end(), tr.right.begin(), tr.right.end());
+    out.value.insert(out.value.end(), tr.value.begin(), tr.value.end());
+    out.tree_offset.push_back((int64_t)out.feature.size());
   }
   return SCOOT_OK;
 }

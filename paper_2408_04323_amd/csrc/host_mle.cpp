@@ -37,25 +37,50 @@ struct MleData {
   std::vector<double> r;   // y - c
 };
 
-// In-place lower Cholesky of the m x m row-major A (upper part ignored);
-// false when not numerically positive definite.
+constexpr int kChunks = 32;  // work split of every parallel step (independent of the thread count)
+constexpr int kBlk = 32;     // block columns of the Cholesky factorisation
+
+double dot(const double* a, const double* b, int n) {
+  double s = 0.0;
+#pragma omp simd reduction(+ : s)
+  for (int k = 0; k < n; ++k) s += a[k] * b[k];
+  return s;
+}
+
+// In-place lower Cholesky of the m x m row-major A (upper part ignored),
+// left-looking by block columns of kBlk: the diagonal block's rows are
+// brought up to date and factored on the calling thread, then every row below
+// it is updated with the earlier columns and solved against the block in
+// parallel (rows independent).  Each entry is formed by the same sequence of
+// operations whatever the thread count.  False when not numerically positive
+// definite.
 bool cholesky(std::vector<double>& A, int m) {
   double* L = A.data();
-  for (int i = 0; i < m; ++i) {
-    double* Li = L + (size_t)i * m;
-    for (int j = 0; j <= i; ++j) {
-      const double* Lj = L + (size_t)j * m;
-      double dot = 0.0;
-#pragma omp simd reduction(+ : dot)
-      for (int k = 0; k < j; ++k) dot += Li[k] * Lj[k];
-      const double s = Li[j] - dot;
-      if (i == j) {
-        if (!(s > 1e-13 * Li[j])) return false;
-        Li[i] = std::sqrt(s);
-      } else {
-        Li[j] = s / Lj[j];
+  for (int J = 0; J < m; J += kBlk) {
+    const int je = std::min(m, J + kBlk);
+    for (int i = J; i < je; ++i) {
+      double* Li = L + (size_t)i * m;
+      for (int j = J; j <= i; ++j) {
+        const double* Lj = L + (size_t)j * m;
+        const double s = Li[j] - dot(Li, Lj, j);
+        if (i == j) {
+          if (!(s > 1e-13 * Li[j])) return false;
+          Li[i] = std::sqrt(s);
+        } else {
+          Li[j] = s / Lj[j];
+        }
       }
     }
+    if (je == m) break;
+    parallel_chunks(kChunks, [&](int c) {
+      for (int i = je + c; i < m; i += kChunks) {
+        double* Li = L + (size_t)i * m;
+        for (int j = J; j < je; ++j) {
+          const double* Lj = L + (size_t)j * m;
+          Li[j] = (Li[j] - dot(Li, Lj, j)) / Lj[j];
+        }
+      }
+    });
   }
   return true;
 }
@@ -63,26 +88,28 @@ bool cholesky(std::vector<double>& A, int m) {
 // NLL and gradient at theta; false when K is not positive definite.
 bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) {
   const int m = D.m, d = D.d;
-  std::vector<double> inv_ls(d);
+  double inv_ls[SCOOT_MAX_DIM];
   for (int k = 0; k < d; ++k) inv_ls[k] = std::exp(-theta[k]);
   const double s2 = std::exp(theta[d]), tau2 = std::exp(theta[d + 1]);
   const bool m52 = D.kernel == SCOOT_MATERN52;
   const double root = m52 ? kSqrt5m : kSqrt3m;
   const double* X = D.Xw.data();
 
-  // K (lower triangle) and its Cholesky factor
+  // K (lower triangle), rows in parallel, then its Cholesky factor
   std::vector<double> L((size_t)m * m, 0.0);
-  for (int i = 0; i < m; ++i)
-    for (int j = 0; j <= i; ++j) {
-      double r2 = 0.0;
-      for (int k = 0; k < d; ++k) {
-        const double t = (X[(size_t)i * d + k] - X[(size_t)j * d + k]) * inv_ls[k];
-        r2 += t * t;
+  parallel_chunks(kChunks, [&](int c) {
+    for (int i = c; i < m; i += kChunks)
+      for (int j = 0; j <= i; ++j) {
+        double r2 = 0.0;
+        for (int k = 0; k < d; ++k) {
+          const double t = (X[(size_t)i * d + k] - X[(size_t)j * d + k]) * inv_ls[k];
+          r2 += t * t;
+        }
+        const double t = root * std::sqrt(r2);
+        const double kv = m52 ? s2 * (1.0 + t + t * t / 3.0) * std::exp(-t) : s2 * (1.0 + t) * std::exp(-t);
+        L[(size_t)i * m + j] = kv + (i == j ? tau2 : 0.0);
       }
-      const double t = root * std::sqrt(r2);
-      const double kv = m52 ? s2 * (1.0 + t + t * t / 3.0) * std::exp(-t) : s2 * (1.0 + t) * std::exp(-t);
-      L[(size_t)i * m + j] = kv + (i == j ? tau2 : 0.0);
-    }
+  });
   if (!cholesky(L, m)) return false;
 
   // alpha = K^-1 r and log det K
@@ -90,10 +117,7 @@ bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) 
   double logdet = 0.0;
   for (int i = 0; i < m; ++i) {
     const double* Li = L.data() + (size_t)i * m;
-    double dot = 0.0;
-#pragma omp simd reduction(+ : dot)
-    for (int k = 0; k < i; ++k) dot += Li[k] * z[k];
-    z[i] = (D.r[i] - dot) / Li[i];
+    z[i] = (D.r[i] - dot(Li, z.data(), i)) / Li[i];
     logdet += 2.0 * std::log(Li[i]);
   }
   for (int i = m - 1; i >= 0; --i) {
@@ -106,54 +130,54 @@ bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) 
   *nll = 0.5 * quad + 0.5 * logdet + 0.5 * m * kLog2Pi;
   if (!grad) return true;
 
-  // K^-1 = L^-T L^-1: Linv by forward substitution, then its Gram matrix.
-  std::vector<double> Li((size_t)m * m, 0.0);
-  std::vector<double> w(m);
-  for (int j = 0; j < m; ++j) {
-    w[j] = 1.0 / L[(size_t)j * m + j];
-    Li[(size_t)j * m + j] = w[j];
-    for (int i = j + 1; i < m; ++i) {
-      const double* Lr = L.data() + (size_t)i * m;
-      double s = 0.0;
-#pragma omp simd reduction(+ : s)
-      for (int k = j; k < i; ++k) s += Lr[k] * w[k];
-      w[i] = -s / Lr[i];
-      Li[(size_t)i * m + j] = w[i];
-    }
-  }
-  // Kinv[i][j] = sum_{k >= max(i, j)} Li[k][i] Li[k][j]; with the columns of
-  // Li stored as rows of its transpose this is a dot product of two rows.
+  // K^-1 = L^-T L^-1.  Column j of L^-1 (forward substitution, columns
+  // independent) is stored as row j of Lt, so that
+  // K^-1[i][j] = sum_{k >= max(i, j)} Lt[i][k] Lt[j][k] is a dot product of two rows.
   std::vector<double> Lt((size_t)m * m, 0.0);
-  for (int k = 0; k < m; ++k)
-    for (int i = 0; i <= k; ++i) Lt[(size_t)i * m + k] = Li[(size_t)k * m + i];
-
-  std::vector<double> g(d + 2, 0.0);
-  for (int i = 0; i < m; ++i) {
-    const double* ti = Lt.data() + (size_t)i * m;
-    for (int j = 0; j <= i; ++j) {
-      const double* tj = Lt.data() + (size_t)j * m;
-      double kinv = 0.0;
-#pragma omp simd reduction(+ : kinv)
-      for (int k = i; k < m; ++k) kinv += ti[k] * tj[k];
-      const double Wij = alpha[i] * alpha[j] - kinv;
-      const double mult = i == j ? 1.0 : 2.0;  // W and dK are symmetric
-      double r2 = 0.0;
-      double D2[SCOOT_MAX_DIM];
-      for (int k = 0; k < d; ++k) {
-        const double t = (X[(size_t)i * d + k] - X[(size_t)j * d + k]) * inv_ls[k];
-        D2[k] = t * t;
-        r2 += D2[k];
+  parallel_chunks(kChunks, [&](int c) {
+    for (int j = c; j < m; j += kChunks) {
+      double* w = Lt.data() + (size_t)j * m;
+      w[j] = 1.0 / L[(size_t)j * m + j];
+      for (int i = j + 1; i < m; ++i) {
+        const double* Lr = L.data() + (size_t)i * m;
+        w[i] = -dot(Lr + j, w + j, i - j) / Lr[i];
       }
-      const double t = root * std::sqrt(r2);
-      const double e = std::exp(-t);
-      const double kf = m52 ? s2 * (1.0 + t + t * t / 3.0) * e : s2 * (1.0 + t) * e;
-      const double radial = m52 ? 5.0 / 3.0 * s2 * (1.0 + t) * e : 3.0 * s2 * e;
-      for (int k = 0; k < d; ++k) g[k] -= 0.5 * mult * Wij * radial * D2[k];
-      g[d] -= 0.5 * mult * Wij * kf;
-      if (i == j) g[d + 1] -= 0.5 * Wij * tau2;
     }
+  });
+
+  // Gradient: pairs (i, j <= i) by rows, partial sums per chunk, added in chunk order.
+  std::vector<double> part((size_t)kChunks * (d + 2), 0.0);
+  parallel_chunks(kChunks, [&](int c) {
+    double* g = part.data() + (size_t)c * (d + 2);
+    for (int i = c; i < m; i += kChunks) {
+      const double* ti = Lt.data() + (size_t)i * m;
+      for (int j = 0; j <= i; ++j) {
+        const double* tj = Lt.data() + (size_t)j * m;
+        const double kinv = dot(ti + i, tj + i, m - i);
+        const double Wij = alpha[i] * alpha[j] - kinv;
+        const double mult = i == j ? 1.0 : 2.0;  // W and dK are symmetric
+        double r2 = 0.0;
+        double D2[SCOOT_MAX_DIM];
+        for (int k = 0; k < d; ++k) {
+          const double t = (X[(size_t)i * d + k] - X[(size_t)j * d + k]) * inv_ls[k];
+          D2[k] = t * t;
+          r2 += D2[k];
+        }
+        const double t = root * std::sqrt(r2);
+        const double e = std::exp(-t);
+        const double kf = m52 ? s2 * (1.0 + t + t * t / 3.0) * e : s2 * (1.0 + t) * e;
+        const double radial = m52 ? 5.0 / 3.0 * s2 * (1.0 + t) * e : 3.0 * s2 * e;
+        for (int k = 0; k < d; ++k) g[k] -= 0.5 * mult * Wij * radial * D2[k];
+        g[d] -= 0.5 * mult * Wij * kf;
+        if (i == j) g[d + 1] -= 0.5 * Wij * tau2;
+      }
+    }
+  });
+  for (int k = 0; k < d + 2; ++k) {
+    double s = 0.0;
+    for (int c = 0; c < kChunks; ++c) s += part[(size_t)c * (d + 2) + k];
+    grad[k] = s;
   }
-  std::memcpy(grad, g.data(), sizeof(double) * (d + 2));
   return true;
 }
 

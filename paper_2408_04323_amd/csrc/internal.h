@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstddef>
 #include <cstdint>
+#include <functional>
 #include <string>
 #include <vector>
 
@@ -120,6 +121,13 @@ inline RowPlan plan_rows(int nb, int W) {
   p.blk_start[8] = b;
   return p;
 }
+
+// Runs fn(c) for every chunk c = 0 .. n_chunks - 1 on the library's pool of
+// host threads (the caller takes part) and returns when all have run.  The
+// chunking is the caller's and must not depend on the thread count; fn must
+// not call parallel_chunks itself.  Pool size: SCOOT_HOST_THREADS, else the
+// hardware threads up to 16.
+void parallel_chunks(int n_chunks, const std::function<void(int)>& fn);
 
 void set_error(const std::string& msg);
 int fail(int status, const std::string& msg);

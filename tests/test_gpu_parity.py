@@ -397,6 +397,44 @@ def test_full_size_two_objective_pool():
     check_topq(b.idx.cpu().numpy(), b.n_valid.cpu()[0], e_o, mask_o, w["q"], 1e-3)
 
 
+def test_full_size_three_objective_pool():
+    """The three-objective workload at its real size (m = 512, n = 2^20, d = 12:
+    the eight-wave posterior, the per-column EHVI, 128 trees of depth 12), in
+    the launch configuration the bench times: mu, sigma, EHVI, votes and the
+    mask on a seeded sample of candidates against the oracle one by one, and
+    the picks eligible, distinct and in order of the library's own scores."""
+    w = wl(4, None)
+    n, p = len(w["Xc"]), 3
+    gps = [S.gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][j], 1.0, w["noise_var"][j], dtype=S.F32)
+           for j in range(p)]
+    f = _forest(w["forest"], w["d"])
+    say("full size cfg4", n)
+    b = S.score_pool(gps, f, dev(w["Xc"]), w["q"], Y_obs=w["Y"], ref=w["ref"], delta=w["delta"])
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(1)
+    sample = np.unique(np.concatenate([rng.integers(0, n, 3000), np.arange(n - 64, n)]))
+    Xs = w["Xc"][sample].astype(np.float64)
+    mu_o = np.empty((len(sample), p))
+    sd_o = np.empty((len(sample), p))
+    for j in range(p):
+        fit = gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][j], 1.0, w["noise_var"][j])
+        mu_o[:, j], sd_o[:, j] = gp_posterior(fit, Xs)
+        assert_close(b.mu[j].cpu().numpy()[sample], mu_o[:, j], 1e-4, np.max(np.abs(mu_o[:, j])), f"mu{j}")
+        assert_close(b.sigma[j].cpu().numpy()[sample], sd_o[:, j], 1e-3, 1.0, f"sigma{j}")
+    e_o = oracle_ehvi(mu_o, sd_o, nondominated(w["Y"], w["ref"]), w["ref"])
+    acq = b.acq.cpu().numpy()
+    assert_close(acq[sample], e_o, 1e-3, np.max(e_o), "ehvi")
+    v_o = forest_votes(w["forest"], w["Xc"][sample])
+    np.testing.assert_array_equal(b.votes.cpu().numpy()[sample], v_o)
+    mask_o = feasibility_mask(v_o, w["delta"], len(w["forest"]["tree_offset"]) - 1)
+    mask_g = b.mask.cpu().numpy()
+    np.testing.assert_array_equal(mask_g[sample], mask_o)
+    got = b.idx.cpu().numpy()
+    assert len(set(got.tolist())) == len(got) and np.all(mask_g[got] == 1)
+    assert np.all(np.diff(acq[got]) <= 0) and acq[got[-1]] >= np.max(np.where(mask_g != 0, acq, -np.inf)[
+        np.setdiff1d(np.arange(n), got)])
+
+
 def test_repeat_runs_bit_identical():
     w = wl(3, 16384)
     gps = [S.gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][j], 1.0, w["noise_var"][j]) for j in range(2)]
