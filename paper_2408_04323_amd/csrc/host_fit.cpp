@@ -81,44 +81,28 @@ int fit_host(const double* X, const double* y, int m, int d, scoot_kernel kernel
       for (int k = 0; k < d; ++k) f.Xw[(size_t)i * d + k] = kumaraswamy(X[(size_t)i * d + k], warp_a[k], warp_b[k]);
   }
 
-  // K = k(X, X) + tau^2 I (lower triangle is all the factorisation reads).
-  std::vector<double> K((size_t)m * m, 0.0);
-  const double* Xw = f.Xw.data();
-  for (int i = 0; i < m; ++i) {
-    for (int j = 0; j <= i; ++j) {
-      double r2 = 0;
-      for (int k = 0; k < d; ++k) {
-        double t = (Xw[(size_t)i * d + k] - Xw[(size_t)j * d + k]) * inv_ls[k];
-        r2 += t * t;
-      }
-      const double t = root * std::sqrt(r2);
-      const double kv = kernel == SCOOT_MATERN52 ? s2 * (1.0 + t + t * t / 3.0) * std::exp(-t)
-                                                 : s2 * (1.0 + t) * std::exp(-t);
-      K[(size_t)i * m + j] = kv + (i == j ? tau2 : 0.0);
-    }
-  }
-
-  // Row-oriented Cholesky, L L^T = K.  A pivot that is not positive, or below
-  // 1e-13 of its diagonal entry, means K is not numerically positive definite.
+  // K = k(X, X) + tau^2 I (lower triangle; rows in parallel), factored in place.
   f.L.assign((size_t)m * m, 0.0);
   double* L = f.L.data();
-  for (int i = 0; i < m; ++i) {
-    const double* Li = L + (size_t)i * m;
-    for (int j = 0; j <= i; ++j) {
-      const double* Lj = L + (size_t)j * m;
-      double dot = 0.0;
-#pragma omp simd reduction(+ : dot)
-      for (int k = 0; k < j; ++k) dot += Li[k] * Lj[k];
-      double s = K[(size_t)i * m + j] - dot;
-      if (i == j) {
-        double kii = K[(size_t)i * m + i];
-        if (!(s > 1e-13 * kii)) return fail(SCOOT_ERR_NOT_PD, "gp fit: K + tau^2 I is not positive definite");
-        L[(size_t)i * m + i] = std::sqrt(s);
-      } else {
-        L[(size_t)i * m + j] = s / Lj[j];
+  const double* Xw = f.Xw.data();
+  constexpr int kChunks = 32;
+  parallel_chunks(kChunks, [&](int ch) {
+    for (int i = ch; i < m; i += kChunks)
+      for (int j = 0; j <= i; ++j) {
+        double r2 = 0;
+        for (int k = 0; k < d; ++k) {
+          double t = (Xw[(size_t)i * d + k] - Xw[(size_t)j * d + k]) * inv_ls[k];
+          r2 += t * t;
+        }
+        const double t = root * std::sqrt(r2);
+        const double kv = kernel == SCOOT_MATERN52 ? s2 * (1.0 + t + t * t / 3.0) * std::exp(-t)
+                                                   : s2 * (1.0 + t) * std::exp(-t);
+        L[(size_t)i * m + j] = kv + (i == j ? tau2 : 0.0);
       }
-    }
-  }
+  });
+  // L L^T = K.  A pivot that is not positive, or below 1e-13 of its diagonal
+  // entry, means K is not numerically positive definite.
+  if (!cholesky_lower(L, m)) return fail(SCOOT_ERR_NOT_PD, "gp fit: K + tau^2 I is not positive definite");
 
   // alpha = L^-T L^-1 (y - c).
   std::vector<double> z(m);
@@ -138,19 +122,7 @@ int fit_host(const double* X, const double* y, int m, int d, scoot_kernel kernel
 
   // L^-1 column by column: forward substitution of L w = e_j.
   f.Linv.assign((size_t)m * m, 0.0);
-  std::vector<double> w(m);
-  for (int j = 0; j < m; ++j) {
-    w[j] = 1.0 / L[(size_t)j * m + j];
-    f.Linv[(size_t)j * m + j] = w[j];
-    for (int i = j + 1; i < m; ++i) {
-      const double* Li = L + (size_t)i * m;
-      double s = 0;
-#pragma omp simd reduction(+ : s)
-      for (int k = j; k < i; ++k) s += Li[k] * w[k];
-      w[i] = -s / Li[i];
-      f.Linv[(size_t)i * m + j] = w[i];
-    }
-  }
+  lower_inverse(L, m, f.Linv.data(), false);
   return SCOOT_OK;
 }
 

@@ -38,51 +38,12 @@ struct MleData {
 };
 
 constexpr int kChunks = 32;  // work split of every parallel step (independent of the thread count)
-constexpr int kBlk = 32;     // block columns of the Cholesky factorisation
 
 double dot(const double* a, const double* b, int n) {
   double s = 0.0;
 #pragma omp simd reduction(+ : s)
   for (int k = 0; k < n; ++k) s += a[k] * b[k];
   return s;
-}
-
-// In-place lower Cholesky of the m x m row-major A (upper part ignored),
-// left-looking by block columns of kBlk: the diagonal block's rows are
-// brought up to date and factored on the calling thread, then every row below
-// it is updated with the earlier columns and solved against the block in
-// parallel (rows independent).  Each entry is formed by the same sequence of
-// operations whatever the thread count.  False when not numerically positive
-// definite.
-bool cholesky(std::vector<double>& A, int m) {
-  double* L = A.data();
-  for (int J = 0; J < m; J += kBlk) {
-    const int je = std::min(m, J + kBlk);
-    for (int i = J; i < je; ++i) {
-      double* Li = L + (size_t)i * m;
-      for (int j = J; j <= i; ++j) {
-        const double* Lj = L + (size_t)j * m;
-        const double s = Li[j] - dot(Li, Lj, j);
-        if (i == j) {
-          if (!(s > 1e-13 * Li[j])) return false;
-          Li[i] = std::sqrt(s);
-        } else {
-          Li[j] = s / Lj[j];
-        }
-      }
-    }
-    if (je == m) break;
-    parallel_chunks(kChunks, [&](int c) {
-      for (int i = je + c; i < m; i += kChunks) {
-        double* Li = L + (size_t)i * m;
-        for (int j = J; j < je; ++j) {
-          const double* Lj = L + (size_t)j * m;
-          Li[j] = (Li[j] - dot(Li, Lj, j)) / Lj[j];
-        }
-      }
-    });
-  }
-  return true;
 }
 
 // NLL and gradient at theta; false when K is not positive definite.
@@ -110,7 +71,7 @@ bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) 
         L[(size_t)i * m + j] = kv + (i == j ? tau2 : 0.0);
       }
   });
-  if (!cholesky(L, m)) return false;
+  if (!cholesky_lower(L.data(), m)) return false;
 
   // alpha = K^-1 r and log det K
   std::vector<double> z(m), alpha(m);
@@ -134,16 +95,7 @@ bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) 
   // independent) is stored as row j of Lt, so that
   // K^-1[i][j] = sum_{k >= max(i, j)} Lt[i][k] Lt[j][k] is a dot product of two rows.
   std::vector<double> Lt((size_t)m * m, 0.0);
-  parallel_chunks(kChunks, [&](int c) {
-    for (int j = c; j < m; j += kChunks) {
-      double* w = Lt.data() + (size_t)j * m;
-      w[j] = 1.0 / L[(size_t)j * m + j];
-      for (int i = j + 1; i < m; ++i) {
-        const double* Lr = L.data() + (size_t)i * m;
-        w[i] = -dot(Lr + j, w + j, i - j) / Lr[i];
-      }
-    }
-  });
+  lower_inverse(L.data(), m, Lt.data(), true);
 
   // Gradient: pairs (i, j <= i) by rows, partial sums per chunk, added in chunk order.
   std::vector<double> part((size_t)kChunks * (d + 2), 0.0);

@@ -129,6 +129,14 @@ inline RowPlan plan_rows(int nb, int W) {
 // hardware threads up to 16.
 void parallel_chunks(int n_chunks, const std::function<void(int)>& fn);
 
+// In-place lower Cholesky factor of the m x m row-major A (the lower
+// triangle is read; the upper is zeroed); false when a pivot is not positive
+// or below 1e-13 of its diagonal entry.  Host threads, fixed chunking.
+bool cholesky_lower(double* A, int m);
+// L^-1 of a lower-triangular L (m x m row-major) into out (m x m, zero above
+// the diagonal; transposed: out[j][i] = L^-1[i][j], zero below).
+void lower_inverse(const double* L, int m, double* out, bool transposed);
+
 void set_error(const std::string& msg);
 int fail(int status, const std::string& msg);
 
