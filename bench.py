@@ -27,7 +27,7 @@ PEAK_FP32_MFMA_TFLOPS = 157.3
 # rocprofv3 FETCH_SIZE / WRITE_SIZE passes (calibrated against a plain copy:
 # FETCH_SIZE x 2.0, WRITE_SIZE x 1.0), valid only for the kernel source they
 # were taken on.
-POSTERIOR_TRAFFIC = {"source_sha1": "b33d99cea65ed4840fa129a5a7f042ac568d71fb", "bytes": 14156244}
+POSTERIOR_TRAFFIC = {"source_sha1": "f07bb5d7aa028e7ad626f935cf8a65b5b3f66c35", "bytes": 14152293}
 
 
 def posterior_traffic():

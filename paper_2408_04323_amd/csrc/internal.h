@@ -266,7 +266,8 @@ int upload_async(void* dst, const void* src, size_t bytes, int slot, void* strea
 // launch_warp_pool; fp64: inside the kernel), unless xc_warped says Xc already is.
 int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, void* sigma,
                      const double* ei_c /* nullable: fused EI with c = best + xi */, void* ei,
-                     void* stream, float* v_out = nullptr, bool xc_warped = false);
+                     void* stream, float* v_out = nullptr, bool xc_warped = false,
+                     int64_t v_ld = 0 /* row stride of v_out; 0: n */);
 int launch_warp_pool(const GPDevice& g, const float* Xc, int64_t n, float* out, void* stream);
 int launch_ei(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double c, void* ei,
               void* stream);

@@ -40,7 +40,14 @@ struct KbArgs {
   float c0, c1, c2;
 };
 
-// New row of V and the variance downdate, one candidate per thread.
+// New row of V and the variance downdate, one candidate per thread: each
+// thread reads its column of V sixteen rows at a time with every load issued
+// before the first is used (a wave keeps 16 x 256 bytes in flight), on two
+// accumulation chains.  Measured at n = 2^20, m = 512 against four rows in
+// flight: 2% less time per suggestion; two or four candidates per thread
+// (8- or 16-byte loads, fewer waves) were slower.
+constexpr int kKbRows = 16;
+
 __global__ __launch_bounds__(kKbThreads) void kb_update_kernel(float* __restrict__ V, const float* __restrict__ vp_g,
                                                                const float* __restrict__ dinv_g,
                                                                const float* __restrict__ Xc, float* __restrict__ sd,
@@ -51,16 +58,21 @@ __global__ __launch_bounds__(kKbThreads) void kb_update_kernel(float* __restrict
   const float dinv = dinv_g[0];
   const float* xp = Xc + a.pick * a.d;
   for (int64_t x = (int64_t)blockIdx.x * kKbThreads + threadIdx.x; x < a.n; x += (int64_t)gridDim.x * kKbThreads) {
-    float acc0 = 0.0f, acc1 = 0.0f, acc2 = 0.0f, acc3 = 0.0f;
+    const float* col = V + x;
+    float acc0 = 0.0f, acc1 = 0.0f;
     int i = 0;
-    for (; i + 3 < a.rows; i += 4) {
-      acc0 = fmaf(vp[i + 0], V[(int64_t)(i + 0) * a.ld + x], acc0);
-      acc1 = fmaf(vp[i + 1], V[(int64_t)(i + 1) * a.ld + x], acc1);
-      acc2 = fmaf(vp[i + 2], V[(int64_t)(i + 2) * a.ld + x], acc2);
-      acc3 = fmaf(vp[i + 3], V[(int64_t)(i + 3) * a.ld + x], acc3);
+    for (; i + kKbRows - 1 < a.rows; i += kKbRows) {
+      float v[kKbRows];
+#pragma unroll
+      for (int r = 0; r < kKbRows; ++r) v[r] = col[(int64_t)(i + r) * a.ld];
+#pragma unroll
+      for (int r = 0; r < kKbRows; r += 2) {
+        acc0 = fmaf(vp[i + r], v[r], acc0);
+        acc1 = fmaf(vp[i + r + 1], v[r + 1], acc1);
+      }
     }
-    for (; i < a.rows; ++i) acc0 = fmaf(vp[i], V[(int64_t)i * a.ld + x], acc0);
-    const float dot = (acc0 + acc1) + (acc2 + acc3);
+    for (; i < a.rows; ++i) acc0 = fmaf(vp[i], col[(int64_t)i * a.ld], acc0);
+    const float dot = acc0 + acc1;
     // k(x, x_p): same covariance and constants as the posterior kernel
     float r2 = 0.0f;
     for (int k = 0; k < a.d; ++k) {
@@ -80,6 +92,8 @@ __global__ void kb_exclude_kernel(uint8_t* __restrict__ eligible, int64_t pick) 
 
 namespace {
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+// Row stride of a kept V: n rounded up to 64 floats (256 bytes).
+int64_t kb_ld(int64_t n) { return (n + 63) / 64 * 64; }
 
 struct KbLayout {
   size_t v, mu, sd, acq, elig, votes, idx, score, nvalid, vp, dinv, xw, total;
@@ -96,7 +110,7 @@ KbLayout kb_layout(const GPDevice* const* g, int p, int64_t n, int q) {
   size_t vbytes = 0;
   int rows_max = 0;
   for (int j = 0; j < p; ++j) {
-    vbytes += align256((size_t)(g[j]->m_pad + q) * n * 4);
+    vbytes += align256((size_t)(g[j]->m_pad + q) * kb_ld(n) * 4);
     rows_max = std::max(rows_max, g[j]->m_pad + q);
   }
   L.v = take(vbytes);
@@ -127,10 +141,11 @@ int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f,
   const KbLayout L = kb_layout(g, p, n, q);
   unsigned char* w = (unsigned char*)ws;
   float* V[SCOOT_MAX_OBJECTIVES];
+  const int64_t ld = kb_ld(n);
   size_t voff = L.v;
   for (int j = 0; j < p; ++j) {
     V[j] = (float*)(w + voff);
-    voff += align256((size_t)(g[j]->m_pad + q) * n * 4);
+    voff += align256((size_t)(g[j]->m_pad + q) * ld * 4);
   }
   float* mu = (float*)(w + L.mu);
   float* sd = (float*)(w + L.sd);
@@ -165,7 +180,7 @@ int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f,
     mus[j] = mu + (size_t)j * n;
     sds[j] = sd + (size_t)j * n;
     int rc = launch_posterior(*g[j], xg[j], n, mu + (size_t)j * n, sd + (size_t)j * n, nullptr, nullptr, stream, V[j],
-                              true);
+                              true, ld);
     if (rc != SCOOT_OK) return rc;
   }
   int rc = f ? launch_forest(*f, Xc, n, vote_min, votes, elig, nullptr, stream, known)
@@ -202,11 +217,11 @@ int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f,
     for (int j = 0; j < p; ++j) {
       const int rows = g[j]->m_pad + k;
       float* vpj = vp + (size_t)j * rows_max;
-      hipLaunchKernelGGL(kb_gather_kernel, dim3(1), dim3(kKbThreads), 0, s, V[j], n, rows, pick,
+      hipLaunchKernelGGL(kb_gather_kernel, dim3(1), dim3(kKbThreads), 0, s, V[j], ld, rows, pick,
                          sd + (size_t)j * n, g[j]->tau2, vpj, dinv + j);
       KbArgs a{};
       a.n = n;
-      a.ld = n;
+      a.ld = ld;
       a.pick = pick;
       a.rows = rows;
       a.d = g[j]->d;

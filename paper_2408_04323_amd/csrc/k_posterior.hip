@@ -59,6 +59,7 @@ struct Post32 {
   float c0, c1, c2;
   double s2, prior, ei_c;
   RowPlan plan;  // row blocks of each wave and where they start in the packed inverse
+  int64_t v_ld;  // row stride of a kept V
 };
 
 // Candidate coordinates (D = the exact number of dimensions, so every load is
@@ -298,7 +299,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
     // ---- phase 2: this wave's row blocks of V = L^-1 K*^T on the matrix cores
     float sq0 = 0.0f, sq1 = 0.0f;
     if (count > 0) {
-      const VStore vs{v_out, a.n, c0, a.n};
+      const VStore vs{v_out, a.v_ld, c0, a.n};
       wave_tile32<KEEP_V>(ap, ks, rows, count, lane, ax, sq0, sq1, vs);
     }
 
@@ -569,7 +570,7 @@ int by_d4(int d4, F&& f) {
 }  // namespace
 
 int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, void* sigma,
-                     const double* ei_c, void* ei, void* stream, float* v_out, bool xc_warped) {
+                     const double* ei_c, void* ei, void* stream, float* v_out, bool xc_warped, int64_t v_ld) {
   if (n == 0) return SCOOT_OK;
   if (n >= ((int64_t)1 << 37)) return fail(SCOOT_ERR_UNSUPPORTED, "posterior: n too large");
   hipStream_t s = (hipStream_t)stream;
@@ -594,6 +595,7 @@ int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, vo
     a.prior = g.c;
     a.ei_c = ei_c ? *ei_c : 0.0;
     a.plan = plan_rows(g.nb, posterior_waves(g.nb));
+    a.v_ld = v_ld > 0 ? v_ld : n;
     for (int e = 0; e < 8; ++e)
       if (a.plan.nrows[e] * kRowBits > 64) return fail(SCOOT_ERR_UNSUPPORTED, "posterior: row plan does not pack");
     float* e = ei_c ? (float*)ei : nullptr;
