@@ -24,6 +24,8 @@ constexpr int kForestThreads = kForestThreadsPerBlock;
 constexpr int kWalks = 4;
 static_assert(kForestThreads * 4 == (1 << 11), "feature << 11 is the byte offset of a feature column");
 
+typedef __attribute__((address_space(3))) const float lds_f32;  // an LDS address
+
 struct ForestArgs {
   int64_t n;
   int d, n_trees, t_begin, t_end;
@@ -37,14 +39,17 @@ __global__ __launch_bounds__(kForestThreads) void forest_kernel(
     const int32_t* __restrict__ leaf_orig, const float* __restrict__ Xc, int32_t* __restrict__ votes,
     uint8_t* __restrict__ mask, int32_t* __restrict__ leaf_idx, const uint8_t* __restrict__ known,
     const ForestArgs a) {
+  // LDS: the feature columns [d][kForestThreads] floats at LDS address 0 (the
+  // kernel declares no static LDS, so its dynamic LDS starts there), so that a
+  // thread's feature address is (feature << 11) | (tid * 4), one and-or; then
+  // the chunk's nodes.
   extern __shared__ __align__(16) unsigned char smem[];
-  uint2* tree = reinterpret_cast<uint2*>(smem);
-  unsigned char* xs = smem + (size_t)a.n_nodes * 8;  // [d][kForestThreads] floats
+  unsigned char* xs = smem;
+  uint2* tree = reinterpret_cast<uint2*>(smem + (size_t)a.d * kForestThreads * 4);
   const int tid = threadIdx.x;
   for (uint32_t i = tid; i < a.n_nodes; i += kForestThreads) tree[i] = nodes[a.node_base + i];
   __syncthreads();
-
-  const unsigned char* my_x = xs + tid * 4;
+  const uint32_t lane4 = (uint32_t)tid * 4u;
   for (int64_t g = blockIdx.x; g * kForestThreads < a.n; g += gridDim.x) {
     const int64_t c = g * kForestThreads + tid;
     if (c >= a.n) continue;
@@ -60,13 +65,14 @@ __global__ __launch_bounds__(kForestThreads) void forest_kernel(
         node[q] = root[t] - a.node_base;
         steps = max(steps, depth[t]);
       }
+      steps = __builtin_amdgcn_readfirstlane(steps);  // the same for every lane: a scalar loop count
       for (uint32_t s = 0; s < steps; ++s) {
         uint2 rec[kWalks];
         float x[kWalks];
 #pragma unroll
         for (int q = 0; q < kWalks; ++q) rec[q] = tree[node[q]];
 #pragma unroll
-        for (int q = 0; q < kWalks; ++q) x[q] = *reinterpret_cast<const float*>(my_x + (rec[q].x & 0x7800u));
+        for (int q = 0; q < kWalks; ++q) x[q] = *reinterpret_cast<const lds_f32*>((size_t)((rec[q].x & 0x7800u) | lane4));
 #pragma unroll
         for (int q = 0; q < kWalks; ++q) node[q] = (rec[q].x >> 15) + (x[q] <= __uint_as_float(rec[q].y) ? 0u : 1u);
       }
