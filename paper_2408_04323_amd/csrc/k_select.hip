@@ -43,17 +43,19 @@ struct Key128 {
   __device__ bool zero() const { return hi == 0 && lo == 0; }
 };
 
+// Branch-free, so that a thread's loads can all be in flight before any key
+// is formed.
 __device__ inline Key64 make_key(float s, int64_t i, bool ok) {
-  if (!ok || s != s) return Key64{0};
   uint32_t b = __float_as_uint(s + 0.0f);
   b = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
-  return Key64{((uint64_t)b << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i)};
+  const uint64_t k = ((uint64_t)b << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i);
+  return Key64{ok && s == s ? k : 0ull};
 }
 __device__ inline Key128 make_key(double s, int64_t i, bool ok) {
-  if (!ok || s != s) return Key128{0, 0};
   uint64_t b = (uint64_t)__double_as_longlong(s + 0.0);
   b = (b & 0x8000000000000000ull) ? ~b : (b | 0x8000000000000000ull);
-  return Key128{b, ~(uint64_t)i};
+  const bool keep = ok && s == s;
+  return Key128{keep ? b : 0ull, keep ? ~(uint64_t)i : 0ull};
 }
 __device__ inline int64_t key_index(const Key64& k) { return (int64_t)(0xFFFFFFFFu - (uint32_t)k.v); }
 __device__ inline int64_t key_index(const Key128& k) { return (int64_t)(~k.lo); }
@@ -99,12 +101,18 @@ __device__ void select_rounds(K (&keys)[kSelPer], K* list, K* wave_best, int q) 
   }
 }
 
-// Key sources for stage 1.
-template <typename T>
+// Key sources for stage 1: load(i) reads what key i needs (no branches),
+// key(raw, i) forms it.
+template <typename T, bool MASKED>
 struct ScoreKeys {
   const T* __restrict__ score;
-  const uint8_t* __restrict__ mask;  // nullable
-  __device__ auto operator()(int64_t i) const { return make_key(score[i], i, mask ? mask[i] != 0 : true); }
+  const uint8_t* __restrict__ mask;  // read only when MASKED
+  struct Raw {
+    T s;
+    uint8_t m;
+  };
+  __device__ Raw load(int64_t i) const { return Raw{score[i], MASKED ? mask[i] : (uint8_t)1}; }
+  __device__ auto key(const Raw& r, int64_t i) const { return make_key(r.s, i, r.m != 0); }
 };
 
 // SplitMix64 (Steele, Lea and Flood, OOPSLA 2014; Stafford's finaliser):
@@ -118,8 +126,11 @@ __device__ inline uint64_t splitmix64(uint64_t seed, uint64_t i) {
 struct DrawKeys {
   const uint8_t* __restrict__ flags;
   uint64_t seed;
-  __device__ Key128 operator()(int64_t i) const {
-    return flags[i] ? Key128{splitmix64(seed, (uint64_t)i), ~(uint64_t)i} : Key128{0, 0};
+  typedef uint8_t Raw;
+  __device__ Raw load(int64_t i) const { return flags[i]; }
+  __device__ Key128 key(Raw f, int64_t i) const {
+    const uint64_t u = splitmix64(seed, (uint64_t)i);
+    return f ? Key128{u, ~(uint64_t)i} : Key128{0, 0};
   }
 };
 
@@ -133,11 +144,20 @@ __global__ __launch_bounds__(kSelThreads) void topq_stage1(const Src src, int64_
   if (tid < q) list[tid] = K{};
   int32_t valid = 0;
   for (int64_t base = (int64_t)blockIdx.x * kSelChunk; base < n; base += (int64_t)gridDim.x * kSelChunk) {
+    // Every load is issued before any is used: the index is clamped and a
+    // key past the end is zeroed afterwards (no branch around the loads).
+    typename Src::Raw raw[kSelPer];
+#pragma unroll
+    for (int j = 0; j < kSelPer; ++j) {
+      const int64_t i = base + (int64_t)j * kSelThreads + tid;
+      raw[j] = src.load(i < n ? i : n - 1);
+    }
     K keys[kSelPer];
 #pragma unroll
     for (int j = 0; j < kSelPer; ++j) {
       const int64_t i = base + (int64_t)j * kSelThreads + tid;
-      keys[j] = i < n ? src(i) : K{};
+      keys[j] = src.key(raw[j], i);
+      if (i >= n) keys[j] = K{};
       valid += keys[j].zero() ? 0 : 1;
     }
     select_rounds<K>(keys, list, wave_best, q);
@@ -169,8 +189,11 @@ __global__ __launch_bounds__(kSelThreads) void topq_stage2(const T* __restrict__
 #pragma unroll
     for (int j = 0; j < kSelPer; ++j) {
       const int64_t i = base + (int64_t)j * kSelThreads + tid;
-      keys[j] = i < total ? part_keys[i] : K{};
+      keys[j] = part_keys[i < total ? i : total - 1];
     }
+#pragma unroll
+    for (int j = 0; j < kSelPer; ++j)
+      if (base + (int64_t)j * kSelThreads + tid >= total) keys[j] = K{};
     select_rounds<K>(keys, list, wave_best, q);
   }
   if (tid < q) {
@@ -225,11 +248,17 @@ int launch_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype d
                 void* score_out, int32_t* n_valid, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   if (dt == SCOOT_F32) {
-    const ScoreKeys<float> src{(const float*)score, mask};
-    return run_select<float, Key64>(src, (const float*)score, n, q, idx, (float*)score_out, n_valid, s);
+    if (mask)
+      return run_select<float, Key64>(ScoreKeys<float, true>{(const float*)score, mask}, (const float*)score, n, q,
+                                      idx, (float*)score_out, n_valid, s);
+    return run_select<float, Key64>(ScoreKeys<float, false>{(const float*)score, mask}, (const float*)score, n, q,
+                                    idx, (float*)score_out, n_valid, s);
   }
-  const ScoreKeys<double> src{(const double*)score, mask};
-  return run_select<double, Key128>(src, (const double*)score, n, q, idx, (double*)score_out, n_valid, s);
+  if (mask)
+    return run_select<double, Key128>(ScoreKeys<double, true>{(const double*)score, mask}, (const double*)score, n,
+                                      q, idx, (double*)score_out, n_valid, s);
+  return run_select<double, Key128>(ScoreKeys<double, false>{(const double*)score, mask}, (const double*)score, n, q,
+                                    idx, (double*)score_out, n_valid, s);
 }
 
 int launch_random_pick(const uint8_t* flags, int64_t n, uint64_t seed, int q, int64_t* idx, int32_t* n_flagged,
