@@ -27,7 +27,7 @@ PEAK_FP32_MFMA_TFLOPS = 157.3
 # rocprofv3 FETCH_SIZE / WRITE_SIZE passes (calibrated against a plain copy:
 # FETCH_SIZE x 2.0, WRITE_SIZE x 1.0), valid only for the kernel source they
 # were taken on.
-POSTERIOR_TRAFFIC = {"source_sha1": "f07bb5d7aa028e7ad626f935cf8a65b5b3f66c35", "bytes": 14152293}
+POSTERIOR_TRAFFIC = {"source_sha1": "6d00e69ec09e2b77d65e2c5741bb16a93839daba", "bytes": 14157427}
 
 
 def posterior_traffic():
