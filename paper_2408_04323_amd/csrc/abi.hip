@@ -6,6 +6,8 @@
 #include <cstring>
 #include <mutex>
 #include <new>
+#include <set>
+#include <utility>
 #include <string>
 #include <vector>
 
@@ -75,6 +77,18 @@ void* device_scratch(size_t bytes, int slot) {
     st.scratch_cap[slot] = cap;
   }
   return st.scratch[slot];
+}
+
+int allow_full_lds(const void* kernel, const char* what) {
+  const int d = current_device();
+  if (d < 0) return fail(SCOOT_ERR_DEVICE, std::string(what) + ": no current device");
+  std::lock_guard<std::mutex> lk(g_mu);
+  static std::set<std::pair<int, const void*>> done;  // (device, kernel) pairs already raised
+  if (done.count({d, kernel})) return SCOOT_OK;
+  if (hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes) != hipSuccess)
+    return fail(SCOOT_ERR_DEVICE, std::string(what) + ": cannot raise the kernel's LDS limit");
+  done.insert({d, kernel});
+  return SCOOT_OK;
 }
 
 int upload_async(void* dst, const void* src, size_t bytes, int slot, void* stream) {

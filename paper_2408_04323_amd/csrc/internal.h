@@ -256,6 +256,10 @@ struct ForestDevice {
 
 // Library-owned scratch of the current device, grown on demand.
 void* device_scratch(size_t bytes, int slot);
+// Lets `kernel` take up to the whole LDS of a CU (160 KiB) as dynamic LDS on
+// the current device; done once per (device, kernel), thread-safe.
+constexpr int kMaxLdsBytes = 160 * 1024;
+int allow_full_lds(const void* kernel, const char* what);
 // Pinned host staging for small uploads on a stream; the previous upload of
 // the same slot is waited for before the buffer is reused.
 int upload_async(void* dst, const void* src, size_t bytes, int slot, void* stream);

@@ -220,11 +220,8 @@ int run_ehvi3(const void* const* mu, const void* const* sigma, int64_t n, const 
   const uint32_t* recs = reinterpret_cast<const uint32_t*>((const unsigned char*)dev + coord_bytes);
   const uint32_t* col_end = reinterpret_cast<const uint32_t*>((const unsigned char*)dev + coord_bytes + rec_bytes);
   const unsigned grid = (unsigned)((n + kEhviThreads - 1) / kEhviThreads);
-  static bool attr_set = false;
-  if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)ehvi3_kernel<T>, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    attr_set = true;
-  }
+  rc = allow_full_lds((const void*)ehvi3_kernel<T>, "ehvi");
+  if (rc != SCOOT_OK) return rc;
   hipLaunchKernelGGL(ehvi3_kernel<T>, dim3(grid), dim3(kEhviThreads), lds, s, (const T*)mu[0], (const T*)mu[1],
                      (const T*)mu[2], (const T*)sigma[0], (const T*)sigma[1], (const T*)sigma[2], coords, recs,
                      col_end, (T*)out, a);

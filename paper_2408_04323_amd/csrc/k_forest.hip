@@ -109,11 +109,8 @@ int launch_forest(const ForestDevice& f, const float* Xc, int64_t n, int64_t vot
   const int per_cu = std::max(1, std::min(4, (int)((160 * 1024) / lds_max)));
   int64_t groups = (n + kForestThreads - 1) / kForestThreads;
   int64_t grid = std::min(groups, (int64_t)cus * per_cu);
-  static bool attr_set = false;
-  if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)forest_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    attr_set = true;
-  }
+  const int rc = allow_full_lds((const void*)forest_kernel, "forest");
+  if (rc != SCOOT_OK) return rc;
   for (int ch = 0; ch < n_chunks; ++ch) {
     ForestArgs a{};
     a.n = n;

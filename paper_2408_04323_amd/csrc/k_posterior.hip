@@ -508,13 +508,8 @@ int run32(const GPDevice& g, const float* Xc, int64_t n, float* mu, float* sd, f
   // K* tile, per-wave partial norms and means, four SIMD counters
   const size_t lds = (size_t)g.nb * 2 * 4 * 64 * 16 + WAVES * 2 * 64 * 4 + WAVES * 64 * 4 + 16;
   auto kern = posterior_f32_kernel<WAVES, D, KEEP_V>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) !=
-        hipSuccess)
-      return fail(SCOOT_ERR_DEVICE, "posterior: cannot raise the LDS limit of the kernel");
-    attr_set = true;
-  }
+  const int rc = allow_full_lds((const void*)kern, "posterior");
+  if (rc != SCOOT_OK) return rc;
   // Persistent grid: as many workgroups as the chip holds at once, each
   // looping over tiles.
   int dev = 0, cus = 256, per_cu = 0;
@@ -536,11 +531,8 @@ int run64(const GPDevice& g, const float* Xc, int64_t n, double* mu, double* sd,
   const int nb16 = g.m_pad / kBlk64;
   const size_t lds = (size_t)nb16 * 2 * 2 * 64 * 16 + WAVES * 4 * 32 * 8 + WAVES * 2 * 32 * 8;
   auto kern = posterior_f64_kernel<WAVES, D4>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    attr_set = true;
-  }
+  const int rc = allow_full_lds((const void*)kern, "posterior");
+  if (rc != SCOOT_OK) return rc;
   const int64_t grid = (n + 31) / 32;
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WAVES * 64), lds, s, Xc,
                      (const d2_t*)g.linv, (const double*)g.xs, g.alpha, mu, sd, ei, a);

@@ -7,12 +7,13 @@
 // ineligible candidate (mask 0 or NaN score); no eligible key is 0.  fp32
 // scores fit score and index in one 64-bit key; fp64 scores use a pair.
 //
-// Stage 1: each workgroup walks its share of the array in chunks of 4096 keys
-// (16 per thread) and keeps a running best-q list: q rounds of a block-wide
-// argmax over the chunk plus the list.  Stage 2: one workgroup runs the same
-// selection over all stage-1 lists and writes indices, scores and the count.
-// Selection is exact integer work, so the result does not depend on the
-// grid shape or on the order in which blocks run.
+// Stage 1: every wave walks its share of the array in chunks of 1024 keys (16
+// per lane) and keeps a running best-q list in its lanes: q rounds of a
+// wave-wide argmax (butterfly of shuffles, no barriers) over the chunk plus
+// the list.  Stage 2: one wave runs the same selection over all the stage-1
+// lists and writes indices, scores and the count.  Selection is exact integer
+// work, so the result does not depend on the grid shape or on the order in
+// which waves run.
 //
 // The same two stages make the random pick of the MACE suggestion (Sec. 4.5.1,
 // Sec. 4.6): candidate i's key is (u_i, inverted index), u_i the i-th output of
@@ -21,16 +22,17 @@
 // flagged set in random order.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "internal.h"
 
 namespace scoot {
 
-constexpr int kSelThreads = 256;
-constexpr int kSelPer = 16;  // keys per thread per chunk
-constexpr int kSelChunk = kSelThreads * kSelPer;
-constexpr int kSelMaxGrid = 1024;
+constexpr int kSelThreads = 256;  // stage 1 workgroup: four independent waves
+constexpr int kSelPer = 16;       // keys per lane per chunk
+constexpr int kSelChunk = 64 * kSelPer;
+constexpr int kSelMaxKeys2 = 16384;  // bound on the stage-1 lists stage 2 reads (waves x q)
 
 struct Key64 {
   uint64_t v;
@@ -67,13 +69,12 @@ __device__ inline Key128 shfl_xor(Key128 k, int m) {
   return Key128{(uint64_t)__shfl_xor((unsigned long long)k.hi, m), (uint64_t)__shfl_xor((unsigned long long)k.lo, m)};
 }
 
-// q rounds of block argmax over the thread's kSelPer keys plus list[] (the
-// running best list in LDS, q entries, zero = empty).  Rewrites list[].
+// q rounds of wave argmax over the lane's kSelPer keys plus the running list
+// (lane r < q holds entry r, zero = empty).  Rewrites the list.
 template <typename K>
-__device__ void select_rounds(K (&keys)[kSelPer], K* list, K* wave_best, int q) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  K extra = tid < q ? list[tid] : K{};
-  __syncthreads();
+__device__ void wave_select(K (&keys)[kSelPer], K& list, int q) {
+  const int lane = threadIdx.x & 63;
+  K extra = list, next{};
   for (int r = 0; r < q; ++r) {
     K best = extra;
 #pragma unroll
@@ -84,21 +85,16 @@ __device__ void select_rounds(K (&keys)[kSelPer], K* list, K* wave_best, int q) 
       K o = shfl_xor(best, m);
       if (o > best) best = o;
     }
-    if (lane == 0) wave_best[wave] = best;
-    __syncthreads();
-    K win = wave_best[0];
-#pragma unroll
-    for (int w = 1; w < kSelThreads / 64; ++w)
-      if (wave_best[w] > win) win = wave_best[w];
-    if (!win.zero()) {  // remove the winner from its owner (keys are unique)
-      if (!(extra > win) && !(win > extra)) extra = K{};
+    // every lane now holds the wave's best; remove it from its owner (keys are unique)
+    if (!best.zero()) {
+      if (!(extra > best) && !(best > extra)) extra = K{};
 #pragma unroll
       for (int j = 0; j < kSelPer; ++j)
-        if (!(keys[j] > win) && !(win > keys[j])) keys[j] = K{};
+        if (!(keys[j] > best) && !(best > keys[j])) keys[j] = K{};
     }
-    if (tid == 0) list[r] = win;
-    __syncthreads();
+    if (lane == r) next = best;
   }
+  list = next;
 }
 
 // Key sources for stage 1: load(i) reads what key i needs (no branches),
@@ -134,91 +130,76 @@ struct DrawKeys {
   }
 };
 
+// part_keys [waves * q], part_count [waves]: each wave's list and its count
+// of eligible keys; wave w takes chunks w, w + W, ... (W waves in the grid).
 template <typename K, typename Src>
 __global__ __launch_bounds__(kSelThreads) void topq_stage1(const Src src, int64_t n, int q, K* __restrict__ part_keys,
                                                            int32_t* __restrict__ part_count) {
-  __shared__ K list[SCOOT_MAX_Q];
-  __shared__ K wave_best[kSelThreads / 64];
-  __shared__ int32_t cnt[kSelThreads / 64];
-  const int tid = threadIdx.x;
-  if (tid < q) list[tid] = K{};
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * (kSelThreads / 64) + (threadIdx.x >> 6);
+  const int64_t waves = (int64_t)gridDim.x * (kSelThreads / 64);
+  K list{};
   int32_t valid = 0;
-  for (int64_t base = (int64_t)blockIdx.x * kSelChunk; base < n; base += (int64_t)gridDim.x * kSelChunk) {
+  for (int64_t base = wave * kSelChunk; base < n; base += waves * kSelChunk) {
     // Every load is issued before any is used: the index is clamped and a
     // key past the end is zeroed afterwards (no branch around the loads).
     typename Src::Raw raw[kSelPer];
 #pragma unroll
     for (int j = 0; j < kSelPer; ++j) {
-      const int64_t i = base + (int64_t)j * kSelThreads + tid;
+      const int64_t i = base + (int64_t)j * 64 + lane;
       raw[j] = src.load(i < n ? i : n - 1);
     }
     K keys[kSelPer];
 #pragma unroll
     for (int j = 0; j < kSelPer; ++j) {
-      const int64_t i = base + (int64_t)j * kSelThreads + tid;
+      const int64_t i = base + (int64_t)j * 64 + lane;
       keys[j] = src.key(raw[j], i);
       if (i >= n) keys[j] = K{};
       valid += keys[j].zero() ? 0 : 1;
     }
-    select_rounds<K>(keys, list, wave_best, q);
+    wave_select<K>(keys, list, q);
   }
   for (int m = 32; m >= 1; m >>= 1) valid += __shfl_xor(valid, m);
-  if ((tid & 63) == 0) cnt[tid >> 6] = valid;
-  __syncthreads();
-  if (tid < q) part_keys[(size_t)blockIdx.x * q + tid] = list[tid];
-  if (tid == 0) {
-    int32_t s = 0;
-    for (int w = 0; w < kSelThreads / 64; ++w) s += cnt[w];
-    part_count[blockIdx.x] = s;
-  }
+  if (lane < q) part_keys[wave * q + lane] = list;
+  if (lane == 0) part_count[wave] = valid;
 }
 
+// One wave: the best q of all stage-1 lists, then indices, scores and the count.
 template <typename T, typename K>
-__global__ __launch_bounds__(kSelThreads) void topq_stage2(const T* __restrict__ score, int n_parts, int q,
-                                                           const K* __restrict__ part_keys,
-                                                           const int32_t* __restrict__ part_count,
-                                                           int64_t* __restrict__ idx, T* __restrict__ score_out,
-                                                           int32_t* __restrict__ n_valid) {
-  __shared__ K list[SCOOT_MAX_Q];
-  __shared__ K wave_best[kSelThreads / 64];
-  const int tid = threadIdx.x;
-  if (tid < q) list[tid] = K{};
+__global__ __launch_bounds__(64) void topq_stage2(const T* __restrict__ score, int n_parts, int q,
+                                                  const K* __restrict__ part_keys,
+                                                  const int32_t* __restrict__ part_count, int64_t* __restrict__ idx,
+                                                  T* __restrict__ score_out, int32_t* __restrict__ n_valid) {
+  const int lane = threadIdx.x;
+  K list{};
   const int64_t total = (int64_t)n_parts * q;
   for (int64_t base = 0; base < total; base += kSelChunk) {
     K keys[kSelPer];
 #pragma unroll
     for (int j = 0; j < kSelPer; ++j) {
-      const int64_t i = base + (int64_t)j * kSelThreads + tid;
+      const int64_t i = base + (int64_t)j * 64 + lane;
       keys[j] = part_keys[i < total ? i : total - 1];
     }
 #pragma unroll
     for (int j = 0; j < kSelPer; ++j)
-      if (base + (int64_t)j * kSelThreads + tid >= total) keys[j] = K{};
-    select_rounds<K>(keys, list, wave_best, q);
+      if (base + (int64_t)j * 64 + lane >= total) keys[j] = K{};
+    wave_select<K>(keys, list, q);
   }
-  if (tid < q) {
-    const K k = list[tid];
-    if (k.zero()) {
-      idx[tid] = -1;
-      if (score_out) score_out[tid] = (T)NAN;
+  if (lane < q) {
+    if (list.zero()) {
+      idx[lane] = -1;
+      if (score_out) score_out[lane] = (T)NAN;
     } else {
-      const int64_t i = key_index(k);
-      idx[tid] = i;
-      if (score_out) score_out[tid] = score[i];
+      const int64_t i = key_index(list);
+      idx[lane] = i;
+      if (score_out) score_out[lane] = score[i];
     }
   }
-  if (n_valid) {  // sum of the stage-1 counts, in parallel
-    __shared__ int32_t wsum[kSelThreads / 64];
+  if (n_valid) {  // sum of the stage-1 counts
     int32_t sum = 0;
-    for (int b = tid; b < n_parts; b += kSelThreads) sum += part_count[b];
+    for (int b = lane; b < n_parts; b += 64) sum += part_count[b];
     for (int m = 32; m >= 1; m >>= 1) sum += __shfl_xor(sum, m);
-    if ((tid & 63) == 0) wsum[tid >> 6] = sum;
-    __syncthreads();
-    if (tid == 0) {
-      int32_t t = 0;
-      for (int w = 0; w < kSelThreads / 64; ++w) t += wsum[w];
-      *n_valid = t;
-    }
+    if (lane == 0) *n_valid = sum;
   }
 }
 
@@ -227,17 +208,20 @@ namespace {
 template <typename T, typename K, typename Src>
 int run_select(const Src& src, const T* score, int64_t n, int q, int64_t* idx, T* score_out, int32_t* n_valid,
                hipStream_t s) {
-  int64_t grid = (n + kSelChunk - 1) / kSelChunk;
-  if (grid < 1) grid = 1;
-  if (grid > kSelMaxGrid) grid = kSelMaxGrid;
-  const size_t kbytes = (size_t)grid * q * sizeof(K);
-  unsigned char* ws = (unsigned char*)device_scratch(kbytes + (size_t)grid * 4, 3);
+  // As many waves as chunks, bounded so that stage 2 reads at most
+  // kSelMaxKeys2 keys; whole workgroups of four waves.
+  int64_t waves = (n + kSelChunk - 1) / kSelChunk;
+  waves = std::max<int64_t>(1, std::min<int64_t>(waves, std::max(4, kSelMaxKeys2 / q)));
+  const int64_t grid = (waves + 3) / 4;
+  waves = grid * 4;
+  const size_t kbytes = (size_t)waves * q * sizeof(K);
+  unsigned char* ws = (unsigned char*)device_scratch(kbytes + (size_t)waves * 4, 3);
   if (!ws) return fail(SCOOT_ERR_NO_MEMORY, "topq: scratch allocation failed");
   K* pk = reinterpret_cast<K*>(ws);
   int32_t* pc = reinterpret_cast<int32_t*>(ws + kbytes);
   hipLaunchKernelGGL((topq_stage1<K, Src>), dim3((unsigned)grid), dim3(kSelThreads), 0, s, src, n, q, pk, pc);
-  hipLaunchKernelGGL((topq_stage2<T, K>), dim3(1), dim3(kSelThreads), 0, s, score, (int)grid, q, pk, pc, idx,
-                     score_out, n_valid);
+  hipLaunchKernelGGL((topq_stage2<T, K>), dim3(1), dim3(64), 0, s, score, (int)waves, q, pk, pc, idx, score_out,
+                     n_valid);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("topq launch: ") + hipGetErrorString(err));
   return SCOOT_OK;
