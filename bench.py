@@ -22,15 +22,18 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_FP64_MFMA_TFLOPS = 78.6
 
-# HBM traffic of one posterior launch on the measured workload, from
-# rocprofv3 FETCH_SIZE / WRITE_SIZE passes (calibrated against a plain copy:
-# FETCH_SIZE x 2.0, WRITE_SIZE x 1.0), valid only for the kernel source they
-# were taken on.
+# HBM traffic of one posterior launch on the two-objective workload (m=256,
+# n=262144, d=10, Matern-5/2, fp32), from rocprofv3 FETCH_SIZE / WRITE_SIZE
+# passes (calibrated against a plain copy: FETCH_SIZE x 2.0, WRITE_SIZE x
+# 1.0), valid only for that workload and the kernel source they were taken on.
 POSTERIOR_TRAFFIC = {"source_sha1": "3ad87c26d61e0ef35def8a033e68885e92aa7cb7", "bytes": 14157728}
 
 
-def posterior_traffic():
+def posterior_traffic(args):
+    if args.config != 3 or args.kernel != "matern52" or args.warp or args.dtype != "f32":
+        return None
     import hashlib
     src = os.path.join(ROOT, "paper_2408_04323_amd", "csrc", "k_posterior.hip")
     with open(src, "rb") as fh:
@@ -54,6 +57,9 @@ def parse():
     ap.add_argument("--kernel", choices=["matern52", "matern32"], default="matern52",
                     help="covariance of the GPs (matern32 = the paper's own)")
     ap.add_argument("--warp", action="store_true", help="Kumaraswamy input warping (the paper's own)")
+    ap.add_argument("--dtype", choices=["f32", "f64"], default="f32",
+                    help="precision of the scoring pass (posterior, acquisition, top-q keys); the pool stays "
+                         "float32")
     ap.add_argument("--mace", action="store_true",
                     help="one-objective workloads: time the MACE suggestion (posterior, UCB/PI/EI, mask, "
                          "Pareto front, seeded pick) and print its own line")
@@ -111,7 +117,7 @@ def main():
     tf = time.perf_counter()
     warps = w.get("warp")
     gps = [S.gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][j], w["signal_var"][j], w["noise_var"][j],
-                    w["prior_mean"][j], dtype="f32", kernel=args.kernel,
+                    w["prior_mean"][j], dtype=args.dtype, kernel=args.kernel,
                     warp_a=None if warps is None else warps[0][j], warp_b=None if warps is None else warps[1][j])
            for j in range(p)]
     fit_ms = (time.perf_counter() - tf) * 1e3
@@ -119,7 +125,7 @@ def main():
     forest = S.forest_create(fd["feature"], fd["threshold"], fd["left"], fd["right"], fd["leaf_q16"],
                              fd["tree_offset"], w["d"])
     Xc = torch.as_tensor(w["Xc"]).to(dev)
-    bufs = S.PoolBuffers(n, p, w["q"], S.F32, dev)
+    bufs = S.PoolBuffers(n, p, w["q"], gps[0].dtype, dev)
     front, n_boxes = S.ehvi_front(w["Y"], w["ref"]) if p > 1 else (np.zeros((0, 1)), 0)
     print(f"[bench] workload {c['name']} m={m} n={n} d={w['d']} p={p} front={len(front)} "
           f"gen {gen_s:.1f}s fit {fit_ms:.1f}ms", file=sys.stderr, flush=True)
@@ -194,14 +200,18 @@ def main():
     # triangular product (m^2 flops) and K* with the mean (m (3d + 10) flops;
     # the m square roots and m exponentials are not counted).  On gfx950 the
     # fp32 matrix instructions and the vector ALU share one datapath (measured:
-    # they do not overlap), so both draw on the same 157.3 TFLOP/s.
+    # they do not overlap), so both draw on the same 157.3 TFLOP/s (78.6 in
+    # fp64, for the matrix instructions and the vector ALU alike).
     flops_trsm = m * m
     flops_per_unit = flops_trsm + m * (3 * w["d"] + 10)
+    peak = PEAK_FP64_MFMA_TFLOPS if args.dtype == "f64" else PEAK_FP32_MFMA_TFLOPS
     achieved = flops_per_unit * n / (post_ms * 1e-3) / 1e12
     achieved_trsm = flops_trsm * n / (post_ms * 1e-3) / 1e12
     out = {
-        "metric": METRIC if (args.config == 3 and args.kernel == "matern52" and not args.warp) else
-        f"candidate configs scored/sec (GP+acq+RF mask), {c['name']}, {args.kernel}{' warped' if args.warp else ''}",
+        "metric": METRIC if (args.config == 3 and args.kernel == "matern52" and not args.warp
+                             and args.dtype == "f32") else
+        f"candidate configs scored/sec (GP+acq+RF mask), {c['name']}, {args.kernel}{' warped' if args.warp else ''}"
+        f"{', fp64' if args.dtype == 'f64' else ''}",
         "value": value,
         "unit": "candidates/s",
         "n_gpus": 1,
@@ -211,7 +221,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": args.dtype,
         "data": "synthetic",
         "config": {
             "workload": f"{c['name']}: m={m} n={n} d={w['d']} p={p} front={len(front)} boxes={n_boxes} "
@@ -227,15 +237,15 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": "posterior_f32_kernel (K*, mean, L^-1 K*^T on fp32 MFMA, variance)",
+            "kernel": f"posterior_{args.dtype}_kernel (K*, mean, L^-1 K*^T on {args.dtype[1:]}-bit MFMA, variance)",
             "achieved": achieved,
-            "peak": PEAK_FP32_MFMA_TFLOPS,
+            "peak": peak,
             "unit": "TFLOP/s",
-            "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
-            "traffic": posterior_traffic(),
+            "frac": achieved / peak,
+            "traffic": posterior_traffic(args),
             "algorithmic_unit": f"m^2 + m(3d+10) = {flops_per_unit} flops per candidate per objective "
                                 f"(triangular product + K* and mean), {n} candidates per launch",
-            "frac_triangular_product_only": achieved_trsm / PEAK_FP32_MFMA_TFLOPS,
+            "frac_triangular_product_only": achieved_trsm / peak,
         },
     }
     if not args.no_cpu_baseline:

@@ -203,7 +203,6 @@ int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel
     g.d = d;
     g.m_pad = f.m_pad;
     g.nb = f.nb;
-    g.d4 = (d + 3) / 4;
     g.s2 = signal_var;
     g.tau2 = noise_var;
     g.c = prior_mean;
@@ -241,13 +240,13 @@ int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel
     img.assign(linv_bytes + xs_bytes + alpha_bytes + alpha32_bytes, 0);
     if (dt == SCOOT_F32) std::memcpy(img.data(), l32.data(), l32.size() * 4);
     else std::memcpy(img.data(), l64.data(), l64.size() * 8);
-    // fp32 rows with a spare column carry alpha_i in column d, so the kernel
-    // reads an observation and its weight with the same scalar loads.
+    // Rows with a spare column carry alpha_i in column d, so the kernels read
+    // an observation and its weight with the same loads.
     for (int i = 0; i < f.m_pad; ++i)
       for (int k = 0; k < kXsStride; ++k) {
         double v = 0.0;
         if (k < d) v = i < m ? f.Xw[(size_t)i * d + k] * f.scale[k] : kPadCoord;
-        else if (k == d && dt == SCOOT_F32 && i < m) v = f.alpha[i];
+        else if (k == d && i < m) v = f.alpha[i];
         unsigned char* at = img.data() + linv_bytes + ((size_t)i * kXsStride + k) * esz;
         if (dt == SCOOT_F32) {
           float fv = (float)v;

@@ -155,19 +155,24 @@ void pack_linv_f32(const FitHost& f, std::vector<float>& out) {
 // fp64 layout, for v_mfma_f64_16x16x4f64: 16 x 16 blocks, four steps per
 // block; at step s lane l holds Linv[16I + l % 16][16J + 4s + l / 16]; steps
 // are paired so a lane reads two consecutive steps as one 16-byte load:
-//   double index = ((blk * 2 + s / 2) * 64 + l) * 2 + s % 2,  blk = I(I+1)/2 + J.
+//   double index = ((blk * 2 + s / 2) * 64 + l) * 2 + s % 2.
+// Blocks are ordered as for fp32: plan entry after plan entry (plan_rows over
+// the 16-row blocks with the fp32 kernel's wave count), J = 0..I.
 void pack_linv_f64(const FitHost& f, std::vector<double>& out) {
   const int nb = f.m_pad / kBlk64, m = f.m;
-  out.assign(((size_t)nb * (nb + 1) / 2 + 2) * 4 * 64, 0.0);
-  for (int I = 0; I < nb; ++I)
-    for (int J = 0; J <= I; ++J) {
-      size_t blk = (size_t)I * (I + 1) / 2 + J;
-      for (int s = 0; s < 4; ++s)
-        for (int l = 0; l < 64; ++l) {
-          int r = 16 * I + (l % 16), col = 16 * J + 4 * s + l / 16;
-          double v = (r < m && col < m) ? f.Linv[(size_t)r * m + col] : 0.0;
-          out[((blk * 2 + s / 2) * 64 + l) * 2 + s % 2] = v;
-        }
+  const RowPlan64 plan = plan_rows64(nb, posterior_waves(f.nb));
+  out.assign((size_t)nb * (nb + 1) / 2 * 4 * 64, 0.0);
+  size_t blk = 0;
+  for (int e = 0; e < 8; ++e)
+    for (int q = 0; q < plan.nrows[e] && q < kMaxRows64; ++q) {
+      const int I = plan64_row(plan, e, q);
+      for (int J = 0; J <= I; ++J, ++blk)
+        for (int s = 0; s < 4; ++s)
+          for (int l = 0; l < 64; ++l) {
+            int r = 16 * I + (l % 16), col = 16 * J + 4 * s + l / 16;
+            double v = (r < m && col < m) ? f.Linv[(size_t)r * m + col] : 0.0;
+            out[((blk * 2 + s / 2) * 64 + l) * 2 + s % 2] = v;
+          }
     }
 }
 

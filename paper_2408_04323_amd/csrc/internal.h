@@ -31,8 +31,8 @@ constexpr double kPadCoord = 1.0e4;    // scaled coordinate of padding rows: k(x
 // so it gets 8 waves; otherwise two 4-wave workgroups share a CU.
 inline int posterior_waves(int nb) { return nb > 9 ? 8 : 4; }
 
-// Which row blocks of V each wave of the fp32 posterior owns.  Row block I
-// costs I + 1 blocks of the triangle.  Plan entry p goes to wave p of a 4-wave
+// Which row blocks of V each wave of the posterior owns (fp32: 32-row blocks,
+// fp64: 16-row blocks).  Row block I costs I + 1 blocks of the triangle.  Plan entry p goes to wave p of a 4-wave
 // workgroup; with 8 waves the two entries p and p + 4 share a SIMD and its
 // matrix unit.  So the rows are first split into four sets of (nearly) equal
 // cost, one per SIMD, by a depth-first search for the smallest capacity that
@@ -45,6 +45,16 @@ struct RowPlan {
   uint64_t rows[8];
   int32_t nrows[8];
   int32_t blk_start[9];  // first block of entry p in the packed stream
+};
+// fp64 (16-row blocks, up to 36): 6 bits per row in one 128-bit value held
+// as two words (row k at bits 6k .. 6k + 5, lo the low word), so an entry
+// holds up to 21 rows.
+constexpr int kRowBits64 = 6;
+constexpr int kMaxRows64 = 128 / kRowBits64;
+struct RowPlan64 {
+  uint64_t lo[8], hi[8];
+  int32_t nrows[8];
+  int32_t blk_start[9];
 };
 
 // Splits rows into two sets whose costs (I + 1) are as equal as possible.
@@ -92,10 +102,12 @@ inline bool pack_rows4(const std::vector<int>& rows, size_t k, int cap, int (&lo
   return false;
 }
 
-inline RowPlan plan_rows(int nb, int W) {
+// The rows of each plan entry, each entry in increasing I.
+inline void plan_entries(int nb, int W, std::vector<int> (&entry)[8]) {
   std::vector<int> all;
   for (int I = nb - 1; I >= 0; --I) all.push_back(I);
-  std::vector<int> quarter[4], entry[8];
+  std::vector<int> quarter[4];
+  for (auto& e : entry) e.clear();
   for (int cap = (nb * (nb + 1) / 2 + 3) / 4;; ++cap) {
     int load[4] = {0, 0, 0, 0};
     for (auto& q : quarter) q.clear();
@@ -106,20 +118,53 @@ inline RowPlan plan_rows(int nb, int W) {
   } else {
     for (int q = 0; q < 4; ++q) entry[q] = quarter[q];
   }
+  for (auto& e : entry) std::sort(e.begin(), e.end());
+}
+
+inline RowPlan plan_rows(int nb, int W) {
+  std::vector<int> entry[8];
+  plan_entries(nb, W, entry);
   RowPlan p{};
   int b = 0;
   for (int e = 0; e < 8; ++e) {
-    std::vector<int> r = entry[e];
-    std::sort(r.begin(), r.end());
+    const std::vector<int>& r = entry[e];
     p.blk_start[e] = b;
     p.nrows[e] = (int)r.size();
     for (size_t k = 0; k < r.size(); ++k) {
-      p.rows[e] |= (uint64_t)r[k] << (kRowBits * k);
+      if ((k + 1) * kRowBits <= 64) p.rows[e] |= (uint64_t)r[k] << (kRowBits * k);
       b += r[k] + 1;
     }
   }
   p.blk_start[8] = b;
   return p;
+}
+
+// Entries of more than kMaxRows64 rows keep only their first kMaxRows64 (nrows
+// tells; the launcher refuses such a plan).
+inline RowPlan64 plan_rows64(int nb16, int W) {
+  std::vector<int> entry[8];
+  plan_entries(nb16, W, entry);
+  RowPlan64 p{};
+  int b = 0;
+  for (int e = 0; e < 8; ++e) {
+    const std::vector<int>& r = entry[e];
+    p.blk_start[e] = b;
+    p.nrows[e] = (int)r.size();
+    unsigned __int128 v = 0;
+    for (size_t k = 0; k < r.size(); ++k) {
+      if ((int)k < kMaxRows64) v |= (unsigned __int128)r[k] << (kRowBits64 * k);
+      b += r[k] + 1;
+    }
+    p.lo[e] = (uint64_t)v;
+    p.hi[e] = (uint64_t)(v >> 64);
+  }
+  p.blk_start[8] = b;
+  return p;
+}
+// Row q of entry e of a fp64 plan.
+inline int plan64_row(const RowPlan64& p, int e, int q) {
+  const unsigned __int128 v = ((unsigned __int128)p.hi[e] << 64) | p.lo[e];
+  return (int)((v >> (kRowBits64 * q)) & ((1u << kRowBits64) - 1));
 }
 
 // Runs fn(c) for every chunk c = 0 .. n_chunks - 1 on the library's pool of
@@ -227,7 +272,7 @@ int pack_forest(const int32_t* feature, const float* threshold, const int32_t* l
 // ---- device state -----------------------------------------------------------
 struct GPDevice {
   scoot_dtype dt = SCOOT_F32;
-  int m = 0, d = 0, m_pad = 0, nb = 0, d4 = 1;
+  int m = 0, d = 0, m_pad = 0, nb = 0;
   double s2 = 1, tau2 = 0, c = 0;
   void* buf = nullptr;        // one allocation holding everything below
   const void* linv = nullptr; // packed L^-1 (float or double)

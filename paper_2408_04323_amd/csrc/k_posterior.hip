@@ -330,9 +330,13 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// fp64: v_mfma_f64_16x16x4f64, 16-row blocks, tiles of 32 candidates (two
-// 16-column MFMA tiles).  B operand at step s: lane l holds
-// K*[16J + 4s + l/16][16 ct + l%16]; stored as (J, ct, s/2, lane) double2.
+// fp64: v_mfma_f64_16x16x4f64 on 16 x 16 blocks, tiles of 32 candidates (two
+// 16-column MFMA tiles ct = 0, 1).  At MFMA step s (0..3) of block (I, J), A
+// lane l holds Linv[16I + l%16][16J + 4s + l/16] and B lane l holds
+// K*[16J + 4s + l/16][16ct + l%16]; K* is stored as (J, ct, s/2, lane)
+// double2, component s%2.  Accumulator register r of lane l holds row
+// 4(l/16) + r, column l%16 of its tile.  Same three phases and persistent
+// loop as the fp32 kernel.
 // ---------------------------------------------------------------------------
 struct Post64 {
   int64_t n;
@@ -342,10 +346,97 @@ struct Post64 {
   double s2, prior, ei_c;
   int warp;  // candidates through kumaraswamy(x, wa, wb) first
   double wa[SCOOT_MAX_DIM], wb[SCOOT_MAX_DIM];
+  RowPlan64 plan;  // 16-row blocks
 };
 
-template <int WAVES, int D4>
-__global__ __launch_bounds__(WAVES * 64) void posterior_f64_kernel(
+__device__ inline void load_block16(d2_t (&a)[2], const d2_t* ap, int k) {
+  a[0] = ap[(size_t)(k * 2 + 0) * 64];
+  a[1] = ap[(size_t)(k * 2 + 1) * 64];
+}
+// b[2 ct + s/2]
+__device__ inline void load_b16(d2_t (&b)[4], const d2_t* ks, int J, int lane) {
+#pragma unroll
+  for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) b[2 * ct + s2] = ks[((J * 2 + ct) * 2 + s2) * 64 + lane];
+}
+
+// The 4 steps of a block on two chains (one per 16-candidate half), issued
+// alternately; FIRST starts both from zero (see mfma_block2).
+template <bool FIRST>
+__device__ inline void mfma_block16(d4_t& l0, d4_t& l1, const d2_t (&a)[2], const d2_t (&b)[4]) {
+  const d4_t zero = {0};
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const bool z = FIRST && s2 == 0 && t == 0;
+      l0 = __builtin_amdgcn_mfma_f64_16x16x4f64(a[s2][t], b[s2][t], z ? zero : l0, 0, 0, 0);
+      l1 = __builtin_amdgcn_mfma_f64_16x16x4f64(a[s2][t], b[2 + s2][t], z ? zero : l1, 0, 0, 0);
+    }
+  }
+}
+__device__ inline void mfma_block16_at(int J, d4_t& l0, d4_t& l1, const d2_t (&a)[2], const d2_t (&b)[4]) {
+  if (J == 0) mfma_block16<true>(l0, l1, a, b);
+  else mfma_block16<false>(l0, l1, a, b);
+}
+
+// One tile's pass over the wave's blocks; the same schedule as wave_tile32
+// (one block of read-ahead, the A stream wrapping to the next tile).
+__device__ inline void wave_tile16(const d2_t* __restrict__ ap, const d2_t* ks, uint64_t lo, uint64_t hi, int count,
+                                   int lane, d2_t (&ax)[2], double& sq0, double& sq1) {
+  d4_t l0 = __builtin_nondeterministic_value(l0), l1 = l0;
+  constexpr uint64_t kMask = (1u << kRowBits64) - 1;
+  int I = (int)(lo & kMask), J = 0;
+  auto next_j = [&](int j, int i) { return j == i ? 0 : j + 1; };
+  auto advance = [&]() {
+    if (J == I) {
+      double p0 = 0.0, p1 = 0.0;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        p0 = fma(l0[r], l0[r], p0);
+        p1 = fma(l1[r], l1[r], p1);
+      }
+      sq0 += p0;
+      sq1 += p1;
+      J = 0;
+      lo = (lo >> kRowBits64) | (hi << (64 - kRowBits64));
+      hi >>= kRowBits64;
+      I = (int)(lo & kMask);
+    } else {
+      ++J;
+    }
+  };
+  d2_t ay[2], bx[4], by[4];
+  load_b16(bx, ks, 0, lane);
+  int k = 0;
+  for (; k + 1 < count; k += 2) {
+    load_block16(ay, ap, k + 1);
+    load_b16(by, ks, next_j(J, I), lane);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_block16_at(J, l0, l1, ax, bx);
+    __builtin_amdgcn_sched_barrier(0);
+    advance();
+    load_block16(ax, ap, k + 2 < count ? k + 2 : 0);
+    load_b16(bx, ks, next_j(J, I), lane);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_block16_at(J, l0, l1, ay, by);
+    __builtin_amdgcn_sched_barrier(0);
+    advance();
+  }
+  if (k < count) {
+    load_block16(ay, ap, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_block16_at(J, l0, l1, ax, bx);
+    __builtin_amdgcn_sched_barrier(0);
+    advance();
+    ax[0] = ay[0];
+    ax[1] = ay[1];
+  }
+}
+
+template <int WAVES, int D>
+__global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f64_kernel(
     const float* __restrict__ Xc, const d2_t* __restrict__ linv, const double* __restrict__ xs,
     const double* __restrict__ alpha, double* __restrict__ mu_out, double* __restrict__ sd_out,
     double* __restrict__ ei_out, const Post64 a) {
@@ -358,101 +449,116 @@ __global__ __launch_bounds__(WAVES * 64) void posterior_f64_kernel(
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int64_t c0 = (int64_t)blockIdx.x * 32;
+  const int64_t n_tiles = (a.n + 31) >> 5;
+  static_assert(WAVES % 2 == 0, "phase 1 relies on an even wave count");
+  // 16-byte loads per observation row: the D coordinates and, below 16, alpha
+  constexpr int kRowVec = D < kXsStride ? (D + 1 + 1) / 2 : kXsStride / 2;
 
-  // ---- phase 1: lane -> candidate c0 + lane % 32, row half h = lane / 32 ----
+  // plan entry of this wave, paired per SIMD as in the fp32 kernel
+  int p = wave;
+  if constexpr (WAVES == 8) {
+    int* on_simd = reinterpret_cast<int*>(mu_red + WAVES * 2 * 32);  // [4]
+    if (tid < 4) on_simd[tid] = 0;
+    __syncthreads();
+    const int simd = (int)((__builtin_amdgcn_s_getreg((31 << 11) | 4) >> 4) & 3);  // HW_ID.SIMD_ID
+    int slot = 0;
+    if (lane == 0) slot = atomicAdd(&on_simd[simd], 1);
+    slot = __shfl(slot, 0);
+    __syncthreads();
+    if (on_simd[0] == 2 && on_simd[1] == 2 && on_simd[2] == 2 && on_simd[3] == 2) p = simd + 4 * slot;
+    p = __builtin_amdgcn_readfirstlane(p);
+  }
+  const uint64_t rows_lo = a.plan.lo[p], rows_hi = a.plan.hi[p];
+  const int count = a.plan.blk_start[p + 1] - a.plan.blk_start[p];
+  const d2_t* ap = linv + (size_t)a.plan.blk_start[p] * 2 * 64 + lane;
+  d2_t ax[2];
+  if (count > 0) load_block16(ax, ap, 0);
+
+  // lane -> candidate 32 tile + cl, row half h
   const int cl = lane & 31, h = lane >> 5;
-  int64_t cg = c0 + cl;
-  if (cg >= a.n) cg = a.n - 1;
-  double xc[4 * D4];
-  {
-    float xf[4 * D4];
-#pragma unroll
-    for (int k = 0; k < 4 * D4; ++k) xf[k] = Xc[cg * a.d + (k < a.d ? k : a.d - 1)];
-#pragma unroll
-    for (int k = 0; k < 4 * D4; ++k) {
-      const double x = a.warp && k < a.d ? kumaraswamy((double)xf[k], a.wa[k], a.wb[k]) : (double)xf[k];
-      xc[k] = k < a.d ? x * a.scale[k] : 0.0;
-    }
-  }
-
-  // Group G = (J, s2, kk): rows 16J + 8 s2 + 4t + k, t = 0..1, k = 2 kk + h.
-  double mu_part = 0.0;
-  const int ngroups = nb * 4;
   const int ct = cl >> 4, ncol = cl & 15;
-  for (int G = wave; G < ngroups; G += WAVES) {
-    const int J = G >> 2, s2 = (G >> 1) & 1, kk = G & 1;
-    const int k = 2 * kk + h;
-    d2_t kv;
+  int64_t tile = blockIdx.x;
+  float xr[D];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int i = 16 * J + 8 * s2 + 4 * t + k;
-      const double* xo = xs + (size_t)i * kXsStride;
-      double acc = 0.0;
-#pragma unroll
-      for (int q = 0; q < 4 * D4; ++q) {
-        double df = xc[q] - xo[q];
-        acc = fma(df, df, acc);
-      }
-      double u = sqrt(acc);
-      double kval = fma(u, fma(u, a.c2, a.c1), a.c0) * exp2(-u);
-      kv[t] = kval;
-      mu_part = fma(kval, alpha[i], mu_part);
-    }
-    ks[((J * 2 + ct) * 2 + s2) * 64 + k * 16 + ncol] = kv;
-  }
-  __syncthreads();
+  for (int q = 0; q < D; ++q) xr[q] = Xc[min(tile * 32 + cl, a.n - 1) * D + q];
 
-  // ---- phase 2 ------------------------------------------------------------
-  double sq0 = 0.0, sq1 = 0.0;
-  for (int base = 0; base < nb; base += 2 * WAVES) {
+  for (; tile < n_tiles; tile += gridDim.x) {
+    const int64_t c0 = tile * 32;
+    double xc[D];
 #pragma unroll
-    for (int side = 0; side < 2; ++side) {
-      const int I = base + (side == 0 ? wave : 2 * WAVES - 1 - wave);
-      if (I >= nb) continue;
-      d4_t acc0 = {0}, acc1 = {0};
-      const d2_t* ap = linv + (size_t)I * (I + 1) / 2 * 2 * 64 + lane;
-      const int steps = 2 * (I + 1);
-      for (int k = 0; k < steps; ++k) {
-        const d2_t av = ap[(size_t)k * 64];
-        const int J = k >> 1, s2 = k & 1;
-        const d2_t b0 = ks[((J * 2 + 0) * 2 + s2) * 64 + lane];
-        const d2_t b1 = ks[((J * 2 + 1) * 2 + s2) * 64 + lane];
+    for (int q = 0; q < D; ++q) {
+      const double x = a.warp ? kumaraswamy((double)xr[q], a.wa[q], a.wb[q]) : (double)xr[q];
+      xc[q] = x * a.scale[q];
+    }
+    const int64_t next = tile + gridDim.x;
+    if (next < n_tiles) {
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(av[t], b0[t], acc0, 0, 0, 0);
-          acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(av[t], b1[t], acc1, 0, 0, 0);
+      for (int q = 0; q < D; ++q) xr[q] = Xc[min(next * 32 + cl, a.n - 1) * D + q];
+    }
+
+    // ---- phase 1: group G = 4J + 2 s2 + kk covers rows
+    // 16J + 8 s2 + 4t + 2kk + h = 4G - 2kk + h + 4t (t = 0, 1) of block J;
+    // WAVES is even, so kk = wave & 1 for all of a wave's groups and each
+    // lane's rows advance by 4 WAVES per group.
+    double mu_part = 0.0;
+    const int ngroups = nb * 4;
+    const int kw = wave & 1;
+    const double* xg = xs + (size_t)(4 * wave - 2 * kw + h) * kXsStride;
+    for (int G = wave; G < ngroups; G += WAVES, xg += 4 * WAVES * kXsStride) {
+      const int J = G >> 2, s2 = (G >> 1) & 1;
+      d2_t kv;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const double* xo = xg + 4 * t * kXsStride;
+        double xv[kRowVec * 2];
+#pragma unroll
+        for (int r = 0; r < kRowVec; ++r) {
+          const d2_t v2 = reinterpret_cast<const d2_t*>(xo)[r];
+          xv[2 * r] = v2[0];
+          xv[2 * r + 1] = v2[1];
         }
-      }
+        double acc = 0.0;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        sq0 = fma(acc0[r], acc0[r], sq0);
-        sq1 = fma(acc1[r], acc1[r], sq1);
+        for (int q = 0; q < D; ++q) {
+          const double df = xc[q] - xv[q];
+          acc = fma(df, df, acc);
+        }
+        const double u = sqrt(acc);
+        const double kval = fma(u, fma(u, a.c2, a.c1), a.c0) * exp2(-u);
+        kv[t] = kval;
+        const double al = D < kXsStride ? xv[D < kXsStride ? D : 0] : alpha[4 * G - 2 * kw + h + 4 * t];
+        mu_part = fma(kval, al, mu_part);
       }
+      ks[((J * 2 + ct) * 2 + s2) * 64 + (2 * kw + h) * 16 + ncol] = kv;
     }
-  }
+    __syncthreads();
 
-  // ---- phase 3: accumulator lane l holds column l % 16, rows of group l/16 --
-  const int g = lane >> 4;
-  sig_red[(wave * 4 + g) * 32 + (lane & 15)] = sq0;
-  sig_red[(wave * 4 + g) * 32 + 16 + (lane & 15)] = sq1;
-  mu_red[(wave * 2 + h) * 32 + cl] = mu_part;
-  __syncthreads();
-  if (tid < 32) {
-    const int64_t c = c0 + tid;
-    if (c < a.n) {
-      double ss = 0.0, mm = 0.0;
+    // ---- phase 2 ----------------------------------------------------------
+    double sq0 = 0.0, sq1 = 0.0;
+    if (count > 0) wave_tile16(ap, ks, rows_lo, rows_hi, count, lane, ax, sq0, sq1);
+
+    // ---- phase 3: accumulator lane l holds column l % 16 of its tile ------
+    const int g = lane >> 4;
+    sig_red[(wave * 4 + g) * 32 + (lane & 15)] = sq0;
+    sig_red[(wave * 4 + g) * 32 + 16 + (lane & 15)] = sq1;
+    mu_red[(wave * 2 + h) * 32 + cl] = mu_part;
+    __syncthreads();
+    if (tid < 32) {
+      const int64_t c = c0 + tid;
+      if (c < a.n) {
+        double ss = 0.0, mm = 0.0;
 #pragma unroll
-      for (int w = 0; w < WAVES; ++w) {
+        for (int w = 0; w < WAVES; ++w) {
 #pragma unroll
-        for (int gg = 0; gg < 4; ++gg) ss += sig_red[(w * 4 + gg) * 32 + tid];
-        mm += mu_red[(w * 2 + 0) * 32 + tid] + mu_red[(w * 2 + 1) * 32 + tid];
+          for (int gg = 0; gg < 4; ++gg) ss += sig_red[(w * 4 + gg) * 32 + tid];
+          mm += mu_red[(w * 2 + 0) * 32 + tid] + mu_red[(w * 2 + 1) * 32 + tid];
+        }
+        const double sd = sqrt(fmax(a.s2 - ss, 0.0));
+        const double mu = a.prior + mm;
+        mu_out[c] = mu;
+        sd_out[c] = sd;
+        if (ei_out) ei_out[c] = partial_expectation_d(a.ei_c, mu, sd);
       }
-      const double sd = sqrt(fmax(a.s2 - ss, 0.0));
-      const double mu = a.prior + mm;
-      mu_out[c] = mu;
-      sd_out[c] = sd;
-      if (ei_out) ei_out[c] = partial_expectation_d(a.ei_c, mu, sd);
     }
   }
 }
@@ -502,6 +608,17 @@ int launch_warp_pool(const GPDevice& g, const float* Xc, int64_t n, float* out, 
 // ---------------------------------------------------------------------------
 namespace {
 
+// Persistent grid: as many workgroups as the chip holds at once (each loops
+// over tiles), at most one per tile.  0 when the workgroup does not fit.
+int64_t persistent_grid(const void* kern, int threads, size_t lds, int64_t tiles) {
+  int dev = 0, cus = 256, per_cu = 0;
+  (void)hipGetDevice(&dev);
+  (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, threads, lds) != hipSuccess || per_cu < 1)
+    return 0;
+  return std::min(tiles, (int64_t)cus * per_cu);
+}
+
 template <int WAVES, int D, bool KEEP_V>
 int run32(const GPDevice& g, const float* Xc, int64_t n, float* mu, float* sd, float* ei, float* v_out,
           const Post32& a, hipStream_t s) {
@@ -510,30 +627,24 @@ int run32(const GPDevice& g, const float* Xc, int64_t n, float* mu, float* sd, f
   auto kern = posterior_f32_kernel<WAVES, D, KEEP_V>;
   const int rc = allow_full_lds((const void*)kern, "posterior");
   if (rc != SCOOT_OK) return rc;
-  // Persistent grid: as many workgroups as the chip holds at once, each
-  // looping over tiles.
-  int dev = 0, cus = 256, per_cu = 0;
-  (void)hipGetDevice(&dev);
-  (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)kern, WAVES * 64, lds) != hipSuccess ||
-      per_cu < 1)
-    return fail(SCOOT_ERR_DEVICE, "posterior: workgroup does not fit on a compute unit");
-  const int64_t tiles = (n + 63) / 64;
-  const int64_t grid = std::min(tiles, (int64_t)cus * per_cu);
+  const int64_t grid = persistent_grid((const void*)kern, WAVES * 64, lds, (n + 63) / 64);
+  if (grid < 1) return fail(SCOOT_ERR_DEVICE, "posterior: workgroup does not fit on a compute unit");
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WAVES * 64), lds, s, Xc,
                      (const f4_t*)g.linv, (const float*)g.xs, g.alpha32, mu, sd, ei, v_out, a);
   return SCOOT_OK;
 }
 
-template <int WAVES, int D4>
+template <int WAVES, int D>
 int run64(const GPDevice& g, const float* Xc, int64_t n, double* mu, double* sd, double* ei,
           const Post64& a, hipStream_t s) {
+  // K* tile, per-wave partial norms and means, four SIMD counters
   const int nb16 = g.m_pad / kBlk64;
-  const size_t lds = (size_t)nb16 * 2 * 2 * 64 * 16 + WAVES * 4 * 32 * 8 + WAVES * 2 * 32 * 8;
-  auto kern = posterior_f64_kernel<WAVES, D4>;
+  const size_t lds = (size_t)nb16 * 2 * 2 * 64 * 16 + WAVES * 4 * 32 * 8 + WAVES * 2 * 32 * 8 + 16;
+  auto kern = posterior_f64_kernel<WAVES, D>;
   const int rc = allow_full_lds((const void*)kern, "posterior");
   if (rc != SCOOT_OK) return rc;
-  const int64_t grid = (n + 31) / 32;
+  const int64_t grid = persistent_grid((const void*)kern, WAVES * 64, lds, (n + 31) / 32);
+  if (grid < 1) return fail(SCOOT_ERR_DEVICE, "posterior: workgroup does not fit on a compute unit");
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WAVES * 64), lds, s, Xc,
                      (const d2_t*)g.linv, (const double*)g.xs, g.alpha, mu, sd, ei, a);
   return SCOOT_OK;
@@ -546,16 +657,6 @@ int by_d_rec(int d, F&& f) {
   } else {
     if (d == D) return f(std::integral_constant<int, D>());
     return by_d_rec<D + 1>(d, std::forward<F>(f));
-  }
-}
-
-template <typename F>
-int by_d4(int d4, F&& f) {
-  switch (d4) {
-    case 1: return f(std::integral_constant<int, 1>());
-    case 2: return f(std::integral_constant<int, 2>());
-    case 3: return f(std::integral_constant<int, 3>());
-    default: return f(std::integral_constant<int, 4>());
   }
 }
 
@@ -610,6 +711,9 @@ int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, vo
       a.wb[k] = g.warp_b[k];
     }
     a.nb16 = g.m_pad / kBlk64;
+    a.plan = plan_rows64(a.nb16, posterior_waves(g.nb));
+    for (int e = 0; e < 8; ++e)
+      if (a.plan.nrows[e] > kMaxRows64) return fail(SCOOT_ERR_UNSUPPORTED, "posterior: row plan does not pack");
     for (int k = 0; k < SCOOT_MAX_DIM; ++k) a.scale[k] = g.scale64[k];
     a.c0 = g.coef64[0];
     a.c1 = g.coef64[1];
@@ -618,8 +722,11 @@ int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, vo
     a.prior = g.c;
     a.ei_c = ei_c ? *ei_c : 0.0;
     double* e = ei_c ? (double*)ei : nullptr;
-    rc = by_d4(g.d4, [&](auto D4) {
-      return run64<4, decltype(D4)::value>(g, Xc, n, (double*)mu, (double*)sigma, e, a, s);
+    rc = by_d_rec<1>(g.d, [&](auto Dc) {
+      constexpr int D = decltype(Dc)::value;
+      double *m64 = (double*)mu, *s64 = (double*)sigma;
+      if (posterior_waves(g.nb) == 8) return run64<8, D>(g, Xc, n, m64, s64, e, a, s);
+      return run64<4, D>(g, Xc, n, m64, s64, e, a, s);
     });
   }
   if (rc != SCOOT_OK) return rc;
