@@ -94,6 +94,31 @@ def test_posterior_parity(case, dt):
     assert_close(sd.cpu().numpy(), sd_o, t["sd"], np.sqrt(w["signal_var"][obj]), f"{name} sigma")
 
 
+_ORACLE_POST = {}
+
+
+@pytest.mark.parametrize("dt", [S.F32, S.F64], ids=["f32", "f64"])
+@pytest.mark.parametrize("cfg,m", [(3, 256), (4, 512)], ids=["m256-4waves", "m512-8waves"])
+def test_posterior_many_tiles_per_workgroup(cfg, m, dt):
+    """The kernels are persistent (one workgroup per slot on the chip, each
+    looping over tiles, the inverse-factor stream and the next tile's
+    coordinates carried across tiles): 100003 candidates give every workgroup
+    several tiles (32 or 64 candidates each) and a ragged last one."""
+    n = 100003
+    w = wl(cfg, n, m)
+    say("posterior many tiles", cfg, "dtype", dt, "m", w["m"], "n", n)
+    args = (w["X"], w["Y"][:, 0], w["lengthscale"][0], w["signal_var"][0], w["noise_var"][0], w["prior_mean"][0])
+    if (cfg, n, m) not in _ORACLE_POST:
+        _ORACLE_POST[(cfg, n, m)] = gp_posterior(gp_fit(*args), w["Xc"].astype(np.float64))
+    mu_o, sd_o = _ORACLE_POST[(cfg, n, m)]
+    g = S.gp_fit(*args, dtype=dt)
+    mu, sd = S.posterior(g, dev(w["Xc"]))
+    torch.cuda.synchronize()
+    t = TOL[dt]
+    assert_close(mu.cpu().numpy(), mu_o, t["mu"], np.max(np.abs(mu_o)), f"many tiles {cfg} mu")
+    assert_close(sd.cpu().numpy(), sd_o, t["sd"], np.sqrt(w["signal_var"][0]), f"many tiles {cfg} sigma")
+
+
 EDGE_SHAPES = [(1, 1, 1, 0.5), (1, 16, 70, 0.5), (31, 16, 63, 0.5), (64, 3, 65, 0.3), (576, 5, 130, 0.4),
                (200, 12, 1, 0.5), (33, 10, 64 * 3 + 1, 0.5)]
 
