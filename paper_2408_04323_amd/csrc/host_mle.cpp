@@ -21,6 +21,7 @@
 #include <deque>
 #include <vector>
 
+#include "host_blas.h"
 #include "internal.h"
 
 namespace scoot {
@@ -35,16 +36,19 @@ struct MleData {
   scoot_kernel kernel;
   std::vector<double> Xw;  // m x d warped inputs
   std::vector<double> r;   // y - c
+  // Work matrices of nll_eval (m x m), allocated on the first evaluation and
+  // reused: fresh allocations of this size are page-faulted in on every
+  // evaluation, by all threads at once.  The entries an evaluation does not
+  // write keep their initial zeros.
+  mutable std::vector<double> L, Kf, Rad, Lt;
 };
 
-constexpr int kChunks = 32;  // work split of every parallel step (independent of the thread count)
-
-double dot(const double* a, const double* b, int n) {
-  double s = 0.0;
-#pragma omp simd reduction(+ : s)
-  for (int k = 0; k < n; ++k) s += a[k] * b[k];
-  return s;
+std::vector<double>& work(std::vector<double>& v, size_t n) {
+  if (v.size() != n) v.assign(n, 0.0);
+  return v;
 }
+
+constexpr int kChunks = 32;  // work split of every parallel step (independent of the thread count)
 
 // NLL and gradient at theta; false when K is not positive definite.
 bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) {
@@ -56,8 +60,12 @@ bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) 
   const double root = m52 ? kSqrt5m : kSqrt3m;
   const double* X = D.Xw.data();
 
-  // K (lower triangle), rows in parallel, then its Cholesky factor
-  std::vector<double> L((size_t)m * m, 0.0);
+  // K (lower triangle), rows in parallel, then its Cholesky factor.  The
+  // gradient reuses K - tau2 I (= dK/dlog s2) and the radial factor of
+  // dK/dlog l_k, kept from here (lower triangles).
+  std::vector<double>& L = work(D.L, (size_t)m * m);
+  double* Kf = grad ? work(D.Kf, (size_t)m * m).data() : nullptr;
+  double* Rad = grad ? work(D.Rad, (size_t)m * m).data() : nullptr;
   parallel_chunks(kChunks, [&](int c) {
     for (int i = c; i < m; i += kChunks)
       for (int j = 0; j <= i; ++j) {
@@ -67,61 +75,73 @@ bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) 
           r2 += t * t;
         }
         const double t = root * std::sqrt(r2);
-        const double kv = m52 ? s2 * (1.0 + t + t * t / 3.0) * std::exp(-t) : s2 * (1.0 + t) * std::exp(-t);
+        const double e = std::exp(-t);
+        const double kv = m52 ? s2 * (1.0 + t + t * t / 3.0) * e : s2 * (1.0 + t) * e;
         L[(size_t)i * m + j] = kv + (i == j ? tau2 : 0.0);
+        if (grad) {
+          Kf[(size_t)i * m + j] = kv;
+          Rad[(size_t)i * m + j] = m52 ? 5.0 / 3.0 * s2 * (1.0 + t) * e : 3.0 * s2 * e;
+        }
       }
   });
   if (!cholesky_lower(L.data(), m)) return false;
 
-  // alpha = K^-1 r and log det K
+  // alpha = K^-1 r and log det K: forward substitution by rows, back
+  // substitution by columns of L^T (rows of L, contiguous).
   std::vector<double> z(m), alpha(m);
   double logdet = 0.0;
   for (int i = 0; i < m; ++i) {
     const double* Li = L.data() + (size_t)i * m;
-    z[i] = (D.r[i] - dot(Li, z.data(), i)) / Li[i];
+    z[i] = (D.r[i] - dot2(Li, z.data(), i)) / Li[i];
     logdet += 2.0 * std::log(Li[i]);
   }
+  alpha = z;
   for (int i = m - 1; i >= 0; --i) {
-    double s = z[i];
-    for (int k = i + 1; k < m; ++k) s -= L[(size_t)k * m + i] * alpha[k];
-    alpha[i] = s / L[(size_t)i * m + i];
+    const double* Li = L.data() + (size_t)i * m;
+    alpha[i] /= Li[i];
+    const double ai = alpha[i];
+    for (int k = 0; k < i; ++k) alpha[k] -= Li[k] * ai;
   }
   double quad = 0.0;
   for (int i = 0; i < m; ++i) quad += D.r[i] * alpha[i];
   *nll = 0.5 * quad + 0.5 * logdet + 0.5 * m * kLog2Pi;
   if (!grad) return true;
 
-  // K^-1 = L^-T L^-1.  Column j of L^-1 (forward substitution, columns
-  // independent) is stored as row j of Lt, so that
-  // K^-1[i][j] = sum_{k >= max(i, j)} Lt[i][k] Lt[j][k] is a dot product of two rows.
-  std::vector<double> Lt((size_t)m * m, 0.0);
+  // K^-1 = L^-T L^-1.  Column j of L^-1 is stored as row j of Lt (zero before
+  // index j), so K^-1[i][j] = sum_{k >= i} Lt[i][k] Lt[j][k] for j <= i; the
+  // entries come in tiles of 4 rows x 2 columns summed from the tile's first
+  // row i0 (the terms below row i are zeros).
+  std::vector<double>& Lt = work(D.Lt, (size_t)m * m);
   lower_inverse(L.data(), m, Lt.data(), true);
 
-  // Gradient: pairs (i, j <= i) by rows, partial sums per chunk, added in chunk order.
+  // Gradient: tiles by groups of four rows, partial sums per chunk, added in
+  // chunk order.
   std::vector<double> part((size_t)kChunks * (d + 2), 0.0);
+  const int groups = (m + 3) / 4;
   parallel_chunks(kChunks, [&](int c) {
     double* g = part.data() + (size_t)c * (d + 2);
-    for (int i = c; i < m; i += kChunks) {
-      const double* ti = Lt.data() + (size_t)i * m;
-      for (int j = 0; j <= i; ++j) {
-        const double* tj = Lt.data() + (size_t)j * m;
-        const double kinv = dot(ti + i, tj + i, m - i);
-        const double Wij = alpha[i] * alpha[j] - kinv;
-        const double mult = i == j ? 1.0 : 2.0;  // W and dK are symmetric
-        double r2 = 0.0;
-        double D2[SCOOT_MAX_DIM];
-        for (int k = 0; k < d; ++k) {
-          const double t = (X[(size_t)i * d + k] - X[(size_t)j * d + k]) * inv_ls[k];
-          D2[k] = t * t;
-          r2 += D2[k];
-        }
-        const double t = root * std::sqrt(r2);
-        const double e = std::exp(-t);
-        const double kf = m52 ? s2 * (1.0 + t + t * t / 3.0) * e : s2 * (1.0 + t) * e;
-        const double radial = m52 ? 5.0 / 3.0 * s2 * (1.0 + t) * e : 3.0 * s2 * e;
-        for (int k = 0; k < d; ++k) g[k] -= 0.5 * mult * Wij * radial * D2[k];
-        g[d] -= 0.5 * mult * Wij * kf;
-        if (i == j) g[d + 1] -= 0.5 * Wij * tau2;
+    for (int gi = c; gi < groups; gi += kChunks) {
+      const int i0 = 4 * gi;
+      const double* a[4];
+      for (int r = 0; r < 4; ++r) a[r] = Lt.data() + (size_t)std::min(i0 + r, m - 1) * m + i0;
+      for (int j0 = 0; j0 <= i0 + 3 && j0 < m; j0 += 2) {
+        const double* b[2] = {Lt.data() + (size_t)j0 * m + i0, Lt.data() + (size_t)std::min(j0 + 1, m - 1) * m + i0};
+        double kinv[4][2];
+        dots_tile<4, 2>(a, b, m - i0, kinv);
+        for (int r = 0; r < 4; ++r)
+          for (int q = 0; q < 2; ++q) {
+            const int i = i0 + r, j = j0 + q;
+            if (i >= m || j > i) continue;
+            const double Wij = alpha[i] * alpha[j] - kinv[r][q];
+            const double w = 0.5 * (i == j ? 1.0 : 2.0) * Wij;  // W and dK are symmetric
+            const double wr = w * Rad[(size_t)i * m + j];
+            for (int k = 0; k < d; ++k) {
+              const double t = (X[(size_t)i * d + k] - X[(size_t)j * d + k]) * inv_ls[k];
+              g[k] -= wr * (t * t);
+            }
+            g[d] -= w * Kf[(size_t)i * m + j];
+            if (i == j) g[d + 1] -= w * tau2;
+          }
       }
     }
   });

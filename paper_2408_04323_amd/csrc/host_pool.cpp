@@ -4,11 +4,14 @@
 // chunks' partial results in chunk order, so results are identical whatever
 // the number of threads.
 //
-// A likelihood evaluation is a dozen short parallel steps, so waking the
-// workers dominates if they sleep between steps (measured: 23 us per empty
-// step with 8 threads).  Idle workers and a waiting caller therefore spin on
-// atomic mirrors of the job state for a bounded time before they block on the
-// condition variables; the state itself still changes only under the mutex.
+// A likelihood evaluation is a few dozen short parallel steps, so the cost of
+// handing out a step matters.  Each step is a job object shared by reference
+// count: threads claim its chunks from an atomic counter and count finished
+// chunks atomically, so no lock is taken on the way.  Idle workers and the
+// waiting caller spin for a bounded time before they sleep on a condition
+// variable; the mutex serves only that sleeping and waking.  A worker that
+// arrives after the last chunk was claimed finds the counter exhausted and
+// never calls the job's function, which may then no longer exist.
 #include <algorithm>
 #include <atomic>
 #include <chrono>
@@ -16,6 +19,7 @@
 #include <cstdlib>
 #include <exception>
 #include <functional>
+#include <memory>
 #include <mutex>
 #include <thread>
 #include <vector>
@@ -26,6 +30,23 @@ namespace scoot {
 
 namespace {
 
+struct Job {
+  const std::function<void(int)>* fn;
+  int n;
+  std::atomic<int> next{0}, done{0};
+  std::mutex err_mu;
+  std::exception_ptr error;
+};
+
+// Polls cond for up to 200 us; the caller blocks afterwards if it is still false.
+template <typename F>
+void spin_until(F&& cond) {
+  constexpr auto kSpin = std::chrono::microseconds(200);
+  const auto t0 = std::chrono::steady_clock::now();
+  for (int k = 0; !cond(); ++k)
+    if ((k & 255) == 255 && std::chrono::steady_clock::now() - t0 > kSpin) return;
+}
+
 class Pool {
  public:
   Pool() {
@@ -35,11 +56,8 @@ class Pool {
     for (int t = 1; t < want; ++t) workers_.emplace_back([this] { loop(); });
   }
   ~Pool() {
-    {
-      std::lock_guard<std::mutex> lk(mu_);
-      stop_ = true;
-      stop_seen_.store(true);
-    }
+    stop_.store(true);
+    { std::lock_guard<std::mutex> lk(mu_); }
     cv_.notify_all();
     for (auto& w : workers_) w.join();
   }
@@ -51,88 +69,67 @@ class Pool {
       return;
     }
     std::lock_guard<std::mutex> one_job(job_mu_);  // one job at a time
-    {
-      // The job's fields change only while no thread is inside work().
+    auto job = std::make_shared<Job>();
+    job->fn = &fn;
+    job->n = n_chunks;
+    std::atomic_store(&cur_, job);
+    gen_.fetch_add(1);
+    if (sleepers_.load() > 0) {
+      { std::lock_guard<std::mutex> lk(mu_); }  // a worker may be between its check and its wait
+      cv_.notify_all();
+    }
+    work(*job);  // the calling thread takes part
+    auto finished = [&] { return job->done.load(std::memory_order_acquire) == n_chunks; };
+    spin_until(finished);
+    if (!finished()) {
       std::unique_lock<std::mutex> lk(mu_);
-      cv_done_.wait(lk, [&] { return active_ == 0; });
-      fn_ = &fn;
-      n_ = n_chunks;
-      next_.store(0);
-      done_ = 0;
-      ++active_;  // the calling thread takes part
-      active_seen_.store(active_, std::memory_order_relaxed);
-      gen_.fetch_add(1, std::memory_order_release);
+      cv_done_.wait(lk, finished);
     }
-    cv_.notify_all();
-    work();
-    spin_until([&] { return active_seen_.load(std::memory_order_acquire) == 0; });
-    std::unique_lock<std::mutex> lk(mu_);
-    cv_done_.wait(lk, [&] { return done_ == n_ && active_ == 0; });
-    fn_ = nullptr;
-    if (error_) {  // a chunk threw: report it to the caller
-      std::exception_ptr e = error_;
-      error_ = nullptr;
-      std::rethrow_exception(e);
-    }
+    std::atomic_store(&cur_, std::shared_ptr<Job>());
+    if (job->error) std::rethrow_exception(job->error);  // a chunk threw: report it to the caller
   }
 
  private:
-  // Entered with active_ counting this thread; claims chunks until none is
-  // left, then reports them and leaves.
-  void work() {
-    int ran = 0;
-    std::exception_ptr err;
-    for (int c; (c = next_.fetch_add(1)) < n_;) {
+  // Claims chunks of job until none is left.
+  void work(Job& job) {
+    for (int c; (c = job.next.fetch_add(1)) < job.n;) {
       try {
-        (*fn_)(c);
+        (*job.fn)(c);
       } catch (...) {
-        if (!err) err = std::current_exception();
+        std::lock_guard<std::mutex> lk(job.err_mu);
+        if (!job.error) job.error = std::current_exception();
       }
-      ++ran;
+      if (job.done.fetch_add(1, std::memory_order_acq_rel) + 1 == job.n) {
+        { std::lock_guard<std::mutex> lk(mu_); }  // the caller may be between its check and its wait
+        cv_done_.notify_all();
+      }
     }
-    std::lock_guard<std::mutex> lk(mu_);
-    if (err && !error_) error_ = err;
-    done_ += ran;
-    --active_;
-    active_seen_.store(active_, std::memory_order_release);
-    cv_done_.notify_all();
   }
   void loop() {
     unsigned long seen = 0;
+    auto wake = [&] { return gen_.load() != seen || stop_.load(); };
     for (;;) {
-      spin_until([&] { return gen_.load(std::memory_order_acquire) != seen || stop_seen_.load(); });
-      {
+      spin_until(wake);
+      if (!wake()) {
         std::unique_lock<std::mutex> lk(mu_);
-        cv_.wait(lk, [&] { return stop_ || gen_.load() != seen; });
-        if (stop_) return;
-        seen = gen_.load();
-        ++active_;
-        active_seen_.store(active_, std::memory_order_relaxed);
+        sleepers_.fetch_add(1);
+        cv_.wait(lk, wake);
+        sleepers_.fetch_sub(1);
       }
-      work();
+      if (stop_.load()) return;
+      seen = gen_.load();
+      std::shared_ptr<Job> job = std::atomic_load(&cur_);
+      if (job) work(*job);
     }
-  }
-  // Polls cond for up to kSpin before the caller falls back to blocking.
-  template <typename F>
-  static void spin_until(F&& cond) {
-    constexpr auto kSpin = std::chrono::microseconds(200);
-    const auto t0 = std::chrono::steady_clock::now();
-    for (int k = 0; !cond(); ++k)
-      if ((k & 255) == 255 && std::chrono::steady_clock::now() - t0 > kSpin) return;
   }
 
   std::vector<std::thread> workers_;
   std::mutex mu_, job_mu_;
   std::condition_variable cv_, cv_done_;
-  const std::function<void(int)>* fn_ = nullptr;
-  std::atomic<int> next_{0};
-  int n_ = 0, done_ = 0, active_ = 0;
+  std::shared_ptr<Job> cur_;  // read and written with std::atomic_load / std::atomic_store
   std::atomic<unsigned long> gen_{0};
-  bool stop_ = false;
-  // lock-free mirrors of active_ and stop_ for the spinning waits
-  std::atomic<int> active_seen_{0};
-  std::atomic<bool> stop_seen_{false};
-  std::exception_ptr error_;
+  std::atomic<int> sleepers_{0};
+  std::atomic<bool> stop_{false};
 };
 
 Pool& pool() {

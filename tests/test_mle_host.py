@@ -43,7 +43,9 @@ def test_fit_reaches_the_oracle_optimum(kernel):
     th, f, it = S.gp_mle(X, y, theta0, lo, hi, kernel=kernel)
     th_o, f_o = fit_hyperparameters(X, y, theta0, lo, hi, kernel)
     assert it > 0 and np.all(th >= lo) and np.all(th <= hi)
-    assert f == pytest.approx(nll_and_grad(th, X, y, kernel)[0], rel=1e-12)
+    # the NLL is a cancelling sum of terms of order m (quadratic form, log
+    # determinant, m/2 log 2 pi): the same bar as the evaluation test above
+    assert f == pytest.approx(nll_and_grad(th, X, y, kernel)[0], rel=1e-11, abs=1e-10)
     # The likelihood is not convex, so the two searches may end in different
     # local minima: the library's must be at least as good as the oracle's,
     # stationary under the oracle's gradient, and a point the oracle's
