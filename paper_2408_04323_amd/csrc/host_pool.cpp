@@ -11,7 +11,9 @@
 // waiting caller spin for a bounded time before they sleep on a condition
 // variable; the mutex serves only that sleeping and waking.  A worker that
 // arrives after the last chunk was claimed finds the counter exhausted and
-// never calls the job's function, which may then no longer exist.
+// never calls the job's function, which may then no longer exist.  Up to
+// kSlots callers (say, the hyperparameter searches of several objectives) may
+// run jobs at the same time; idle threads take chunks from any of them.
 #include <algorithm>
 #include <atomic>
 #include <chrono>
@@ -68,11 +70,22 @@ class Pool {
       for (int c = 0; c < n_chunks; ++c) fn(c);
       return;
     }
-    std::lock_guard<std::mutex> one_job(job_mu_);  // one job at a time
     auto job = std::make_shared<Job>();
     job->fn = &fn;
     job->n = n_chunks;
-    std::atomic_store(&cur_, job);
+    int slot = -1;
+    {
+      std::unique_lock<std::mutex> lk(slots_mu_);
+      slot_free_.wait(lk, [&] {
+        for (int k = 0; k < kSlots; ++k)
+          if (!busy_[k]) return true;
+        return false;
+      });
+      for (int k = 0; k < kSlots && slot < 0; ++k)
+        if (!busy_[k]) slot = k;
+      busy_[slot] = true;
+    }
+    std::atomic_store(&slots_[slot], job);
     gen_.fetch_add(1);
     if (sleepers_.load() > 0) {
       { std::lock_guard<std::mutex> lk(mu_); }  // a worker may be between its check and its wait
@@ -85,14 +98,20 @@ class Pool {
       std::unique_lock<std::mutex> lk(mu_);
       cv_done_.wait(lk, finished);
     }
-    std::atomic_store(&cur_, std::shared_ptr<Job>());
+    std::atomic_store(&slots_[slot], std::shared_ptr<Job>());
+    {
+      std::lock_guard<std::mutex> lk(slots_mu_);
+      busy_[slot] = false;
+    }
+    slot_free_.notify_one();
     if (job->error) std::rethrow_exception(job->error);  // a chunk threw: report it to the caller
   }
 
  private:
-  // Claims chunks of job until none is left.
-  void work(Job& job) {
-    for (int c; (c = job.next.fetch_add(1)) < job.n;) {
+  // Claims chunks of job until none is left; whether it ran any.
+  bool work(Job& job) {
+    bool ran = false;
+    for (int c; (c = job.next.fetch_add(1)) < job.n; ran = true) {
       try {
         (*job.fn)(c);
       } catch (...) {
@@ -104,6 +123,7 @@ class Pool {
         cv_done_.notify_all();
       }
     }
+    return ran;
   }
   void loop() {
     unsigned long seen = 0;
@@ -117,16 +137,25 @@ class Pool {
         sleepers_.fetch_sub(1);
       }
       if (stop_.load()) return;
+      // every slot until a whole round finds nothing to do; a job published
+      // meanwhile moves gen_ past seen, so it is not missed
       seen = gen_.load();
-      std::shared_ptr<Job> job = std::atomic_load(&cur_);
-      if (job) work(*job);
+      for (bool any = true; any;) {
+        any = false;
+        for (int k = 0; k < kSlots; ++k) {
+          std::shared_ptr<Job> job = std::atomic_load(&slots_[k]);
+          if (job && work(*job)) any = true;
+        }
+      }
     }
   }
 
+  static constexpr int kSlots = 4;
   std::vector<std::thread> workers_;
-  std::mutex mu_, job_mu_;
-  std::condition_variable cv_, cv_done_;
-  std::shared_ptr<Job> cur_;  // read and written with std::atomic_load / std::atomic_store
+  std::mutex mu_, slots_mu_;
+  std::condition_variable cv_, cv_done_, slot_free_;
+  std::shared_ptr<Job> slots_[kSlots];  // read and written with std::atomic_load / std::atomic_store
+  bool busy_[kSlots] = {};              // under slots_mu_
   std::atomic<unsigned long> gen_{0};
   std::atomic<int> sleepers_{0};
   std::atomic<bool> stop_{false};

@@ -13,6 +13,8 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <system_error>
+#include <thread>
 #include <vector>
 
 #include "internal.h"
@@ -172,21 +174,51 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
       // ---- 2. hyperparameters and GPs ----------------------------------
       const int nt = d + 2;
       std::vector<double> theta((size_t)p * nt);
+      // The objectives' searches run side by side, each on its own thread and
+      // each spreading its likelihood evaluations over the library's host
+      // threads; every search is deterministic, so the result is the same as
+      // one after the other.
+      std::vector<int> search_rc(p, SCOOT_OK);
+      std::vector<std::string> search_err(p);
+      auto search = [&](int j) {
+        try {
+          double lo[SCOOT_MAX_DIM + 2], hi[SCOOT_MAX_DIM + 2], th[SCOOT_MAX_DIM + 2];
+          theta_box(o, j, d, lo, hi, th);
+          bool all_fixed = true;
+          for (int t = 0; t < nt; ++t) all_fixed = all_fixed && lo[t] == hi[t];
+          std::vector<double> yj(m);
+          for (int r = 0; r < m; ++r) yj[r] = Yv[(size_t)r * p + j];
+          const double* wa = o.warp_a ? o.warp_a + (size_t)j * d : nullptr;
+          const double* wb = o.warp_b ? o.warp_b + (size_t)j * d : nullptr;
+          if (!all_fixed) {
+            search_rc[j] = scoot_gp_mle(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, wa, wb, 0.0, lo, hi,
+                                        o.mle_max_iter > 0 ? o.mle_max_iter : kDefaultMleIter, th, nullptr, nullptr);
+            if (search_rc[j] != SCOOT_OK) search_err[j] = scoot_last_error();  // this thread's message
+          }
+          std::memcpy(&theta[(size_t)j * nt], th, sizeof(double) * nt);
+        } catch (...) {
+          search_rc[j] = SCOOT_ERR_NO_MEMORY;
+          search_err[j] = "suggest: hyperparameter search ran out of memory";
+        }
+      };
+      std::vector<std::thread> searches;
+      for (int j = 1; j < p; ++j) {
+        try {
+          searches.emplace_back(search, j);
+        } catch (const std::system_error&) {
+          search(j);  // no thread to spare: run it here
+        }
+      }
+      search(0);
+      for (auto& t : searches) t.join();
+      for (int j = 0; j < p; ++j)
+        if (search_rc[j] != SCOOT_OK) return fail(search_rc[j], search_err[j]);
       for (int j = 0; j < p; ++j) {
-        double lo[SCOOT_MAX_DIM + 2], hi[SCOOT_MAX_DIM + 2], th[SCOOT_MAX_DIM + 2];
-        theta_box(o, j, d, lo, hi, th);
-        bool all_fixed = true;
-        for (int t = 0; t < nt; ++t) all_fixed = all_fixed && lo[t] == hi[t];
+        const double* th = &theta[(size_t)j * nt];
         std::vector<double> yj(m);
         for (int r = 0; r < m; ++r) yj[r] = Yv[(size_t)r * p + j];
         const double* wa = o.warp_a ? o.warp_a + (size_t)j * d : nullptr;
         const double* wb = o.warp_b ? o.warp_b + (size_t)j * d : nullptr;
-        if (!all_fixed) {
-          rc = scoot_gp_mle(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, wa, wb, 0.0, lo, hi,
-                            o.mle_max_iter > 0 ? o.mle_max_iter : kDefaultMleIter, th, nullptr, nullptr);
-          if (rc != SCOOT_OK) return rc;
-        }
-        std::memcpy(&theta[(size_t)j * nt], th, sizeof(double) * nt);
         double ell[SCOOT_MAX_DIM];
         for (int t = 0; t < d; ++t) ell[t] = std::exp(th[t]);
         scoot_gp g = nullptr;

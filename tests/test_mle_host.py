@@ -92,3 +92,29 @@ def test_fit_on_a_workload_and_its_time():
     _, g = nll_and_grad(th, X, y)
     interior = (th > lo + 1e-3) & (th < hi - 1e-3)
     assert np.max(np.abs(g[interior])) < 1e-3
+
+
+def test_concurrent_searches_match_sequential():
+    """Several searches at once (the suggestion step runs one per objective on
+    its own thread, all sharing the library's host threads) give bit for bit
+    what they give one after the other."""
+    import threading
+
+    cases = [_case(10 + k, 40 + 7 * k, 3) for k in range(3)]
+    theta0 = np.log(np.array([0.5, 0.5, 0.5, 1.0, 0.05]))
+    lo = np.log(np.array([0.02] * 3 + [0.05, 1e-6]))
+    hi = np.log(np.array([10.0] * 3 + [20.0, 1.0]))
+    alone = [S.gp_mle(X, y, theta0, lo, hi, max_iter=40) for X, y in cases]
+    for _ in range(3):
+        together = [None] * len(cases)
+
+        def run(k):
+            together[k] = S.gp_mle(cases[k][0], cases[k][1], theta0, lo, hi, max_iter=40)
+
+        threads = [threading.Thread(target=run, args=(k,)) for k in range(len(cases))]
+        for t in threads:
+            t.start()
+        for t in threads:
+            t.join()
+        for a, b in zip(alone, together):
+            assert np.array_equal(a[0], b[0]) and a[1] == b[1] and a[2] == b[2]
