@@ -394,9 +394,22 @@ def bench_suggest(args):
     lo = np.log(np.array([0.01] * d + [0.05, 1e-6]))
     hi = np.log(np.array([10.0] * d + [20.0, 1.0]))
     th0 = np.log(np.array([0.5] * d + [1.0, 1e-3]))
+    # the searches alone, one objective at a time and side by side on threads
+    # (as the step runs them)
+    iters, one = [], []
+    for j in range(p):
+        t0 = time.perf_counter()
+        iters.append(S.gp_mle(X_obs[ok], Ys[:, j], th0, lo, hi)[2])
+        one.append((time.perf_counter() - t0) * 1e3)
+    parts["mle_each_objective_alone"] = one
+    import threading
+    threads = [threading.Thread(target=S.gp_mle, args=(X_obs[ok], Ys[:, j], th0, lo, hi)) for j in range(p)]
     t0 = time.perf_counter()
-    iters = [S.gp_mle(X_obs[ok], Ys[:, j], th0, lo, hi)[2] for j in range(p)]
-    parts["mle_all_objectives"] = (time.perf_counter() - t0) * 1e3
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    parts["mle_objectives_side_by_side"] = (time.perf_counter() - t0) * 1e3
     t0 = time.perf_counter()
     S.forest_train_create(X_obs, valid.astype(np.float64), c["trees"], c["depth"], seed=0)
     parts["forest_train"] = (time.perf_counter() - t0) * 1e3
