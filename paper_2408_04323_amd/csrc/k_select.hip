@@ -10,10 +10,11 @@
 // Stage 1: every wave walks its share of the array in chunks of 1024 keys (16
 // per lane) and keeps a running best-q list in its lanes: q rounds of a
 // wave-wide argmax (butterfly of shuffles, no barriers) over the chunk plus
-// the list.  Stage 2: one wave runs the same selection over all the stage-1
-// lists and writes indices, scores and the count.  Selection is exact integer
-// work, so the result does not depend on the grid shape or on the order in
-// which waves run.
+// the list.  Stage 2: one workgroup with a wave per chunk of the stage-1
+// lists (at most kSel2Waves) runs the same selection over them; with more
+// than one wave, the first selects again over the waves' lists (at most one
+// chunk).  It writes indices, scores and the count.  Selection is exact integer work, so the result does not
+// depend on the grid shape or on the order in which waves run.
 //
 // The same two stages make the random pick of the MACE suggestion (Sec. 4.5.1,
 // Sec. 4.6): candidate i's key is (u_i, inverted index), u_i the i-th output of
@@ -33,6 +34,7 @@ constexpr int kSelThreads = 256;  // stage 1 workgroup: four independent waves
 constexpr int kSelPer = 16;       // keys per lane per chunk
 constexpr int kSelChunk = 64 * kSelPer;
 constexpr int kSelMaxKeys2 = 16384;  // bound on the stage-1 lists stage 2 reads (waves x q)
+constexpr int kSel2Waves = 16;       // stage 2 workgroup; kSel2Waves x q (q <= 64) keys fit one chunk
 
 struct Key64 {
   uint64_t v;
@@ -164,16 +166,22 @@ __global__ __launch_bounds__(kSelThreads) void topq_stage1(const Src src, int64_
   if (lane == 0) part_count[wave] = valid;
 }
 
-// One wave: the best q of all stage-1 lists, then indices, scores and the count.
+// One workgroup of W waves: the best q of all stage-1 lists (wave w takes
+// chunks w, w + W, ... of them; wave 0 then merges the waves' lists), then
+// indices, scores and the count.
 template <typename T, typename K>
-__global__ __launch_bounds__(64) void topq_stage2(const T* __restrict__ score, int n_parts, int q,
-                                                  const K* __restrict__ part_keys,
-                                                  const int32_t* __restrict__ part_count, int64_t* __restrict__ idx,
-                                                  T* __restrict__ score_out, int32_t* __restrict__ n_valid) {
-  const int lane = threadIdx.x;
+__global__ __launch_bounds__(64 * kSel2Waves) void topq_stage2(const T* __restrict__ score, int n_parts, int q,
+                                                               const K* __restrict__ part_keys,
+                                                               const int32_t* __restrict__ part_count,
+                                                               int64_t* __restrict__ idx, T* __restrict__ score_out,
+                                                               int32_t* __restrict__ n_valid) {
+  __shared__ K wave_lists[kSel2Waves * 64];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
   K list{};
   const int64_t total = (int64_t)n_parts * q;
-  for (int64_t base = 0; base < total; base += kSelChunk) {
+  const int W = blockDim.x >> 6;
+  for (int64_t base = (int64_t)wave * kSelChunk; base < total; base += (int64_t)W * kSelChunk) {
     K keys[kSelPer];
 #pragma unroll
     for (int j = 0; j < kSelPer; ++j) {
@@ -183,6 +191,19 @@ __global__ __launch_bounds__(64) void topq_stage2(const T* __restrict__ score, i
 #pragma unroll
     for (int j = 0; j < kSelPer; ++j)
       if (base + (int64_t)j * 64 + lane >= total) keys[j] = K{};
+    wave_select<K>(keys, list, q);
+  }
+  if (W > 1) {
+    if (lane < q) wave_lists[wave * q + lane] = list;
+    __syncthreads();
+    if (wave != 0) return;
+    K keys[kSelPer];
+#pragma unroll
+    for (int j = 0; j < kSelPer; ++j) {
+      const int i = j * 64 + lane;
+      keys[j] = i < W * q ? wave_lists[i] : K{};
+    }
+    list = K{};
     wave_select<K>(keys, list, q);
   }
   if (lane < q) {
@@ -220,8 +241,9 @@ int run_select(const Src& src, const T* score, int64_t n, int q, int64_t* idx, T
   K* pk = reinterpret_cast<K*>(ws);
   int32_t* pc = reinterpret_cast<int32_t*>(ws + kbytes);
   hipLaunchKernelGGL((topq_stage1<K, Src>), dim3((unsigned)grid), dim3(kSelThreads), 0, s, src, n, q, pk, pc);
-  hipLaunchKernelGGL((topq_stage2<T, K>), dim3(1), dim3(64), 0, s, score, (int)waves, q, pk, pc, idx, score_out,
-                     n_valid);
+  const int w2 = (int)std::min<int64_t>(kSel2Waves, (waves * q + kSelChunk - 1) / kSelChunk);
+  hipLaunchKernelGGL((topq_stage2<T, K>), dim3(1), dim3(64 * w2), 0, s, score, (int)waves, q, pk, pc, idx,
+                     score_out, n_valid);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("topq launch: ") + hipGetErrorString(err));
   return SCOOT_OK;
