@@ -24,6 +24,12 @@
  *   them: library-owned scratch of a device is reused from call to call.
  * - Handles are library-owned and not thread-safe; destroy them with the
  *   matching *_destroy call.
+ * - Host-side steps (GP fit, likelihood and its search, forest training) run
+ *   on a pool of host threads the library starts on first use
+ *   (SCOOT_HOST_THREADS, else the hardware threads up to 16).  Their results
+ *   do not depend on the thread count, and calls that share no handle may run
+ *   from several threads at once (scoot_suggest runs its objectives' searches
+ *   that way).
  * - Every call returns a scoot_status.  On error the outputs are undefined and
  *   scoot_last_error() returns a message for the calling thread.  No C++
  *   exception crosses the ABI.
