@@ -383,16 +383,18 @@ int scoot_forest_create(const int32_t* feature, const float* threshold, const in
     f.chunk_tree = fh.chunk_tree;
     f.chunk_first_node = fh.chunk_first_node;
     const size_t nb = fh.nodes.size() * 4, rb = fh.root.size() * 4, db = fh.depth.size() * 4,
-                 lb = fh.leaf_orig.size() * 4;
-    hipError_t e = hipMalloc(&f.nodes, nb + rb + db + lb);
+                 lb = fh.leaf_orig.size() * 4, tb = fh.tree_orig.size() * 4;
+    hipError_t e = hipMalloc(&f.nodes, nb + rb + db + lb + tb);
     if (e != hipSuccess) return fail(SCOOT_ERR_NO_MEMORY, "forest: device allocation failed");
     f.root = (uint32_t*)((unsigned char*)f.nodes + nb);
     f.depth = (uint32_t*)((unsigned char*)f.root + rb);
     f.leaf_orig = (int32_t*)((unsigned char*)f.depth + db);
+    f.tree_orig = (int32_t*)((unsigned char*)f.leaf_orig + lb);
     e = hipMemcpy(f.nodes, fh.nodes.data(), nb, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(f.root, fh.root.data(), rb, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(f.depth, fh.depth.data(), db, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(f.leaf_orig, fh.leaf_orig.data(), lb, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(f.tree_orig, fh.tree_orig.data(), tb, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       hipFree(f.nodes);
       return device_error("forest: upload", e);

@@ -1,7 +1,9 @@
 // Host side of the random-forest feasibility mask (Sec. 4.7, Eq. 3): checks
 // the flat tree arrays and repacks every tree breadth-first so that the two
 // children of a node are adjacent (one child index per node), 8 bytes per
-// node (encoding in internal.h), and groups consecutive trees into chunks
+// node (encoding in internal.h), orders the trees deepest first (a thread
+// walks four trees for as many steps as the deepest of them; votes are sums,
+// so the order does not change them) and groups consecutive trees into chunks
 // that fit the on-chip memory of one workgroup.
 #include <algorithm>
 #include <cmath>
@@ -59,14 +61,26 @@ int pack_forest(const int32_t* feature, const float* threshold, const int32_t* l
     }
   }
 
-  // Chunks of consecutive trees: one unused node, then whole trees, at most
+  // Slots: trees deepest first, ties by index.
+  fh.tree_orig.resize(n_trees);
+  for (int t = 0; t < n_trees; ++t) fh.tree_orig[t] = t;
+  std::stable_sort(fh.tree_orig.begin(), fh.tree_orig.end(),
+                   [&](int a, int b) { return fh.depth[a] > fh.depth[b]; });
+  {
+    std::vector<uint32_t> by_slot(n_trees);
+    for (int s = 0; s < n_trees; ++s) by_slot[s] = fh.depth[fh.tree_orig[s]];
+    fh.depth = by_slot;
+  }
+
+  // Chunks of consecutive slots: one unused node, then whole trees, at most
   // kChunkNodes nodes in all.
   fh.chunk_tree.push_back(0);
   int in_chunk = 1;
-  for (int t = 0; t < n_trees; ++t) {
+  for (int s = 0; s < n_trees; ++s) {
+    const int t = fh.tree_orig[s];
     int sz = (int)order[t].size();
     if (in_chunk + sz > kChunkNodes) {
-      fh.chunk_tree.push_back(t);
+      fh.chunk_tree.push_back(s);
       in_chunk = 1;
     }
     in_chunk += sz;
@@ -86,7 +100,8 @@ int pack_forest(const int32_t* feature, const float* threshold, const int32_t* l
     fh.nodes[2 * next] = 0;  // the unused node
     fh.nodes[2 * next + 1] = kLeafNaN;
     ++next;
-    for (int t = fh.chunk_tree[ch]; t < fh.chunk_tree[ch + 1]; ++t) {
+    for (int s = fh.chunk_tree[ch]; s < fh.chunk_tree[ch + 1]; ++s) {
+      const int t = fh.tree_orig[s];
       int64_t base = tree_offset[t];
       std::vector<uint32_t> pos(tree_offset[t + 1] - base, 0);
       uint32_t cursor = next;
@@ -98,7 +113,7 @@ int pack_forest(const int32_t* feature, const float* threshold, const int32_t* l
           pos[right[g]] = cursor++;
         }
       }
-      fh.root[t] = pos[0];
+      fh.root[s] = pos[0];
       for (int u : order[t]) {
         int64_t g = base + u;
         uint32_t at = pos[u];

@@ -259,10 +259,13 @@ constexpr int kChunkNodes = 8192;
 struct ForestHost {
   int n_trees = 0, d = 0;
   std::vector<uint32_t> nodes;             // 2 words per node
-  std::vector<uint32_t> root;              // packed index of each tree's root (n_trees + 1 entries)
-  std::vector<uint32_t> depth;             // edges from each tree's root to its deepest leaf
+  // Trees are packed in slots ordered by depth (deepest first, then by index),
+  // so that the four trees a thread walks together have similar depths.
+  std::vector<int32_t> tree_orig;          // tree index (as given) in each slot
+  std::vector<uint32_t> root;              // packed index of each slot's root (n_trees + 1 entries)
+  std::vector<uint32_t> depth;             // edges from each slot's root to its deepest leaf
   std::vector<int32_t> leaf_orig;          // per packed node: tree-local index of a leaf, -1 otherwise
-  std::vector<int> chunk_tree;             // first tree of each LDS chunk (+ end)
+  std::vector<int> chunk_tree;             // first slot of each LDS chunk (+ end)
   std::vector<uint32_t> chunk_first_node;  // packed index of each chunk's unused first node (+ end)
 };
 int pack_forest(const int32_t* feature, const float* threshold, const int32_t* left,
@@ -291,10 +294,11 @@ struct GPDevice {
 
 struct ForestDevice {
   int n_trees = 0, d = 0;
-  uint32_t* nodes = nullptr;     // one allocation: nodes | root | depth | leaf_orig
+  uint32_t* nodes = nullptr;     // one allocation: nodes | root | depth | leaf_orig | tree_orig
   uint32_t* root = nullptr;
   uint32_t* depth = nullptr;
   int32_t* leaf_orig = nullptr;
+  int32_t* tree_orig = nullptr;
   std::vector<int> chunk_tree;
   std::vector<uint32_t> chunk_first_node;
 };

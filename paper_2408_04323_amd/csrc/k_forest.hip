@@ -9,8 +9,9 @@
 // feature it names, go to child + (x <= threshold ? 0 : 1) (a float32
 // compare; NaN goes right).  Leaves carry a NaN threshold and point one below
 // themselves, so a walk that has arrived stays put; each group of trees runs
-// exactly as many steps as its deepest tree, then reads the leaves' values
-// from the NaN payloads.  Forests larger than one chunk take one launch per
+// exactly as many steps as its deepest tree (the host orders the trees deepest
+// first, so the four are alike), then reads the leaves' values from the NaN
+// payloads.  Forests larger than one chunk take one launch per
 // chunk, the vote counts carried in the votes array between launches.
 #include <hip/hip_runtime.h>
 
@@ -36,7 +37,8 @@ struct ForestArgs {
 
 __global__ __launch_bounds__(kForestThreads) void forest_kernel(
     const uint2* __restrict__ nodes, const uint32_t* __restrict__ root, const uint32_t* __restrict__ depth,
-    const int32_t* __restrict__ leaf_orig, const float* __restrict__ Xc, int32_t* __restrict__ votes,
+    const int32_t* __restrict__ leaf_orig, const int32_t* __restrict__ tree_orig, const float* __restrict__ Xc,
+    int32_t* __restrict__ votes,
     uint8_t* __restrict__ mask, int32_t* __restrict__ leaf_idx, const uint8_t* __restrict__ known,
     const ForestArgs a) {
   // LDS: the feature columns [d][kForestThreads] floats at LDS address 0 (the
@@ -80,7 +82,7 @@ __global__ __launch_bounds__(kForestThreads) void forest_kernel(
       for (int q = 0; q < kWalks; ++q) {
         if (q < cnt) {
           v += (int32_t)(tree[node[q]].y & 0x1FFFFu);
-          if (leaf_idx) leaf_idx[c * a.n_trees + t0 + q] = leaf_orig[a.node_base + node[q]];
+          if (leaf_idx) leaf_idx[c * a.n_trees + tree_orig[t0 + q]] = leaf_orig[a.node_base + node[q]];
         }
       }
     }
@@ -125,7 +127,7 @@ int launch_forest(const ForestDevice& f, const float* Xc, int64_t n, int64_t vot
     a.vote_min = (int32_t)vote_min;
     const size_t lds = (size_t)a.n_nodes * 8 + (size_t)f.d * kForestThreads * 4;
     hipLaunchKernelGGL(forest_kernel, dim3((unsigned)grid), dim3(kForestThreads), lds, s, (const uint2*)f.nodes,
-                       f.root, f.depth, f.leaf_orig, Xc, votes, mask, leaf_idx, known, a);
+                       f.root, f.depth, f.leaf_orig, f.tree_orig, Xc, votes, mask, leaf_idx, known, a);
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("forest launch: ") + hipGetErrorString(err));
