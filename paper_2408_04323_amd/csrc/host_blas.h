@@ -71,7 +71,10 @@ __attribute__((target("avx2,fma"))) void dots_tile_avx2(const double* const (&a)
 // Whether the AVX2 form is used: decided once per process from the CPU, so
 // every sum of a run is formed the same way whatever the thread count.
 inline bool use_avx2() {
-  static const bool yes = __builtin_cpu_supports("avx2") && __builtin_cpu_supports("fma");
+  static const bool yes = [] {
+    __builtin_cpu_init();
+    return __builtin_cpu_supports("avx2") && __builtin_cpu_supports("fma");
+  }();
   return yes;
 }
 
