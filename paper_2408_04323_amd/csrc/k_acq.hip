@@ -22,6 +22,7 @@
 //   the box records (k, h) arrive through wave-uniform loads.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "internal.h"
@@ -42,12 +43,21 @@ __global__ __launch_bounds__(256) void ei_kernel(const T* __restrict__ mu, const
 constexpr int kEhviThreads = 64;
 constexpr int kStripThreads = 256;
 
-// p <= 2: boxes in strip order; coords holds, per box, a_{i+1} (axis 0) and
-// h_i (axis 1, unused when p = 1); a_0 = -inf.
-template <typename T, int P>
+// p <= 2: boxes in strip order; hi holds, per box, a_{i+1} (axis 0) and
+// h_i (axis 1, unused when p = 1); a_0 = -inf.  The table is read with
+// wave-uniform indices: either from device memory (a pointer) or, when it
+// fits, straight from the kernel arguments (StripArgTable), which spares an
+// upload before every launch.
+constexpr int kStripArgBytes = 2048;
+template <typename T>
+struct StripArgTable {
+  T v[kStripArgBytes / sizeof(T)];
+  __device__ T operator[](int i) const { return v[i]; }
+};
+template <typename T, int P, typename Table>
 __global__ __launch_bounds__(kStripThreads) void ehvi_strip_kernel(const T* __restrict__ mu0, const T* __restrict__ mu1,
                                                                    const T* __restrict__ sd0, const T* __restrict__ sd1,
-                                                                   const T* __restrict__ hi, int n_boxes, int64_t n,
+                                                                   const Table hi, int n_boxes, int64_t n,
                                                                    T* __restrict__ out) {
   for (int64_t c = (int64_t)blockIdx.x * kStripThreads + threadIdx.x; c < n; c += (int64_t)gridDim.x * kStripThreads) {
     const T m0 = mu0[c], s0 = sd0[c], r0 = reciprocal(s0);
@@ -151,22 +161,33 @@ int run_ehvi_strip(const void* const* mu, const void* const* sigma, int p, int64
     hi[2 * b] = (T)bt.coord[0][bt.hi[(size_t)b * p]];
     if (p == 2) hi[2 * b + 1] = (T)bt.coord[1][bt.hi[(size_t)b * p + 1]];
   }
-  void* dev = device_scratch(hi.size() * sizeof(T), 1);
-  if (!dev) return fail(SCOOT_ERR_NO_MEMORY, "ehvi: device scratch allocation failed");
-  int rc = upload_async(dev, hi.data(), hi.size() * sizeof(T), 0, s);
-  if (rc != SCOOT_OK) return rc;
   int64_t blocks = (n + kStripThreads - 1) / kStripThreads;
   if (blocks > 8192) blocks = 8192;
   const T* m0 = (const T*)mu[0];
   const T* s0 = (const T*)sigma[0];
   const T* m1 = (const T*)(p == 2 ? mu[1] : mu[0]);
   const T* s1 = (const T*)(p == 2 ? sigma[1] : sigma[0]);
-  if (p == 2)
-    hipLaunchKernelGGL((ehvi_strip_kernel<T, 2>), dim3((unsigned)blocks), dim3(kStripThreads), 0, s, m0, m1, s0, s1,
-                       (const T*)dev, nbx, n, (T*)out);
-  else
-    hipLaunchKernelGGL((ehvi_strip_kernel<T, 1>), dim3((unsigned)blocks), dim3(kStripThreads), 0, s, m0, m1, s0, s1,
-                       (const T*)dev, nbx, n, (T*)out);
+  if (hi.size() * sizeof(T) <= kStripArgBytes) {
+    StripArgTable<T> tab{};
+    std::copy(hi.begin(), hi.end(), tab.v);
+    if (p == 2)
+      hipLaunchKernelGGL((ehvi_strip_kernel<T, 2, StripArgTable<T>>), dim3((unsigned)blocks), dim3(kStripThreads), 0,
+                         s, m0, m1, s0, s1, tab, nbx, n, (T*)out);
+    else
+      hipLaunchKernelGGL((ehvi_strip_kernel<T, 1, StripArgTable<T>>), dim3((unsigned)blocks), dim3(kStripThreads), 0,
+                         s, m0, m1, s0, s1, tab, nbx, n, (T*)out);
+  } else {
+    void* dev = device_scratch(hi.size() * sizeof(T), 1);
+    if (!dev) return fail(SCOOT_ERR_NO_MEMORY, "ehvi: device scratch allocation failed");
+    int rc = upload_async(dev, hi.data(), hi.size() * sizeof(T), 0, s);
+    if (rc != SCOOT_OK) return rc;
+    if (p == 2)
+      hipLaunchKernelGGL((ehvi_strip_kernel<T, 2, const T*>), dim3((unsigned)blocks), dim3(kStripThreads), 0, s, m0,
+                         m1, s0, s1, (const T*)dev, nbx, n, (T*)out);
+    else
+      hipLaunchKernelGGL((ehvi_strip_kernel<T, 1, const T*>), dim3((unsigned)blocks), dim3(kStripThreads), 0, s, m0,
+                         m1, s0, s1, (const T*)dev, nbx, n, (T*)out);
+  }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("ehvi launch: ") + hipGetErrorString(err));
   return SCOOT_OK;
