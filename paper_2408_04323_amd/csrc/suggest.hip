@@ -202,6 +202,7 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
         }
       };
       std::vector<std::thread> searches;
+      searches.reserve(p);  // no reallocation once a thread runs
       for (int j = 1; j < p; ++j) {
         try {
           searches.emplace_back(search, j);
