@@ -21,9 +21,9 @@
 // the result is stored as float32.  A candidate is admissible when every
 // constraint row sum_k A[r][k] x_k <= b[r] holds, the sum taken over k in
 // order in double with each product and each sum rounded separately.  Linear
-// rows express every rule the paper lists: an order between two knobs, "not
-// both", "one implies the other", and a bound that applies unless a boolean is
-// set (big-M on the boolean).
+// rows express every rule the paper lists: an order between two knobs, two
+// switches that exclude each other, one switch that requires another, and a
+// bound that applies unless a boolean is set (big-M on the boolean).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
