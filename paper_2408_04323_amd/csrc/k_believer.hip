@@ -92,13 +92,23 @@ __global__ __launch_bounds__(kKbThreads) void kb_update_kernel(float* __restrict
 
 __global__ void kb_exclude_kernel(uint8_t* __restrict__ eligible, int64_t pick) { eligible[pick] = 0; }
 
+// What the host needs after a top-1, in one place: out = (score, mu_0(pick),
+// ..., mu_{p-1}(pick)); the means are left alone when there is no pick.
+__global__ void kb_pick_kernel(const int64_t* __restrict__ idx, const float* __restrict__ score,
+                               const float* __restrict__ mu, int64_t n, int p, float* __restrict__ out) {
+  const int j = threadIdx.x;
+  const int64_t pick = idx[0];
+  if (j == 0) out[0] = score[0];
+  if (j < p && pick >= 0) out[1 + j] = mu[(int64_t)j * n + pick];
+}
+
 namespace {
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 // Row stride of a kept V: n rounded up to 64 floats (256 bytes).
 int64_t kb_ld(int64_t n) { return (n + 63) / 64 * 64; }
 
 struct KbLayout {
-  size_t v, mu, sd, acq, elig, votes, idx, score, nvalid, vp, dinv, xw, total;
+  size_t v, mu, sd, acq, elig, votes, idx, score, nvalid, vp, dinv, pickinfo, xw, total;
 };
 
 KbLayout kb_layout(const GPDevice* const* g, int p, int64_t n, int q) {
@@ -126,6 +136,7 @@ KbLayout kb_layout(const GPDevice* const* g, int p, int64_t n, int q) {
   L.nvalid = take(4);
   L.vp = take((size_t)p * rows_max * 4);
   L.dinv = take((size_t)p * 4);
+  L.pickinfo = take((size_t)(1 + SCOOT_MAX_OBJECTIVES) * 4);
   size_t xw = 0;  // the pool after each warped GP's input warping
   for (int j = 0; j < p; ++j) xw += g[j]->warp ? align256((size_t)n * g[j]->d * 4) : 0;
   L.xw = take(xw);
@@ -159,6 +170,7 @@ int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f,
   int32_t* nvalid = (int32_t*)(w + L.nvalid);
   float* vp = (float*)(w + L.vp);
   float* dinv = (float*)(w + L.dinv);
+  float* pickinfo = (float*)(w + L.pickinfo);
   int rows_max = 0;
   for (int j = 0; j < p; ++j) rows_max = std::max(rows_max, g[j]->m_pad + q);
   // candidates as each GP sees them: warped copies kept for the whole loop
@@ -199,23 +211,24 @@ int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f,
     if (rc != SCOOT_OK) return rc;
     rc = launch_topq(acq, elig, n, SCOOT_F32, 1, idx, score, nvalid, stream);
     if (rc != SCOOT_OK) return rc;
+    // One read-back per pick: the index, its score and its means (the
+    // fantasies).  The row updates below are left running while the host
+    // builds the next front.
+    hipLaunchKernelGGL(kb_pick_kernel, dim3(1), dim3(64), 0, s, idx, score, mu, n, p, pickinfo);
     int64_t pick = -1;
-    float best = 0.0f;
-    hipError_t e = hipMemcpyAsync(&pick, idx, 8, hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(&best, score, 4, hipMemcpyDeviceToHost, s);
+    float info[1 + SCOOT_MAX_OBJECTIVES] = {};
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess) e = hipMemcpyAsync(&pick, idx, 8, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(info, pickinfo, (size_t)(1 + p) * 4, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("believer: ") + hipGetErrorString(e));
     if (pick < 0) break;
     picks[k] = pick;
-    if (pick_acq) pick_acq[k] = best;
+    if (pick_acq) pick_acq[k] = info[0];
     *n_picked = k + 1;
     if (k + 1 == q) break;
     // fantasies for the front, then the bordered update of every objective
-    std::vector<float> mp(p);
-    for (int j = 0; j < p; ++j) {
-      e = hipMemcpyAsync(&mp[j], mu + (size_t)j * n + pick, 4, hipMemcpyDeviceToHost, s);
-      if (e != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("believer: ") + hipGetErrorString(e));
-    }
+    for (int j = 0; j < p; ++j) Yaug.push_back((double)info[1 + j]);
     for (int j = 0; j < p; ++j) {
       const int rows = g[j]->m_pad + k;
       float* vpj = vp + (size_t)j * rows_max;
@@ -238,9 +251,7 @@ int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f,
     }
     hipLaunchKernelGGL(kb_exclude_kernel, dim3(1), dim3(1), 0, s, elig, pick);
     e = hipGetLastError();
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("believer: ") + hipGetErrorString(e));
-    for (int j = 0; j < p; ++j) Yaug.push_back((double)mp[j]);
   }
   return SCOOT_OK;
 }
