@@ -33,6 +33,17 @@ def test_ei_monte_carlo():
         assert abs(float(expected_improvement(mu, sd, best)) - imp.mean()) <= 5 * se + 1e-12
 
 
+def test_ei_monte_carlo_with_xi():
+    # a margin as large as the spread, so that its sign shows (the paper adds
+    # xi to the improvement, Eq. 8; at xi = 1e-4 the test above cannot tell)
+    rng = np.random.default_rng(12)
+    for mu, sd, best, xi in [(0.3, 0.8, 0.1, 0.5), (-1.0, 0.2, -0.9, 0.1)]:
+        y = mu + sd * rng.standard_normal(1_000_000)
+        imp = np.maximum(0.0, best + xi - y)
+        se = imp.std() / np.sqrt(len(imp))
+        assert abs(float(expected_improvement(mu, sd, best, xi=xi)) - imp.mean()) <= 5 * se + 1e-12
+
+
 def test_ei_jensen_and_monotone_in_sigma():
     mu = np.linspace(-2, 2, 41)
     for sd in [0.01, 0.3, 1.0]:

@@ -1,0 +1,165 @@
+"""The oracle's pins catch plausible mistakes.  Each case plants one mistake in
+a copy of an oracle function (a wrong constant, a dropped term, a flipped
+sign, a transposed operand, a strict comparison, the wrong tie order), swaps
+it in for the real one, and runs the pin that should notice: the pin must
+fail.  Nothing here touches the library; the real oracle is restored after
+each case."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+from scipy.linalg import solve_triangular
+from scipy.spatial.distance import cdist
+from scipy.special import ndtr
+
+import oracle.acquisition as acq
+import oracle.forest as forest
+import oracle.gp as gp
+import oracle.hypervolume as hv
+import oracle.select as select
+import test_oracle_acq as pins_acq
+import test_oracle_forest_select as pins_forest
+import test_oracle_gp as pins_gp
+
+
+@pytest.fixture(scope="module")
+def textbook(golden_dir):
+    with open(os.path.join(golden_dir, "textbook_values.json")) as fh:
+        return json.load(fh)
+
+
+def _swap(monkeypatch, name, fn, *modules):
+    for mod in modules:
+        monkeypatch.setattr(mod, name, fn)
+
+
+def _must_fail(pin, *args):
+    with pytest.raises(AssertionError):
+        pin(*args)
+
+
+# ---------------------------------------------------------------- GP (Eq. 4-5)
+
+def test_matern52_wrong_constant(monkeypatch):
+    def matern52(A, B, lengthscale, signal_var):  # 5/2 where 5/3 belongs
+        r = cdist(np.asarray(A) / lengthscale, np.asarray(B) / lengthscale)
+        s5 = math.sqrt(5.0)
+        return signal_var * (1.0 + s5 * r + 2.5 * r * r) * np.exp(-s5 * r)
+    _swap(monkeypatch, "matern52", matern52, gp, pins_gp)
+    _must_fail(pins_gp.test_matern52_matches_sklearn)
+
+
+def _posterior(fit, Xc, mistake):
+    Ks = gp._cross(fit, np.asarray(Xc, dtype=np.float64))
+    mu = Ks @ fit["alpha"] + (0.0 if mistake == "no prior mean" else fit["prior_mean"])
+    L = fit["L"]
+    V = solve_triangular(L.T, Ks.T, lower=False) if mistake == "transposed factor" else \
+        solve_triangular(L, Ks.T, lower=True)
+    var = fit["signal_var"] - np.sum(V * V, axis=0)
+    if mistake == "noisy variance":
+        var = var + fit["noise_var"]
+    return mu, np.sqrt(np.maximum(var, 0.0))
+
+
+@pytest.mark.parametrize("mistake,pin", [
+    ("no prior mean", "test_single_observation_closed_form"),
+    ("noisy variance", "test_posterior_matches_sklearn"),
+    ("transposed factor", "test_posterior_matches_sklearn"),
+])
+def test_posterior_mistakes(monkeypatch, mistake, pin):
+    _swap(monkeypatch, "gp_posterior", lambda fit, Xc, chunk=8192: _posterior(fit, Xc, mistake), gp, pins_gp)
+    _must_fail(getattr(pins_gp, pin))
+
+
+# ------------------------------------------------------------ EI (Eq. 8)
+
+def test_partial_expectation_flipped_sign(monkeypatch, textbook):
+    def partial_expectation(c, mu, sigma):  # - sigma phi(u) where + belongs
+        c, mu, sigma = np.broadcast_arrays(*(np.asarray(v, dtype=np.float64) for v in (c, mu, sigma)))
+        u = (c - mu) / sigma
+        return (c - mu) * ndtr(u) - sigma * acq.norm_pdf(u)
+    _swap(monkeypatch, "partial_expectation", partial_expectation, acq, pins_acq)
+    _must_fail(pins_acq.test_partial_expectation_table, textbook)
+
+
+def test_ei_xi_sign(monkeypatch):
+    def expected_improvement(mu, sigma, best_y, xi=acq.XI_PAPER):  # best - xi where best + xi belongs
+        return acq.partial_expectation(best_y - xi, mu, sigma)
+    _swap(monkeypatch, "expected_improvement", expected_improvement, acq, pins_acq)
+    _must_fail(pins_acq.test_ei_monte_carlo_with_xi)
+
+
+# ----------------------------------------------------------- EHVI (Eq. 9)
+
+def _ehvi(mu, sigma, P, ref, mistake, boxes="columns", chunk=4096):
+    mu = np.atleast_2d(np.asarray(mu, dtype=np.float64))
+    sigma = np.atleast_2d(np.asarray(sigma, dtype=np.float64))
+    lo, hi = (hv.column_boxes if boxes == "columns" else hv.nondominated_cells)(P, ref)
+    if mistake == "last box dropped":
+        lo, hi = lo[:-1], hi[:-1]
+    if mistake == "objectives swapped":
+        mu, sigma = mu[:, ::-1], sigma[:, ::-1]
+    out = np.zeros(mu.shape[0])
+    for b in range(len(lo)):
+        term = np.ones(mu.shape[0])
+        for j in range(mu.shape[1]):
+            term *= acq.partial_expectation(hi[b, j], mu[:, j], sigma[:, j]) - \
+                acq.partial_expectation(lo[b, j], mu[:, j], sigma[:, j])
+        out += term
+    return out
+
+
+@pytest.mark.parametrize("mistake", ["last box dropped", "objectives swapped"])
+def test_ehvi_mistakes(monkeypatch, mistake):
+    _swap(monkeypatch, "ehvi", lambda mu, sigma, P, ref, boxes="columns", chunk=4096:
+          _ehvi(mu, sigma, P, ref, mistake, boxes), hv, pins_acq)
+    _must_fail(pins_acq.test_ehvi_monte_carlo)
+
+
+# ------------------------------------------------------ forest (Eq. 3)
+
+def test_forest_strict_comparison(monkeypatch):
+    def forest_apply(f, Xc):  # x < t where x <= t belongs
+        Xc = np.asarray(Xc, dtype=np.float32)
+        feat, thr = f["feature"], f["threshold"].astype(np.float32)
+        left, right, off = f["left"], f["right"], f["tree_offset"]
+        leaves = np.empty((len(Xc), len(off) - 1), dtype=np.int32)
+        rows = np.arange(len(Xc))
+        for t in range(len(off) - 1):
+            node = np.zeros(len(Xc), dtype=np.int64)
+            while True:
+                internal = left[off[t] + node] >= 0
+                if not internal.any():
+                    break
+                g = off[t] + node[internal]
+                node[internal] = np.where(Xc[rows[internal], feat[g]] < thr[g], left[g], right[g])
+            leaves[:, t] = node
+        return leaves
+    _swap(monkeypatch, "forest_apply", forest_apply, forest, pins_forest)
+    _must_fail(pins_forest.test_matches_sklearn_forest)
+
+
+def test_vote_threshold_rounded_down(monkeypatch):
+    def vote_threshold(delta, n_trees):  # floor where ceil belongs
+        return int(math.floor(float(delta) * float(n_trees * 65536)))
+    _swap(monkeypatch, "vote_threshold", vote_threshold, forest, pins_forest)
+    _must_fail(pins_forest.test_vote_threshold)
+
+
+# ------------------------------------------------------- top-q (Sec. 4.6)
+
+def test_top_q_ties_to_highest_index(monkeypatch):
+    def top_q(score, mask, q):  # highest index first on ties
+        score = np.asarray(score, dtype=np.float64)
+        ok = (np.asarray(mask) != 0) & ~np.isnan(score)
+        cand = np.arange(len(score))[ok]
+        pick = cand[np.lexsort((-cand, -score[cand]))[:q]]
+        idx = np.full(q, -1, dtype=np.int64)
+        val = np.full(q, np.nan)
+        idx[:len(pick)] = pick
+        val[:len(pick)] = score[pick]
+        return idx, val, int(ok.sum())
+    _swap(monkeypatch, "top_q", top_q, select, pins_forest)
+    _must_fail(pins_forest.test_top_q_brute_force_and_ties)
