@@ -45,6 +45,15 @@ def test_pi_monte_carlo():
     assert probability_of_improvement(np.array([mu]), np.array([sd]), best, xi)[0] == pytest.approx(mc, abs=2e-3)
 
 
+def test_pi_monte_carlo_with_xi():
+    # a margin as large as the spread, so that its sign shows (Eq. 7 adds xi)
+    rng = np.random.default_rng(6)
+    mu, sd, best, xi = 0.4, 0.7, 0.1, 0.3
+    y = rng.normal(mu, sd, 2_000_000)
+    mc = np.mean(y < best + xi)
+    assert probability_of_improvement(np.array([mu]), np.array([sd]), best, xi)[0] == pytest.approx(mc, abs=2e-3)
+
+
 def test_pi_zero_sigma_is_a_step():
     got = probability_of_improvement(np.array([-1.0, 1.0, 0.5]), np.zeros(3), 0.5, 0.0)
     np.testing.assert_array_equal(got, [1.0, 0.0, 0.0])
@@ -142,6 +151,11 @@ def test_golden_gamma_is_the_odd_integer_nearest_2_64_over_phi():
     # 2^64 / phi = 2^63 (sqrt 5 - 1); floor via an exact integer square root
     floor_val = math.isqrt(5 << 126) - (1 << 63)
     assert GOLDEN_GAMMA in (floor_val, floor_val + 1) and GOLDEN_GAMMA % 2 == 1
+
+
+def test_splitmix_reference_outputs():
+    # the published first outputs of SplitMix64 seeded with 0
+    assert [splitmix64(0, i) for i in range(3)] == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
 
 
 def test_splitmix_stream_and_bijection():

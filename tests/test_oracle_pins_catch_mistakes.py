@@ -18,10 +18,14 @@ import oracle.acquisition as acq
 import oracle.forest as forest
 import oracle.gp as gp
 import oracle.hypervolume as hv
+import oracle.mace as mace
+import oracle.mle as mle
 import oracle.select as select
 import test_oracle_acq as pins_acq
 import test_oracle_forest_select as pins_forest
 import test_oracle_gp as pins_gp
+import test_oracle_mace as pins_mace
+import test_oracle_mle as pins_mle
 
 
 @pytest.fixture(scope="module")
@@ -163,3 +167,59 @@ def test_top_q_ties_to_highest_index(monkeypatch):
         return idx, val, int(ok.sum())
     _swap(monkeypatch, "top_q", top_q, select, pins_forest)
     _must_fail(pins_forest.test_top_q_brute_force_and_ties)
+
+
+# ------------------------------------- hyperparameters (Sec. 4.3) and MACE
+
+def test_nll_log_determinant_doubled(monkeypatch):
+    real = mle.nll_and_grad
+
+    def nll_and_grad(theta, X, y, kernel="matern52", warp=None, prior_mean=0.0):  # log det K, not half of it
+        nll, grad = real(theta, X, y, kernel, warp, prior_mean)
+        d = np.asarray(X).shape[1]
+        K = gp.COVARIANCES[kernel](np.asarray(X, dtype=np.float64), np.asarray(X, dtype=np.float64),
+                                   np.exp(theta[:d]), np.exp(theta[d])) + np.exp(theta[d + 1]) * np.eye(len(X))
+        return nll + 0.5 * np.linalg.slogdet(K)[1], grad
+    _swap(monkeypatch, "nll_and_grad", nll_and_grad, mle, pins_mle)
+    _must_fail(pins_mle.test_nll_and_gradient_match_sklearn, "matern52", 2.5)
+
+
+def test_ucb_mean_sign(monkeypatch):
+    def ucb_score(mu, sigma, beta):  # + mu where the minimised objective needs - mu
+        return beta * np.asarray(sigma, dtype=np.float64) + np.asarray(mu, dtype=np.float64)
+    _swap(monkeypatch, "ucb_score", ucb_score, mace, pins_mace)
+    _must_fail(pins_mace.test_ucb_score_is_the_mirrored_eq6)
+
+
+def test_pi_xi_sign(monkeypatch):
+    real = mace.probability_of_improvement
+
+    def probability_of_improvement(mu, sigma, best_y, xi):  # best - xi where best + xi belongs
+        return real(mu, sigma, best_y - 2 * xi, xi)
+    _swap(monkeypatch, "probability_of_improvement", probability_of_improvement, mace, pins_mace)
+    _must_fail(pins_mace.test_pi_monte_carlo_with_xi)
+
+
+def test_front_weak_dominance(monkeypatch):
+    def pareto_front_max(scores, mask=None):  # an equal score vector counted as dominating
+        S = np.asarray(scores, dtype=np.float64)
+        ok = ~np.isnan(S).any(axis=1)
+        if mask is not None:
+            ok &= np.asarray(mask) != 0
+        front = np.zeros(len(S), dtype=bool)
+        for i in np.flatnonzero(ok):
+            others = np.flatnonzero(ok)
+            others = others[others != i]
+            front[i] = not (S[others] >= S[i]).all(axis=1).any()
+        return front
+    _swap(monkeypatch, "pareto_front_max", pareto_front_max, mace, pins_mace)
+    _must_fail(pins_mace.test_front_hand_example)
+
+
+def test_splitmix_wrong_shift(monkeypatch):
+    def splitmix64_mix(z):  # 31 where the first shift is 30
+        z = (z ^ (z >> 31)) * mace.MIX_M1 & mace.MASK64
+        z = (z ^ (z >> 27)) * mace.MIX_M2 & mace.MASK64
+        return z ^ (z >> 31)
+    monkeypatch.setattr(mace, "splitmix64_mix", splitmix64_mix)
+    _must_fail(pins_mace.test_splitmix_reference_outputs)
