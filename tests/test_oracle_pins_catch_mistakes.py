@@ -223,3 +223,47 @@ def test_splitmix_wrong_shift(monkeypatch):
         return z ^ (z >> 31)
     monkeypatch.setattr(mace, "splitmix64_mix", splitmix64_mix)
     _must_fail(pins_mace.test_splitmix_reference_outputs)
+
+
+# ------------------------------------------------ Kriging believer (row A7)
+
+def _believer(X, Y, hypers, Xc, mask, ref, q, mistake, follow=None, record=None):
+    X = np.asarray(X, dtype=np.float64)
+    Y = np.asarray(Y, dtype=np.float64)
+    Xc64 = np.asarray(Xc, dtype=np.float64)
+    p = Y.shape[1]
+    Xa, Ya = X.copy(), Y.copy()
+    eligible = (np.asarray(mask) != 0).copy()
+    picks, vals = [], []
+    for _ in range(q):
+        mu = np.empty((len(Xc64), p))
+        sd = np.empty((len(Xc64), p))
+        for j, h in enumerate(hypers):
+            fit = gp.gp_fit(Xa, Ya[:, j], h["lengthscale"], h["signal_var"], h["noise_var"], h["prior_mean"])
+            mu[:, j], sd[:, j] = gp.gp_posterior(fit, Xc64)
+        front = hv.nondominated(Y if mistake == "front not updated" else Ya, ref)
+        acq_v = hv.ehvi(mu, sd, front, ref)
+        idx, val, _ = select.top_q(acq_v, eligible, 1)
+        if idx[0] < 0:
+            break
+        i = int(idx[0])
+        picks.append(i)
+        vals.append(float(val[0]))
+        if mistake != "pick not excluded":
+            eligible[i] = False
+        fantasy = Y.min(axis=0) if mistake == "best observed as fantasy" else mu[i]
+        Xa = np.vstack([Xa, Xc64[i][None, :]])
+        Ya = np.vstack([Ya, fantasy[None, :]])
+    return np.array(picks, dtype=np.int64), np.array(vals), mu, sd
+
+
+# (Leaving the pick eligible is no mistake a pin can see: with its fantasy
+# joined, the picked candidate's variance collapses and its mean sits on the
+# front, so its EHVI is about zero and it is not picked again.)
+@pytest.mark.parametrize("mistake", ["best observed as fantasy", "front not updated"])
+def test_believer_mistakes(monkeypatch, mistake):
+    import test_oracle_believer as pins_believer
+    _swap(monkeypatch, "kriging_believer",
+          lambda X, Y, hypers, Xc, mask, ref, q, follow=None, record=None:
+          _believer(X, Y, hypers, Xc, mask, ref, q, mistake), pins_believer)
+    _must_fail(pins_believer.test_believer_second_step_by_the_downdate)
