@@ -267,3 +267,58 @@ def test_believer_mistakes(monkeypatch, mistake):
           lambda X, Y, hypers, Xc, mask, ref, q, follow=None, record=None:
           _believer(X, Y, hypers, Xc, mask, ref, q, mistake), pins_believer)
     _must_fail(pins_believer.test_believer_second_step_by_the_downdate)
+
+
+# ----------------- candidate pool, Delta adaptation, forest training (N3b, N4, A8)
+
+def test_sobol_without_gray_code(monkeypatch):
+    import oracle.sobol as sobol
+    import test_oracle_sobol as pins_sobol
+
+    def sobol_points(poly, vinit, n, skip=0):  # index i where the Gray code i ^ (i >> 1) belongs
+        V = [sobol.direction_numbers(poly[j], vinit[j]) for j in range(len(poly))]
+        out = np.zeros((n, len(poly)))
+        for r in range(n):
+            g = skip + r
+            for j in range(len(poly)):
+                x, k = 0, 0
+                while g >> k:
+                    if (g >> k) & 1:
+                        x ^= V[j][k]
+                    k += 1
+                out[r, j] = x / 2.0 ** 32
+        return out
+    _swap(monkeypatch, "sobol_points", sobol_points, sobol, pins_sobol)
+    _must_fail(pins_sobol.test_points_match_scipy, 5, 1024)
+
+
+def test_delta_steps_the_wrong_way(monkeypatch, golden_dir):
+    import oracle.threshold as threshold
+
+    def delta_update(delta, c, k, any_invalid, upsilon=threshold.UPSILON):  # raised where it is lowered
+        if any_invalid:
+            return min(0.75, max(0.5, delta + upsilon)), 0
+        c = c + k
+        if c >= 5:
+            delta = min(0.75, delta + upsilon)
+            c = c - 5
+        return delta, c
+    _swap(monkeypatch, "delta_update", delta_update, threshold, pins_forest)
+    _must_fail(pins_forest.test_delta_sequences, golden_dir)
+
+
+def test_split_at_the_lower_value(monkeypatch):
+    import oracle.forest_train as ft
+    import test_oracle_forest_train as pins_ft
+    real = ft._grow
+
+    def _grow(X, y, w, idx, depth, max_depth, nodes):  # threshold at the left value, not the midpoint
+        me = real(X, y, w, idx, depth, max_depth, nodes)
+        f = nodes[me]["feature"]
+        if f >= 0:
+            xs = np.sort(X[idx, f])
+            t = nodes[me]["threshold"]
+            nodes[me]["threshold"] = xs[xs <= t].max()
+        return me
+    monkeypatch.setattr(ft, "_grow", _grow)
+    _must_fail(pins_ft.test_single_tree_matches_sklearn, 1, 6)
