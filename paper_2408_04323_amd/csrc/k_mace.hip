@@ -16,8 +16,9 @@
 //     weightings of the tile's range-normalised scores -- strong, spread
 //     points (a point that maximises a positive weighting has no dominator,
 //     up to rounding; nothing below relies on it);
-//  B. the front of the pivot set: every pivot against every pivot;
-//  C. every candidate checked against that pivot front (staged through LDS);
+//  B. the front of the pivot set: every pivot against every pivot, then its
+//     members gathered once into a packed list (one global atomic per wave);
+//  C. every candidate checked against that list (staged through LDS);
 //     survivors set their flag and append their index to a list (one global
 //     atomic per wave);
 //  D. every listed candidate against every listed one.
@@ -86,7 +87,7 @@ __global__ __launch_bounds__(kMaceThreads) void pareto_pivot_kernel(const T* __r
   __shared__ int piv_idx[kPivotsPerTile];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t base = (int64_t)blockIdx.x * kParetoTile;
-  if (blockIdx.x == 0 && tid == 0) *count = 0;  // for stage C, which runs after this kernel
+  if (blockIdx.x == 0 && tid < 2) count[tid] = 0;  // for the gather and stage C, which run after this kernel
   T v[4][3];
   bool ok[4];
 #pragma unroll
@@ -180,17 +181,50 @@ __global__ __launch_bounds__(kMaceThreads) void pareto_pivot_kernel(const T* __r
   }
 }
 
+template <typename T>
+struct Vec4;
+template <>
+struct Vec4<float> {
+  typedef float type __attribute__((ext_vector_type(4)));
+};
+template <>
+struct Vec4<double> {
+  typedef double type __attribute__((ext_vector_type(4)));
+};
+
+// ---- B': the pivot front, packed ----------------------------------------------
+// Slots whose flag B left set go to front[0 .. count[1]) as (a, b, c, -), in
+// no particular order (C only asks whether some member dominates a candidate).
+template <typename T>
+__global__ __launch_bounds__(kMaceThreads) void pareto_gather_kernel(const T* __restrict__ pa,
+                                                                     const T* __restrict__ pb,
+                                                                     const T* __restrict__ pc,
+                                                                     const uint8_t* __restrict__ pfront, int64_t P,
+                                                                     typename Vec4<T>::type* __restrict__ front,
+                                                                     int32_t* __restrict__ count) {
+  const int lane = threadIdx.x & 63;
+  const int64_t k = (int64_t)blockIdx.x * kMaceThreads + threadIdx.x;
+  const bool live = k < P && pfront[k] != 0;
+  const uint64_t bal = __ballot(live);
+  if (!bal) return;
+  int at = 0;
+  if (lane == 0) at = atomicAdd(count + 1, (int)__popcll(bal));
+  at = __shfl(at, 0);
+  const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+  if (live) front[at + below] = typename Vec4<T>::type{pa[k], pb[k], pc[k], T(0)};
+}
+
 // ---- C: candidates against the pivot front ----------------------------------------
 template <typename T>
 __global__ __launch_bounds__(kMaceThreads) void pareto_filter_kernel(
     const T* __restrict__ a, const T* __restrict__ b, const T* __restrict__ c, const uint8_t* __restrict__ mask,
-    int64_t n, const T* __restrict__ pa, const T* __restrict__ pb, const T* __restrict__ pc,
-    const uint8_t* __restrict__ pfront, int64_t P, uint8_t* __restrict__ flags, int32_t* __restrict__ list,
-    int32_t* __restrict__ count) {
-  __shared__ T sa[kParetoTile], sb[kParetoTile], sc[kParetoTile];
-  __shared__ int n_live;
+    int64_t n, const typename Vec4<T>::type* __restrict__ front, uint8_t* __restrict__ flags,
+    int32_t* __restrict__ list, int32_t* __restrict__ count) {
+  typedef typename Vec4<T>::type V;
+  __shared__ V pts[kParetoTile];
   const int tid = threadIdx.x, lane = tid & 63;
   const int64_t base = (int64_t)blockIdx.x * kParetoTile;
+  const int64_t F = count[1];  // size of the packed pivot front
   T va[4], vb[4], vc[4];
   bool alive[4];
 #pragma unroll
@@ -205,24 +239,16 @@ __global__ __launch_bounds__(kMaceThreads) void pareto_filter_kernel(
       alive[r] = (!mask || mask[i] != 0) && va[r] == va[r] && vb[r] == vb[r] && vc[r] == vc[r];
     }
   }
-  for (int64_t cb = 0; cb < P; cb += kParetoTile) {
+  for (int64_t cb = 0; cb < F; cb += kParetoTile) {
+    const int live = (int)std::min<int64_t>(kParetoTile, F - cb);
     __syncthreads();  // the previous chunk is no longer read
-    if (tid == 0) n_live = 0;
+    for (int k = tid; k < live; k += kMaceThreads) pts[k] = front[cb + k];
     __syncthreads();
-    for (int k = tid; k < kParetoTile && cb + k < P; k += kMaceThreads)
-      if (pfront[cb + k]) {
-        const int at = atomicAdd(&n_live, 1);
-        sa[at] = pa[cb + k];
-        sb[at] = pb[cb + k];
-        sc[at] = pc[cb + k];
-      }
-    __syncthreads();
-    const int live = n_live;
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       if (alive[r])
         for (int j = 0; j < live; ++j)
-          if (dominates(sa[j], sb[j], sc[j], va[r], vb[r], vc[r])) {
+          if (dominates(pts[j].x, pts[j].y, pts[j].z, va[r], vb[r], vc[r])) {
             alive[r] = false;
             break;
           }
@@ -244,17 +270,6 @@ __global__ __launch_bounds__(kMaceThreads) void pareto_filter_kernel(
 }
 
 constexpr int kMergeChunk = 256;
-
-template <typename T>
-struct Vec4;
-template <>
-struct Vec4<float> {
-  typedef float type __attribute__((ext_vector_type(4)));
-};
-template <>
-struct Vec4<double> {
-  typedef double type __attribute__((ext_vector_type(4)));
-};
 
 // B and D.  Owners and dominators are the S entries of `list` (S = *count),
 // or, when list is null, the slots 0..S_slots-1 themselves with flags[]
@@ -334,15 +349,17 @@ int run_pareto(const T* a, const T* b, const T* c, const uint8_t* mask, int64_t 
                int32_t* n_front, hipStream_t s) {
   const int64_t tiles = (n + kParetoTile - 1) / kParetoTile;
   const int64_t P = tiles * kPivotsPerTile;
-  // scratch: count | list [n] | pa pb pc [P] | pivot flags [P]
+  // scratch: counts (survivors, pivot front) | list [n] | pa pb pc [P] | pivot flags [P] | packed front [P]
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t at = off;
     off += align256(bytes);
     return at;
   };
-  const size_t o_cnt = take(4), o_list = take((size_t)n * 4), o_pa = take((size_t)P * sizeof(T)),
-               o_pb = take((size_t)P * sizeof(T)), o_pc = take((size_t)P * sizeof(T)), o_pf = take((size_t)P);
+  typedef typename Vec4<T>::type V;
+  const size_t o_cnt = take(8), o_list = take((size_t)n * 4), o_pa = take((size_t)P * sizeof(T)),
+               o_pb = take((size_t)P * sizeof(T)), o_pc = take((size_t)P * sizeof(T)), o_pf = take((size_t)P),
+               o_fr = take((size_t)P * sizeof(V));
   unsigned char* ws = (unsigned char*)device_scratch(off, 4);
   if (!ws) return fail(SCOOT_ERR_NO_MEMORY, "pareto: scratch allocation failed");
   int32_t* count = reinterpret_cast<int32_t*>(ws + o_cnt);
@@ -351,16 +368,19 @@ int run_pareto(const T* a, const T* b, const T* c, const uint8_t* mask, int64_t 
   T* pb = reinterpret_cast<T*>(ws + o_pb);
   T* pc = reinterpret_cast<T*>(ws + o_pc);
   uint8_t* pfront = ws + o_pf;
+  V* front = reinterpret_cast<V*>(ws + o_fr);
   const int64_t pb_ = (P + kMaceThreads - 1) / kMaceThreads, pc_ = (P + kMergeChunk - 1) / kMergeChunk;
   const int64_t grid_p = std::max<int64_t>(1, std::min<int64_t>(pb_ * pc_, (int64_t)device_cus() * 4));
   const int64_t grid_d = std::min<int64_t>((n + kMaceThreads - 1) / kMaceThreads, (int64_t)device_cus() * 4);
-  // A (also zeroes the survivor count), B, C, D
+  // A (also zeroes both counts), B, B', C, D
   hipLaunchKernelGGL((pareto_pivot_kernel<T>), dim3((unsigned)tiles), dim3(kMaceThreads), 0, s, a, b, c, mask, n, pa,
                      pb, pc, pfront, count);
   hipLaunchKernelGGL((pareto_merge_kernel<T>), dim3((unsigned)grid_p), dim3(kMaceThreads), 0, s, (const T*)pa,
                      (const T*)pb, (const T*)pc, (const int32_t*)nullptr, (const int32_t*)nullptr, P, pfront);
+  hipLaunchKernelGGL((pareto_gather_kernel<T>), dim3((unsigned)pb_), dim3(kMaceThreads), 0, s, (const T*)pa,
+                     (const T*)pb, (const T*)pc, (const uint8_t*)pfront, P, front, count);
   hipLaunchKernelGGL((pareto_filter_kernel<T>), dim3((unsigned)tiles), dim3(kMaceThreads), 0, s, a, b, c, mask, n,
-                     (const T*)pa, (const T*)pb, (const T*)pc, (const uint8_t*)pfront, P, flags, list, count);
+                     (const V*)front, flags, list, count);
   hipLaunchKernelGGL((pareto_merge_kernel<T>), dim3((unsigned)grid_d), dim3(kMaceThreads), 0, s, a, b, c,
                      (const int32_t*)list, (const int32_t*)count, (int64_t)0, flags);
   if (n_front) {
