@@ -63,7 +63,7 @@ __device__ inline bool dominates(T ja, T jb, T jc, T ia, T ib, T ic) {
 // Weights (w0, w1, w2) of the tile-normalised scores: the ten with w_k >= 1,
 // sum 6, and three near the axes.
 constexpr int kPivotsPerTile = 13;
-__constant__ float kPivotW[kPivotsPerTile][3] = {
+constexpr float kPivotW[kPivotsPerTile][3] = {  // folds into the code as immediates
     {1, 1, 4}, {1, 2, 3}, {1, 3, 2}, {1, 4, 1}, {2, 1, 3}, {2, 2, 2}, {2, 3, 1}, {3, 1, 2}, {3, 2, 1}, {4, 1, 1},
     {16, 1, 1}, {1, 16, 1}, {1, 1, 16}};
 
@@ -110,11 +110,10 @@ __global__ __launch_bounds__(kMaceThreads) void pareto_pivot_kernel(const T* __r
     m6[k] = -INFINITY;
     m6[3 + k] = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (ok[r]) {
-        m6[k] = fmaxf(m6[k], (float)v[r][k]);
-        m6[3 + k] = fmaxf(m6[3 + k], -(float)v[r][k]);
-      }
+    for (int r = 0; r < 4; ++r) {
+      m6[k] = fmaxf(m6[k], ok[r] ? (float)v[r][k] : -INFINITY);
+      m6[3 + k] = fmaxf(m6[3 + k], ok[r] ? -(float)v[r][k] : -INFINITY);
+    }
   }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1)
@@ -137,19 +136,22 @@ __global__ __launch_bounds__(kMaceThreads) void pareto_pivot_kernel(const T* __r
     scale[k] = hi > lo[k] ? 1.0f / (hi - lo[k]) : 0.0f;
   }
   // the 13 weighted maximisers
+  // (branch-free: an ineligible candidate's key is 0, which never wins)
+  float x[4][3];
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+#pragma unroll
+    for (int k = 0; k < 3; ++k) x[r][k] = ((float)v[r][k] - lo[k]) * scale[k];
   uint64_t best[kPivotsPerTile];
 #pragma unroll
   for (int d = 0; d < kPivotsPerTile; ++d) {
     best[d] = 0;
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (ok[r]) {
-        const float val = kPivotW[d][0] * (((float)v[r][0] - lo[0]) * scale[0]) +
-                          kPivotW[d][1] * (((float)v[r][1] - lo[1]) * scale[1]) +
-                          kPivotW[d][2] * (((float)v[r][2] - lo[2]) * scale[2]);
-        const uint64_t key = pivot_key(val, r * kMaceThreads + tid);
-        best[d] = key > best[d] ? key : best[d];
-      }
+    for (int r = 0; r < 4; ++r) {
+      const float val = kPivotW[d][0] * x[r][0] + kPivotW[d][1] * x[r][1] + kPivotW[d][2] * x[r][2];
+      const uint64_t key = ok[r] ? pivot_key(val, r * kMaceThreads + tid) : 0;
+      best[d] = key > best[d] ? key : best[d];
+    }
   }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1)
