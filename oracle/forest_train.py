@@ -119,8 +119,8 @@ def predict(forest, X):
 
 
 def voting_format(tf):
-    """A trained forest in the form the vote count reads (reading 10 of the
-    design notes): each float64 threshold t becomes the largest float32 not
+    """A trained forest in the form the vote count of Eq. 3 reads (float32
+    compares, integer Q16 votes): each float64 threshold t becomes the largest float32 not
     above t, so a float32 feature x goes left exactly when x <= t; each leaf
     value v becomes round(v * 2^16), ties to even."""
     t64 = np.asarray(tf["threshold"], dtype=np.float64)

@@ -4,7 +4,7 @@ import numpy as np
 import pytest
 from sklearn.tree import DecisionTreeRegressor
 
-from oracle.forest_train import bootstrap_weights, predict, train_forest, train_tree
+from oracle.forest_train import bootstrap_weights, predict, train_forest, train_tree, voting_format
 
 
 def _sk_nodes(model):
@@ -95,3 +95,84 @@ def test_bootstrap_sampling_law():
     assert frac == pytest.approx(1 - np.exp(-1), abs=0.01)
     assert W.mean() == pytest.approx(1.0) and W.var() == pytest.approx(1 - 1 / n, rel=0.05)
     assert not np.array_equal(W[0], W[1])
+
+
+# ------------------------------------------------ the voting format (Eq. 3)
+def _f32_neighbours(t):
+    t = np.float32(t)
+    return [np.nextafter(t, np.float32(-np.inf)), t, np.nextafter(t, np.float32(np.inf))]
+
+
+def _one_split(threshold, left_value=0.0, right_value=1.0):
+    return dict(feature=np.array([0, -1, -1], np.int32), threshold=np.array([threshold, 0.0, 0.0]),
+                left=np.array([1, -1, -1], np.int32), right=np.array([2, -1, -1], np.int32),
+                value=np.array([0.5, left_value, right_value]), tree_offset=np.array([0, 3], np.int64))
+
+
+A32 = float(np.float32(0.3))                     # 0.3 rounded to float32, exactly
+UP32 = float(np.nextafter(np.float32(0.3), np.float32(1)))
+THRESHOLDS = [
+    (A32, A32),                                  # already a float32: kept
+    (A32 + 1e-12, A32),                          # just above a float32 (rounds to nearest A32): down to A32
+    (A32 - 1e-12, float(np.nextafter(np.float32(A32), np.float32(0)))),   # just below: the float32 below
+    (UP32 - 1e-12, A32),                         # just below the next float32 (nearest is UP32): A32
+    (0.1, float(np.float32(0.1)) if float(np.float32(0.1)) <= 0.1 else
+     float(np.nextafter(np.float32(0.1), np.float32(0)))),
+]
+
+
+@pytest.mark.parametrize("t64,want", THRESHOLDS)
+def test_voting_format_threshold_is_the_float32_below(t64, want):
+    """The float32 threshold is the largest float32 not above the float64 one,
+    so every float32 feature goes the same way under both."""
+    f = voting_format(_one_split(t64))
+    t32 = f["threshold"][0]
+    assert f["threshold"].dtype == np.float32
+    assert float(t32) == want
+    assert float(t32) <= t64 < float(np.nextafter(t32, np.float32(np.inf)))
+    for x in _f32_neighbours(want) + _f32_neighbours(t64):
+        assert (x <= t32) == (float(x) <= t64)
+
+
+@pytest.mark.parametrize("value,q16", [
+    (0.0, 0), (1.0, 65536), (0.5, 32768), (0.7, 45875),          # 0.7 * 2^16 = 45875.2
+    (0.5 / 65536, 0), (1.5 / 65536, 2), (2.5 / 65536, 2), (3.5 / 65536, 4),   # exact half steps: to even
+    (12345.5 / 65536, 12346), (12346.5 / 65536, 12346),
+])
+def test_voting_format_leaf_q16_ties_to_even(value, q16):
+    f = voting_format(_one_split(0.5, left_value=value))
+    assert f["leaf_q16"][1] == q16
+    assert f["leaf_q16"][0] == 0 and f["leaf_q16"][2] == 65536 and f["feature"][1] == 0
+
+
+def test_voting_format_votes_match_the_float64_walk():
+    """Votes of a trained forest in the voting format, over float32 inputs that
+    include every threshold and its float32 neighbours, equal the sum over
+    trees of round(2^16 v), v the value the float64 walk of the trained trees
+    reaches."""
+    rng = np.random.default_rng(11)
+    X = rng.random((300, 3)).astype(np.float32)
+    y = ((X[:, 0] + X[:, 1] > 1.0) ^ (rng.random(300) < 0.1)).astype(float)
+    tf = train_forest(X, y, 5, 7, seed=5)
+    fmt = voting_format(tf)
+    from oracle.forest import forest_votes
+    probes = [X]
+    for k in np.flatnonzero(tf["left"] >= 0):
+        f = tf["feature"][k]
+        for x in _f32_neighbours(tf["threshold"][k]):
+            row = X[k % len(X)].copy()
+            row[f] = x
+            probes.append(row[None, :])
+    P = np.vstack(probes).astype(np.float32)
+    want = np.zeros(len(P), np.int64)
+    for t in range(len(tf["tree_offset"]) - 1):
+        base = tf["tree_offset"][t]
+        for i, x in enumerate(P.astype(np.float64)):
+            k = 0
+            while tf["left"][base + k] >= 0:
+                k = tf["left"][base + k] if x[tf["feature"][base + k]] <= tf["threshold"][base + k] \
+                    else tf["right"][base + k]
+            want[i] += int(np.rint(tf["value"][base + k] * 65536.0))
+    np.testing.assert_array_equal(forest_votes(fmt, P), want)
+    # and POF is the float64 prediction to within half a step per tree
+    np.testing.assert_allclose(want / (65536.0 * 5), predict(tf, P), rtol=0, atol=0.5 / 65536)

@@ -322,3 +322,78 @@ def test_split_at_the_lower_value(monkeypatch):
         return me
     monkeypatch.setattr(ft, "_grow", _grow)
     _must_fail(pins_ft.test_single_tree_matches_sklearn, 1, 6)
+
+
+# --------------------------------------- the voting format (Eq. 3, Sec. 4.7)
+
+def _voting_format(tf, mistake):
+    t64 = np.asarray(tf["threshold"], dtype=np.float64)
+    t32 = t64.astype(np.float32)
+    if mistake != "threshold to nearest":
+        above = t32.astype(np.float64) > t64
+        t32[above] = np.nextafter(t32[above], np.float32(-np.inf))
+    leaf = np.asarray(tf["left"]) < 0
+    v = np.asarray(tf["value"]) * 65536.0
+    q = {"leaf half up": np.floor(v + 0.5), "leaf truncated": np.floor(v)}.get(mistake, np.rint(v))
+    return dict(feature=np.where(leaf, 0, tf["feature"]).astype(np.int32),
+                threshold=np.where(leaf, np.float32(0), t32).astype(np.float32),
+                left=np.asarray(tf["left"], np.int32), right=np.asarray(tf["right"], np.int32),
+                leaf_q16=np.where(leaf, q, 0).astype(np.int32), tree_offset=np.asarray(tf["tree_offset"], np.int64))
+
+
+@pytest.mark.parametrize("mistake,pin,args", [
+    ("threshold to nearest", "test_voting_format_threshold_is_the_float32_below", (0.3 - 1e-9, None)),
+    ("threshold to nearest", "test_voting_format_votes_match_the_float64_walk", ()),
+    ("leaf half up", "test_voting_format_leaf_q16_ties_to_even", (2.5 / 65536, 2)),
+    ("leaf truncated", "test_voting_format_leaf_q16_ties_to_even", (1.5 / 65536, 2)),
+])
+def test_voting_format_mistakes(monkeypatch, mistake, pin, args):
+    import test_oracle_forest_train as pins_ft
+    if args and args[1] is None:    # a float64 threshold just below float32(0.3): the float32 below it
+        args = (float(np.float32(0.3)) - 1e-12, float(np.nextafter(np.float32(0.3), np.float32(0))))
+    monkeypatch.setattr(pins_ft, "voting_format", lambda tf: _voting_format(tf, mistake))
+    _must_fail(getattr(pins_ft, pin), *args)
+
+
+# ---------------------------------- the whole scoring pass (Sec. 4.1, 3-8)
+
+def _score_pool(w, mistake):
+    from oracle.acquisition import expected_improvement
+    from oracle.forest import feasibility_mask, forest_votes
+    from oracle.hypervolume import ehvi, nondominated
+    p = w["Y"].shape[1]
+    fits = []
+    for j in range(p):
+        h = 0 if mistake == "first objective's hyperparameters" else j
+        fits.append(gp.gp_fit(w["X"], w["Y"][:, j], w["lengthscale"][h], w["signal_var"][h], w["noise_var"][h],
+                              w["prior_mean"][h]))
+    Xc = w["Xc"]
+    mu = np.empty((len(Xc), p))
+    sigma = np.empty((len(Xc), p))
+    for j, f in enumerate(fits):
+        mu[:, j], sigma[:, j] = gp.gp_posterior(f, Xc)
+    front = None
+    if p == 1:
+        acq_ = expected_improvement(mu[:, 0], sigma[:, 0], w["best_y"], w["xi"])
+    else:
+        front = nondominated(w["Y"], w["ref"])
+        acq_ = ehvi(mu, sigma, front, w["ref"])
+    votes = forest_votes(w["forest"], Xc)
+    T = len(w["forest"]["tree_offset"]) - (0 if mistake == "tree count off by one" else 1)
+    mask = feasibility_mask(votes, w["delta"], T)
+    if mistake == "mask ignored":
+        mask = np.ones_like(mask)
+    idx, val, n_valid = select.top_q(acq_, mask, w["q"])
+    return dict(mu=mu, sigma=sigma, acq=acq_, front=front, votes=votes, mask=mask, idx=idx, val=val,
+                n_valid=n_valid)
+
+
+@pytest.mark.parametrize("mistake,pin,args", [
+    ("first objective's hyperparameters", "test_two_objective_pass_by_hand", ([1.0, 1.0], 1)),
+    ("mask ignored", "test_single_objective_pass_by_hand", ()),
+    ("tree count off by one", "test_single_objective_pass_by_hand", ()),
+])
+def test_score_pool_mistakes(monkeypatch, mistake, pin, args):
+    import test_oracle_pipeline as pins_pipe
+    monkeypatch.setattr(pins_pipe, "score_pool", lambda w, Xc=None: _score_pool(w, mistake))
+    _must_fail(getattr(pins_pipe, pin), *args)
