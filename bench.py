@@ -79,7 +79,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the scoring pass shards by candidate, see the design notes)", file=sys.stderr)
+              "(this build runs on a single GPU; the scoring pass would shard by candidate)", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch

@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define SCOOT_ABI_VERSION 1
+#define SCOOT_ABI_VERSION 2
 
 typedef enum scoot_dtype { SCOOT_F32 = 0, SCOOT_F64 = 1 } scoot_dtype;
 
@@ -326,11 +326,16 @@ int scoot_suggest_kb(const scoot_gp* gps, int p, scoot_forest f, const float* Xc
                      const double* Y_obs, int m_obs, const double* ref, double delta, int q, void* workspace,
                      uint64_t workspace_bytes, int64_t* picks, double* pick_acq, int* n_picked, void* stream);
 /* As scoot_suggest_kb; known [n] u8 device (nullable) restricts the
- * eligible candidates to the admissible ones, as in scoot_score_pool_ex. */
+ * eligible candidates to the admissible ones, as in scoot_score_pool_ex.
+ * mu_out, sigma_out [p*n] float32 device (objective-major, each nullable):
+ * the posterior the last scoring round was computed from — the mean of the
+ * observations (unchanged by the fantasies) and the standard deviation after
+ * the fantasies of every pick before that round (q - 1 of them when all q
+ * picks are made, *n_picked of them on a shortfall). */
 int scoot_suggest_kb_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_t* known, const float* Xc,
                         int64_t n, const double* Y_obs, int m_obs, const double* ref, double delta, int q,
                         void* workspace, uint64_t workspace_bytes, int64_t* picks, double* pick_acq, int* n_picked,
-                        void* stream);
+                        float* mu_out, float* sigma_out, void* stream);
 
 /* ---------------------------------------------------------------------------
  * MACE suggestion for one objective (Sec. 4.5.1: UCB, PI and EI, their Pareto

@@ -384,16 +384,21 @@ def suggest_kb_workspace(gps, n, q):
     return b.value
 
 
-def suggest_kb(gps, forest, Xc, q, Y_obs, ref, delta=0.5, workspace=None, stream=None, known=None):
+def suggest_kb(gps, forest, Xc, q, Y_obs, ref, delta=0.5, workspace=None, stream=None, known=None, mu_out=None,
+               sigma_out=None):
     """Sequential Kriging-believer picks among the feasible (and, with
     ``known``, admissible) candidates.  Returns (picks int64 (k,), EHVI at
-    each pick (k,))."""
+    each pick (k,)).  ``mu_out``/``sigma_out`` (float32 (p, n) device, optional)
+    receive the posterior the last scoring round was computed from."""
     import torch
     p = len(gps)
     n = Xc.shape[0]
     _require_device(Xc, "Xc", torch.float32, n * gps[0].d)
     if known is not None:
         _require_device(known, "known", torch.uint8, n)
+    for t, name in ((mu_out, "mu_out"), (sigma_out, "sigma_out")):
+        if t is not None:
+            _require_device(t, name, torch.float32, p * n)
     hs = (C.c_void_p * p)(*[g.handle.value for g in gps])
     r, pr = _host(ref, np.float64)
     Y, pY = _host(np.asarray(Y_obs, dtype=np.float64).reshape(-1, p), np.float64)
@@ -405,7 +410,8 @@ def suggest_kb(gps, forest, Xc, q, Y_obs, ref, delta=0.5, workspace=None, stream
                                     pY, Y.shape[0],
                                  pr, delta, q, _dptr(workspace), ws_bytes,
                                  picks.ctypes.data_as(C.POINTER(C.c_int64)),
-                                 acq.ctypes.data_as(C.POINTER(C.c_double)), C.byref(k), _stream(stream)),
+                                 acq.ctypes.data_as(C.POINTER(C.c_double)), C.byref(k), _dptr(mu_out),
+                                 _dptr(sigma_out), _stream(stream)),
           "suggest_kb")
     return picks[:k.value], acq[:k.value]
 

@@ -56,7 +56,7 @@ SIGNATURES = {
     "scoot_score_pool_ex": [C.POINTER(c_vp), c_int, c_vp, c_vp, c_vp, c_i64, c_dbl, c_dbl, P_dbl, c_int, P_dbl,
                             c_dbl, c_int, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp],
     "scoot_suggest_kb_ex": [C.POINTER(c_vp), c_int, c_vp, c_vp, c_vp, c_i64, P_dbl, c_int, P_dbl, c_dbl, c_int, c_vp,
-                            C.c_uint64, P_i64, P_dbl, P_int, c_vp],
+                            C.c_uint64, P_i64, P_dbl, P_int, c_vp, c_vp, c_vp],
     "scoot_suggest_mace_ex": [c_vp, c_vp, c_vp, c_vp, c_i64, c_dbl, c_dbl, c_dbl, c_dbl, C.c_uint64, c_int, c_vp,
                               c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp],
     "scoot_sobol_pool": [P_u32, P_u32, c_int, P_i32, c_i64, c_i64, P_dbl, P_dbl, c_int, c_vp, c_vp, c_vp],

@@ -629,7 +629,8 @@ int scoot_score_pool_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_
   for (int j = 0; j < p; ++j)
     if (!gps[j] || gps[j]->dev.dt != gps[0]->dev.dt || gps[j]->dev.d != gps[0]->dev.d)
       return fail(SCOOT_ERR_INVALID_ARG, "score pool: GPs must share dtype and d");
-  if (n < 0 || (n > 0 && (!Xc || !mu || !sigma || !acq || !mask))) return fail(SCOOT_ERR_INVALID_ARG, "score pool: null pointer");
+  if (n < 0 || n >= ((int64_t)1 << 31)) return fail(SCOOT_ERR_INVALID_ARG, "score pool: n out of range");
+  if (n > 0 && (!Xc || !mu || !sigma || !acq || !mask)) return fail(SCOOT_ERR_INVALID_ARG, "score pool: null pointer");
   if (!idx) return fail(SCOOT_ERR_INVALID_ARG, "score pool: null idx");
   if (q < 1 || q > SCOOT_MAX_Q) return fail(SCOOT_ERR_INVALID_ARG, "score pool: q out of range");
   const scoot_dtype dt = gps[0]->dev.dt;
@@ -679,7 +680,8 @@ int scoot_score_pool_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_
 namespace {
 int kb_check(const scoot_gp* gps, int p, int64_t n, int q, const GPDevice** g) {
   if (!gps || p < 1 || p > SCOOT_MAX_OBJECTIVES) return fail(SCOOT_ERR_INVALID_ARG, "believer: bad p or gps");
-  if (n < 1 || q < 1 || q > SCOOT_MAX_Q) return fail(SCOOT_ERR_INVALID_ARG, "believer: bad n or q");
+  if (n < 1 || n >= ((int64_t)1 << 31) || q < 1 || q > SCOOT_MAX_Q)
+    return fail(SCOOT_ERR_INVALID_ARG, "believer: bad n or q");
   for (int j = 0; j < p; ++j) {
     if (!gps[j]) return fail(SCOOT_ERR_INVALID_ARG, "believer: null GP");
     if (gps[j]->dev.dt != SCOOT_F32) return fail(SCOOT_ERR_UNSUPPORTED, "believer: float32 GPs only");
@@ -704,12 +706,13 @@ int scoot_suggest_kb(const scoot_gp* gps, int p, scoot_forest f, const float* Xc
                      int m_obs, const double* ref, double delta, int q, void* workspace, uint64_t workspace_bytes,
                      int64_t* picks, double* pick_acq, int* n_picked, void* stream) {
   return scoot_suggest_kb_ex(gps, p, f, nullptr, Xc, n, Y_obs, m_obs, ref, delta, q, workspace, workspace_bytes, picks,
-                             pick_acq, n_picked, stream);
+                             pick_acq, n_picked, nullptr, nullptr, stream);
 }
 
 int scoot_suggest_kb_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_t* known, const float* Xc, int64_t n,
                         const double* Y_obs, int m_obs, const double* ref, double delta, int q, void* workspace,
-                        uint64_t workspace_bytes, int64_t* picks, double* pick_acq, int* n_picked, void* stream) {
+                        uint64_t workspace_bytes, int64_t* picks, double* pick_acq, int* n_picked, float* mu_out,
+                        float* sigma_out, void* stream) {
   g_last_error.clear();
   const GPDevice* g[SCOOT_MAX_OBJECTIVES];
   int rc = kb_check(gps, p, n, q, g);
@@ -732,7 +735,7 @@ int scoot_suggest_kb_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_
   }
   try {
     rc = run_kriging_believer(g, p, f ? &f->dev : nullptr, known, vmin, Xc, n, Y_obs, m_obs, ref, q, ws, picks, pick_acq,
-                              n_picked, stream);
+                              n_picked, mu_out, sigma_out, stream);
   } catch (const std::bad_alloc&) {
     rc = fail(SCOOT_ERR_NO_MEMORY, "believer: host allocation failed");
   }

@@ -349,6 +349,7 @@ int launch_pareto_front3(const void* a, const void* b, const void* c, const uint
 size_t kb_workspace_bytes(const GPDevice* const* g, int p, int64_t n, int q);
 int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f, const uint8_t* known,
                          int64_t vote_min, const float* Xc, int64_t n, const double* Y_obs, int m_obs, const double* ref, int q, void* ws,
-                         int64_t* picks, double* pick_acq, int* n_picked, void* stream);
+                         int64_t* picks, double* pick_acq, int* n_picked, float* mu_out, float* sigma_out,
+                         void* stream);
 
 }  // namespace scoot

@@ -149,7 +149,8 @@ size_t kb_workspace_bytes(const GPDevice* const* g, int p, int64_t n, int q) { r
 
 int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f, const uint8_t* known,
                          int64_t vote_min, const float* Xc, int64_t n, const double* Y_obs, int m_obs,
-                         const double* ref, int q, void* ws, int64_t* picks, double* pick_acq, int* n_picked, void* stream) {
+                         const double* ref, int q, void* ws, int64_t* picks, double* pick_acq, int* n_picked,
+                         float* mu_out, float* sigma_out, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   const KbLayout L = kb_layout(g, p, n, q);
   unsigned char* w = (unsigned char*)ws;
@@ -253,6 +254,12 @@ int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f,
     e = hipGetLastError();
     if (e != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("believer: ") + hipGetErrorString(e));
   }
+  // the posterior the last scoring round saw (mu never moves; sigma carries
+  // the downdates of every pick before that round)
+  hipError_t e = hipSuccess;
+  if (mu_out) e = hipMemcpyAsync(mu_out, mu, (size_t)p * n * 4, hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess && sigma_out) e = hipMemcpyAsync(sigma_out, sd, (size_t)p * n * 4, hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("believer: ") + hipGetErrorString(e));
   return SCOOT_OK;
 }
 

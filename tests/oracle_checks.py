@@ -15,19 +15,22 @@ def say(*a):
     sys.stdout.flush()
 
 
-def check_believer(w, q, picks, acq_g, mask, hyp=None):
+def check_believer(w, q, picks, acq_g, mask, hyp=None, min_steps=1):
     """The oracle runs its own greedy sequence from the same inputs (a full
     refit per pick).  Step by step, while the two sequences agree, the
     library's pick must be the oracle's where the oracle's best is clear of the
     runner-up by more than twice the bar, and within the bar of it otherwise,
     and its reported EHVI must match.  At a near tie the sequences may part;
-    their histories differ from there on, so the comparison stops.  Returns
-    the number of steps compared."""
+    their histories differ from there on, so the comparison stops there; at
+    least ``min_steps`` steps must be compared.  Returns (steps compared, the
+    oracle's mean (n, p) and deviation (n, p) of its last scoring round); the
+    last two describe the library's last round when every step was compared
+    and the picks agree."""
     if hyp is None:
         hyp = [dict(lengthscale=w["lengthscale"][j], signal_var=w["signal_var"][j], noise_var=w["noise_var"][j],
                     prior_mean=w["prior_mean"][j]) for j in range(w["p"])]
     steps = []
-    picks_o, _, _, _ = kriging_believer(w["X"], w["Y"], hyp, w["Xc"], mask, w["ref"], q, record=steps)
+    picks_o, _, mu_o, sd_o = kriging_believer(w["X"], w["Y"], hyp, w["Xc"], mask, w["ref"], q, record=steps)
     assert len(picks_o) == len(picks)
     compared = 0
     for j, (acq_o, elig) in enumerate(steps):
@@ -42,24 +45,43 @@ def check_believer(w, q, picks, acq_g, mask, hyp=None):
             assert acq_o[io] - second <= 2 * tol, f"step {j}: decided pick {io} but got {i}"
             break
     say("believer steps compared", compared, "of", len(picks))
-    return compared
+    assert compared >= min_steps, f"only {compared} believer steps compared, {min_steps} required"
+    return compared, mu_o, sd_o
+
+
+def believer_gaps(w, q, mask, hyp=None):
+    """The oracle's own greedy run: at each step, the gap between its best and
+    its runner-up in units of the bar (1e-3 of the step's largest eligible
+    EHVI).  A gap above 2 everywhere means the whole sequence is decided."""
+    if hyp is None:
+        hyp = [dict(lengthscale=w["lengthscale"][j], signal_var=w["signal_var"][j], noise_var=w["noise_var"][j],
+                    prior_mean=w["prior_mean"][j]) for j in range(w["p"])]
+    steps = []
+    kriging_believer(w["X"], w["Y"], hyp, w["Xc"], mask, w["ref"], q, record=steps)
+    out = []
+    for acq_o, elig in steps:
+        ranked = np.sort(np.where(elig != 0, acq_o, -np.inf))[::-1]
+        out.append((ranked[0] - ranked[1]) / (1e-3 * ranked[0]))
+    return out
 
 
 def check_mace_front_and_pick(front_g, idx_g, scores_o, mask_o, seed, q, tol):
     """front_g, idx_g: the library's front (bool) and picks; scores_o: the
     oracle's (UCB, PI, EI) on the same candidates, mask_o the oracle's mask,
-    tol the per-score bar.  Where the two fronts disagree on a candidate, some
-    other eligible candidate must sit within twice the bar of dominating it
-    (a near tie, not a wrong front).  With equal fronts the picks must be the
-    oracle's draw from its front exactly; otherwise each pick must be a
+    tol the bar of each score: (3,) for every candidate, or (n, 3) per
+    candidate.  Where the two fronts disagree on a candidate, some other
+    eligible candidate must sit within the two candidates' bars of dominating
+    it (a near tie, not a wrong front).  With equal fronts the picks must be
+    the oracle's draw from its front exactly; otherwise each pick must be a
     distinct member of the library's front."""
     fo = pareto_front_max(scores_o, mask_o)
     fg = np.asarray(front_g).astype(bool)
-    tol2 = 2 * np.asarray(tol, dtype=np.float64)
+    tol = np.broadcast_to(np.asarray(tol, dtype=np.float64), scores_o.shape)
     elig = np.flatnonzero(np.asarray(mask_o) != 0)
     for i in np.flatnonzero(fg != fo):
         others = elig[elig != i]
         dlt = scores_o[others] - scores_o[i]
+        tol2 = tol[others] + tol[i]
         near = (dlt >= -tol2).all(axis=1) & (np.abs(dlt) <= tol2).any(axis=1)
         assert near.any(), f"front disagreement at {i} is not a near tie"
     idx_g = np.asarray(idx_g)
