@@ -273,6 +273,23 @@ int scoot_suggest_topq(const void* score, const uint8_t* mask, int64_t n, scoot_
                        int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * scoot_suggest_topq for callers that cannot allocate memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same arguments, kernels and results, but the selection's intermediate lists
+ * live in one fixed device array of 327,680 bytes per GPU (enough for every
+ * n < 2^31 and q <= SCOOT_MAX_Q), held from the first call on that GPU until
+ * the process ends, instead of the library's grow-only scratch.  The call
+ * allocates no host or device memory, also on its error paths.  Every call on
+ * one GPU uses that GPU's array: calls that overlap on one GPU (other streams,
+ * other host threads) race and must be serialised by the caller.  Each call
+ * writes every entry it later reads, so no clearing between calls is needed.
+ * Errors: INVALID_ARG (as scoot_suggest_topq), UNSUPPORTED (lists larger than
+ * the array; cannot happen within the limits above), DEVICE.
+ * ------------------------------------------------------------------------- */
+int scoot_suggest_topq_noalloc(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q,
+                               int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Adaptation of Delta after a batch of k evaluated suggestions (Algorithm 1,
  * Sec. 4.7), host only.  Some result invalid: Delta = min(0.75, max(0.5,
  * Delta + 0.05)), c = 0.  Otherwise c += k and, if c >= 5, Delta =

@@ -327,6 +327,24 @@ def suggest_topq(score, mask, q, stream=None):
     return idx, sc, nv
 
 
+def suggest_topq_noalloc(score, mask, q, idx, score_out=None, n_valid=None, stream=None):
+    """As suggest_topq into caller-provided outputs (idx int64 (q,), score_out
+    of the score's dtype (q,), n_valid int32 (1,)); the library allocates
+    nothing in this call."""
+    import torch
+    n = score.numel()
+    _require_device(score, "score")
+    if mask is not None:
+        _require_device(mask, "mask", torch.uint8, n)
+    _require_device(idx, "idx", torch.int64, q)
+    if score_out is not None:
+        _require_device(score_out, "score_out", score.dtype, q)
+    if n_valid is not None:
+        _require_device(n_valid, "n_valid", torch.int32, 1)
+    check(lib().scoot_suggest_topq_noalloc(_dptr(score), _dptr(mask), n, _dt(score.dtype), q, _dptr(idx),
+                                           _dptr(score_out), _dptr(n_valid), _stream(stream)), "suggest_topq_noalloc")
+
+
 # ---------------------------------------------------------------------- Delta
 def delta_update(delta, c, k, any_invalid):
     dd, cc = C.c_double(delta), C.c_int(c)

@@ -41,6 +41,7 @@ SIGNATURES = {
     "scoot_vote_threshold": [c_dbl, c_int, P_i64],
     "scoot_rf_feasibility": [c_vp, c_vp, c_i64, c_dbl, c_vp, c_vp, c_vp, c_vp],
     "scoot_suggest_topq": [c_vp, c_vp, c_i64, c_int, c_int, c_vp, c_vp, c_vp, c_vp],
+    "scoot_suggest_topq_noalloc": [c_vp, c_vp, c_i64, c_int, c_int, c_vp, c_vp, c_vp, c_vp],
     "scoot_delta_update": [P_dbl, P_int, c_int, c_int],
     "scoot_score_pool": [C.POINTER(c_vp), c_int, c_vp, c_vp, c_i64, c_dbl, c_dbl, P_dbl, c_int, P_dbl,
                          c_dbl, c_int, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp],

@@ -26,6 +26,7 @@ namespace scoot {
 
 namespace {
 thread_local std::string g_last_error;
+thread_local const char* g_static_error = nullptr;  // set by fail_static, which allocates nothing
 
 constexpr int kMaxDevices = 64;
 constexpr int kScratchSlots = 7;  // used: 1 boxes, 2 votes, 3 top-q, 4 MACE front, 5 warped pool, 6 suggestion step
@@ -52,9 +53,21 @@ int current_device() {
 }
 }  // namespace
 
-void set_error(const std::string& msg) { g_last_error = msg; }
-int fail(int status, const std::string& msg) {
+void clear_error() {
+  g_last_error.clear();
+  g_static_error = nullptr;
+}
+void set_error(const std::string& msg) {
+  g_static_error = nullptr;
   g_last_error = msg;
+}
+int fail(int status, const std::string& msg) {
+  set_error(msg);
+  return status;
+}
+int fail_static(int status, const char* msg) {
+  g_last_error.clear();
+  g_static_error = msg;
   return status;
 }
 
@@ -154,12 +167,12 @@ const char* scoot_status_string(int status) {
   }
 }
 
-const char* scoot_last_error(void) { return g_last_error.c_str(); }
+const char* scoot_last_error(void) { return g_static_error ? g_static_error : g_last_error.c_str(); }
 
 int scoot_gp_factor_host_ex(const double* X, const double* y, int m, int d, scoot_kernel kernel,
                             const double* lengthscale, const double* warp_a, const double* warp_b,
                             double signal_var, double noise_var, double prior_mean, double* L, double* alpha) {
-  g_last_error.clear();
+  clear_error();
   if (!L || !alpha) return fail(SCOOT_ERR_INVALID_ARG, "gp factor: null output");
   try {
     FitHost f;
@@ -188,7 +201,7 @@ int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* l
 int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* lengthscale,
                     const double* warp_a, const double* warp_b, double signal_var, double noise_var,
                     double prior_mean, scoot_dtype dt, void* stream, scoot_gp* out) {
-  g_last_error.clear();
+  clear_error();
   (void)stream;
   if (!out) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: null output handle");
   *out = nullptr;
@@ -286,7 +299,7 @@ int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel
 
 int scoot_gp_nll(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
                  const double* warp_b, double prior_mean, const double* theta, double* nll, double* grad) {
-  g_last_error.clear();
+  clear_error();
   try {
     return mle_nll(X, y, m, d, kernel, warp_a, warp_b, prior_mean, theta, nll, grad);
   } catch (const std::bad_alloc&) {
@@ -297,7 +310,7 @@ int scoot_gp_nll(const double* X, const double* y, int m, int d, scoot_kernel ke
 int scoot_gp_mle(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
                  const double* warp_b, double prior_mean, const double* lower, const double* upper, int max_iter,
                  double* theta, double* nll, int* iterations) {
-  g_last_error.clear();
+  clear_error();
   try {
     return mle_fit(X, y, m, d, kernel, warp_a, warp_b, prior_mean, lower, upper, max_iter, theta, nll, iterations);
   } catch (const std::bad_alloc&) {
@@ -306,7 +319,7 @@ int scoot_gp_mle(const double* X, const double* y, int m, int d, scoot_kernel ke
 }
 
 int scoot_gp_destroy(scoot_gp gp) {
-  g_last_error.clear();
+  clear_error();
   if (!gp) return SCOOT_OK;
   if (gp->dev.buf) hipFree(gp->dev.buf);
   delete gp;
@@ -314,7 +327,7 @@ int scoot_gp_destroy(scoot_gp gp) {
 }
 
 int scoot_posterior(scoot_gp gp, const float* Xc, int64_t n, void* mu, void* sigma, void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (!gp) return fail(SCOOT_ERR_INVALID_ARG, "posterior: null handle");
   if (n < 0) return fail(SCOOT_ERR_INVALID_ARG, "posterior: n < 0");
   if (n > 0 && (!Xc || !mu || !sigma)) return fail(SCOOT_ERR_INVALID_ARG, "posterior: null pointer");
@@ -323,7 +336,7 @@ int scoot_posterior(scoot_gp gp, const float* Xc, int64_t n, void* mu, void* sig
 
 int scoot_acq_ei(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double best_y, double xi,
                  void* ei, void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (!check_dtype(dt) || n < 0) return fail(SCOOT_ERR_INVALID_ARG, "ei: bad dtype or n");
   if (n > 0 && (!mu || !sigma || !ei)) return fail(SCOOT_ERR_INVALID_ARG, "ei: null pointer");
   if (!std::isfinite(best_y) || !std::isfinite(xi)) return fail(SCOOT_ERR_INVALID_ARG, "ei: non-finite best_y/xi");
@@ -332,7 +345,7 @@ int scoot_acq_ei(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, d
 
 int scoot_ehvi_front(const double* Y_obs, int m_obs, int p, const double* ref, double* front, int* n_front,
                      int* n_boxes) {
-  g_last_error.clear();
+  clear_error();
   if (!n_front) return fail(SCOOT_ERR_INVALID_ARG, "ehvi front: null n_front");
   try {
     BoxTable bt;
@@ -349,7 +362,7 @@ int scoot_ehvi_front(const double* Y_obs, int m_obs, int p, const double* ref, d
 
 int scoot_acq_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, scoot_dtype dt,
                    const double* Y_obs, int m_obs, const double* ref, void* ehvi, void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (!check_dtype(dt) || n < 0 || p < 1 || p > SCOOT_MAX_OBJECTIVES)
     return fail(SCOOT_ERR_INVALID_ARG, "ehvi: bad dtype, n or p");
   if (n > 0) {
@@ -370,7 +383,7 @@ int scoot_acq_ehvi(const void* const* mu, const void* const* sigma, int p, int64
 int scoot_forest_create(const int32_t* feature, const float* threshold, const int32_t* left, const int32_t* right,
                         const int32_t* leaf_q16, const int64_t* tree_offset, int n_trees, int d,
                         scoot_forest* out) {
-  g_last_error.clear();
+  clear_error();
   if (!out) return fail(SCOOT_ERR_INVALID_ARG, "forest: null output handle");
   *out = nullptr;
   try {
@@ -412,7 +425,7 @@ int scoot_forest_create(const int32_t* feature, const float* threshold, const in
 int scoot_forest_train(const double* X, const double* y, int n, int d, int n_trees, int max_depth, uint64_t seed,
                        int bootstrap, int64_t capacity, int32_t* feature, double* threshold, int32_t* left,
                        int32_t* right, double* value, int64_t* tree_offset, int64_t* n_nodes) {
-  g_last_error.clear();
+  clear_error();
   if (!n_nodes) return fail(SCOOT_ERR_INVALID_ARG, "forest train: null n_nodes");
   try {
     TrainedForest tf;
@@ -438,7 +451,7 @@ int scoot_forest_train(const double* X, const double* y, int n, int d, int n_tre
 
 int scoot_forest_train_create(const double* X, const double* y, int n, int d, int n_trees, int max_depth,
                               uint64_t seed, int bootstrap, scoot_forest* out) {
-  g_last_error.clear();
+  clear_error();
   if (!out) return fail(SCOOT_ERR_INVALID_ARG, "forest train: null output handle");
   *out = nullptr;
   try {
@@ -469,7 +482,7 @@ int scoot_forest_train_create(const double* X, const double* y, int n, int d, in
 }
 
 int scoot_forest_destroy(scoot_forest f) {
-  g_last_error.clear();
+  clear_error();
   if (!f) return SCOOT_OK;
   if (f->dev.nodes) hipFree(f->dev.nodes);
   delete f;
@@ -477,7 +490,7 @@ int scoot_forest_destroy(scoot_forest f) {
 }
 
 int scoot_vote_threshold(double delta, int n_trees, int64_t* votes_min) {
-  g_last_error.clear();
+  clear_error();
   if (!votes_min || !(delta >= 0.0 && delta <= 1.0) || n_trees < 1 || n_trees > SCOOT_MAX_TREES)
     return fail(SCOOT_ERR_INVALID_ARG, "vote threshold: delta must be in [0,1], 1 <= T <= SCOOT_MAX_TREES");
   *votes_min = (int64_t)std::ceil(delta * (double)((int64_t)n_trees * 65536));
@@ -486,7 +499,7 @@ int scoot_vote_threshold(double delta, int n_trees, int64_t* votes_min) {
 
 int scoot_rf_feasibility(scoot_forest f, const float* Xc, int64_t n, double delta, int32_t* votes, uint8_t* mask,
                          int32_t* leaf_idx, void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (!f) return fail(SCOOT_ERR_INVALID_ARG, "rf: null forest");
   if (n < 0 || (n > 0 && !Xc)) return fail(SCOOT_ERR_INVALID_ARG, "rf: bad n or null pool");
   int64_t vmin = 0;
@@ -497,7 +510,7 @@ int scoot_rf_feasibility(scoot_forest f, const float* Xc, int64_t n, double delt
 
 int scoot_suggest_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q, int64_t* idx,
                        void* score_out, int32_t* n_valid, void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (!check_dtype(dt)) return fail(SCOOT_ERR_INVALID_ARG, "topq: bad dtype");
   if (q < 1 || q > SCOOT_MAX_Q) return fail(SCOOT_ERR_INVALID_ARG, "topq: q must be in 1..SCOOT_MAX_Q");
   if (n < 0 || n >= ((int64_t)1 << 31)) return fail(SCOOT_ERR_INVALID_ARG, "topq: n out of range");
@@ -505,8 +518,19 @@ int scoot_suggest_topq(const void* score, const uint8_t* mask, int64_t n, scoot_
   return launch_topq(score, mask, n, dt, q, idx, score_out, n_valid, stream);
 }
 
+int scoot_suggest_topq_noalloc(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q, int64_t* idx,
+                               void* score_out, int32_t* n_valid, void* stream) {
+  clear_error();
+  if (!check_dtype(dt)) return fail_static(SCOOT_ERR_INVALID_ARG, "topq (no allocation): bad dtype");
+  if (q < 1 || q > SCOOT_MAX_Q)
+    return fail_static(SCOOT_ERR_INVALID_ARG, "topq (no allocation): q must be in 1..SCOOT_MAX_Q");
+  if (n < 0 || n >= ((int64_t)1 << 31)) return fail_static(SCOOT_ERR_INVALID_ARG, "topq (no allocation): n out of range");
+  if (!idx || (n > 0 && !score)) return fail_static(SCOOT_ERR_INVALID_ARG, "topq (no allocation): null pointer");
+  return launch_topq_static(score, mask, n, dt, q, idx, score_out, n_valid, stream);
+}
+
 int scoot_ucb_beta(int t, double* beta) {
-  g_last_error.clear();
+  clear_error();
   if (!beta || t < 1) return fail(SCOOT_ERR_INVALID_ARG, "ucb beta: null beta or t < 1");
   const double tt = (double)t, delta = 1.0 / (tt * tt), pi = 3.14159265358979323846;
   *beta = 2.0 * std::log(tt * tt * pi * pi / (6.0 * delta));
@@ -515,7 +539,7 @@ int scoot_ucb_beta(int t, double* beta) {
 
 int scoot_acq_mace(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double best_y, double xi, double beta,
                    void* ucb, void* pi, void* ei, void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (!check_dtype(dt) || n < 0) return fail(SCOOT_ERR_INVALID_ARG, "mace: bad dtype or n");
   if (n > 0 && (!mu || !sigma || !ucb || !pi || !ei)) return fail(SCOOT_ERR_INVALID_ARG, "mace: null pointer");
   if (!std::isfinite(best_y) || !std::isfinite(xi) || !std::isfinite(beta))
@@ -525,7 +549,7 @@ int scoot_acq_mace(const void* mu, const void* sigma, int64_t n, scoot_dtype dt,
 
 int scoot_pareto_front3(const void* a, const void* b, const void* c, const uint8_t* mask, int64_t n, scoot_dtype dt,
                         uint8_t* front, int32_t* n_front, void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (!check_dtype(dt)) return fail(SCOOT_ERR_INVALID_ARG, "pareto: bad dtype");
   if (n < 0 || n >= ((int64_t)1 << 31)) return fail(SCOOT_ERR_INVALID_ARG, "pareto: n out of range");
   if (n > 0 && (!a || !b || !c || !front)) return fail(SCOOT_ERR_INVALID_ARG, "pareto: null pointer");
@@ -534,7 +558,7 @@ int scoot_pareto_front3(const void* a, const void* b, const void* c, const uint8
 
 int scoot_random_pick(const uint8_t* flags, int64_t n, uint64_t seed, int q, int64_t* idx, int32_t* n_flagged,
                       void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (q < 1 || q > SCOOT_MAX_Q) return fail(SCOOT_ERR_INVALID_ARG, "pick: q must be in 1..SCOOT_MAX_Q");
   if (n < 0 || n >= ((int64_t)1 << 31)) return fail(SCOOT_ERR_INVALID_ARG, "pick: n out of range");
   if (!idx || (n > 0 && !flags)) return fail(SCOOT_ERR_INVALID_ARG, "pick: null pointer");
@@ -552,7 +576,7 @@ int scoot_suggest_mace_ex(scoot_gp gp, scoot_forest f, const uint8_t* known, con
                           double best_y, double xi, double beta, double delta, uint64_t seed, int q, void* mu,
                           void* sigma, void* ucb, void* pi, void* ei, int32_t* votes, uint8_t* mask, uint8_t* front,
                           int64_t* idx, int32_t* n_front, void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (!gp) return fail(SCOOT_ERR_INVALID_ARG, "mace suggest: null GP");
   if (n < 0 || n >= ((int64_t)1 << 31)) return fail(SCOOT_ERR_INVALID_ARG, "mace suggest: n out of range");
   if (n > 0 && (!Xc || !mu || !sigma || !ucb || !pi || !ei || !mask || !front))
@@ -582,18 +606,18 @@ int scoot_suggest_mace_ex(scoot_gp gp, scoot_forest f, const uint8_t* known, con
 
 int scoot_sobol_pool(const uint32_t* poly, const uint32_t* vinit, int d, const int32_t* levels, int64_t skip, int64_t n,
                      const double* A, const double* b, int r, float* Xc, uint8_t* known, void* stream) {
-  g_last_error.clear();
+  clear_error();
   return launch_sobol_pool(poly, vinit, d, levels, skip, n, A, b, r, Xc, known, stream);
 }
 
 int scoot_known_constraints(const float* Xc, int64_t n, int d, const double* A, const double* b, int r,
                             uint8_t* known, void* stream) {
-  g_last_error.clear();
+  clear_error();
   return launch_known_constraints(Xc, n, d, A, b, r, known, stream);
 }
 
 int scoot_delta_update(double* delta, int* c, int k, int any_invalid) {
-  g_last_error.clear();
+  clear_error();
   if (!delta || !c || k < 0) return fail(SCOOT_ERR_INVALID_ARG, "delta update: null pointer or k < 0");
   if (any_invalid) {
     double v = *delta + 0.05;
@@ -624,7 +648,7 @@ int scoot_score_pool_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_
                         double best_y, double xi, const double* Y_obs, int m_obs, const double* ref, double delta,
                         int q, void* mu, void* sigma, void* acq, int32_t* votes, uint8_t* mask, int64_t* idx,
                         void* score_out, int32_t* n_valid, void* stream) {
-  g_last_error.clear();
+  clear_error();
   if (!gps || p < 1 || p > SCOOT_MAX_OBJECTIVES) return fail(SCOOT_ERR_INVALID_ARG, "score pool: bad p or gps");
   for (int j = 0; j < p; ++j)
     if (!gps[j] || gps[j]->dev.dt != gps[0]->dev.dt || gps[j]->dev.d != gps[0]->dev.d)
@@ -693,7 +717,7 @@ int kb_check(const scoot_gp* gps, int p, int64_t n, int q, const GPDevice** g) {
 }  // namespace
 
 int scoot_suggest_kb_workspace(const scoot_gp* gps, int p, int64_t n, int q, uint64_t* bytes) {
-  g_last_error.clear();
+  clear_error();
   const GPDevice* g[SCOOT_MAX_OBJECTIVES];
   if (!bytes) return fail(SCOOT_ERR_INVALID_ARG, "believer: null bytes");
   int rc = kb_check(gps, p, n, q, g);
@@ -713,7 +737,7 @@ int scoot_suggest_kb_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_
                         const double* Y_obs, int m_obs, const double* ref, double delta, int q, void* workspace,
                         uint64_t workspace_bytes, int64_t* picks, double* pick_acq, int* n_picked, float* mu_out,
                         float* sigma_out, void* stream) {
-  g_last_error.clear();
+  clear_error();
   const GPDevice* g[SCOOT_MAX_OBJECTIVES];
   int rc = kb_check(gps, p, n, q, g);
   if (rc != SCOOT_OK) return rc;

@@ -182,8 +182,11 @@ bool cholesky_lower(double* A, int m);
 // the diagonal; transposed: out[j][i] = L^-1[i][j], zero below).
 void lower_inverse(const double* L, int m, double* out, bool transposed);
 
+void clear_error();
 void set_error(const std::string& msg);
 int fail(int status, const std::string& msg);
+// As fail, for a message with static storage: allocates nothing.
+int fail_static(int status, const char* msg);
 
 // ---- fit (host) -----------------------------------------------------------
 struct FitHost {
@@ -338,6 +341,9 @@ int launch_known_constraints(const float* Xc, int64_t n, int d, const double* A,
                              uint8_t* known, void* stream);
 int launch_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q,
                 int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
+// As launch_topq, with the stage-1 lists in a fixed device array: allocates nothing.
+int launch_topq_static(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q, int64_t* idx,
+                       void* score_out, int32_t* n_valid, void* stream);
 int launch_random_pick(const uint8_t* flags, int64_t n, uint64_t seed, int q, int64_t* idx, int32_t* n_flagged,
                        void* stream);
 int launch_mace_scores(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double c, double beta, void* ucb,

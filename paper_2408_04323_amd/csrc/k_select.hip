@@ -25,6 +25,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "internal.h"
 
@@ -225,26 +226,44 @@ __global__ __launch_bounds__(64 * kSel2Waves) void topq_stage2(const T* __restri
 }
 
 namespace {
-// score / score_out may be null (the random pick writes indices only).
-template <typename T, typename K, typename Src>
-int run_select(const Src& src, const T* score, int64_t n, int q, int64_t* idx, T* score_out, int32_t* n_valid,
-               hipStream_t s) {
-  // As many waves as chunks, bounded so that stage 2 reads at most
-  // kSelMaxKeys2 keys; whole workgroups of four waves.
+// Stage-1 waves for n keys and q picks: as many as chunks, bounded so that
+// stage 2 reads at most kSelMaxKeys2 keys; whole workgroups of four waves.
+int64_t select_waves(int64_t n, int q) {
   int64_t waves = (n + kSelChunk - 1) / kSelChunk;
   waves = std::max<int64_t>(1, std::min<int64_t>(waves, std::max(4, kSelMaxKeys2 / q)));
-  const int64_t grid = (waves + 3) / 4;
-  waves = grid * 4;
+  return (waves + 3) / 4 * 4;
+}
+// Bytes of the stage-1 lists and counts.
+template <typename K>
+size_t select_scratch_bytes(int64_t n, int q) {
+  const int64_t waves = select_waves(n, q);
+  return (size_t)waves * q * sizeof(K) + (size_t)waves * 4;
+}
+
+// Launches both stages with the stage-1 lists in ws (at least
+// select_scratch_bytes<K>(n, q) bytes of device memory).  score / score_out
+// may be null (the random pick writes indices only).
+template <typename T, typename K, typename Src>
+hipError_t run_select(const Src& src, const T* score, int64_t n, int q, int64_t* idx, T* score_out,
+                      int32_t* n_valid, unsigned char* ws, hipStream_t s) {
+  const int64_t waves = select_waves(n, q);
   const size_t kbytes = (size_t)waves * q * sizeof(K);
-  unsigned char* ws = (unsigned char*)device_scratch(kbytes + (size_t)waves * 4, 3);
-  if (!ws) return fail(SCOOT_ERR_NO_MEMORY, "topq: scratch allocation failed");
   K* pk = reinterpret_cast<K*>(ws);
   int32_t* pc = reinterpret_cast<int32_t*>(ws + kbytes);
-  hipLaunchKernelGGL((topq_stage1<K, Src>), dim3((unsigned)grid), dim3(kSelThreads), 0, s, src, n, q, pk, pc);
+  hipLaunchKernelGGL((topq_stage1<K, Src>), dim3((unsigned)(waves / 4)), dim3(kSelThreads), 0, s, src, n, q, pk, pc);
   const int w2 = (int)std::min<int64_t>(kSel2Waves, (waves * q + kSelChunk - 1) / kSelChunk);
   hipLaunchKernelGGL((topq_stage2<T, K>), dim3(1), dim3(64 * w2), 0, s, score, (int)waves, q, pk, pc, idx,
                      score_out, n_valid);
-  hipError_t err = hipGetLastError();
+  return hipGetLastError();
+}
+
+// As run_select, with the stage-1 lists in the library's grow-only scratch.
+template <typename T, typename K, typename Src>
+int run_select_scratch(const Src& src, const T* score, int64_t n, int q, int64_t* idx, T* score_out,
+                       int32_t* n_valid, hipStream_t s) {
+  unsigned char* ws = (unsigned char*)device_scratch(select_scratch_bytes<K>(n, q), 3);
+  if (!ws) return fail(SCOOT_ERR_NO_MEMORY, "topq: scratch allocation failed");
+  const hipError_t err = run_select<T, K>(src, score, n, q, idx, score_out, n_valid, ws, s);
   if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("topq launch: ") + hipGetErrorString(err));
   return SCOOT_OK;
 }
@@ -255,23 +274,83 @@ int launch_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype d
   hipStream_t s = (hipStream_t)stream;
   if (dt == SCOOT_F32) {
     if (mask)
-      return run_select<float, Key64>(ScoreKeys<float, true>{(const float*)score, mask}, (const float*)score, n, q,
-                                      idx, (float*)score_out, n_valid, s);
-    return run_select<float, Key64>(ScoreKeys<float, false>{(const float*)score, mask}, (const float*)score, n, q,
-                                    idx, (float*)score_out, n_valid, s);
+      return run_select_scratch<float, Key64>(ScoreKeys<float, true>{(const float*)score, mask}, (const float*)score,
+                                              n, q, idx, (float*)score_out, n_valid, s);
+    return run_select_scratch<float, Key64>(ScoreKeys<float, false>{(const float*)score, mask}, (const float*)score,
+                                            n, q, idx, (float*)score_out, n_valid, s);
   }
   if (mask)
-    return run_select<double, Key128>(ScoreKeys<double, true>{(const double*)score, mask}, (const double*)score, n,
-                                      q, idx, (double*)score_out, n_valid, s);
-  return run_select<double, Key128>(ScoreKeys<double, false>{(const double*)score, mask}, (const double*)score, n, q,
-                                    idx, (double*)score_out, n_valid, s);
+    return run_select_scratch<double, Key128>(ScoreKeys<double, true>{(const double*)score, mask},
+                                              (const double*)score, n, q, idx, (double*)score_out, n_valid, s);
+  return run_select_scratch<double, Key128>(ScoreKeys<double, false>{(const double*)score, mask},
+                                            (const double*)score, n, q, idx, (double*)score_out, n_valid, s);
 }
 
 int launch_random_pick(const uint8_t* flags, int64_t n, uint64_t seed, int q, int64_t* idx, int32_t* n_flagged,
                        void* stream) {
   const DrawKeys src{flags, seed};
-  return run_select<double, Key128>(src, (const double*)nullptr, n, q, idx, (double*)nullptr, n_flagged,
-                                    (hipStream_t)stream);
+  return run_select_scratch<double, Key128>(src, (const double*)nullptr, n, q, idx, (double*)nullptr, n_flagged,
+                                            (hipStream_t)stream);
+}
+
+// ---------------------------------------------------------------------------
+// Top-q without any allocation, for callers that cannot allocate device
+// memory.  The stage-1 lists live in `scratch`, one fixed array per GPU that
+// stays allocated until the process ends.  The largest need over every
+// n < 2^31 and 1 <= q <= SCOOT_MAX_Q is 327,680 bytes (q = 1, fp64 keys: 16384
+// waves x (16 + 4) bytes); the array is that size.  Stage 1 writes every list
+// entry and count stage 2 reads, so nothing needs clearing between calls;
+// calls that overlap on one GPU share the array and race.
+constexpr size_t kTopqStaticBytes = 327680;
+static __device__ __align__(256) unsigned char scratch[kTopqStaticBytes];
+
+namespace {
+constexpr int kStaticMaxDevices = 64;
+std::mutex g_static_mu;
+unsigned char* g_static_ptr[kStaticMaxDevices] = {};
+
+// The device address of `scratch` on the current device, looked up on the
+// first call on that device (with it current) and kept: the host-side name
+// of a __device__ array is not a device address.
+int static_scratch(unsigned char** out) {
+  int d = -1;
+  if (hipGetDevice(&d) != hipSuccess || d < 0 || d >= kStaticMaxDevices)
+    return fail_static(SCOOT_ERR_DEVICE, "topq (no allocation): no usable current device");
+  std::lock_guard<std::mutex> lk(g_static_mu);
+  if (!g_static_ptr[d]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p)
+      return fail_static(SCOOT_ERR_DEVICE, "topq (no allocation): cannot resolve the scratch array's address");
+    g_static_ptr[d] = (unsigned char*)p;
+  }
+  *out = g_static_ptr[d];
+  return SCOOT_OK;
+}
+}  // namespace
+
+int launch_topq_static(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q, int64_t* idx,
+                       void* score_out, int32_t* n_valid, void* stream) {
+  const size_t need = dt == SCOOT_F32 ? select_scratch_bytes<Key64>(n, q) : select_scratch_bytes<Key128>(n, q);
+  if (need > kTopqStaticBytes)
+    return fail_static(SCOOT_ERR_UNSUPPORTED, "topq (no allocation): the stage-1 lists exceed the scratch array");
+  unsigned char* ws = nullptr;
+  const int rc = static_scratch(&ws);
+  if (rc != SCOOT_OK) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t err;
+  if (dt == SCOOT_F32) {
+    err = mask ? run_select<float, Key64>(ScoreKeys<float, true>{(const float*)score, mask}, (const float*)score, n, q,
+                                          idx, (float*)score_out, n_valid, ws, s)
+               : run_select<float, Key64>(ScoreKeys<float, false>{(const float*)score, mask}, (const float*)score, n,
+                                          q, idx, (float*)score_out, n_valid, ws, s);
+  } else {
+    err = mask ? run_select<double, Key128>(ScoreKeys<double, true>{(const double*)score, mask},
+                                            (const double*)score, n, q, idx, (double*)score_out, n_valid, ws, s)
+               : run_select<double, Key128>(ScoreKeys<double, false>{(const double*)score, mask},
+                                            (const double*)score, n, q, idx, (double*)score_out, n_valid, ws, s);
+  }
+  if (err != hipSuccess) return fail_static(SCOOT_ERR_DEVICE, "topq (no allocation): kernel launch failed");
+  return SCOOT_OK;
 }
 
 }  // namespace scoot
