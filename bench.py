@@ -23,6 +23,7 @@ if ROOT not in sys.path:
 
 PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_FP64_MFMA_TFLOPS = 78.6
+PEAK_HBM_GBPS = 8000.0
 
 # HBM traffic of one posterior launch on the two-objective workload (m=256,
 # n=262144, d=10, Matern-5/2) per precision, from rocprofv3 FETCH_SIZE /
@@ -184,8 +185,13 @@ def main():
     wall = time.perf_counter() - t_start
     ms_per_step = e0.elapsed_time(e1) / args.steps
     value = n / (ms_per_step * 1e-3)
-    print(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall:.3f}s), posterior "
-          f"{post_ms:.3f} ms/objective", file=sys.stderr, flush=True)
+    # The median step: 21 more loops of 20 back-to-back passes, each between
+    # one event pair (a pair around every single pass would add its own gap,
+    # and a short loop would carry the start-up of its first pass).
+    reps = sorted(time_loop(step, 20) for _ in range(21))
+    median_ms = reps[len(reps) // 2]
+    print(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step (wall {wall:.3f}s), median {median_ms:.3f}, "
+          f"posterior {post_ms:.3f} ms/objective", file=sys.stderr, flush=True)
 
     # other kernels, for the record
     ehvi_ms = rf_ms = topq_ms = None
@@ -195,6 +201,22 @@ def main():
     rf_ms = time_loop(lambda: S.rf_feasibility(forest, Xc, w["delta"], votes=bufs.votes, mask=bufs.mask),
                       args.kernel_loops)
     topq_ms = time_loop(lambda: S.suggest_topq(bufs.acq, bufs.mask, w["q"]), args.kernel_loops)
+    esz = 8 if args.dtype == "f64" else 4
+    # Algorithmic HBM bytes per candidate of the other kernels (what each must
+    # read and write once): EHVI reads p means and p deviations and writes the
+    # score; the forest reads the d features and writes votes (int32) and the
+    # mask byte; top-q reads the score and the mask byte.
+    hbm = {"ehvi": (2 * p + 1) * esz if p > 1 else None, "forest": 4 * w["d"] + 5, "topq": esz + 1}
+    kernels = {}
+    for name, ms in (("ehvi", ehvi_ms), ("forest", rf_ms), ("topq", topq_ms)):
+        if ms is None:
+            continue
+        gbs = hbm[name] * n / (ms * 1e-3) / 1e9
+        kernels[name] = {"ms_per_call": ms, "bytes_per_candidate": hbm[name], "achieved_GBps": gbs,
+                         "hbm_peak_GBps": PEAK_HBM_GBPS, "hbm_frac": gbs / PEAK_HBM_GBPS}
+    kernels["note"] = ("one library call each, host-side argument work included; these kernels are bound by "
+                       "VALU issue (EHVI), LDS latency (forest) and launch latency (top-q) rather than HBM, so "
+                       "hbm_frac is small by design; the VALU and LDS counters are in profiles/")
 
     # Algorithmic work of the fused posterior per candidate and objective: the
     # triangular product (m^2 flops) and K* with the mean (m (3d + 10) flops;
@@ -230,10 +252,10 @@ def main():
             "timed": "posterior x p + acquisition + forest mask + top-q on the device; host GP fit excluded",
             "fit_ms": fit_ms,
             "value_incl_fit": n / ((ms_per_step + fit_ms) * 1e-3),
+            "ms_per_step_median": median_ms,
+            "median_of": "21 loops of 20 back-to-back passes, one event pair per loop",
             "kernel_ms": {"posterior_per_objective": post_ms},
-            "call_ms": {"ehvi": ehvi_ms, "forest": rf_ms, "topq": topq_ms,
-                        "note": "one library call each, host-side argument work included (the kernel trace "
-                                "in profiles/ has the kernels alone)"},
+            "other_kernels": kernels,
         },
         "roofline": {
             "bound": "mfma",
@@ -466,8 +488,17 @@ def cpu_baseline(w, seconds):
         done += len(Xs)
     el = time.perf_counter() - t0
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), None)
+    except OSError:
+        pass
     return {"value": done / el, "unit": "candidates/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {done} candidates of the same pool in chunks of {chunk}, {el:.1f}s, fit excluded"}
+            "sample": f"first {done} candidates of the same pool in chunks of {chunk}, {el:.1f}s, fit excluded",
+            "cpu_model": model, "os_cpu_count": os.cpu_count(),
+            "threads_note": "cores = the BLAS thread count the oracle's triangular solves ran on; the rest of "
+                            "the oracle is single-threaded NumPy"}
 
 
 if __name__ == "__main__":

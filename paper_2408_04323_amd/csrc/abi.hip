@@ -678,6 +678,10 @@ int scoot_score_pool_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_
     rc = scoot_vote_threshold(delta, f->dev.n_trees, &vmin);
     if (rc != SCOOT_OK) return rc;
   }
+  // The mask first, so that the selection can run in the acquisition's epilogue.
+  rc = f ? launch_forest(f->dev, Xc, n, vmin, votes, mask, nullptr, stream, known)
+         : launch_mask_init(mask, known, n, stream);
+  if (rc != SCOOT_OK) return rc;
   for (int j = 0; j < p; ++j) {
     void* mj = (unsigned char*)mu + (size_t)j * n * esz;
     void* sj = (unsigned char*)sigma + (size_t)j * n * esz;
@@ -691,13 +695,7 @@ int scoot_score_pool_ex(const scoot_gp* gps, int p, scoot_forest f, const uint8_
     }
     if (rc != SCOOT_OK) return rc;
   }
-  if (p > 1) {
-    rc = launch_ehvi(mus, sds, p, n, dt, bt, acq, stream);
-    if (rc != SCOOT_OK) return rc;
-  }
-  rc = f ? launch_forest(f->dev, Xc, n, vmin, votes, mask, nullptr, stream, known)
-         : launch_mask_init(mask, known, n, stream);
-  if (rc != SCOOT_OK) return rc;
+  if (p > 1) return launch_ehvi_topq(mus, sds, p, n, dt, bt, acq, mask, q, idx, score_out, n_valid, stream);
   return launch_topq(acq, mask, n, dt, q, idx, score_out, n_valid, stream);
 }
 

@@ -329,6 +329,12 @@ int launch_ei(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, doub
               void* stream);
 int launch_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, scoot_dtype dt,
                 const BoxTable& boxes, void* ehvi, void* stream);
+// EHVI followed by the masked top-q over it (mask nullable): for p <= 2 the
+// first selection stage runs in the EHVI kernel's epilogue; as launch_ehvi
+// then launch_topq otherwise.
+int launch_ehvi_topq(const void* const* mu, const void* const* sigma, int p, int64_t n, scoot_dtype dt,
+                     const BoxTable& boxes, void* ehvi, const uint8_t* mask, int q, int64_t* idx, void* score_out,
+                     int32_t* n_valid, void* stream);
 // mask[c] = votes >= vote_min and (known nullable) known[c] != 0.
 int launch_forest(const ForestDevice& f, const float* Xc, int64_t n, int64_t vote_min,
                   int32_t* votes, uint8_t* mask, int32_t* leaf_idx, void* stream,
@@ -344,6 +350,10 @@ int launch_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype d
 // As launch_topq, with the stage-1 lists in a fixed device array: allocates nothing.
 int launch_topq_static(const void* score, const uint8_t* mask, int64_t n, scoot_dtype dt, int q, int64_t* idx,
                        void* score_out, int32_t* n_valid, void* stream);
+// Stage 2 of top-q alone, over n_parts lists of q keys (Key64 for F32,
+// Key128 for F64) and their eligible counts, written by a fused producer.
+int launch_topq_stage2(const void* score, scoot_dtype dt, int n_parts, int q, const void* part_keys,
+                       const int32_t* part_count, int64_t* idx, void* score_out, int32_t* n_valid, void* stream);
 int launch_random_pick(const uint8_t* flags, int64_t n, uint64_t seed, int q, int64_t* idx, int32_t* n_flagged,
                        void* stream);
 int launch_mace_scores(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, double c, double beta, void* ucb,

@@ -24,9 +24,11 @@
 
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 #include "internal.h"
 #include "normal.h"
+#include "select.h"
 
 namespace scoot {
 
@@ -54,27 +56,93 @@ struct StripArgTable {
   T v[kStripArgBytes / sizeof(T)];
   __device__ T operator[](int i) const { return v[i]; }
 };
+// EHVI of one candidate over the strips: G_0 at consecutive a's carried.
+template <typename T, int P, typename Table>
+__device__ inline T strip_ehvi(const Table& hi, int n_boxes, T m0, T s0, T m1, T s1) {
+  const T r0 = reciprocal(s0);
+  const T r1 = P == 2 ? reciprocal(s1) : T(0);
+  T g_prev = T(0), acc = T(0);
+  for (int b = 0; b < n_boxes; ++b) {
+    const T g_next = partial_expectation<T>(hi[2 * b], m0, s0, r0);
+    const T w = P == 2 ? partial_expectation<T>(hi[2 * b + 1], m1, s1, r1) : T(1);
+    acc += (g_next - g_prev) * w;
+    g_prev = g_next;
+  }
+  return acc;
+}
+
 template <typename T, int P, typename Table>
 __global__ __launch_bounds__(kStripThreads) void ehvi_strip_kernel(const T* __restrict__ mu0, const T* __restrict__ mu1,
                                                                    const T* __restrict__ sd0, const T* __restrict__ sd1,
                                                                    const Table hi, int n_boxes, int64_t n,
                                                                    T* __restrict__ out) {
   for (int64_t c = (int64_t)blockIdx.x * kStripThreads + threadIdx.x; c < n; c += (int64_t)gridDim.x * kStripThreads) {
-    const T m0 = mu0[c], s0 = sd0[c], r0 = reciprocal(s0);
-    T m1 = T(0), s1 = T(0), r1 = T(0);
-    if (P == 2) {
-      m1 = mu1[c];
-      s1 = sd1[c];
-      r1 = reciprocal(s1);
+    const T m0 = mu0[c], s0 = sd0[c];
+    const T m1 = P == 2 ? mu1[c] : T(0), s1 = P == 2 ? sd1[c] : T(0);
+    out[c] = strip_ehvi<T, P>(hi, n_boxes, m0, s0, m1, s1);
+  }
+}
+
+// The same EHVI with the first stage of the top-q selection (Sec. 4.6) in its
+// epilogue, so that the scores are not read back: every candidate's score and
+// mask byte form its key in registers (select.h), each wave keeps a running
+// best-q list over its chunks of 64 candidates (a chunk enters the list only
+// when some key beats the list's q-th entry), and at the end the workgroup's
+// sixteen lists are merged into one: part_keys [grid x q] and part_count
+// [grid] (eligible candidates) go to stage 2.  The EHVI scores are still
+// written.  Workgroups of sixteen waves keep the lists stage 2 reads few
+// (n / 1024 x q) while every wave still scores a single chunk of 64 at the
+// pool sizes of the workloads, as in the plain EHVI kernel.
+constexpr int kStripSelThreads = 1024;
+constexpr int kStripSelWaves = kStripSelThreads / 64;
+
+template <typename T, typename K, int P, typename Table>
+__global__ __launch_bounds__(kStripSelThreads) void ehvi_strip_select_kernel(
+    const T* __restrict__ mu0, const T* __restrict__ mu1, const T* __restrict__ sd0, const T* __restrict__ sd1,
+    const Table hi, int n_boxes, int64_t n, T* __restrict__ out, const uint8_t* __restrict__ mask, int q,
+    K* __restrict__ part_keys, int32_t* __restrict__ part_count) {
+  __shared__ K wave_lists[kStripSelWaves * SCOOT_MAX_Q];
+  __shared__ int32_t wave_valid[kStripSelWaves];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  K list{};
+  int32_t valid = 0;
+  for (int64_t base = ((int64_t)blockIdx.x * kStripSelWaves + wave) * 64; base < n;
+       base += (int64_t)gridDim.x * kStripSelThreads) {
+    const int64_t c = base + lane;
+    const bool live = c < n;
+    const int64_t ci = live ? c : n - 1;
+    const T m0 = mu0[ci], s0 = sd0[ci];
+    const T m1 = P == 2 ? mu1[ci] : T(0), s1 = P == 2 ? sd1[ci] : T(0);
+    const uint8_t ok = mask ? mask[ci] : (uint8_t)1;
+    const T acc = strip_ehvi<T, P>(hi, n_boxes, m0, s0, m1, s1);
+    if (live) out[c] = acc;
+    const K key = make_key(acc, c, live && ok != 0);
+    valid += key.zero() ? 0 : 1;
+    if (__any(key > list_entry(list, q - 1))) {
+      K keys[1] = {key};
+      wave_select<K, 1>(keys, list, q);
     }
-    T g_prev = T(0), acc = T(0);
-    for (int b = 0; b < n_boxes; ++b) {
-      const T g_next = partial_expectation<T>(hi[2 * b], m0, s0, r0);
-      const T w = P == 2 ? partial_expectation<T>(hi[2 * b + 1], m1, s1, r1) : T(1);
-      acc += (g_next - g_prev) * w;
-      g_prev = g_next;
-    }
-    out[c] = acc;
+  }
+  for (int m = 32; m >= 1; m >>= 1) valid += __shfl_xor(valid, m);
+  if (lane < q) wave_lists[wave * q + lane] = list;
+  if (lane == 0) wave_valid[wave] = valid;
+  __syncthreads();
+  if (wave != 0) return;
+  K keys[kStripSelWaves];  // kStripSelWaves x q <= kStripSelWaves x 64 entries
+#pragma unroll
+  for (int j = 0; j < kStripSelWaves; ++j) {
+    const int i = j * 64 + lane;
+    keys[j] = i < kStripSelWaves * q ? wave_lists[i] : K{};
+  }
+  K merged{};
+  wave_select<K, kStripSelWaves>(keys, merged, q);
+  if (lane < q) part_keys[(int64_t)blockIdx.x * q + lane] = merged;
+  if (lane == 0) {
+    int32_t sum = 0;
+#pragma unroll
+    for (int w = 0; w < kStripSelWaves; ++w) sum += wave_valid[w];
+    part_count[blockIdx.x] = sum;
   }
 }
 
@@ -151,10 +219,32 @@ int launch_ei(const void* mu, const void* sigma, int64_t n, scoot_dtype dt, doub
 }
 
 namespace {
+// Where the fused selection writes (null: EHVI alone).
+struct StripSelect {
+  const uint8_t* mask;
+  int q;
+  void* part_keys;
+  int32_t* part_count;
+  int blocks;
+};
+
+template <typename T, int P, typename Table>
+void launch_strip(const T* m0, const T* m1, const T* s0, const T* s1, const Table& tab, int nbx, int64_t n, T* out,
+                  const StripSelect* sel, int64_t blocks, hipStream_t s) {
+  typedef typename std::conditional<std::is_same<T, float>::value, Key64, Key128>::type K;
+  if (sel)
+    hipLaunchKernelGGL((ehvi_strip_select_kernel<T, K, P, Table>), dim3((unsigned)sel->blocks),
+                       dim3(kStripSelThreads), 0, s, m0, m1, s0, s1, tab, nbx, n, out, sel->mask, sel->q,
+                       (K*)sel->part_keys, sel->part_count);
+  else
+    hipLaunchKernelGGL((ehvi_strip_kernel<T, P, Table>), dim3((unsigned)blocks), dim3(kStripThreads), 0, s, m0, m1,
+                       s0, s1, tab, nbx, n, out);
+}
+
 // One or two objectives: per-box upper coordinates (a_{i+1}, h_i) in strip order.
 template <typename T>
 int run_ehvi_strip(const void* const* mu, const void* const* sigma, int p, int64_t n, const BoxTable& bt, void* out,
-                   hipStream_t s) {
+                   hipStream_t s, const StripSelect* sel = nullptr) {
   const int nbx = bt.n_boxes();
   std::vector<T> hi((size_t)nbx * 2, T(0));
   for (int b = 0; b < nbx; ++b) {
@@ -171,22 +261,19 @@ int run_ehvi_strip(const void* const* mu, const void* const* sigma, int p, int64
     StripArgTable<T> tab{};
     std::copy(hi.begin(), hi.end(), tab.v);
     if (p == 2)
-      hipLaunchKernelGGL((ehvi_strip_kernel<T, 2, StripArgTable<T>>), dim3((unsigned)blocks), dim3(kStripThreads), 0,
-                         s, m0, m1, s0, s1, tab, nbx, n, (T*)out);
+      launch_strip<T, 2>(m0, m1, s0, s1, tab, nbx, n, (T*)out, sel, blocks, s);
     else
-      hipLaunchKernelGGL((ehvi_strip_kernel<T, 1, StripArgTable<T>>), dim3((unsigned)blocks), dim3(kStripThreads), 0,
-                         s, m0, m1, s0, s1, tab, nbx, n, (T*)out);
+      launch_strip<T, 1>(m0, m1, s0, s1, tab, nbx, n, (T*)out, sel, blocks, s);
   } else {
     void* dev = device_scratch(hi.size() * sizeof(T), 1);
     if (!dev) return fail(SCOOT_ERR_NO_MEMORY, "ehvi: device scratch allocation failed");
     int rc = upload_async(dev, hi.data(), hi.size() * sizeof(T), 0, s);
     if (rc != SCOOT_OK) return rc;
+    const T* tab = (const T*)dev;
     if (p == 2)
-      hipLaunchKernelGGL((ehvi_strip_kernel<T, 2, const T*>), dim3((unsigned)blocks), dim3(kStripThreads), 0, s, m0,
-                         m1, s0, s1, (const T*)dev, nbx, n, (T*)out);
+      launch_strip<T, 2>(m0, m1, s0, s1, tab, nbx, n, (T*)out, sel, blocks, s);
     else
-      hipLaunchKernelGGL((ehvi_strip_kernel<T, 1, const T*>), dim3((unsigned)blocks), dim3(kStripThreads), 0, s, m0,
-                         m1, s0, s1, (const T*)dev, nbx, n, (T*)out);
+      launch_strip<T, 1>(m0, m1, s0, s1, tab, nbx, n, (T*)out, sel, blocks, s);
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("ehvi launch: ") + hipGetErrorString(err));
@@ -251,6 +338,30 @@ int run_ehvi3(const void* const* mu, const void* const* sigma, int64_t n, const 
   return SCOOT_OK;
 }
 }  // namespace
+
+int launch_ehvi_topq(const void* const* mu, const void* const* sigma, int p, int64_t n, scoot_dtype dt,
+                     const BoxTable& bt, void* ehvi, const uint8_t* mask, int q, int64_t* idx, void* score_out,
+                     int32_t* n_valid, void* stream) {
+  if (p > 2 || n == 0) {
+    const int rc = launch_ehvi(mu, sigma, p, n, dt, bt, ehvi, stream);
+    if (rc != SCOOT_OK) return rc;
+    return launch_topq(ehvi, mask, n, dt, q, idx, score_out, n_valid, stream);
+  }
+  hipStream_t s = (hipStream_t)stream;
+  // One chunk of 64 per wave up to 512 workgroups (larger pools loop), and at
+  // most kSelMaxKeys2 keys for stage 2.
+  int64_t blocks = (n + kStripSelThreads - 1) / kStripSelThreads;
+  blocks = std::max<int64_t>(1, std::min<int64_t>({blocks, 512, kSelMaxKeys2 / q}));
+  const size_t ksz = dt == SCOOT_F32 ? sizeof(Key64) : sizeof(Key128);
+  const size_t kbytes = ((size_t)blocks * q * ksz + 255) / 256 * 256;
+  unsigned char* ws = (unsigned char*)device_scratch(kbytes + (size_t)blocks * 4, 3);
+  if (!ws) return fail(SCOOT_ERR_NO_MEMORY, "ehvi: selection scratch allocation failed");
+  const StripSelect sel{mask, q, ws, reinterpret_cast<int32_t*>(ws + kbytes), (int)blocks};
+  const int rc = dt == SCOOT_F32 ? run_ehvi_strip<float>(mu, sigma, p, n, bt, ehvi, s, &sel)
+                                 : run_ehvi_strip<double>(mu, sigma, p, n, bt, ehvi, s, &sel);
+  if (rc != SCOOT_OK) return rc;
+  return launch_topq_stage2(ehvi, dt, (int)blocks, q, sel.part_keys, sel.part_count, idx, score_out, n_valid, stream);
+}
 
 int launch_ehvi(const void* const* mu, const void* const* sigma, int p, int64_t n, scoot_dtype dt,
                 const BoxTable& bt, void* ehvi, void* stream) {

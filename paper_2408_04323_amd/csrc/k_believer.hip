@@ -208,9 +208,7 @@ int run_kriging_believer(const GPDevice* const* g, int p, const ForestDevice* f,
     BoxTable bt;
     rc = build_boxes(Yaug.data(), (int)(Yaug.size() / p), p, ref, bt);
     if (rc != SCOOT_OK) return rc;
-    rc = launch_ehvi(mus, sds, p, n, SCOOT_F32, bt, acq, stream);
-    if (rc != SCOOT_OK) return rc;
-    rc = launch_topq(acq, elig, n, SCOOT_F32, 1, idx, score, nvalid, stream);
+    rc = launch_ehvi_topq(mus, sds, p, n, SCOOT_F32, bt, acq, elig, 1, idx, score, nvalid, stream);
     if (rc != SCOOT_OK) return rc;
     // One read-back per pick: the index, its score and its means (the
     // fantasies).  The row updates below are left running while the host

@@ -28,77 +28,9 @@
 #include <mutex>
 
 #include "internal.h"
+#include "select.h"
 
 namespace scoot {
-
-constexpr int kSelThreads = 256;  // stage 1 workgroup: four independent waves
-constexpr int kSelPer = 16;       // keys per lane per chunk
-constexpr int kSelChunk = 64 * kSelPer;
-constexpr int kSelMaxKeys2 = 16384;  // bound on the stage-1 lists stage 2 reads (waves x q)
-constexpr int kSel2Waves = 16;       // stage 2 workgroup; kSel2Waves x q (q <= 64) keys fit one chunk
-
-struct Key64 {
-  uint64_t v;
-  __device__ bool operator>(const Key64& o) const { return v > o.v; }
-  __device__ bool zero() const { return v == 0; }
-};
-struct Key128 {
-  uint64_t hi, lo;
-  __device__ bool operator>(const Key128& o) const { return hi > o.hi || (hi == o.hi && lo > o.lo); }
-  __device__ bool zero() const { return hi == 0 && lo == 0; }
-};
-
-// Branch-free, so that a thread's loads can all be in flight before any key
-// is formed.
-__device__ inline Key64 make_key(float s, int64_t i, bool ok) {
-  uint32_t b = __float_as_uint(s + 0.0f);
-  b = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
-  const uint64_t k = ((uint64_t)b << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i);
-  return Key64{ok && s == s ? k : 0ull};
-}
-__device__ inline Key128 make_key(double s, int64_t i, bool ok) {
-  uint64_t b = (uint64_t)__double_as_longlong(s + 0.0);
-  b = (b & 0x8000000000000000ull) ? ~b : (b | 0x8000000000000000ull);
-  const bool keep = ok && s == s;
-  return Key128{keep ? b : 0ull, keep ? ~(uint64_t)i : 0ull};
-}
-__device__ inline int64_t key_index(const Key64& k) { return (int64_t)(0xFFFFFFFFu - (uint32_t)k.v); }
-__device__ inline int64_t key_index(const Key128& k) { return (int64_t)(~k.lo); }
-
-__device__ inline Key64 shfl_xor(Key64 k, int m) {
-  return Key64{(uint64_t)__shfl_xor((unsigned long long)k.v, m)};
-}
-__device__ inline Key128 shfl_xor(Key128 k, int m) {
-  return Key128{(uint64_t)__shfl_xor((unsigned long long)k.hi, m), (uint64_t)__shfl_xor((unsigned long long)k.lo, m)};
-}
-
-// q rounds of wave argmax over the lane's kSelPer keys plus the running list
-// (lane r < q holds entry r, zero = empty).  Rewrites the list.
-template <typename K>
-__device__ void wave_select(K (&keys)[kSelPer], K& list, int q) {
-  const int lane = threadIdx.x & 63;
-  K extra = list, next{};
-  for (int r = 0; r < q; ++r) {
-    K best = extra;
-#pragma unroll
-    for (int j = 0; j < kSelPer; ++j)
-      if (keys[j] > best) best = keys[j];
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      K o = shfl_xor(best, m);
-      if (o > best) best = o;
-    }
-    // every lane now holds the wave's best; remove it from its owner (keys are unique)
-    if (!best.zero()) {
-      if (!(extra > best) && !(best > extra)) extra = K{};
-#pragma unroll
-      for (int j = 0; j < kSelPer; ++j)
-        if (!(keys[j] > best) && !(best > keys[j])) keys[j] = K{};
-    }
-    if (lane == r) next = best;
-  }
-  list = next;
-}
 
 // Key sources for stage 1: load(i) reads what key i needs (no branches),
 // key(raw, i) forms it.
@@ -179,6 +111,10 @@ __global__ __launch_bounds__(64 * kSel2Waves) void topq_stage2(const T* __restri
   __shared__ K wave_lists[kSel2Waves * 64];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  // the eligible count first: its loads are in flight during the selection
+  int32_t count = 0;
+  if (n_valid && wave == 0)
+    for (int b = lane; b < n_parts; b += 64) count += part_count[b];
   K list{};
   const int64_t total = (int64_t)n_parts * q;
   const int W = blockDim.x >> 6;
@@ -214,14 +150,16 @@ __global__ __launch_bounds__(64 * kSel2Waves) void topq_stage2(const T* __restri
     } else {
       const int64_t i = key_index(list);
       idx[lane] = i;
-      if (score_out) score_out[lane] = score[i];
+      // the key carries the score; only a zero (which may have been -0) is read back
+      if (score_out) {
+        const T v = key_score(list);
+        score_out[lane] = v == T(0) ? score[i] : v;
+      }
     }
   }
   if (n_valid) {  // sum of the stage-1 counts
-    int32_t sum = 0;
-    for (int b = lane; b < n_parts; b += 64) sum += part_count[b];
-    for (int m = 32; m >= 1; m >>= 1) sum += __shfl_xor(sum, m);
-    if (lane == 0) *n_valid = sum;
+    for (int m = 32; m >= 1; m >>= 1) count += __shfl_xor(count, m);
+    if (lane == 0) *n_valid = count;
   }
 }
 
@@ -284,6 +222,21 @@ int launch_topq(const void* score, const uint8_t* mask, int64_t n, scoot_dtype d
                                               (const double*)score, n, q, idx, (double*)score_out, n_valid, s);
   return run_select_scratch<double, Key128>(ScoreKeys<double, false>{(const double*)score, mask},
                                             (const double*)score, n, q, idx, (double*)score_out, n_valid, s);
+}
+
+int launch_topq_stage2(const void* score, scoot_dtype dt, int n_parts, int q, const void* part_keys,
+                       const int32_t* part_count, int64_t* idx, void* score_out, int32_t* n_valid, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  const int w2 = (int)std::min<int64_t>(kSel2Waves, ((int64_t)n_parts * q + kSelChunk - 1) / kSelChunk);
+  if (dt == SCOOT_F32)
+    hipLaunchKernelGGL((topq_stage2<float, Key64>), dim3(1), dim3(64 * w2), 0, s, (const float*)score, n_parts, q,
+                       (const Key64*)part_keys, part_count, idx, (float*)score_out, n_valid);
+  else
+    hipLaunchKernelGGL((topq_stage2<double, Key128>), dim3(1), dim3(64 * w2), 0, s, (const double*)score, n_parts,
+                       q, (const Key128*)part_keys, part_count, idx, (double*)score_out, n_valid);
+  const hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(SCOOT_ERR_DEVICE, std::string("topq launch: ") + hipGetErrorString(err));
+  return SCOOT_OK;
 }
 
 int launch_random_pick(const uint8_t* flags, int64_t n, uint64_t seed, int q, int64_t* idx, int32_t* n_flagged,
