@@ -30,7 +30,7 @@ from .forest_train import train_forest, voting_format
 from .gp import gp_fit, gp_posterior
 from .hypervolume import ehvi, nondominated
 from .mace import mace_suggest, ucb_beta
-from .mle import fit_hyperparameters
+from .mle import fit_hyperparameters, fit_hyperparameters_warp
 from .select import top_q
 from .sobol import known_constraints_mask, sobol_pool
 
@@ -46,11 +46,20 @@ def _box(values, defaults, p, d):
     return np.tile(row, (p, 1))
 
 
+WARP_LOWER, WARP_UPPER = 0.2, 5.0   # box of each learned Kumaraswamy parameter
+
+
 def suggest(X_obs, Y_obs, valid, space, k, delta=0.5, pool_size=4096, pool_skip=0, kernel="matern52",
             warp=None, theta_lower=None, theta_upper=None, theta_start=None, n_trees=16, max_depth=6,
-            forest_seed=0, bootstrap=True, xi=1e-4, t=1, pick_seed=0, ref=None):
+            forest_seed=0, bootstrap=True, xi=1e-4, t=1, pick_seed=0, ref=None, learn_warp=False):
     """Returns dict(x (n_out, d), source (n_out,) 0 = acquisition / 1 = fill,
-    theta (p, d + 2), idx (pool indices), and the intermediates)."""
+    theta (p, d + 2), idx (pool indices), and the intermediates).
+
+    learn_warp: the input warping is learned with the other hyperparameters
+    (Sec. 4.3, the paper's Matern-3/2 with input warping): each objective's
+    search runs over (log l, log s^2, log tau^2, log a, log b) with the warp
+    parameters in [WARP_LOWER, WARP_UPPER], starting from ``warp`` (else the
+    identity a = b = 1), and theta is then (p, 3d + 2)."""
     levels = np.asarray(space["levels"])
     d = len(levels)
     X_obs = np.asarray(X_obs, dtype=np.float64).reshape(-1, d)
@@ -67,7 +76,7 @@ def suggest(X_obs, Y_obs, valid, space, k, delta=0.5, pool_size=4096, pool_skip=
     else:
         known = np.ones(pool_size, dtype=np.uint8)
 
-    out = dict(pool=pool, known=known, theta=np.full((p, d + 2), np.nan))
+    out = dict(pool=pool, known=known, theta=np.full((p, 3 * d + 2 if learn_warp else d + 2), np.nan))
     picked = []
     Xv, Yv = X_obs[ok], Y_obs[ok]
     if len(Xv) > 0:
@@ -83,9 +92,19 @@ def suggest(X_obs, Y_obs, valid, space, k, delta=0.5, pool_size=4096, pool_skip=
         for j in range(p):
             wj = None if warp is None else (np.asarray(warp[0]).reshape(p, d)[j], np.asarray(warp[1]).reshape(p, d)[j])
             th = start[j].copy()
-            if np.any(lo[j] != hi[j]):
+            if learn_warp:
+                w0 = (np.ones(d), np.ones(d)) if wj is None else wj
+                wlo, whi = np.full(2 * d, np.log(WARP_LOWER)), np.full(2 * d, np.log(WARP_UPPER))
+                thw = np.clip(np.concatenate([th, np.log(w0[0]), np.log(w0[1])]),
+                              np.concatenate([lo[j], wlo]), np.concatenate([hi[j], whi]))
+                thw, _ = fit_hyperparameters_warp(Xv, Ys[:, j], thw, np.concatenate([lo[j], wlo]),
+                                                  np.concatenate([hi[j], whi]), kernel)
+                out["theta"][j] = thw
+                th, wj = thw[:d + 2], (np.exp(thw[d + 2:2 * d + 2]), np.exp(thw[2 * d + 2:]))
+            elif np.any(lo[j] != hi[j]):
                 th, _ = fit_hyperparameters(Xv, Ys[:, j], th, lo[j], hi[j], kernel, wj)
-            out["theta"][j] = th
+            if not learn_warp:
+                out["theta"][j] = th
             fits.append(gp_fit(Xv, Ys[:, j], np.exp(th[:d]), np.exp(th[d]), np.exp(th[d + 1]), 0.0, kernel=kernel,
                                warp=wj))
         # 3. the forest on every observation

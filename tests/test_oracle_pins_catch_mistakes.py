@@ -397,3 +397,24 @@ def test_score_pool_mistakes(monkeypatch, mistake, pin, args):
     import test_oracle_pipeline as pins_pipe
     monkeypatch.setattr(pins_pipe, "score_pool", lambda w, Xc=None: _score_pool(w, mistake))
     _must_fail(getattr(pins_pipe, pin), *args)
+
+
+# -------------------------------- learned input warping (Sec. 4.3, Snoek et al.)
+
+def _warp_derivatives(X, a, b, mistake):
+    X = np.clip(np.asarray(X, dtype=np.float64), 0.0, 1.0)
+    inner = (X > 0) & (X < 1)
+    Xi = np.where(inner, X, 0.5)
+    u = Xi ** a
+    w = 1.0 - (1.0 - X ** a) ** b
+    fa = 1.0 if mistake == "derivative in a, not log a" else a
+    da = np.where(inner, fa * b * (1.0 - u) ** (b - 1.0) * u * np.log(Xi), 0.0)
+    sb = 1.0 if mistake == "sign of the b derivative" else -1.0
+    db = np.where(inner, sb * b * (1.0 - u) ** b * np.log(1.0 - u), 0.0)
+    return w, da, db
+
+
+@pytest.mark.parametrize("mistake", ["derivative in a, not log a", "sign of the b derivative"])
+def test_warp_gradient_mistakes(monkeypatch, mistake):
+    monkeypatch.setattr(mle, "warp_derivatives", lambda X, a, b: _warp_derivatives(X, a, b, mistake))
+    _must_fail(pins_mle.test_warp_gradient_matches_finite_differences, "matern32")

@@ -99,3 +99,28 @@ def test_fixed_hyperparameters_are_used_as_given():
     X, Y, v = observations(20, p=2)
     r = suggest(X, Y, v, sp, k=2, pool_size=64, n_trees=4, max_depth=3, **_fixed(2, 4))
     np.testing.assert_array_equal(r["theta"], fixed_theta(2, 4))
+
+
+def test_learned_warp_is_at_least_as_likely_as_the_identity():
+    """With the warping learned (the paper's covariance), every objective's
+    likelihood at the learned parameters is at least that of the search
+    without warping, the warp parameters stay in their box, and the
+    suggestion is still a set of distinct admissible pool points."""
+    from oracle.mle import nll_and_grad, nll_and_grad_warp
+    from oracle.suggest import WARP_LOWER, WARP_UPPER
+    sp = space()
+    X, Y, v = observations(30, p=2)
+    rw = suggest(X, Y, v, sp, k=3, pool_size=POOL, kernel="matern32", learn_warp=True)
+    r0 = suggest(X, Y, v, sp, k=3, pool_size=POOL, kernel="matern32")
+    d = len(sp["levels"])
+    ok = v != 0
+    Yv = Y[ok]
+    Ys = (Yv - Yv.mean(axis=0)) / np.where(Yv.std(axis=0) > 0, Yv.std(axis=0), 1.0)
+    assert rw["theta"].shape == (2, 3 * d + 2)
+    for j in range(2):
+        fw, _ = nll_and_grad_warp(rw["theta"][j], X[ok], Ys[:, j], "matern32")
+        f0, _ = nll_and_grad(r0["theta"][j], X[ok], Ys[:, j], "matern32")
+        assert fw <= f0 + 1e-9
+        w = np.exp(rw["theta"][j][d + 2:])
+        assert np.all(w >= WARP_LOWER * (1 - 1e-12)) and np.all(w <= WARP_UPPER * (1 + 1e-12))
+    assert len(set(rw["idx"].tolist())) == len(rw["idx"]) == 3
