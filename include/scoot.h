@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define SCOOT_ABI_VERSION 2
+#define SCOOT_ABI_VERSION 3
 
 typedef enum scoot_dtype { SCOOT_F32 = 0, SCOOT_F64 = 1 } scoot_dtype;
 
@@ -148,6 +148,25 @@ int scoot_gp_nll(const double* X, const double* y, int m, int d, scoot_kernel ke
 int scoot_gp_mle(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
                  const double* warp_b, double prior_mean, const double* lower, const double* upper, int max_iter,
                  double* theta, double* nll, int* iterations);
+
+/* ---------------------------------------------------------------------------
+ * As scoot_gp_nll and scoot_gp_mle with the input warping learned as well
+ * (Sec. 4.3: the paper's covariance is Matern-3/2 with input warping after
+ * Snoek et al., whose warp parameters are fitted together with the GP).
+ * theta [3d + 2] = (log l_1..d, log s2, log tau2, log a_1..d, log b_1..d):
+ * every input x passes through w = 1 - (1 - x^a_k)^b_k (x clamped to [0, 1])
+ * before the covariance sees it, and grad [3d + 2] (nullable) is the
+ * analytic gradient in all of them (through the warped inputs:
+ * dK_ij/dlog a_k = -R_ij (w_ik - w_jk)(dw_ik - dw_jk)/l_k^2 with R the radial
+ * factor of the lengthscale derivatives).  lower, upper [3d + 2] as in
+ * scoot_gp_mle.  The learned (a, b) go to scoot_gp_fit_ex as warp_a, warp_b.
+ * Errors: as scoot_gp_nll / scoot_gp_mle.
+ * ------------------------------------------------------------------------- */
+int scoot_gp_nll_warp(const double* X, const double* y, int m, int d, scoot_kernel kernel, double prior_mean,
+                      const double* theta, double* nll, double* grad);
+int scoot_gp_mle_warp(const double* X, const double* y, int m, int d, scoot_kernel kernel, double prior_mean,
+                      const double* lower, const double* upper, int max_iter, double* theta, double* nll,
+                      int* iterations);
 
 /* ---------------------------------------------------------------------------
  * Posterior (device).  Eq. 4 and Eq. 5 of Sec. 4.3 at every candidate:
@@ -480,7 +499,12 @@ int scoot_known_constraints(const float* Xc, int64_t n, int d, const double* A, 
  *   iteration of the UCB schedule and pick_seed of the random pick (one
  *   objective: MACE); ref [p] (nullable: worst valid observation + 10% of the
  *   range) the EHVI reference point in the caller's units (several
- *   objectives).
+ *   objectives); learn_warp 1: the Kumaraswamy warping is learned with the
+ *   other hyperparameters (scoot_gp_mle_warp; Sec. 4.3, the paper's
+ *   Matern-3/2 with input warping), each warp parameter in [0.2, 5] starting
+ *   from warp_a / warp_b when given, else from the identity a = b = 1; theta
+ *   then has 3d + 2 entries per objective (theta_lower/upper/start keep their
+ *   d + 2); 0: the warping is fixed (or absent) as given.
  *
  * scoot_suggest: X_obs [n_obs*d] observed configurations (finite), Y_obs
  *   [n_obs*p] their objective values (minimised; read only where valid),
@@ -502,8 +526,8 @@ int scoot_known_constraints(const float* Xc, int64_t n, int d, const double* A, 
  *      initial design of Algorithm 1 is a call with n_obs = 0).
  *   x_out [k*d] host receives the configurations (the float32 pool points,
  *   widened), source [k] host (nullable) 0 = picked by the acquisition,
- *   1 = Sobol fill, theta_out [p*(d+2)] host (nullable) the hyperparameters
- *   used, *n_out the number written (below k only when the pool holds too
+ *   1 = Sobol fill, theta_out [p*(d+2)], or [p*(3d+2)] with learn_warp, host
+ *   (nullable) the hyperparameters used, *n_out the number written (below k only when the pool holds too
  *   few admissible points).  Library scratch on the current device holds the
  *   pool and the scores between calls.
  * Errors: INVALID_ARG (null pointer, bad sizes, non-finite input, p out of
@@ -541,6 +565,7 @@ typedef struct scoot_suggest_opts {
   int t;
   uint64_t pick_seed;
   const double* ref;
+  int learn_warp;
 } scoot_suggest_opts;
 
 int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid, int n_obs, int p,

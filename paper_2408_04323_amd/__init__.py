@@ -164,6 +164,41 @@ def gp_mle(X, y, theta0, lower, upper, kernel="matern52", warp_a=None, warp_b=No
     return th, nll.value, it.value
 
 
+def gp_nll_warp(X, y, theta, kernel="matern32", prior_mean=0.0):
+    """(nll, grad) with the warping learned: theta = (log l_1..d, log s2,
+    log tau2, log a_1..d, log b_1..d)."""
+    X, pX = _host(X, np.float64)
+    y, py = _host(y, np.float64)
+    m, d = X.shape
+    th, pt = _host(theta, np.float64)
+    if th.size != 3 * d + 2:
+        raise ValueError("theta must have 3d + 2 entries")
+    nll = C.c_double(0.0)
+    grad = np.zeros(3 * d + 2)
+    check(lib().scoot_gp_nll_warp(pX, py, m, d, _kernel(kernel), prior_mean, pt, C.byref(nll),
+                                  grad.ctypes.data_as(C.POINTER(C.c_double))), "gp_nll_warp")
+    return nll.value, grad
+
+
+def gp_mle_warp(X, y, theta0, lower, upper, kernel="matern32", prior_mean=0.0, max_iter=200):
+    """Maximum-likelihood theta (3d + 2 entries, the warping included) in
+    [lower, upper] from theta0.  Returns (theta, nll, iterations)."""
+    X, pX = _host(X, np.float64)
+    y, py = _host(y, np.float64)
+    m, d = X.shape
+    th = np.array(theta0, dtype=np.float64).copy()
+    lo, plo = _host(lower, np.float64)
+    hi, phi = _host(upper, np.float64)
+    if not (th.size == lo.size == hi.size == 3 * d + 2):
+        raise ValueError("theta0, lower and upper must have 3d + 2 entries")
+    nll = C.c_double(0.0)
+    it = C.c_int(0)
+    check(lib().scoot_gp_mle_warp(pX, py, m, d, _kernel(kernel), prior_mean, plo, phi, max_iter,
+                                  th.ctypes.data_as(C.POINTER(C.c_double)), C.byref(nll), C.byref(it)),
+          "gp_mle_warp")
+    return th, nll.value, it.value
+
+
 # --------------------------------------------------------------------- posterior
 def posterior(gp, Xc, mu=None, sigma=None, stream=None):
     """mu, sigma of the latent f at every row of Xc (n x d float32 device)."""
@@ -601,19 +636,20 @@ class _SuggestOpts(C.Structure):
                 ("theta_upper", C.POINTER(C.c_double)), ("theta_start", C.POINTER(C.c_double)),
                 ("mle_max_iter", C.c_int), ("n_trees", C.c_int), ("max_depth", C.c_int),
                 ("forest_seed", C.c_uint64), ("bootstrap", C.c_int), ("xi", C.c_double), ("t", C.c_int),
-                ("pick_seed", C.c_uint64), ("ref", C.POINTER(C.c_double))]
+                ("pick_seed", C.c_uint64), ("ref", C.POINTER(C.c_double)), ("learn_warp", C.c_int)]
 
 
 def suggest(X_obs, Y_obs, valid, space, k, delta=0.5, pool_size=262144, pool_skip=0, kernel="matern52",
             dtype="f32", warp_a=None, warp_b=None, theta_lower=None, theta_upper=None, theta_start=None,
             mle_max_iter=0, n_trees=64, max_depth=10, forest_seed=0, bootstrap=True, xi=1e-4, t=1, pick_seed=0,
-            ref=None, stream=None):
+            ref=None, stream=None, learn_warp=False):
     """One SUGGEST of Algorithm 1 (scoot_suggest).  ``space`` is a dict with
     ``levels``, ``poly``, ``vinit`` and optionally ``A``, ``b`` (known
     constraints).  X_obs (n_obs, d), Y_obs (n_obs, p) minimised, valid (n_obs,)
     host arrays; per-objective options (warps (p, d), theta bounds (p, d + 2))
-    host arrays.  Returns (x (n_out, d) float64, source (n_out,) int32,
-    theta (p, d + 2) float64)."""
+    host arrays; learn_warp: the warping is learned with the other
+    hyperparameters.  Returns (x (n_out, d) float64, source (n_out,) int32,
+    theta (p, d + 2), or (p, 3d + 2) with learn_warp, float64)."""
     pu, vi, lv, d = _sobol_inputs(space["poly"], space["vinit"], space["levels"])
     A, bb, r = _constraint_inputs(space.get("A"), space.get("b"), d)
     X = np.ascontiguousarray(np.asarray(X_obs, dtype=np.float64).reshape(-1, d))
@@ -641,10 +677,10 @@ def suggest(X_obs, Y_obs, valid, space, k, delta=0.5, pool_size=262144, pool_ski
                       arr(warp_a, (p, d)), arr(warp_b, (p, d)), arr(theta_lower, (p, d + 2)),
                       arr(theta_upper, (p, d + 2)), arr(theta_start, (p, d + 2)), int(mle_max_iter), int(n_trees),
                       int(max_depth), int(forest_seed), int(bool(bootstrap)), float(xi), int(t), int(pick_seed),
-                      arr(ref, (p,)))
+                      arr(ref, (p,)), int(bool(learn_warp)))
     x = np.zeros((k, d), dtype=np.float64)
     src = np.zeros(k, dtype=np.int32)
-    theta = np.zeros((p, d + 2), dtype=np.float64)
+    theta = np.zeros((p, 3 * d + 2 if learn_warp else d + 2), dtype=np.float64)
     n_out = C.c_int(0)
     check(lib().scoot_suggest(X.ctypes.data_as(C.POINTER(C.c_double)), Y.ctypes.data_as(C.POINTER(C.c_double)),
                               ok.ctypes.data_as(C.POINTER(C.c_uint8)), n_obs, p, C.byref(sp), C.byref(op),

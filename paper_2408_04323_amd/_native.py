@@ -29,6 +29,8 @@ SIGNATURES = {
     "scoot_gp_nll": [P_dbl, P_dbl, c_int, c_int, c_int, P_dbl, P_dbl, c_dbl, P_dbl, P_dbl, P_dbl],
     "scoot_gp_mle": [P_dbl, P_dbl, c_int, c_int, c_int, P_dbl, P_dbl, c_dbl, P_dbl, P_dbl, c_int, P_dbl, P_dbl,
                      P_int],
+    "scoot_gp_nll_warp": [P_dbl, P_dbl, c_int, c_int, c_int, c_dbl, P_dbl, P_dbl, P_dbl],
+    "scoot_gp_mle_warp": [P_dbl, P_dbl, c_int, c_int, c_int, c_dbl, P_dbl, P_dbl, c_int, P_dbl, P_dbl, P_int],
     "scoot_posterior": [c_vp, c_vp, c_i64, c_vp, c_vp, c_vp],
     "scoot_acq_ei": [c_vp, c_vp, c_i64, c_int, c_dbl, c_dbl, c_vp, c_vp],
     "scoot_ehvi_front": [P_dbl, c_int, c_int, P_dbl, P_dbl, P_int, P_int],

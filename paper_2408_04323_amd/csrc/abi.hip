@@ -318,6 +318,28 @@ int scoot_gp_mle(const double* X, const double* y, int m, int d, scoot_kernel ke
   }
 }
 
+int scoot_gp_nll_warp(const double* X, const double* y, int m, int d, scoot_kernel kernel, double prior_mean,
+                      const double* theta, double* nll, double* grad) {
+  clear_error();
+  try {
+    return mle_nll(X, y, m, d, kernel, nullptr, nullptr, prior_mean, theta, nll, grad, true);
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "gp nll: host allocation failed");
+  }
+}
+
+int scoot_gp_mle_warp(const double* X, const double* y, int m, int d, scoot_kernel kernel, double prior_mean,
+                      const double* lower, const double* upper, int max_iter, double* theta, double* nll,
+                      int* iterations) {
+  clear_error();
+  try {
+    return mle_fit(X, y, m, d, kernel, nullptr, nullptr, prior_mean, lower, upper, max_iter, theta, nll, iterations,
+                   true);
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "gp mle: host allocation failed");
+  }
+}
+
 int scoot_gp_destroy(scoot_gp gp) {
   clear_error();
   if (!gp) return SCOOT_OK;

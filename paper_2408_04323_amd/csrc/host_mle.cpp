@@ -11,6 +11,15 @@
 //   Matern-5/2: 5/3 s2 (1 + sqrt5 r) exp(-sqrt5 r) D_k^2
 //   Matern-3/2: 3 s2 exp(-sqrt3 r) D_k^2.
 //
+// With the input warping learned as well (the paper's Matern-3/2 with input
+// warping after Snoek et al., whose warp parameters are fitted with the GP),
+// theta gains (log a_1 .. log a_d, log b_1 .. log b_d): the inputs are warped
+// by w = 1 - (1 - x^a)^b at every evaluation, and since dk/dw_ik =
+// -R_ij (w_ik - w_jk) / l_k^2 with R the radial factor above,
+//   dK_ij/dlog a_k = -R_ij (w_ik - w_jk) (g_ik - g_jk) / l_k^2,
+// g_ik = dw_ik/dlog a_k = a b (1 - x^a)^(b-1) x^a ln x (likewise for log b_k
+// with dw/dlog b = -b (1 - x^a)^b ln(1 - x^a)), both 0 at x = 0 and 1.
+//
 // The search runs unconstrained L-BFGS (10 pairs, backtracking line search
 // with the Armijo condition) in z with theta = lo + (hi - lo) sigmoid(z), so
 // every iterate stays inside the box [lo, hi]; a parameter with lo == hi is
@@ -34,7 +43,10 @@ constexpr double kLog2Pi = 1.83787706640934548356;
 struct MleData {
   int m, d;
   scoot_kernel kernel;
-  std::vector<double> Xw;  // m x d warped inputs
+  bool learn_warp = false;  // theta carries log a, log b; Xw is recomputed per evaluation
+  std::vector<double> X;   // m x d inputs as given (learn_warp)
+  mutable std::vector<double> Xw;  // m x d warped inputs
+  mutable std::vector<double> Ga, Gb;  // m x d: dw/dlog a, dw/dlog b (learn_warp)
   std::vector<double> r;   // y - c
   // Work matrices of nll_eval (m x m), allocated on the first evaluation and
   // reused: fresh allocations of this size are page-faulted in on every
@@ -50,6 +62,23 @@ std::vector<double>& work(std::vector<double>& v, size_t n) {
 
 constexpr int kChunks = 32;  // work split of every parallel step (independent of the thread count)
 
+// The warp of x and its derivatives in log a and log b (0 at x = 0 and 1),
+// written without cancellation: ln x from log1p(x - 1) above 1/2, 1 - x^a =
+// -expm1(a ln x).
+void warp_with_derivatives(double x, double a, double b, double* w, double* ga, double* gb) {
+  x = x < 0.0 ? 0.0 : (x > 1.0 ? 1.0 : x);
+  *w = kumaraswamy(x, a, b);
+  if (x <= 0.0 || x >= 1.0) {
+    *ga = *gb = 0.0;
+    return;
+  }
+  const double lx = x > 0.5 ? std::log1p(x - 1.0) : std::log(x);
+  const double u = std::exp(a * lx);
+  const double l1u = std::log(-std::expm1(a * lx));  // ln(1 - x^a)
+  *ga = a * b * std::exp((b - 1.0) * l1u) * u * lx;
+  *gb = -b * std::exp(b * l1u) * l1u;
+}
+
 // NLL and gradient at theta; false when K is not positive definite.
 bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) {
   const int m = D.m, d = D.d;
@@ -58,7 +87,20 @@ bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) 
   const double s2 = std::exp(theta[d]), tau2 = std::exp(theta[d + 1]);
   const bool m52 = D.kernel == SCOOT_MATERN52;
   const double root = m52 ? kSqrt5m : kSqrt3m;
+  if (D.learn_warp) {
+    work(D.Xw, (size_t)m * d);
+    work(D.Ga, (size_t)m * d);
+    work(D.Gb, (size_t)m * d);
+    for (int k = 0; k < d; ++k) {
+      const double a = std::exp(theta[d + 2 + k]), b = std::exp(theta[2 * d + 2 + k]);
+      for (int i = 0; i < m; ++i) {
+        const size_t at = (size_t)i * d + k;
+        warp_with_derivatives(D.X[at], a, b, &D.Xw[at], &D.Ga[at], &D.Gb[at]);
+      }
+    }
+  }
   const double* X = D.Xw.data();
+  const int P = D.learn_warp ? 3 * d + 2 : d + 2;
 
   // K (lower triangle), rows in parallel, then its Cholesky factor.  The
   // gradient reuses K - tau2 I (= dK/dlog s2) and the radial factor of
@@ -116,10 +158,12 @@ bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) 
 
   // Gradient: tiles by groups of four rows, partial sums per chunk, added in
   // chunk order.
-  std::vector<double> part((size_t)kChunks * (d + 2), 0.0);
+  std::vector<double> part((size_t)kChunks * P, 0.0);
   const int groups = (m + 3) / 4;
+  const double* Ga = D.learn_warp ? D.Ga.data() : nullptr;
+  const double* Gb = D.learn_warp ? D.Gb.data() : nullptr;
   parallel_chunks(kChunks, [&](int c) {
-    double* g = part.data() + (size_t)c * (d + 2);
+    double* g = part.data() + (size_t)c * P;
     for (int gi = c; gi < groups; gi += kChunks) {
       const int i0 = 4 * gi;
       const double* a[4];
@@ -138,6 +182,11 @@ bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) 
             for (int k = 0; k < d; ++k) {
               const double t = (X[(size_t)i * d + k] - X[(size_t)j * d + k]) * inv_ls[k];
               g[k] -= wr * (t * t);
+              if (Ga) {
+                const double wt = wr * t * inv_ls[k];
+                g[d + 2 + k] += wt * (Ga[(size_t)i * d + k] - Ga[(size_t)j * d + k]);
+                g[2 * d + 2 + k] += wt * (Gb[(size_t)i * d + k] - Gb[(size_t)j * d + k]);
+              }
             }
             g[d] -= w * Kf[(size_t)i * m + j];
             if (i == j) g[d + 1] -= w * tau2;
@@ -145,16 +194,16 @@ bool nll_eval(const MleData& D, const double* theta, double* nll, double* grad) 
       }
     }
   });
-  for (int k = 0; k < d + 2; ++k) {
+  for (int k = 0; k < P; ++k) {
     double s = 0.0;
-    for (int c = 0; c < kChunks; ++c) s += part[(size_t)c * (d + 2) + k];
+    for (int c = 0; c < kChunks; ++c) s += part[(size_t)c * P + k];
     grad[k] = s;
   }
   return true;
 }
 
 int prepare(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
-            const double* warp_b, double c, MleData& D) {
+            const double* warp_b, double c, MleData& D, bool learn_warp = false) {
   if (!X || !y) return fail(SCOOT_ERR_INVALID_ARG, "gp mle: null pointer");
   if (m < 1 || d < 1) return fail(SCOOT_ERR_INVALID_ARG, "gp mle: m and d must be >= 1");
   if (d > SCOOT_MAX_DIM) return fail(SCOOT_ERR_UNSUPPORTED, "gp mle: d exceeds SCOOT_MAX_DIM");
@@ -174,6 +223,8 @@ int prepare(const double* X, const double* y, int m, int d, scoot_kernel kernel,
   D.m = m;
   D.d = d;
   D.kernel = kernel;
+  D.learn_warp = learn_warp;
+  if (learn_warp) D.X.assign(X, X + (size_t)m * d);
   D.Xw.assign(X, X + (size_t)m * d);
   if (warp_a)
     for (int i = 0; i < m; ++i)
@@ -187,12 +238,12 @@ double sigmoid(double z) { return z >= 0 ? 1.0 / (1.0 + std::exp(-z)) : std::exp
 }  // namespace
 
 int mle_nll(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
-            const double* warp_b, double c, const double* theta, double* nll, double* grad) {
+            const double* warp_b, double c, const double* theta, double* nll, double* grad, bool learn_warp) {
   if (!theta || !nll) return fail(SCOOT_ERR_INVALID_ARG, "gp nll: null pointer");
   MleData D;
-  int rc = prepare(X, y, m, d, kernel, warp_a, warp_b, c, D);
+  int rc = prepare(X, y, m, d, kernel, warp_a, warp_b, c, D, learn_warp);
   if (rc != SCOOT_OK) return rc;
-  for (int k = 0; k < d + 2; ++k)
+  for (int k = 0; k < (learn_warp ? 3 * d + 2 : d + 2); ++k)
     if (!std::isfinite(theta[k])) return fail(SCOOT_ERR_INVALID_ARG, "gp nll: non-finite theta");
   if (!nll_eval(D, theta, nll, grad)) return fail(SCOOT_ERR_NOT_PD, "gp nll: K is not positive definite");
   return SCOOT_OK;
@@ -200,13 +251,13 @@ int mle_nll(const double* X, const double* y, int m, int d, scoot_kernel kernel,
 
 int mle_fit(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
             const double* warp_b, double c, const double* lower, const double* upper, int max_iter, double* theta,
-            double* nll_out, int* iters_out) {
+            double* nll_out, int* iters_out, bool learn_warp) {
   if (!lower || !upper || !theta) return fail(SCOOT_ERR_INVALID_ARG, "gp mle: null pointer");
   if (max_iter < 1) return fail(SCOOT_ERR_INVALID_ARG, "gp mle: max_iter must be >= 1");
   MleData D;
-  int rc = prepare(X, y, m, d, kernel, warp_a, warp_b, c, D);
+  int rc = prepare(X, y, m, d, kernel, warp_a, warp_b, c, D, learn_warp);
   if (rc != SCOOT_OK) return rc;
-  const int P = d + 2;
+  const int P = learn_warp ? 3 * d + 2 : d + 2;
   for (int k = 0; k < P; ++k)
     if (!std::isfinite(lower[k]) || !std::isfinite(upper[k]) || lower[k] > upper[k] || !std::isfinite(theta[k]))
       return fail(SCOOT_ERR_INVALID_ARG, "gp mle: bounds must be finite with lower <= upper, theta finite");
@@ -247,100 +298,133 @@ int mle_fit(const double* X, const double* y, int m, int d, scoot_kernel kernel,
   if (!eval(z, f, g)) return fail(SCOOT_ERR_NOT_PD, "gp mle: K is not positive definite at the start");
   std::deque<std::vector<double>> S, Y;
   int it = 0;
-  for (; it < max_iter && F > 0; ++it) {
-    double gmax = 0.0;
-    for (double v : g) gmax = std::max(gmax, std::fabs(v));
-    if (gmax < 1e-9) break;
-    // two-loop recursion: p = -H g
-    std::vector<double> q = g;
-    const int h = (int)S.size();
-    std::vector<double> al(h), rho(h);
-    for (int i = h - 1; i >= 0; --i) {
-      double sy = 0, sq = 0;
-      for (int k = 0; k < F; ++k) {
-        sy += S[i][k] * Y[i][k];
-        sq += S[i][k] * q[k];
+  // A parameter pushed against a bound sits where the sigmoid is flat, so its
+  // z-gradient vanishes even where the likelihood still falls inwards: after
+  // the search stops, such parameters are moved 1% of their range inside and
+  // the search restarts (fresh history), up to kRestarts times; the best
+  // point seen is returned.
+  constexpr int kRestarts = 4;
+  std::vector<double> z_best = z;
+  double f_best = f;
+  for (int restart = 0; restart <= kRestarts; ++restart) {
+    for (; it < max_iter && F > 0; ++it) {
+      double gmax = 0.0;
+      for (double v : g) gmax = std::max(gmax, std::fabs(v));
+      if (gmax < 1e-9) break;
+      // two-loop recursion: p = -H g
+      std::vector<double> q = g;
+      const int h = (int)S.size();
+      std::vector<double> al(h), rho(h);
+      for (int i = h - 1; i >= 0; --i) {
+        double sy = 0, sq = 0;
+        for (int k = 0; k < F; ++k) {
+          sy += S[i][k] * Y[i][k];
+          sq += S[i][k] * q[k];
+        }
+        rho[i] = 1.0 / sy;
+        al[i] = rho[i] * sq;
+        for (int k = 0; k < F; ++k) q[k] -= al[i] * Y[i][k];
       }
-      rho[i] = 1.0 / sy;
-      al[i] = rho[i] * sq;
-      for (int k = 0; k < F; ++k) q[k] -= al[i] * Y[i][k];
-    }
-    double gamma = 1.0;
-    if (h > 0) {
-      double sy = 0, yy = 0;
-      for (int k = 0; k < F; ++k) {
-        sy += S[h - 1][k] * Y[h - 1][k];
-        yy += Y[h - 1][k] * Y[h - 1][k];
+      double gamma = 1.0;
+      if (h > 0) {
+        double sy = 0, yy = 0;
+        for (int k = 0; k < F; ++k) {
+          sy += S[h - 1][k] * Y[h - 1][k];
+          yy += Y[h - 1][k] * Y[h - 1][k];
+        }
+        gamma = sy / yy;
       }
-      gamma = sy / yy;
-    }
-    for (int k = 0; k < F; ++k) q[k] *= gamma;
-    for (int i = 0; i < h; ++i) {
-      double yq = 0;
-      for (int k = 0; k < F; ++k) yq += Y[i][k] * q[k];
-      const double b = rho[i] * yq;
-      for (int k = 0; k < F; ++k) q[k] += S[i][k] * (al[i] - b);
-    }
-    std::vector<double> p(F);
-    double gp = 0;
-    for (int k = 0; k < F; ++k) {
-      p[k] = -q[k];
-      gp += p[k] * g[k];
-    }
-    if (!(gp < 0)) {  // not a descent direction: restart from steepest descent
-      S.clear();
-      Y.clear();
-      gp = 0;
-      for (int k = 0; k < F; ++k) {
-        p[k] = -g[k];
-        gp -= g[k] * g[k];
+      for (int k = 0; k < F; ++k) q[k] *= gamma;
+      for (int i = 0; i < h; ++i) {
+        double yq = 0;
+        for (int k = 0; k < F; ++k) yq += Y[i][k] * q[k];
+        const double b = rho[i] * yq;
+        for (int k = 0; k < F; ++k) q[k] += S[i][k] * (al[i] - b);
       }
-    }
-    // step: at most 2 in z per coordinate on the first iteration
-    double step = 1.0;
-    if (h == 0) {
-      double pmax = 0;
-      for (double v : p) pmax = std::max(pmax, std::fabs(v));
-      if (pmax > 2.0) step = 2.0 / pmax;
-    }
-    std::vector<double> zn(F), gn;
-    double fn = 0;
-    bool ok = false;
-    for (int ls = 0; ls < 40; ++ls, step *= 0.5) {
-      for (int k = 0; k < F; ++k) zn[k] = z[k] + step * p[k];
-      if (eval(zn, fn, gn) && fn <= f + 1e-4 * step * gp) {
-        ok = true;
+      std::vector<double> p(F);
+      double gp = 0;
+      for (int k = 0; k < F; ++k) {
+        p[k] = -q[k];
+        gp += p[k] * g[k];
+      }
+      if (!(gp < 0)) {  // not a descent direction: restart from steepest descent
+        S.clear();
+        Y.clear();
+        gp = 0;
+        for (int k = 0; k < F; ++k) {
+          p[k] = -g[k];
+          gp -= g[k] * g[k];
+        }
+      }
+      // step: at most 2 in z per coordinate on the first iteration
+      double step = 1.0;
+      if (h == 0) {
+        double pmax = 0;
+        for (double v : p) pmax = std::max(pmax, std::fabs(v));
+        if (pmax > 2.0) step = 2.0 / pmax;
+      }
+      std::vector<double> zn(F), gn;
+      double fn = 0;
+      bool ok = false;
+      for (int ls = 0; ls < 40; ++ls, step *= 0.5) {
+        for (int k = 0; k < F; ++k) zn[k] = z[k] + step * p[k];
+        if (eval(zn, fn, gn) && fn <= f + 1e-4 * step * gp) {
+          ok = true;
+          break;
+        }
+      }
+      if (!ok) break;  // no decrease along p: converged to rounding
+      std::vector<double> s(F), yv(F);
+      double sy = 0;
+      for (int k = 0; k < F; ++k) {
+        s[k] = zn[k] - z[k];
+        yv[k] = gn[k] - g[k];
+        sy += s[k] * yv[k];
+      }
+      if (sy > 1e-14) {
+        S.push_back(s);
+        Y.push_back(yv);
+        if (S.size() > 10) {
+          S.pop_front();
+          Y.pop_front();
+        }
+      }
+      const double df = f - fn;
+      z = zn;
+      f = fn;
+      g = gn;
+      if (df <= 1e-13 * std::max(1.0, std::fabs(f))) {
+        ++it;
         break;
       }
     }
-    if (!ok) break;  // no decrease along p: converged to rounding
-    std::vector<double> s(F), yv(F);
-    double sy = 0;
-    for (int k = 0; k < F; ++k) {
-      s[k] = zn[k] - z[k];
-      yv[k] = gn[k] - g[k];
-      sy += s[k] * yv[k];
+    if (f < f_best) {
+      f_best = f;
+      z_best = z;
     }
-    if (sy > 1e-14) {
-      S.push_back(s);
-      Y.push_back(yv);
-      if (S.size() > 10) {
-        S.pop_front();
-        Y.pop_front();
+    if (restart == kRestarts || it >= max_iter || F == 0) break;
+    // the gradient in theta at the point reached (eval leaves it in gth)
+    double f_here;
+    std::vector<double> g_here;
+    if (!eval(z, f_here, g_here)) break;
+    bool moved = false;
+    for (int q = 0; q < F; ++q) {
+      const double u = sigmoid(z[q]), gk = gth[fr[q]];
+      if (u > 1.0 - 1e-6 && gk > 0) {
+        z[q] = std::log(0.99 / 0.01);
+        moved = true;
+      } else if (u < 1e-6 && gk < 0) {
+        z[q] = std::log(0.01 / 0.99);
+        moved = true;
       }
     }
-    const double df = f - fn;
-    z = zn;
-    f = fn;
-    g = gn;
-    if (df <= 1e-13 * std::max(1.0, std::fabs(f))) {
-      ++it;
-      break;
-    }
+    if (!moved || !eval(z, f, g)) break;
+    S.clear();
+    Y.clear();
   }
-  to_theta(z, t);
+  to_theta(z_best, t);
   std::memcpy(theta, t.data(), sizeof(double) * P);
-  if (nll_out) *nll_out = f;
+  if (nll_out) *nll_out = f_best;
   if (iters_out) *iters_out = it;
   return SCOOT_OK;
 }

@@ -216,12 +216,14 @@ SCOOT_HOST_DEVICE inline double kumaraswamy(double x, double a, double b) {
   return -expm1(b * log(-expm1(a * lx)));
 }
 
-// Maximum-likelihood hyperparameters (host_mle.cpp); theta = (log l_1..d, log s2, log tau2).
+// Maximum-likelihood hyperparameters (host_mle.cpp); theta = (log l_1..d, log s2, log tau2),
+// followed by (log a_1..d, log b_1..d) when learn_warp (warp_a / warp_b must then be null).
 int mle_nll(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
-            const double* warp_b, double c, const double* theta, double* nll, double* grad);
+            const double* warp_b, double c, const double* theta, double* nll, double* grad,
+            bool learn_warp = false);
 int mle_fit(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
             const double* warp_b, double c, const double* lower, const double* upper, int max_iter, double* theta,
-            double* nll, int* iterations);
+            double* nll, int* iterations, bool learn_warp = false);
 
 // Forest training (host_forest_train.cpp): tree-local child indices, preorder.
 struct TrainedForest {

@@ -25,7 +25,21 @@ namespace {
 constexpr double kDefaultLo[3] = {0.01, 0.05, 1e-6};   // lengthscale, signal var, noise var
 constexpr double kDefaultHi[3] = {10.0, 20.0, 1.0};
 constexpr double kDefaultStart[3] = {0.5, 1.0, 1e-3};
+constexpr double kWarpLo = 0.2, kWarpHi = 5.0;         // box of each learned Kumaraswamy parameter
 constexpr int kDefaultMleIter = 200;
+
+// With the warping learned: the box and start of the warp parameters (log a,
+// then log b), after the d + 2 of theta_box; the start is the caller's fixed
+// warp when given, else the identity a = b = 1.
+void warp_box(const scoot_suggest_opts& o, int j, int d, double* lo, double* hi, double* th) {
+  for (int t = 0; t < 2 * d; ++t) {
+    lo[t] = std::log(kWarpLo);
+    hi[t] = std::log(kWarpHi);
+    const double* w = t < d ? o.warp_a : o.warp_b;
+    th[t] = w ? std::log(w[(size_t)j * d + t % d]) : 0.0;
+    th[t] = std::fmin(std::fmax(th[t], lo[t]), hi[t]);
+  }
+}
 
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
@@ -78,6 +92,11 @@ int check_opts(const scoot_suggest_opts* o, int p, int d) {
   if (o->dtype != SCOOT_F32 && o->dtype != SCOOT_F64) return fail(SCOOT_ERR_INVALID_ARG, "suggest: unknown dtype");
   if ((o->warp_a == nullptr) != (o->warp_b == nullptr))
     return fail(SCOOT_ERR_INVALID_ARG, "suggest: warp_a and warp_b go together");
+  if (o->learn_warp != 0 && o->learn_warp != 1) return fail(SCOOT_ERR_INVALID_ARG, "suggest: learn_warp is 0 or 1");
+  if (o->warp_a)
+    for (size_t t = 0; t < (size_t)p * d; ++t)
+      if (!(o->warp_a[t] > 0) || !(o->warp_b[t] > 0) || !std::isfinite(o->warp_a[t]) || !std::isfinite(o->warp_b[t]))
+        return fail(SCOOT_ERR_INVALID_ARG, "suggest: warping parameters must be finite and > 0");
   if (o->n_trees < 1 || o->n_trees > SCOOT_MAX_TREES) return fail(SCOOT_ERR_INVALID_ARG, "suggest: n_trees out of range");
   if (o->max_depth < 0) return fail(SCOOT_ERR_INVALID_ARG, "suggest: max_depth < 0");
   if (!std::isfinite(o->xi)) return fail(SCOOT_ERR_INVALID_ARG, "suggest: non-finite xi");
@@ -172,7 +191,9 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
     Handles h;
     if (m > 0) {
       // ---- 2. hyperparameters and GPs ----------------------------------
-      const int nt = d + 2;
+      // theta per objective: d + 2 entries, or 3d + 2 with the warping learned
+      const bool lw = o.learn_warp != 0;
+      const int nt = lw ? 3 * d + 2 : d + 2;
       std::vector<double> theta((size_t)p * nt);
       // The objectives' searches run side by side, each on its own thread and
       // each spreading its likelihood evaluations over the library's host
@@ -182,17 +203,21 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
       std::vector<std::string> search_err(p);
       auto search = [&](int j) {
         try {
-          double lo[SCOOT_MAX_DIM + 2], hi[SCOOT_MAX_DIM + 2], th[SCOOT_MAX_DIM + 2];
+          double lo[3 * SCOOT_MAX_DIM + 2], hi[3 * SCOOT_MAX_DIM + 2], th[3 * SCOOT_MAX_DIM + 2];
           theta_box(o, j, d, lo, hi, th);
+          if (lw) warp_box(o, j, d, lo + d + 2, hi + d + 2, th + d + 2);
           bool all_fixed = true;
           for (int t = 0; t < nt; ++t) all_fixed = all_fixed && lo[t] == hi[t];
           std::vector<double> yj(m);
           for (int r = 0; r < m; ++r) yj[r] = Yv[(size_t)r * p + j];
           const double* wa = o.warp_a ? o.warp_a + (size_t)j * d : nullptr;
           const double* wb = o.warp_b ? o.warp_b + (size_t)j * d : nullptr;
+          const int iters = o.mle_max_iter > 0 ? o.mle_max_iter : kDefaultMleIter;
           if (!all_fixed) {
-            search_rc[j] = scoot_gp_mle(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, wa, wb, 0.0, lo, hi,
-                                        o.mle_max_iter > 0 ? o.mle_max_iter : kDefaultMleIter, th, nullptr, nullptr);
+            search_rc[j] = lw ? scoot_gp_mle_warp(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, 0.0, lo, hi,
+                                                  iters, th, nullptr, nullptr)
+                              : scoot_gp_mle(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, wa, wb, 0.0, lo,
+                                             hi, iters, th, nullptr, nullptr);
             if (search_rc[j] != SCOOT_OK) search_err[j] = scoot_last_error();  // this thread's message
           }
           std::memcpy(&theta[(size_t)j * nt], th, sizeof(double) * nt);
@@ -220,8 +245,16 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
         for (int r = 0; r < m; ++r) yj[r] = Yv[(size_t)r * p + j];
         const double* wa = o.warp_a ? o.warp_a + (size_t)j * d : nullptr;
         const double* wb = o.warp_b ? o.warp_b + (size_t)j * d : nullptr;
-        double ell[SCOOT_MAX_DIM];
+        double ell[SCOOT_MAX_DIM], la[SCOOT_MAX_DIM], lb[SCOOT_MAX_DIM];
         for (int t = 0; t < d; ++t) ell[t] = std::exp(th[t]);
+        if (lw) {
+          for (int t = 0; t < d; ++t) {
+            la[t] = std::exp(th[d + 2 + t]);
+            lb[t] = std::exp(th[2 * d + 2 + t]);
+          }
+          wa = la;
+          wb = lb;
+        }
         scoot_gp g = nullptr;
         rc = scoot_gp_fit_ex(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, ell, wa, wb, std::exp(th[d]),
                              std::exp(th[d + 1]), 0.0, (scoot_dtype)o.dtype, stream, &g);
@@ -277,7 +310,7 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
       for (int r = 0; r < k; ++r)
         if (idx_host[r] >= 0) picked.push_back(idx_host[r]);
     } else if (theta_out) {
-      for (size_t t = 0; t < (size_t)p * (d + 2); ++t) theta_out[t] = NAN;
+      for (size_t t = 0; t < (size_t)p * (o.learn_warp ? 3 * d + 2 : d + 2); ++t) theta_out[t] = NAN;
     }
     const int n_solver = (int)picked.size();
 

@@ -150,3 +150,35 @@ def test_algorithm1_loop(p):
         X, Y, v = np.vstack([X, want["x"]]), np.vstack([Y, y_new]), np.concatenate([v, v_new])
         rnd += 1
     assert 0.25 <= delta <= 0.75
+
+
+def test_suggest_learns_the_warping():
+    """With learn_warp (the paper's Matern-3/2 with input warping learned with
+    the GP), each objective's parameters (3d + 2: lengthscales, variances and
+    the Kumaraswamy a, b) are a likelihood optimum at least as good as the
+    oracle's from the same start and inside their boxes, and the rest of the
+    step is the fixed-parameter step at that optimum (the same picks with the
+    learned warp and hyperparameters given)."""
+    from oracle.mle import fit_hyperparameters_warp, nll_and_grad_warp
+    sp = space()
+    X, Y, v = observations(28, p=2, seed=23)
+    d = 4
+    kw = dict(k=3, pool_size=1024, n_trees=8, max_depth=5, forest_seed=4, kernel="matern32")
+    say("suggest learning the warp")
+    x, src, theta = S.suggest(X, Y, v, sp, learn_warp=True, **kw)
+    assert theta.shape == (2, 3 * d + 2)
+    ok = v != 0
+    Ys = (Y[ok] - Y[ok].mean(0)) / Y[ok].std(0)
+    lo = np.log(np.array([0.01] * d + [0.05, 1e-6] + [0.2] * (2 * d)))
+    hi = np.log(np.array([10.0] * d + [20.0, 1.0] + [5.0] * (2 * d)))
+    start = np.log(np.array([0.5] * d + [1.0, 1e-3] + [1.0] * (2 * d)))
+    for j in range(2):
+        _, f_o = fit_hyperparameters_warp(X[ok], Ys[:, j], start, lo, hi, "matern32")
+        f_g, _ = nll_and_grad_warp(theta[j], X[ok], Ys[:, j], "matern32")
+        assert f_g <= f_o + 1e-6 * max(1.0, abs(f_o))
+        assert np.all(theta[j] >= lo - 1e-12) and np.all(theta[j] <= hi + 1e-12)
+    th = theta[:, :d + 2]
+    x2, src2, _ = S.suggest(X, Y, v, sp, theta_lower=th, theta_upper=th, warp_a=np.exp(theta[:, d + 2:2 * d + 2]),
+                            warp_b=np.exp(theta[:, 2 * d + 2:]), **kw)
+    np.testing.assert_array_equal(x2, x)
+    np.testing.assert_array_equal(src2, src)

@@ -118,3 +118,39 @@ def test_concurrent_searches_match_sequential():
             t.join()
         for a, b in zip(alone, together):
             assert np.array_equal(a[0], b[0]) and a[1] == b[1] and a[2] == b[2]
+
+
+# ----------------------------------------------- the input warping learned too
+@pytest.mark.parametrize("kernel", ["matern32", "matern52"])
+def test_warped_nll_and_gradient_match_oracle(kernel):
+    from oracle.mle import nll_and_grad_warp
+    X, y = _case(5, 55, 4)
+    X[0, 0], X[1, 1], X[2, 2], X[3, 3] = 0.0, 1.0, 0.5, 1e-12     # endpoints, grid, near-endpoint
+    rng = np.random.default_rng(6)
+    for trial in range(3):
+        theta = np.concatenate([np.log(rng.uniform(0.1, 2.0, 4)), [np.log(rng.uniform(0.3, 3)),
+                                np.log(rng.uniform(1e-4, 0.3))], 0.5 * rng.standard_normal(8)])
+        nll, g = S.gp_nll_warp(X, y, theta, kernel=kernel, prior_mean=-0.05)
+        nll_o, g_o = nll_and_grad_warp(theta, X, y, kernel, prior_mean=-0.05)
+        assert nll == pytest.approx(nll_o, rel=1e-11, abs=1e-10)
+        np.testing.assert_allclose(g, g_o, rtol=1e-8, atol=1e-8)
+
+
+def test_warped_fit_reaches_the_oracle_optimum():
+    from oracle.mle import fit_hyperparameters_warp, nll_and_grad_warp
+    rng = np.random.default_rng(8)
+    X = rng.random((50, 2))
+    y = np.sin(6 * X[:, 0] ** 3) + 0.5 * X[:, 1] ** 0.3 + 0.02 * rng.standard_normal(50)
+    y = (y - y.mean()) / y.std()
+    d = 2
+    lo = np.log(np.array([0.02] * d + [0.05, 1e-6] + [0.2] * (2 * d)))
+    hi = np.log(np.array([10.0] * d + [20.0, 1.0] + [5.0] * (2 * d)))
+    theta0 = np.log(np.array([0.5] * d + [1.0, 1e-3] + [1.0] * (2 * d)))
+    th, f, it = S.gp_mle_warp(X, y, theta0, lo, hi, kernel="matern32", max_iter=300)
+    th_o, f_o = fit_hyperparameters_warp(X, y, theta0, lo, hi, "matern32")
+    assert it > 0 and np.all(th >= lo) and np.all(th <= hi)
+    assert f == pytest.approx(nll_and_grad_warp(th, X, y, "matern32")[0], rel=1e-11, abs=1e-10)
+    assert f <= f_o + 1e-7 * max(1.0, abs(f_o))
+    _, g = nll_and_grad_warp(th, X, y, "matern32")
+    interior = (th > lo + 1e-3) & (th < hi - 1e-3)
+    assert np.all(np.abs(g[interior]) < 1e-4)
