@@ -247,27 +247,30 @@ int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel
       linv_bytes = l64.size() * 8;
     }
     linv_bytes = (linv_bytes + 255) / 256 * 256;
-    xs_bytes = ((size_t)f.m_pad * kXsStride * esz + 255) / 256 * 256;
+    // fp32: the augmented observation rows of the cross-term chain (double);
+    // fp64: scaled rows of kXsStride doubles
+    std::vector<double> q32;
+    if (dt == SCOOT_F32) pack_obs_f32(f, q32);
+    xs_bytes = dt == SCOOT_F32 ? (q32.size() * 8 + 255) / 256 * 256
+                               : ((size_t)f.m_pad * kXsStride * esz + 255) / 256 * 256;
     const size_t alpha_bytes = (size_t)f.m_pad * 8;
     const size_t alpha32_bytes = ((size_t)f.m_pad * 4 + 255) / 256 * 256;
     img.assign(linv_bytes + xs_bytes + alpha_bytes + alpha32_bytes, 0);
     if (dt == SCOOT_F32) std::memcpy(img.data(), l32.data(), l32.size() * 4);
     else std::memcpy(img.data(), l64.data(), l64.size() * 8);
-    // Rows with a spare column carry alpha_i in column d, so the kernels read
-    // an observation and its weight with the same loads.
-    for (int i = 0; i < f.m_pad; ++i)
-      for (int k = 0; k < kXsStride; ++k) {
-        double v = 0.0;
-        if (k < d) v = i < m ? f.Xw[(size_t)i * d + k] * f.scale[k] : kPadCoord;
-        else if (k == d && i < m) v = f.alpha[i];
-        unsigned char* at = img.data() + linv_bytes + ((size_t)i * kXsStride + k) * esz;
-        if (dt == SCOOT_F32) {
-          float fv = (float)v;
-          std::memcpy(at, &fv, 4);
-        } else {
-          std::memcpy(at, &v, 8);
+    // fp64 rows with a spare column carry alpha_i in column d, so the kernel
+    // reads an observation and its weight with the same loads.
+    if (dt == SCOOT_F32) {
+      std::memcpy(img.data() + linv_bytes, q32.data(), q32.size() * 8);
+    } else {
+      for (int i = 0; i < f.m_pad; ++i)
+        for (int k = 0; k < kXsStride; ++k) {
+          double v = 0.0;
+          if (k < d) v = i < m ? f.Xw[(size_t)i * d + k] * f.scale[k] : kPadCoord;
+          else if (k == d && i < m) v = f.alpha[i];
+          std::memcpy(img.data() + linv_bytes + ((size_t)i * kXsStride + k) * 8, &v, 8);
         }
-      }
+    }
     std::vector<double> apad(f.m_pad, 0.0);
     std::memcpy(apad.data(), f.alpha.data(), sizeof(double) * m);
     std::memcpy(img.data() + linv_bytes + xs_bytes, apad.data(), alpha_bytes);

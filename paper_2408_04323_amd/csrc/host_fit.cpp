@@ -126,46 +126,83 @@ int fit_host(const double* X, const double* y, int m, int d, scoot_kernel kernel
   return SCOOT_OK;
 }
 
-// fp32 layout.  Block (I, J) (32 x 32, J <= I) of L^-1 feeds a
-// v_mfma_f32_32x32x2f32 chain as its A operand: at step s (0..15) lane l
-// holds A[i][k] = Linv[32I + i][32J + 2s + k] with i = l % 32, k = l / 32.
-// Inside a block the 16 steps are grouped in fours so a lane reads four
-// consecutive steps as one 16-byte load:
-//   float index = ((blk * 4 + s / 4) * 64 + l) * 4 + s % 4.
-// Blocks are ordered the way the kernel's waves consume them: plan entry after
-// plan entry (plan_rows), J = 0..I within a row block.
+// fp32 layout, for v_mfma_f32_16x16x4f32: 16 x 16 blocks (J <= I), the
+// block's contraction index ordered k = 4g + s (g = lane / 16, s the step),
+// so at step s lane l holds Linv[16I + l % 16][16J + 4 (l / 16) + s] and a
+// lane reads the four steps of a block as one 16-byte load:
+//   float index = (blk * 64 + l) * 4 + s.
+// Blocks are ordered the way the kernel's waves consume them: plan entry
+// after plan entry (plan_rows16 with the kernel's wave count), J = 0..I.
 void pack_linv_f32(const FitHost& f, std::vector<float>& out) {
-  const int nb = f.nb, m = f.m, W = posterior_waves(nb);
-  const RowPlan plan = plan_rows(nb, W);
-  out.assign((size_t)nb * (nb + 1) / 2 * 16 * 64, 0.0f);
+  const int nb = f.m_pad / kBlk16, m = f.m;
+  const RowPlan16 plan = plan_rows16(nb, posterior_waves(f.nb));
+  out.assign((size_t)nb * (nb + 1) / 2 * 4 * 64, 0.0f);
   size_t blk = 0;
   for (int e = 0; e < 8; ++e)
-    for (int r = 0; r < plan.nrows[e]; ++r) {
-      const int I = (int)((plan.rows[e] >> (kRowBits * r)) & 31);
+    for (int q = 0; q < plan.nrows[e] && q < kMaxRows16; ++q) {
+      const int I = plan16_row(plan, e, q);
       for (int J = 0; J <= I; ++J, ++blk)
-        for (int s = 0; s < 16; ++s)
-          for (int l = 0; l < 64; ++l) {
-            int row = 32 * I + (l % 32), col = 32 * J + 2 * s + l / 32;
-            double v = (row < m && col < m) ? f.Linv[(size_t)row * m + col] : 0.0;
-            out[((blk * 4 + s / 4) * 64 + l) * 4 + s % 4] = (float)v;
+        for (int l = 0; l < 64; ++l)
+          for (int s = 0; s < 4; ++s) {
+            const int row = 16 * I + (l % 16), col = 16 * J + 4 * (l / 16) + s;
+            const double v = (row < m && col < m) ? f.Linv[(size_t)row * m + col] : 0.0;
+            out[(blk * 64 + l) * 4 + s] = (float)v;
           }
     }
+}
+
+// The fp32 kernel's observation operand: per 16-observation block J and step
+// s of a v_mfma_f64_16x16x4f64 chain, lane l holds component k = 4s + l / 16
+// of an observation's augmented row (2 Xs_i, -|Xs_i|^2, -1, 0 ...) (Xs the
+// warped inputs times the per-dimension scales), so that with the
+// candidates' rows (xs, 1, |xs|^2) the chain yields -|xs - Xs_i|^2:
+//   double index = (J * S + s) * 64 + l,  S = ceil((d + 2) / 4).
+// That instruction leaves output row t = g + 4r in register r of lanes
+// 16g .. 16g + 15 (measured), while the float triangle wants observation
+// 16J + 4g + r there, so A-operand row t carries observation
+// 16J + 4 (t % 4) + t / 4.  Padding rows (i >= m) carry -1e30 in the norm's
+// place: their covariance underflows to exactly 0.
+void pack_obs_f32(const FitHost& f, std::vector<double>& out) {
+  const int nb = f.m_pad / kBlk16, m = f.m, d = f.d, S = (d + 2 + 3) / 4;
+  out.assign((size_t)nb * S * 64, 0.0);
+  for (int J = 0; J < nb; ++J)
+    for (int s = 0; s < S; ++s)
+      for (int l = 0; l < 64; ++l) {
+        const int t = l % 16, i = 16 * J + 4 * (t % 4) + t / 4, k = 4 * s + l / 16;
+        double v = 0.0;
+        if (i < m) {
+          if (k < d) {
+            v = 2.0 * f.Xw[(size_t)i * d + k] * f.scale[k];
+          } else if (k == d) {
+            double nrm = 0.0;
+            for (int q = 0; q < d; ++q) {
+              const double t = f.Xw[(size_t)i * d + q] * f.scale[q];
+              nrm += t * t;
+            }
+            v = -nrm;
+          } else if (k == d + 1) {
+            v = -1.0;
+          }
+        } else {
+          v = k == d ? -1e30 : (k == d + 1 ? -1.0 : 0.0);
+        }
+        out[((size_t)J * S + s) * 64 + l] = v;
+      }
 }
 
 // fp64 layout, for v_mfma_f64_16x16x4f64: 16 x 16 blocks, four steps per
 // block; at step s lane l holds Linv[16I + l % 16][16J + 4s + l / 16]; steps
 // are paired so a lane reads two consecutive steps as one 16-byte load:
 //   double index = ((blk * 2 + s / 2) * 64 + l) * 2 + s % 2.
-// Blocks are ordered as for fp32: plan entry after plan entry (plan_rows over
-// the 16-row blocks with the fp32 kernel's wave count), J = 0..I.
+// Blocks are ordered as for fp32: plan entry after plan entry, J = 0..I.
 void pack_linv_f64(const FitHost& f, std::vector<double>& out) {
-  const int nb = f.m_pad / kBlk64, m = f.m;
-  const RowPlan64 plan = plan_rows64(nb, posterior_waves(f.nb));
+  const int nb = f.m_pad / kBlk16, m = f.m;
+  const RowPlan16 plan = plan_rows16(nb, posterior_waves(f.nb));
   out.assign((size_t)nb * (nb + 1) / 2 * 4 * 64, 0.0);
   size_t blk = 0;
   for (int e = 0; e < 8; ++e)
-    for (int q = 0; q < plan.nrows[e] && q < kMaxRows64; ++q) {
-      const int I = plan64_row(plan, e, q);
+    for (int q = 0; q < plan.nrows[e] && q < kMaxRows16; ++q) {
+      const int I = plan16_row(plan, e, q);
       for (int J = 0; J <= I; ++J, ++blk)
         for (int s = 0; s < 4; ++s)
           for (int l = 0; l < 64; ++l) {

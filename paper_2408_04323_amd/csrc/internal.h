@@ -13,10 +13,11 @@
 
 namespace scoot {
 
-// Rows of the inverse factor handled by one MFMA row block (fp32 path: the
-// 32x32x2 instruction) and the padded row stride of the scaled observations.
+// Granule the observation count is padded to (the posterior sizes its LDS
+// and picks its wave count in units of it), the 16-row MFMA block of the
+// triangular product, and the padded row stride of the scaled observations.
 constexpr int kBlk32 = 32;
-constexpr int kBlk64 = 16;
+constexpr int kBlk16 = 16;
 constexpr int kXsStride = 16;          // floats / doubles per observation row
 constexpr double kPadCoord = 1.0e4;    // scaled coordinate of padding rows: k(x, pad) == 0
 
@@ -26,32 +27,25 @@ constexpr double kPadCoord = 1.0e4;    // scaled coordinate of padding rows: k(x
 #define SCOOT_HOST_DEVICE
 #endif
 
-// Waves per workgroup of the fp32 posterior: more than 9 row blocks of K*
+// Waves per workgroup of the posterior: more than 9 granules of K*
 // (72 KiB of LDS per 64-candidate tile) leave room for one workgroup per CU,
 // so it gets 8 waves; otherwise two 4-wave workgroups share a CU.
 inline int posterior_waves(int nb) { return nb > 9 ? 8 : 4; }
 
-// Which row blocks of V each wave of the posterior owns (fp32: 32-row blocks,
-// fp64: 16-row blocks).  Row block I costs I + 1 blocks of the triangle.  Plan entry p goes to wave p of a 4-wave
-// workgroup; with 8 waves the two entries p and p + 4 share a SIMD and its
-// matrix unit.  So the rows are first split into four sets of (nearly) equal
-// cost, one per SIMD, by a depth-first search for the smallest capacity that
-// admits a packing; with 8 waves each set is then halved between its two
-// waves by an exact subset-sum split.  The packed inverse streams the blocks
-// entry by entry, each entry's rows in increasing I, blocks J = 0..I.
-constexpr int kMaxRowBlocks = SCOOT_MAX_OBS / kBlk32;
-constexpr int kRowBits = 5;  // rows of an entry packed 5 bits each, first row lowest
-struct RowPlan {
-  uint64_t rows[8];
-  int32_t nrows[8];
-  int32_t blk_start[9];  // first block of entry p in the packed stream
-};
-// fp64 (16-row blocks, up to 36): 6 bits per row in one 128-bit value held
-// as two words (row k at bits 6k .. 6k + 5, lo the low word), so an entry
-// holds up to 21 rows.
-constexpr int kRowBits64 = 6;
-constexpr int kMaxRows64 = 128 / kRowBits64;
-struct RowPlan64 {
+// Which 16-row blocks of V each wave of the posterior owns (both
+// precisions).  Row block I costs I + 1 blocks of the triangle.  Plan entry p
+// goes to wave p of a 4-wave workgroup; with 8 waves the two entries p and
+// p + 4 share a SIMD and its matrix unit.  So the rows are first split into
+// four sets of (nearly) equal cost, one per SIMD, by a depth-first search for
+// the smallest capacity that admits a packing; with 8 waves each set is then
+// halved between its two waves by an exact subset-sum split.  The packed
+// inverse streams the blocks entry by entry, each entry's rows in increasing
+// I, blocks J = 0..I.  Up to 36 row blocks: 6 bits per row in one 128-bit
+// value held as two words (row k at bits 6k .. 6k + 5, lo the low word), so
+// an entry holds up to 21 rows.
+constexpr int kRowBits16 = 6;
+constexpr int kMaxRows16 = 128 / kRowBits16;
+struct RowPlan16 {
   uint64_t lo[8], hi[8];
   int32_t nrows[8];
   int32_t blk_start[9];
@@ -121,30 +115,12 @@ inline void plan_entries(int nb, int W, std::vector<int> (&entry)[8]) {
   for (auto& e : entry) std::sort(e.begin(), e.end());
 }
 
-inline RowPlan plan_rows(int nb, int W) {
-  std::vector<int> entry[8];
-  plan_entries(nb, W, entry);
-  RowPlan p{};
-  int b = 0;
-  for (int e = 0; e < 8; ++e) {
-    const std::vector<int>& r = entry[e];
-    p.blk_start[e] = b;
-    p.nrows[e] = (int)r.size();
-    for (size_t k = 0; k < r.size(); ++k) {
-      if ((k + 1) * kRowBits <= 64) p.rows[e] |= (uint64_t)r[k] << (kRowBits * k);
-      b += r[k] + 1;
-    }
-  }
-  p.blk_start[8] = b;
-  return p;
-}
-
-// Entries of more than kMaxRows64 rows keep only their first kMaxRows64 (nrows
+// Entries of more than kMaxRows16 rows keep only their first kMaxRows16 (nrows
 // tells; the launcher refuses such a plan).
-inline RowPlan64 plan_rows64(int nb16, int W) {
+inline RowPlan16 plan_rows16(int nb16, int W) {
   std::vector<int> entry[8];
   plan_entries(nb16, W, entry);
-  RowPlan64 p{};
+  RowPlan16 p{};
   int b = 0;
   for (int e = 0; e < 8; ++e) {
     const std::vector<int>& r = entry[e];
@@ -152,7 +128,7 @@ inline RowPlan64 plan_rows64(int nb16, int W) {
     p.nrows[e] = (int)r.size();
     unsigned __int128 v = 0;
     for (size_t k = 0; k < r.size(); ++k) {
-      if ((int)k < kMaxRows64) v |= (unsigned __int128)r[k] << (kRowBits64 * k);
+      if ((int)k < kMaxRows16) v |= (unsigned __int128)r[k] << (kRowBits16 * k);
       b += r[k] + 1;
     }
     p.lo[e] = (uint64_t)v;
@@ -162,9 +138,9 @@ inline RowPlan64 plan_rows64(int nb16, int W) {
   return p;
 }
 // Row q of entry e of a fp64 plan.
-inline int plan64_row(const RowPlan64& p, int e, int q) {
+inline int plan16_row(const RowPlan16& p, int e, int q) {
   const unsigned __int128 v = ((unsigned __int128)p.hi[e] << 64) | p.lo[e];
-  return (int)((v >> (kRowBits64 * q)) & ((1u << kRowBits64) - 1));
+  return (int)((v >> (kRowBits16 * q)) & ((1u << kRowBits16) - 1));
 }
 
 // Runs fn(c) for every chunk c = 0 .. n_chunks - 1 on the library's pool of
@@ -236,6 +212,8 @@ int train_forest_host(const double* X, const double* y, int n, int d, int n_tree
 
 // Packs L^-1 into matrix-core A-operand order (see the posterior kernels).
 void pack_linv_f32(const FitHost& f, std::vector<float>& out);
+// The fp32 posterior's augmented observation rows (fp64 cross-term operand).
+void pack_obs_f32(const FitHost& f, std::vector<double>& out);
 void pack_linv_f64(const FitHost& f, std::vector<double>& out);
 
 // ---- EHVI boxes (host) ------------------------------------------------------
@@ -284,8 +262,8 @@ struct GPDevice {
   double s2 = 1, tau2 = 0, c = 0;
   void* buf = nullptr;        // one allocation holding everything below
   const void* linv = nullptr; // packed L^-1 (float or double)
-  const void* xs = nullptr;   // m_pad x kXsStride scaled observations (float or double); fp32 rows
-                              // hold (float)alpha_i in column d when d < kXsStride
+  const void* xs = nullptr;   // fp32: the augmented observation rows (pack_obs_f32, double);
+                              // fp64: m_pad x kXsStride scaled rows, alpha_i in column d when d < kXsStride
   const double* alpha = nullptr;  // m_pad
   const float* alpha32 = nullptr; // m_pad, float copy
   float scale32[SCOOT_MAX_DIM];

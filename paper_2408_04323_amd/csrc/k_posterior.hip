@@ -11,8 +11,8 @@
 //   1. generate: every wave computes K* for a share of the observation rows,
 //      for all candidates of the tile, straight into LDS in the B-operand
 //      order of the MFMA instruction; alpha is folded in on the way (mu);
-//   2. multiply: every wave takes whole row blocks I of V (a snake order keeps
-//      the triangular work balanced), accumulates sum_{J<=I} Linv[I,J] K*[J]
+//   2. multiply: every wave takes whole row blocks I of V (a per-SIMD row plan
+//      keeps the triangular work balanced), accumulates sum_{J<=I} Linv[I,J] K*[J]
 //      on the matrix cores (A from the packed L^-1 in L2, B from LDS), and
 //      keeps only the squared norms of its rows;
 //   3. reduce: partial norms and means of all waves are summed per candidate.
@@ -22,7 +22,8 @@
 // w_k = sqrt5 * log2(e) / l_k, u = sqrt(sum_k (w_k (x_k - X_ik))^2) equals
 // sqrt5 r log2(e), and k = (c0 + u (c1 + u c2)) 2^-u with c0 = s2,
 // c1 = s2 ln2, c2 = s2 ln2^2 / 3.  Observations arrive pre-scaled; padding rows
-// sit at coordinate 1e4 so their covariance underflows to exactly 0, and their
+// sit at coordinate 1e4 (fp64) or carry a squared norm of 1e30 (the fp32
+// augmented rows), so their covariance underflows to exactly 0, and their
 // alpha and L^-1 entries are 0.
 #include <hip/hip_runtime.h>
 
@@ -50,69 +51,72 @@ __device__ inline double partial_expectation_d(double c, double mu, double sd) {
 }
 
 // ---------------------------------------------------------------------------
-// fp32
+// fp32.  Everything runs on 16 x 16 MFMA tiles; a candidate tile is 64
+// candidates, four column tiles ct of 16.  Lane l has g = l / 16 and
+// c = l % 16.
+//
+// Phase 1, squared distances on the fp64 matrix cores: with augmented rows
+// A_i = (2 X_i, -|X_i|^2, -1) for the observations and B_x = (x, 1, |x|^2)
+// for the candidates (scaled coordinates, fp64), A_i . B_x = -|x - X_i|^2, so
+// one v_mfma_f64_16x16x4f64 chain over ceil((d + 2) / 4) steps gives -u^2
+// for 16 observations x 16 candidates, exact to double rounding (no
+// cancellation that float could see).  The observations are packed so that
+// output lane l, register r holds observation 16J + 4g + r of candidate c
+// (the instruction's own order is row g + 4r there): the lane turns its four values
+// into K* in float (sqrt, exp2, the polynomial), folds alpha into the mean,
+// and stores them as one float4 -- which is exactly the B operand the
+// triangular product reads.
+//
+// Phase 2, V = L^-1 K*^T on v_mfma_f32_16x16x4f32 over 16 x 16 blocks of the
+// triangle (executed work (nb16 + 1) / nb16 of the triangle's, against
+// (nb32 + 1) / nb32 for 32 x 32 blocks).  The contraction index of a block is
+// ordered k = 4g + s (s the MFMA step), so at step s lane l holds
+// L^-1[16I + c][16J + 4g + s] and K*[16J + 4g + s][candidate c] -- the
+// float4 phase 1 stored.  Output lane l, register r holds row 16I + 4g + r of
+// candidate c.
 // ---------------------------------------------------------------------------
 struct Post32 {
   int64_t n;
-  int d, nb;
-  float scale[SCOOT_MAX_DIM];
+  int d, nb16;
+  double scale[SCOOT_MAX_DIM];
   float c0, c1, c2;
   double s2, prior, ei_c;
-  RowPlan plan;  // row blocks of each wave and where they start in the packed inverse
-  int64_t v_ld;  // row stride of a kept V
+  RowPlan16 plan;  // 16-row blocks of each wave and where they start in the packed inverse
+  int64_t v_ld;    // row stride of a kept V
 };
 
-// Candidate coordinates (D = the exact number of dimensions, so every load is
-// unconditional and all are in flight at once); scaled once they have landed.
-template <int D>
-__device__ inline void load_coords_f32(float (&xr)[D], const float* __restrict__ row) {
+// The 16 MFMA steps of a block: four k-steps for each of the four column
+// tiles, the tiles' chains interleaved.  The next block's A (from L2 at
+// an_src) is requested first, a block ahead of its use; its B (from LDS at
+// bn_src) between the steps, not in one burst before them.
+__device__ inline void mfma_block16f(f4_t (&acc)[4], const f4_t& a, const f4_t (&b)[4], f4_t (&bn)[4],
+                                     const f4_t* bn_src, f4_t& an, const f4_t* an_src) {
+  an = *an_src;
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-  for (int q = 0; q < D; ++q) xr[q] = row[q];
+  for (int ct = 0; ct < 4; ++ct) acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[ct][0], acc[ct], 0, 0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  bn[0] = bn_src[0];
+  bn[1] = bn_src[64];
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[ct][1], acc[ct], 0, 0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  bn[2] = bn_src[128];
+  bn[3] = bn_src[192];
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[ct][2], acc[ct], 0, 0, 0);
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[ct][3], acc[ct], 0, 0, 0);
 }
-
-// Operands of one 32 x 32 block (row block I, column block J): A = four
-// 16-byte loads per lane from the packed inverse (16 steps), B = K*[J] for the
-// tile's two 32-candidate halves, eight 16-byte LDS reads per lane.
-__device__ inline void load_block32(f4_t (&a)[4], const f4_t* ap, int k) {
+__device__ inline void load_b16f(f4_t (&b)[4], const f4_t* ks, int J, int lane) {
 #pragma unroll
-  for (int s4 = 0; s4 < 4; ++s4) a[s4] = ap[(size_t)(k * 4 + s4) * 64];
-}
-__device__ inline void load_b32(f4_t (&b)[8], const f4_t* ks, int J, int lane) {
-#pragma unroll
-  for (int s4 = 0; s4 < 4; ++s4) {
-    b[2 * s4 + 0] = ks[((J * 2 + 0) * 4 + s4) * 64 + lane];
-    b[2 * s4 + 1] = ks[((J * 2 + 1) * 4 + s4) * 64 + lane];
-  }
-}
-
-// The 16 MFMA steps of a block on two accumulation chains, one per
-// 32-candidate half, issued alternately so that each MFMA waits on the one
-// before the last (measured: 1% faster than four chains summed before
-// squaring, which cost an extra add per accumulator).  FIRST (the row's block
-// J = 0) starts both chains from zero instead of from the accumulators, so
-// they need no clearing.
-template <bool FIRST>
-__device__ inline void mfma_block2(f16_t& l0, f16_t& l1, const f4_t (&a)[4], const f4_t (&b)[8]) {
-  const f16_t zero = {0};
-#pragma unroll
-  for (int s4 = 0; s4 < 2; ++s4) {
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const bool z = FIRST && s4 == 0 && t == 0;
-      l0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4][t], b[2 * s4 + 0][t], z ? zero : l0, 0, 0, 0);
-      l1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4][t], b[2 * s4 + 1][t], z ? zero : l1, 0, 0, 0);
-      l0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4 + 2][t], b[2 * (s4 + 2) + 0][t], l0, 0, 0, 0);
-      l1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s4 + 2][t], b[2 * (s4 + 2) + 1][t], l1, 0, 0, 0);
-    }
-  }
-}
-__device__ inline void mfma_block2_at(int J, f16_t& l0, f16_t& l1, const f4_t (&a)[4], const f4_t (&b)[8]) {
-  if (J == 0) mfma_block2<true>(l0, l1, a, b);
-  else mfma_block2<false>(l0, l1, a, b);
+  for (int ct = 0; ct < 4; ++ct) b[ct] = ks[(J * 4 + ct) * 64 + lane];
 }
 
 // Where V goes when it is kept (the sequential believer needs it): row-major,
-// rows = observations in their order, row stride ld = number of candidates.
+// rows = observations in their order, row stride ld.
 struct VStore {
   float* v;
   int64_t ld;
@@ -120,104 +124,95 @@ struct VStore {
   int64_t n;
 };
 
-// Completes a row block: squared norms of its V columns into sq0 / sq1, and
-// the block itself into V when kept.  The accumulators are left as they are
-// (the next row's first block overwrites them).  Accumulator register r of lane l holds
-// row 8 (r / 4) + 4 (l / 32) + r % 4 of the block, column l % 32.
+// Completes a row block: squared norms of its V columns into sq[ct], the
+// block itself into V when kept, and clears the accumulators for the next row.
 template <bool KEEP_V>
-__device__ inline void finish_row(const f16_t& l0, const f16_t& l1, float& sq0, float& sq1, const VStore& vs, int I,
-                                  int lane) {
-  float p0 = 0.0f, p1 = 0.0f;
-  const int64_t c_a = vs.c0 + (lane & 31), c_b = c_a + 32;
+__device__ inline void finish_row16(f4_t (&acc)[4], float (&sq)[4], const VStore& vs, int I, int lane) {
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const float v0 = l0[r], v1 = l1[r];
-    if constexpr (KEEP_V) {
-      const int64_t row = 32 * I + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      if (c_a < vs.n) vs.v[row * vs.ld + c_a] = v0;
-      if (c_b < vs.n) vs.v[row * vs.ld + c_b] = v1;
+  for (int ct = 0; ct < 4; ++ct) {
+    float p = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float v = acc[ct][r];
+      if constexpr (KEEP_V) {
+        const int64_t cand = vs.c0 + ct * 16 + (lane & 15);
+        const int64_t row = 16 * I + 4 * (lane >> 4) + r;
+        if (cand < vs.n) vs.v[row * vs.ld + cand] = v;
+      }
+      p = fmaf(v, v, p);
     }
-    p0 = fmaf(v0, v0, p0);
-    p1 = fmaf(v1, v1, p1);
+    sq[ct] += p;
+    acc[ct] = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
   }
-  sq0 += p0;
-  sq1 += p1;
 }
 
 // One tile's pass over the wave's blocks, one block of read-ahead of both
-// operands in two fixed buffer sets.  The A stream is the same for every tile,
-// so its read-ahead wraps: on entry ax holds the wave's first block, and on
-// exit it holds it again for the next tile.  B (K* of this tile) is read
-// ahead only within the tile; past the last block it reads K*[0], unused.
+// operands in two fixed register sets.  The A stream is the same for every
+// tile, so its read-ahead wraps: on entry ax holds the wave's first block,
+// and on exit it holds it again for the next tile.
 template <bool KEEP_V>
-__device__ inline void wave_tile32(const f4_t* __restrict__ ap, const f4_t* ks, uint64_t rows, int count,
-                                   int lane, f4_t (&ax)[4], float& sq0, float& sq1, const VStore& vs) {
-  // every row starts at J = 0, whose block writes the accumulators without
-  // reading them: no clearing needed, only a defined (frozen) initial value
-  f16_t l0 = __builtin_nondeterministic_value(l0), l1 = l0;
-  // (I, J): row block and column block of the block being computed; the
-  // wave's remaining rows sit in `rows`, kRowBits each (0 past the last).
-  int I = (int)(rows & 31), J = 0;
+__device__ inline void wave_tile16f(const f4_t* __restrict__ ap, const f4_t* ks, uint64_t lo, uint64_t hi, int count,
+                                    int lane, f4_t& ax, float (&sq)[4], const VStore& vs) {
+  // the accumulators start each row at zero (finish_row16 clears them)
+  f4_t acc[4];
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) acc[ct] = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  constexpr uint64_t kMask = (1u << kRowBits16) - 1;
+  int I = (int)(lo & kMask), J = 0;
   auto next_j = [&](int j, int i) { return j == i ? 0 : j + 1; };
   auto advance = [&]() {
     if (J == I) {
-      finish_row<KEEP_V>(l0, l1, sq0, sq1, vs, I, lane);
+      finish_row16<KEEP_V>(acc, sq, vs, I, lane);
       J = 0;
-      rows >>= kRowBits;
-      I = (int)(rows & 31);
+      lo = (lo >> kRowBits16) | (hi << (64 - kRowBits16));
+      hi >>= kRowBits16;
+      I = (int)(lo & kMask);
     } else {
       ++J;
     }
   };
-  f4_t ay[4], bx[8], by[8];
-  load_b32(bx, ks, 0, lane);
+  f4_t ay, bx[4], by[4];
+  load_b16f(bx, ks, 0, lane);
+  const f4_t* kl = ks + lane;
   int k = 0;
   for (; k + 1 < count; k += 2) {
-    load_block32(ay, ap, k + 1);
-    load_b32(by, ks, next_j(J, I), lane);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_block2_at(J, l0, l1, ax, bx);
+    mfma_block16f(acc, ax, bx, by, kl + next_j(J, I) * 256, ay, ap + (size_t)(k + 1) * 64);
     __builtin_amdgcn_sched_barrier(0);
     advance();
-    load_block32(ax, ap, k + 2 < count ? k + 2 : 0);
-    load_b32(bx, ks, next_j(J, I), lane);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_block2_at(J, l0, l1, ay, by);
+    mfma_block16f(acc, ay, by, bx, kl + next_j(J, I) * 256, ax, ap + (size_t)(k + 2 < count ? k + 2 : 0) * 64);
     __builtin_amdgcn_sched_barrier(0);
     advance();
   }
   if (k < count) {
-    load_block32(ay, ap, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_block2_at(J, l0, l1, ax, bx);
+    mfma_block16f(acc, ax, bx, by, kl + next_j(J, I) * 256, ay, ap);
     __builtin_amdgcn_sched_barrier(0);
     advance();
-#pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) ax[s4] = ay[s4];
+    ax = ay;
   }
 }
 
 // Persistent: workgroup g takes tiles g, g + G, g + 2G, ... (G = grid size),
 // so the inverse-factor stream and the next tile's coordinates are in flight
-// across tile boundaries.
+// across tile boundaries.  Phase 1: wave w takes the 16-observation blocks
+// J = w, w + WAVES, ...  Phase 2: the wave's row blocks from the plan.
+// Phase 3: partial norms and means summed per candidate.
 template <int WAVES, int D, bool KEEP_V>
 __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
-    const float* __restrict__ Xc, const f4_t* __restrict__ linv, const float* __restrict__ xs,
+    const float* __restrict__ Xc, const f4_t* __restrict__ linv, const double* __restrict__ xq,
     const float* __restrict__ alpha, float* __restrict__ mu_out, float* __restrict__ sd_out,
     float* __restrict__ ei_out, float* __restrict__ v_out, const Post32 a) {
+  constexpr int S = (D + 2 + 3) / 4;  // fp64 MFMA steps of the augmented rows
   extern __shared__ __align__(16) unsigned char smem[];
-  f4_t* ks = reinterpret_cast<f4_t*>(smem);  // [nb][2 ct][4 s4][64 lanes] float4
-  const int nb = a.nb;
-  float* sig_red = reinterpret_cast<float*>(ks + (size_t)nb * 2 * 4 * 64);  // [WAVES][2 h][64]
-  float* mu_red = sig_red + WAVES * 2 * 64;                                  // [WAVES][64]
+  f4_t* ks = reinterpret_cast<f4_t*>(smem);  // [nb16][4 ct][64 lanes] float4
+  const int nb16 = a.nb16;
+  float* sig_red = reinterpret_cast<float*>(ks + (size_t)nb16 * 4 * 64);  // [WAVES][4 ct][16]
+  float* mu_red = sig_red + WAVES * 64;                                    // [WAVES][4 ct][16]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
+  const int g = lane >> 4, c = lane & 15;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int64_t n_tiles = (a.n + 63) >> 6;
-  static_assert(WAVES % 2 == 0, "phase 1 relies on an even wave count");
-  // float4 loads per observation row: the D coordinates and, below 16, alpha
-  constexpr int kRowVec = D < kXsStride ? (D + 1 + 3) / 4 : kXsStride / 4;
 
   // Plan entry of this wave.  With 8 waves, entries p and p + 4 are meant to
   // share a SIMD: each wave takes simd + 4 * (its arrival order on the SIMD),
@@ -236,94 +231,134 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
     if (on_simd[0] == 2 && on_simd[1] == 2 && on_simd[2] == 2 && on_simd[3] == 2) p = simd + 4 * slot;
     p = __builtin_amdgcn_readfirstlane(p);
   }
-  const uint64_t rows = a.plan.rows[p];
+  const uint64_t rows_lo = a.plan.lo[p], rows_hi = a.plan.hi[p];
   const int count = a.plan.blk_start[p + 1] - a.plan.blk_start[p];
-  const f4_t* ap = linv + (size_t)a.plan.blk_start[p] * 4 * 64 + lane;
-  f4_t ax[4];
-  if (count > 0) load_block32(ax, ap, 0);
+  const f4_t* ap = linv + (size_t)a.plan.blk_start[p] * 64 + lane;
+  f4_t ax = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (count > 0) ax = ap[0];
+
+  // The lane's components of the candidates' augmented rows: step s of the
+  // cross-term chain reads component k = 4s + g.
+  double wk[S];
+#pragma unroll
+  for (int s = 0; s < S; ++s) wk[s] = 4 * s + g < D ? a.scale[4 * s + g] : 0.0;
 
   int64_t tile = blockIdx.x;
-  float xr[D];
-  load_coords_f32<D>(xr, Xc + min(tile * 64 + lane, a.n - 1) * D);
+  float xr[D];  // candidate tile * 64 + lane, for its squared norm
+  float xb[4][S];  // component 4s + g of candidate 16 ct + c (raw float)
+  auto load_tile = [&](int64_t t) {
+    const int64_t own = min(t * 64 + lane, a.n - 1);
+#pragma unroll
+    for (int q = 0; q < D; ++q) xr[q] = Xc[own * D + q];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      const int64_t cand = min(t * 64 + ct * 16 + c, a.n - 1);
+#pragma unroll
+      for (int s = 0; s < S; ++s) xb[ct][s] = 4 * s + g < D ? Xc[cand * D + min(4 * s + g, D - 1)] : 0.0f;
+    }
+  };
+  load_tile(tile);
 
   for (; tile < n_tiles; tile += gridDim.x) {
     const int64_t c0 = tile * 64;
-    float xc[D];
+    // squared norm of the lane's own candidate, then the B operands
+    double nrm = 0.0;
 #pragma unroll
-    for (int q = 0; q < D; ++q) xc[q] = xr[q] * a.scale[q];
+    for (int q = 0; q < D; ++q) {
+      const double t = (double)xr[q] * a.scale[q];
+      nrm = fma(t, t, nrm);
+    }
+    double bq[4][S];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      const double nc = __shfl(nrm, ct * 16 + c);
+#pragma unroll
+      for (int s = 0; s < S; ++s) {
+        const int k = 4 * s + g;
+        bq[ct][s] = k < D ? (double)xb[ct][s] * wk[s] : (k == D ? 1.0 : (k == D + 1 ? nc : 0.0));
+      }
+    }
     // next tile's coordinates, in flight during this one
     const int64_t next = tile + gridDim.x;
-    if (next < n_tiles) load_coords_f32<D>(xr, Xc + min(next * 64 + lane, a.n - 1) * D);
+    if (next < n_tiles) load_tile(next);
 
-    // ---- phase 1: K* for candidate c0 + lane, rows of this wave's groups --
-    // Group G = 8J + 2 s4 + h covers rows 32J + 8 s4 + h + 2t = 4G - 3h + 2t,
-    // t = 0..3, of block J; lane l writes them as one float4 to B-operand slot
-    // (J, ct = l/32, s4, h*32 + l%32).  WAVES is even, so h = wave & 1 for all
-    // of a wave's groups and its rows advance by 4 WAVES per group: one
-    // running row pointer, the four rows at fixed offsets from it.
-    float mu_part = 0.0f;
-    const int ngroups = nb * 8;
-    const int hw = wave & 1;
-    const float* xg = xs + (size_t)(4 * wave - 3 * hw) * kXsStride;
-    for (int G = wave; G < ngroups; G += WAVES, xg += 4 * WAVES * kXsStride) {
-      const int J = G >> 3, s4 = (G >> 1) & 3;
-      f4_t kv;
+    // ---- phase 1: K* of observation blocks J = wave, wave + WAVES, ... ---
+    // The block's operands are loaded one block ahead; its four column
+    // tiles' chains are issued interleaved (independent accumulators), then
+    // their values are turned into K*.
+    float mu_part[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    double aq[S];
+    f4_t al = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (wave < nb16) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const float* xo = xg + 2 * t * kXsStride;
-        float xv[kRowVec * 4];
+      for (int s = 0; s < S; ++s) aq[s] = xq[((size_t)wave * S + s) * 64 + lane];
+      al = *reinterpret_cast<const f4_t*>(alpha + 16 * wave + 4 * g);
+    }
+    for (int J = wave; J < nb16; J += WAVES) {
+      d4_t cr[4];
 #pragma unroll
-        for (int r = 0; r < kRowVec; ++r) {
-          const f4_t v4 = reinterpret_cast<const f4_t*>(xo)[r];
+      for (int ct = 0; ct < 4; ++ct) cr[ct] = d4_t{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-          for (int c = 0; c < 4; ++c) xv[4 * r + c] = v4[c];
+      for (int s = 0; s < S; ++s)
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) cr[ct] = __builtin_amdgcn_mfma_f64_16x16x4f64(aq[s], bq[ct][s], cr[ct], 0, 0, 0);
+      const f4_t alj = al;
+      const int Jn = J + WAVES < nb16 ? J + WAVES : J;
+#pragma unroll
+      for (int s = 0; s < S; ++s) aq[s] = xq[((size_t)Jn * S + s) * 64 + lane];
+      al = *reinterpret_cast<const f4_t*>(alpha + 16 * Jn + 4 * g);
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct) {
+        f4_t kv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float u = __builtin_amdgcn_sqrtf(fmaxf((float)(-cr[ct][r]), 0.0f));
+          const float kval = fmaf(u, fmaf(u, a.c2, a.c1), a.c0) * __builtin_amdgcn_exp2f(-u);
+          kv[r] = kval;
+          mu_part[ct] = fmaf(kval, alj[r], mu_part[ct]);
         }
-        float acc = 0.0f;
-#pragma unroll
-        for (int k = 0; k < D; ++k) {
-          float df = xc[k] - xv[k];
-          acc = fmaf(df, df, acc);
-        }
-        float u = __builtin_amdgcn_sqrtf(acc);
-        float e = __builtin_amdgcn_exp2f(-u);
-        float kval = fmaf(u, fmaf(u, a.c2, a.c1), a.c0) * e;
-        kv[t] = kval;
-        // alpha_i rides in column D of the row when there is room
-        const float al = D < kXsStride ? xv[D < kXsStride ? D : 0] : alpha[4 * G - 3 * hw + 2 * t];
-        mu_part = fmaf(kval, al, mu_part);
+        ks[(J * 4 + ct) * 64 + lane] = kv;
       }
-      ks[((J * 2 + (lane >> 5)) * 4 + s4) * 64 + hw * 32 + (lane & 31)] = kv;
     }
     __syncthreads();
 
-    // ---- phase 2: this wave's row blocks of V = L^-1 K*^T on the matrix cores
-    float sq0 = 0.0f, sq1 = 0.0f;
+    // ---- phase 2: this wave's row blocks of V = L^-1 K*^T -----------------
+    float sq[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     if (count > 0) {
       const VStore vs{v_out, a.v_ld, c0, a.n};
-      wave_tile32<KEEP_V>(ap, ks, rows, count, lane, ax, sq0, sq1, vs);
+      wave_tile16f<KEEP_V>(ap, ks, rows_lo, rows_hi, count, lane, ax, sq, vs);
     }
 
-    // ---- phase 3: reduce over waves and row halves, write ----------------
-    // Accumulator lane l holds column l % 32 of its tile (ct = 0 / 1).
-    const int h = lane >> 5;
-    sig_red[(wave * 2 + h) * 64 + (lane & 31)] = sq0;
-    sig_red[(wave * 2 + h) * 64 + 32 + (lane & 31)] = sq1;
-    mu_red[wave * 64 + lane] = mu_part;
+    // ---- phase 3: reduce over the four lane rows, the waves, write ---------
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      sq[ct] += __shfl_xor(sq[ct], 16);
+      sq[ct] += __shfl_xor(sq[ct], 32);
+      mu_part[ct] += __shfl_xor(mu_part[ct], 16);
+      mu_part[ct] += __shfl_xor(mu_part[ct], 32);
+    }
+    if (g == 0) {
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct) {
+        sig_red[(wave * 4 + ct) * 16 + c] = sq[ct];
+        mu_red[(wave * 4 + ct) * 16 + c] = mu_part[ct];
+      }
+    }
     __syncthreads();
     if (tid < 64) {
-      const int64_t c = c0 + tid;
-      if (c < a.n) {
+      const int64_t cand = c0 + tid;
+      if (cand < a.n) {
         double ss = 0.0, mm = 0.0;
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) {
-          ss += (double)sig_red[(w * 2 + 0) * 64 + tid] + (double)sig_red[(w * 2 + 1) * 64 + tid];
+          ss += (double)sig_red[w * 64 + tid];
           mm += (double)mu_red[w * 64 + tid];
         }
         const double sd = sqrt(fmax(a.s2 - ss, 0.0));
         const double mu = a.prior + mm;
-        mu_out[c] = (float)mu;
-        sd_out[c] = (float)sd;
-        if (ei_out) ei_out[c] = (float)partial_expectation_d(a.ei_c, (double)(float)mu, (double)(float)sd);
+        mu_out[cand] = (float)mu;
+        sd_out[cand] = (float)sd;
+        if (ei_out) ei_out[cand] = (float)partial_expectation_d(a.ei_c, (double)(float)mu, (double)(float)sd);
       }
     }
   }
@@ -335,7 +370,8 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
 // lane l holds Linv[16I + l%16][16J + 4s + l/16] and B lane l holds
 // K*[16J + 4s + l/16][16ct + l%16]; K* is stored as (J, ct, s/2, lane)
 // double2, component s%2.  Accumulator register r of lane l holds row
-// 4(l/16) + r, column l%16 of its tile.  Same three phases and persistent
+// l/16 + 4r, column l%16 of its tile (only column sums of squares are taken,
+// so the row order does not matter here).  Same three phases and persistent
 // loop as the fp32 kernel.
 // ---------------------------------------------------------------------------
 struct Post64 {
@@ -346,7 +382,7 @@ struct Post64 {
   double s2, prior, ei_c;
   int warp;  // candidates through kumaraswamy(x, wa, wb) first
   double wa[SCOOT_MAX_DIM], wb[SCOOT_MAX_DIM];
-  RowPlan64 plan;  // 16-row blocks
+  RowPlan16 plan;  // 16-row blocks
 };
 
 __device__ inline void load_block16(d2_t (&a)[2], const d2_t* ap, int k) {
@@ -362,7 +398,8 @@ __device__ inline void load_b16(d2_t (&b)[4], const d2_t* ks, int J, int lane) {
 }
 
 // The 4 steps of a block on two chains (one per 16-candidate half), issued
-// alternately; FIRST starts both from zero (see mfma_block2).
+// alternately; FIRST (the row's block J = 0) starts both from zero, so they need no
+// clearing.
 template <bool FIRST>
 __device__ inline void mfma_block16(d4_t& l0, d4_t& l1, const d2_t (&a)[2], const d2_t (&b)[4]) {
   const d4_t zero = {0};
@@ -381,12 +418,12 @@ __device__ inline void mfma_block16_at(int J, d4_t& l0, d4_t& l1, const d2_t (&a
   else mfma_block16<false>(l0, l1, a, b);
 }
 
-// One tile's pass over the wave's blocks; the same schedule as wave_tile32
+// One tile's pass over the wave's blocks; the same schedule as wave_tile16f
 // (one block of read-ahead, the A stream wrapping to the next tile).
 __device__ inline void wave_tile16(const d2_t* __restrict__ ap, const d2_t* ks, uint64_t lo, uint64_t hi, int count,
                                    int lane, d2_t (&ax)[2], double& sq0, double& sq1) {
   d4_t l0 = __builtin_nondeterministic_value(l0), l1 = l0;
-  constexpr uint64_t kMask = (1u << kRowBits64) - 1;
+  constexpr uint64_t kMask = (1u << kRowBits16) - 1;
   int I = (int)(lo & kMask), J = 0;
   auto next_j = [&](int j, int i) { return j == i ? 0 : j + 1; };
   auto advance = [&]() {
@@ -400,8 +437,8 @@ __device__ inline void wave_tile16(const d2_t* __restrict__ ap, const d2_t* ks, 
       sq0 += p0;
       sq1 += p1;
       J = 0;
-      lo = (lo >> kRowBits64) | (hi << (64 - kRowBits64));
-      hi >>= kRowBits64;
+      lo = (lo >> kRowBits16) | (hi << (64 - kRowBits16));
+      hi >>= kRowBits16;
       I = (int)(lo & kMask);
     } else {
       ++J;
@@ -623,14 +660,14 @@ template <int WAVES, int D, bool KEEP_V>
 int run32(const GPDevice& g, const float* Xc, int64_t n, float* mu, float* sd, float* ei, float* v_out,
           const Post32& a, hipStream_t s) {
   // K* tile, per-wave partial norms and means, four SIMD counters
-  const size_t lds = (size_t)g.nb * 2 * 4 * 64 * 16 + WAVES * 2 * 64 * 4 + WAVES * 64 * 4 + 16;
+  const size_t lds = (size_t)a.nb16 * 4 * 64 * 16 + 2 * WAVES * 64 * 4 + 16;
   auto kern = posterior_f32_kernel<WAVES, D, KEEP_V>;
   const int rc = allow_full_lds((const void*)kern, "posterior");
   if (rc != SCOOT_OK) return rc;
   const int64_t grid = persistent_grid((const void*)kern, WAVES * 64, lds, (n + 63) / 64);
   if (grid < 1) return fail(SCOOT_ERR_DEVICE, "posterior: workgroup does not fit on a compute unit");
   hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(WAVES * 64), lds, s, Xc,
-                     (const f4_t*)g.linv, (const float*)g.xs, g.alpha32, mu, sd, ei, v_out, a);
+                     (const f4_t*)g.linv, (const double*)g.xs, g.alpha32, mu, sd, ei, v_out, a);
   return SCOOT_OK;
 }
 
@@ -638,7 +675,7 @@ template <int WAVES, int D>
 int run64(const GPDevice& g, const float* Xc, int64_t n, double* mu, double* sd, double* ei,
           const Post64& a, hipStream_t s) {
   // K* tile, per-wave partial norms and means, four SIMD counters
-  const int nb16 = g.m_pad / kBlk64;
+  const int nb16 = g.m_pad / kBlk16;
   const size_t lds = (size_t)nb16 * 2 * 2 * 64 * 16 + WAVES * 4 * 32 * 8 + WAVES * 2 * 32 * 8 + 16;
   auto kern = posterior_f64_kernel<WAVES, D>;
   const int rc = allow_full_lds((const void*)kern, "posterior");
@@ -679,18 +716,18 @@ int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, vo
     Post32 a{};
     a.n = n;
     a.d = g.d;
-    a.nb = g.nb;
-    for (int k = 0; k < SCOOT_MAX_DIM; ++k) a.scale[k] = g.scale32[k];
+    a.nb16 = g.m_pad / kBlk16;
+    for (int k = 0; k < SCOOT_MAX_DIM; ++k) a.scale[k] = g.scale64[k];
     a.c0 = g.coef32[0];
     a.c1 = g.coef32[1];
     a.c2 = g.coef32[2];
     a.s2 = g.s2;
     a.prior = g.c;
     a.ei_c = ei_c ? *ei_c : 0.0;
-    a.plan = plan_rows(g.nb, posterior_waves(g.nb));
+    a.plan = plan_rows16(a.nb16, posterior_waves(g.nb));
     a.v_ld = v_ld > 0 ? v_ld : n;
     for (int e = 0; e < 8; ++e)
-      if (a.plan.nrows[e] * kRowBits > 64) return fail(SCOOT_ERR_UNSUPPORTED, "posterior: row plan does not pack");
+      if (a.plan.nrows[e] > kMaxRows16) return fail(SCOOT_ERR_UNSUPPORTED, "posterior: row plan does not pack");
     float* e = ei_c ? (float*)ei : nullptr;
     rc = by_d_rec<1>(g.d, [&](auto Dc) {
       constexpr int D = decltype(Dc)::value;
@@ -710,10 +747,10 @@ int launch_posterior(const GPDevice& g, const float* Xc, int64_t n, void* mu, vo
       a.wa[k] = g.warp_a[k];
       a.wb[k] = g.warp_b[k];
     }
-    a.nb16 = g.m_pad / kBlk64;
-    a.plan = plan_rows64(a.nb16, posterior_waves(g.nb));
+    a.nb16 = g.m_pad / kBlk16;
+    a.plan = plan_rows16(a.nb16, posterior_waves(g.nb));
     for (int e = 0; e < 8; ++e)
-      if (a.plan.nrows[e] > kMaxRows64) return fail(SCOOT_ERR_UNSUPPORTED, "posterior: row plan does not pack");
+      if (a.plan.nrows[e] > kMaxRows16) return fail(SCOOT_ERR_UNSUPPORTED, "posterior: row plan does not pack");
     for (int k = 0; k < SCOOT_MAX_DIM; ++k) a.scale[k] = g.scale64[k];
     a.c0 = g.coef64[0];
     a.c1 = g.coef64[1];
