@@ -377,9 +377,10 @@ def bench_mace(args):
 def bench_suggest(args):
     """One SUGGEST of Algorithm 1 on the workload's observations (every draw,
     crashed ones included), the pool as large as the workload's, k = its q.
-    Wall time per call (host steps included), and the parts timed on their
-    own: hyperparameter search per objective, forest training, pool
-    generation, scoring pass."""
+    Wall time per call (host steps included) with the likelihood search on the
+    device (the default) and, for comparison, on the host; and the parts timed
+    on their own: hyperparameter search per objective (device and host, one
+    at a time and side by side), forest training, pool generation."""
     import numpy as np
     import torch
 
@@ -398,8 +399,8 @@ def bench_suggest(args):
     space = dict(levels=levels(c), poly=poly, vinit=vinit, A=A, b=b)
     kw = dict(k=k, delta=w["delta"], pool_size=n, n_trees=c["trees"], max_depth=c["depth"], t=max(1, w["m"] // k))
 
-    def call():
-        out = S.suggest(X_obs, Y_obs, valid, space, **kw)
+    def call(host_search=False):
+        out = S.suggest(X_obs, Y_obs, valid, space, host_search=host_search, **kw)
         torch.cuda.synchronize()
         return out
 
@@ -409,6 +410,11 @@ def bench_suggest(args):
     for _ in range(args.steps):
         x, src, theta = call()
     ms = (time.perf_counter() - t0) / args.steps * 1e3
+    call(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        x_h, src_h, theta_h = call(True)
+    ms_host = (time.perf_counter() - t0) / args.steps * 1e3
 
     parts = {}
     ok = valid != 0
@@ -417,21 +423,25 @@ def bench_suggest(args):
     hi = np.log(np.array([10.0] * d + [20.0, 1.0]))
     th0 = np.log(np.array([0.5] * d + [1.0, 1e-3]))
     # the searches alone, one objective at a time and side by side on threads
-    # (as the step runs them)
-    iters, one = [], []
-    for j in range(p):
-        t0 = time.perf_counter()
-        iters.append(S.gp_mle(X_obs[ok], Ys[:, j], th0, lo, hi)[2])
-        one.append((time.perf_counter() - t0) * 1e3)
-    parts["mle_each_objective_alone"] = one
+    # (as the step runs them; on the device each with a stream of its own)
     import threading
-    threads = [threading.Thread(target=S.gp_mle, args=(X_obs[ok], Ys[:, j], th0, lo, hi)) for j in range(p)]
-    t0 = time.perf_counter()
-    for t in threads:
-        t.start()
-    for t in threads:
-        t.join()
-    parts["mle_objectives_side_by_side"] = (time.perf_counter() - t0) * 1e3
+    streams = [torch.cuda.Stream() for _ in range(p)]
+    for name, fn in (("device", lambda j: S.gp_mle_device(X_obs[ok], Ys[:, j], th0, lo, hi, stream=streams[j].cuda_stream)),
+                     ("host", lambda j: S.gp_mle(X_obs[ok], Ys[:, j], th0, lo, hi))):
+        iters, one = [], []
+        for j in range(p):
+            t0 = time.perf_counter()
+            iters.append(fn(j)[2])
+            one.append((time.perf_counter() - t0) * 1e3)
+        parts[f"mle_{name}_each_objective_alone"] = one
+        parts[f"mle_{name}_iterations"] = iters
+        threads = [threading.Thread(target=fn, args=(j,)) for j in range(p)]
+        t0 = time.perf_counter()
+        for t in threads:
+            t.start()
+        for t in threads:
+            t.join()
+        parts[f"mle_{name}_objectives_side_by_side"] = (time.perf_counter() - t0) * 1e3
     t0 = time.perf_counter()
     S.forest_train_create(X_obs, valid.astype(np.float64), c["trees"], c["depth"], seed=0)
     parts["forest_train"] = (time.perf_counter() - t0) * 1e3
@@ -449,8 +459,8 @@ def bench_suggest(args):
                       "warmup": args.warmup, "higher_is_better": True, "dtype": "f32", "data": "synthetic",
                       "config": {"workload": f"{c['name']}: {len(X_obs)} observations ({int(ok.sum())} valid) "
                                              f"d={d} p={p} pool={n} k={k} trees={c['trees']} depth={c['depth']}",
-                                 "parts_ms": parts, "mle_iterations": iters,
-                                 "sources": src.tolist()}}), flush=True)
+                                 "ms_per_step_host_search": ms_host, "parts_ms": parts,
+                                 "sources": src.tolist(), "sources_host_search": src_h.tolist()}}), flush=True)
 
 
 def cpu_baseline(w, seconds):

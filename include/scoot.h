@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define SCOOT_ABI_VERSION 3
+#define SCOOT_ABI_VERSION 4
 
 typedef enum scoot_dtype { SCOOT_F32 = 0, SCOOT_F64 = 1 } scoot_dtype;
 
@@ -167,6 +167,31 @@ int scoot_gp_nll_warp(const double* X, const double* y, int m, int d, scoot_kern
 int scoot_gp_mle_warp(const double* X, const double* y, int m, int d, scoot_kernel kernel, double prior_mean,
                       const double* lower, const double* upper, int max_iter, double* theta, double* nll,
                       int* iterations);
+
+/* ---------------------------------------------------------------------------
+ * The likelihood of Sec. 4.3 evaluated on the current device (fp64), and the
+ * search with every evaluation there.  Arguments as scoot_gp_nll /
+ * scoot_gp_mle (host pointers in and out; the library uploads X and y once
+ * and reads back the value and gradient per evaluation); learn_warp = 0:
+ * theta [d + 2] with the fixed warp_a/warp_b (nullable); learn_warp = 1:
+ * theta, lower, upper [3d + 2] as in scoot_gp_nll_warp, warp_a and warp_b
+ * must be NULL.  The work of an evaluation runs on `stream` (NULL: the null
+ * stream) and the call returns after it: K and its Cholesky factor by
+ * 16 x 16 blocks (products on the fp64 matrix cores), K^-1 from the factor,
+ * alpha, the NLL, then the gradient's trace terms.  Results agree with the
+ * host calls to rounding (same definitions, other summation order).  The
+ * search is the host's L-BFGS (same stopping rules) and allocates its device
+ * work space (about 16 m^2 bytes) once per call.
+ * Errors: as scoot_gp_nll / scoot_gp_mle; INVALID_ARG also for learn_warp
+ *   with a fixed warp given; DEVICE for a failed allocation or launch.
+ * ------------------------------------------------------------------------- */
+int scoot_gp_nll_device(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+                        const double* warp_b, double prior_mean, int learn_warp, const double* theta, double* nll,
+                        double* grad, void* stream);
+int scoot_gp_mle_device(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+                        const double* warp_b, double prior_mean, int learn_warp, const double* lower,
+                        const double* upper, int max_iter, double* theta, double* nll, int* iterations,
+                        void* stream);
 
 /* ---------------------------------------------------------------------------
  * Posterior (device).  Eq. 4 and Eq. 5 of Sec. 4.3 at every candidate:
@@ -504,7 +529,10 @@ int scoot_known_constraints(const float* Xc, int64_t n, int d, const double* A, 
  *   Matern-3/2 with input warping), each warp parameter in [0.2, 5] starting
  *   from warp_a / warp_b when given, else from the identity a = b = 1; theta
  *   then has 3d + 2 entries per objective (theta_lower/upper/start keep their
- *   d + 2); 0: the warping is fixed (or absent) as given.
+ *   d + 2); 0: the warping is fixed (or absent) as given; host_search 0: the
+ *   likelihood evaluations of the search run on the device
+ *   (scoot_gp_mle_device, each objective on a stream of its own, the
+ *   objectives side by side), 1: on the host (scoot_gp_mle).
  *
  * scoot_suggest: X_obs [n_obs*d] observed configurations (finite), Y_obs
  *   [n_obs*p] their objective values (minimised; read only where valid),
@@ -566,6 +594,7 @@ typedef struct scoot_suggest_opts {
   uint64_t pick_seed;
   const double* ref;
   int learn_warp;
+  int host_search;
 } scoot_suggest_opts;
 
 int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid, int n_obs, int p,

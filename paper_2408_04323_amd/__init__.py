@@ -199,6 +199,48 @@ def gp_mle_warp(X, y, theta0, lower, upper, kernel="matern32", prior_mean=0.0, m
     return th, nll.value, it.value
 
 
+def gp_nll_device(X, y, theta, kernel="matern52", warp_a=None, warp_b=None, prior_mean=0.0, learn_warp=False,
+                  stream=None):
+    """gp_nll (learn_warp=False) or gp_nll_warp (learn_warp=True) evaluated on
+    the current device."""
+    X, pX = _host(X, np.float64)
+    y, py = _host(y, np.float64)
+    m, d = X.shape
+    a, b, pa, pb = _warp(warp_a, warp_b, d)
+    th, pt = _host(theta, np.float64)
+    P = 3 * d + 2 if learn_warp else d + 2
+    if th.size != P:
+        raise ValueError(f"theta must have {P} entries")
+    nll = C.c_double(0.0)
+    grad = np.zeros(P)
+    check(lib().scoot_gp_nll_device(pX, py, m, d, _kernel(kernel), pa, pb, prior_mean, int(bool(learn_warp)), pt,
+                                    C.byref(nll), grad.ctypes.data_as(C.POINTER(C.c_double)), _stream(stream)),
+          "gp_nll_device")
+    return nll.value, grad
+
+
+def gp_mle_device(X, y, theta0, lower, upper, kernel="matern52", warp_a=None, warp_b=None, prior_mean=0.0,
+                  learn_warp=False, max_iter=200, stream=None):
+    """gp_mle / gp_mle_warp with every likelihood evaluation on the current
+    device.  Returns (theta, nll, iterations)."""
+    X, pX = _host(X, np.float64)
+    y, py = _host(y, np.float64)
+    m, d = X.shape
+    a, b, pa, pb = _warp(warp_a, warp_b, d)
+    P = 3 * d + 2 if learn_warp else d + 2
+    th = np.array(theta0, dtype=np.float64).copy()
+    lo, plo = _host(lower, np.float64)
+    hi, phi = _host(upper, np.float64)
+    if not (th.size == lo.size == hi.size == P):
+        raise ValueError(f"theta0, lower and upper must have {P} entries")
+    nll = C.c_double(0.0)
+    it = C.c_int(0)
+    check(lib().scoot_gp_mle_device(pX, py, m, d, _kernel(kernel), pa, pb, prior_mean, int(bool(learn_warp)), plo,
+                                    phi, max_iter, th.ctypes.data_as(C.POINTER(C.c_double)), C.byref(nll),
+                                    C.byref(it), _stream(stream)), "gp_mle_device")
+    return th, nll.value, it.value
+
+
 # --------------------------------------------------------------------- posterior
 def posterior(gp, Xc, mu=None, sigma=None, stream=None):
     """mu, sigma of the latent f at every row of Xc (n x d float32 device)."""
@@ -636,19 +678,21 @@ class _SuggestOpts(C.Structure):
                 ("theta_upper", C.POINTER(C.c_double)), ("theta_start", C.POINTER(C.c_double)),
                 ("mle_max_iter", C.c_int), ("n_trees", C.c_int), ("max_depth", C.c_int),
                 ("forest_seed", C.c_uint64), ("bootstrap", C.c_int), ("xi", C.c_double), ("t", C.c_int),
-                ("pick_seed", C.c_uint64), ("ref", C.POINTER(C.c_double)), ("learn_warp", C.c_int)]
+                ("pick_seed", C.c_uint64), ("ref", C.POINTER(C.c_double)), ("learn_warp", C.c_int),
+                ("host_search", C.c_int)]
 
 
 def suggest(X_obs, Y_obs, valid, space, k, delta=0.5, pool_size=262144, pool_skip=0, kernel="matern52",
             dtype="f32", warp_a=None, warp_b=None, theta_lower=None, theta_upper=None, theta_start=None,
             mle_max_iter=0, n_trees=64, max_depth=10, forest_seed=0, bootstrap=True, xi=1e-4, t=1, pick_seed=0,
-            ref=None, stream=None, learn_warp=False):
+            ref=None, stream=None, learn_warp=False, host_search=False):
     """One SUGGEST of Algorithm 1 (scoot_suggest).  ``space`` is a dict with
     ``levels``, ``poly``, ``vinit`` and optionally ``A``, ``b`` (known
     constraints).  X_obs (n_obs, d), Y_obs (n_obs, p) minimised, valid (n_obs,)
     host arrays; per-objective options (warps (p, d), theta bounds (p, d + 2))
     host arrays; learn_warp: the warping is learned with the other
-    hyperparameters.  Returns (x (n_out, d) float64, source (n_out,) int32,
+    hyperparameters; host_search: the likelihood search evaluates on the host
+    instead of the device.  Returns (x (n_out, d) float64, source (n_out,) int32,
     theta (p, d + 2), or (p, 3d + 2) with learn_warp, float64)."""
     pu, vi, lv, d = _sobol_inputs(space["poly"], space["vinit"], space["levels"])
     A, bb, r = _constraint_inputs(space.get("A"), space.get("b"), d)
@@ -677,7 +721,7 @@ def suggest(X_obs, Y_obs, valid, space, k, delta=0.5, pool_size=262144, pool_ski
                       arr(warp_a, (p, d)), arr(warp_b, (p, d)), arr(theta_lower, (p, d + 2)),
                       arr(theta_upper, (p, d + 2)), arr(theta_start, (p, d + 2)), int(mle_max_iter), int(n_trees),
                       int(max_depth), int(forest_seed), int(bool(bootstrap)), float(xi), int(t), int(pick_seed),
-                      arr(ref, (p,)), int(bool(learn_warp)))
+                      arr(ref, (p,)), int(bool(learn_warp)), int(bool(host_search)))
     x = np.zeros((k, d), dtype=np.float64)
     src = np.zeros(k, dtype=np.int32)
     theta = np.zeros((p, 3 * d + 2 if learn_warp else d + 2), dtype=np.float64)

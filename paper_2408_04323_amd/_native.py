@@ -31,6 +31,10 @@ SIGNATURES = {
                      P_int],
     "scoot_gp_nll_warp": [P_dbl, P_dbl, c_int, c_int, c_int, c_dbl, P_dbl, P_dbl, P_dbl],
     "scoot_gp_mle_warp": [P_dbl, P_dbl, c_int, c_int, c_int, c_dbl, P_dbl, P_dbl, c_int, P_dbl, P_dbl, P_int],
+    "scoot_gp_nll_device": [P_dbl, P_dbl, c_int, c_int, c_int, P_dbl, P_dbl, c_dbl, c_int, P_dbl, P_dbl, P_dbl,
+                            c_vp],
+    "scoot_gp_mle_device": [P_dbl, P_dbl, c_int, c_int, c_int, P_dbl, P_dbl, c_dbl, c_int, P_dbl, P_dbl, c_int,
+                            P_dbl, P_dbl, P_int, c_vp],
     "scoot_posterior": [c_vp, c_vp, c_i64, c_vp, c_vp, c_vp],
     "scoot_acq_ei": [c_vp, c_vp, c_i64, c_int, c_dbl, c_dbl, c_vp, c_vp],
     "scoot_ehvi_front": [P_dbl, c_int, c_int, P_dbl, P_dbl, P_int, P_int],
@@ -83,6 +87,14 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2408_04323_amd.build.build() "
                                "(the scoring path has no CPU fallback)")
+        # torch ships its own HIP runtime; loaded first, it is the one the
+        # library binds to, so device memory and streams are shared.  Loaded
+        # after the library, a second runtime ends up in the process and the
+        # library's first allocation fails.
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         L = C.CDLL(LIB_PATH)
         for name, args in SIGNATURES.items():
             fn = getattr(L, name)

@@ -343,6 +343,30 @@ int scoot_gp_mle_warp(const double* X, const double* y, int m, int d, scoot_kern
   }
 }
 
+int scoot_gp_nll_device(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+                        const double* warp_b, double prior_mean, int learn_warp, const double* theta, double* nll,
+                        double* grad, void* stream) {
+  clear_error();
+  try {
+    return mle_nll_device(X, y, m, d, kernel, warp_a, warp_b, prior_mean, learn_warp != 0, theta, nll, grad, stream);
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "gp nll: host allocation failed");
+  }
+}
+
+int scoot_gp_mle_device(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+                        const double* warp_b, double prior_mean, int learn_warp, const double* lower,
+                        const double* upper, int max_iter, double* theta, double* nll, int* iterations,
+                        void* stream) {
+  clear_error();
+  try {
+    return mle_fit_device(X, y, m, d, kernel, warp_a, warp_b, prior_mean, learn_warp != 0, lower, upper, max_iter,
+                          theta, nll, iterations, stream);
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "gp mle: host allocation failed");
+  }
+}
+
 int scoot_gp_destroy(scoot_gp gp) {
   clear_error();
   if (!gp) return SCOOT_OK;

@@ -249,6 +249,16 @@ int mle_nll(const double* X, const double* y, int m, int d, scoot_kernel kernel,
   return SCOOT_OK;
 }
 
+int mle_inputs(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+               const double* warp_b, double c, bool learn_warp, std::vector<double>& Xuse, std::vector<double>& r) {
+  MleData D;
+  int rc = prepare(X, y, m, d, kernel, warp_a, warp_b, c, D, learn_warp);
+  if (rc != SCOOT_OK) return rc;
+  Xuse = learn_warp ? D.X : D.Xw;
+  r = D.r;
+  return SCOOT_OK;
+}
+
 int mle_fit(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
             const double* warp_b, double c, const double* lower, const double* upper, int max_iter, double* theta,
             double* nll_out, int* iters_out, bool learn_warp) {
@@ -258,6 +268,14 @@ int mle_fit(const double* X, const double* y, int m, int d, scoot_kernel kernel,
   int rc = prepare(X, y, m, d, kernel, warp_a, warp_b, c, D, learn_warp);
   if (rc != SCOOT_OK) return rc;
   const int P = learn_warp ? 3 * d + 2 : d + 2;
+  return lbfgs_box([&](const double* t, double* f, double* g) { return nll_eval(D, t, f, g); }, P, lower, upper,
+                   max_iter, theta, nll_out, iters_out);
+}
+
+int lbfgs_box(const NllFn& nll_fn, int P, const double* lower, const double* upper, int max_iter, double* theta,
+              double* nll_out, int* iters_out) {
+  if (!lower || !upper || !theta) return fail(SCOOT_ERR_INVALID_ARG, "gp mle: null pointer");
+  if (max_iter < 1) return fail(SCOOT_ERR_INVALID_ARG, "gp mle: max_iter must be >= 1");
   for (int k = 0; k < P; ++k)
     if (!std::isfinite(lower[k]) || !std::isfinite(upper[k]) || lower[k] > upper[k] || !std::isfinite(theta[k]))
       return fail(SCOOT_ERR_INVALID_ARG, "gp mle: bounds must be finite with lower <= upper, theta finite");
@@ -283,7 +301,7 @@ int mle_fit(const double* X, const double* y, int m, int d, scoot_kernel kernel,
   std::vector<double> gth(P), t(P);
   auto eval = [&](const std::vector<double>& zz, double& f, std::vector<double>& gz) {
     to_theta(zz, t);
-    if (!nll_eval(D, t.data(), &f, gth.data())) return false;
+    if (!nll_fn(t.data(), &f, gth.data())) return false;
     gz.assign(F, 0.0);
     for (int q = 0; q < F; ++q) {
       const int k = fr[q];

@@ -200,6 +200,23 @@ int mle_nll(const double* X, const double* y, int m, int d, scoot_kernel kernel,
 int mle_fit(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
             const double* warp_b, double c, const double* lower, const double* upper, int max_iter, double* theta,
             double* nll, int* iterations, bool learn_warp = false);
+// The inputs a likelihood evaluation sees, validated as mle_nll / mle_fit do:
+// Xuse = the inputs warped by (warp_a, warp_b) when given, the raw inputs when
+// the warp is learned; r = y - c.
+int mle_inputs(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+               const double* warp_b, double c, bool learn_warp, std::vector<double>& Xuse, std::vector<double>& r);
+// NLL and gradient at theta; false when K is not positive definite.
+typedef std::function<bool(const double* theta, double* nll, double* grad)> NllFn;
+// The box-constrained L-BFGS search of mle_fit over any evaluator of P parameters.
+int lbfgs_box(const NllFn& nll_fn, int P, const double* lower, const double* upper, int max_iter, double* theta,
+              double* nll_out, int* iters_out);
+// mle_fit with every evaluation on the device (k_mle.hip), on `stream`.
+int mle_fit_device(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+                   const double* warp_b, double c, bool learn_warp, const double* lower, const double* upper,
+                   int max_iter, double* theta, double* nll_out, int* iters_out, void* stream);
+int mle_nll_device(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+                   const double* warp_b, double c, bool learn_warp, const double* theta, double* nll, double* grad,
+                   void* stream);
 
 // Forest training (host_forest_train.cpp): tree-local child indices, preorder.
 struct TrainedForest {

@@ -201,6 +201,19 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
       // one after the other.
       std::vector<int> search_rc(p, SCOOT_OK);
       std::vector<std::string> search_err(p);
+      // Device searches: each objective's evaluations on a stream of its own,
+      // so the objectives' kernels run side by side.
+      const bool on_device = o.host_search == 0;
+      int device = 0;
+      std::vector<hipStream_t> streams(p, nullptr);
+      if (on_device) {
+        if (hipGetDevice(&device) != hipSuccess) return fail(SCOOT_ERR_DEVICE, "suggest: no current device");
+        for (int j = 0; j < p; ++j)
+          if (hipStreamCreateWithFlags(&streams[j], hipStreamNonBlocking) != hipSuccess) {
+            for (int q = 0; q < j; ++q) (void)hipStreamDestroy(streams[q]);
+            return fail(SCOOT_ERR_DEVICE, "suggest: cannot create a stream");
+          }
+      }
       auto search = [&](int j) {
         try {
           double lo[3 * SCOOT_MAX_DIM + 2], hi[3 * SCOOT_MAX_DIM + 2], th[3 * SCOOT_MAX_DIM + 2];
@@ -213,7 +226,17 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
           const double* wa = o.warp_a ? o.warp_a + (size_t)j * d : nullptr;
           const double* wb = o.warp_b ? o.warp_b + (size_t)j * d : nullptr;
           const int iters = o.mle_max_iter > 0 ? o.mle_max_iter : kDefaultMleIter;
-          if (!all_fixed) {
+          if (!all_fixed && on_device) {
+            if (hipSetDevice(device) != hipSuccess) {
+              search_rc[j] = SCOOT_ERR_DEVICE;
+              search_err[j] = "suggest: cannot select the device";
+              return;
+            }
+            search_rc[j] = scoot_gp_mle_device(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel,
+                                               lw ? nullptr : wa, lw ? nullptr : wb, 0.0, lw ? 1 : 0, lo, hi, iters, th,
+                                               nullptr, nullptr, streams[j]);
+            if (search_rc[j] != SCOOT_OK) search_err[j] = scoot_last_error();  // this thread's message
+          } else if (!all_fixed) {
             search_rc[j] = lw ? scoot_gp_mle_warp(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, 0.0, lo, hi,
                                                   iters, th, nullptr, nullptr)
                               : scoot_gp_mle(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, wa, wb, 0.0, lo,
@@ -228,15 +251,26 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
       };
       std::vector<std::thread> searches;
       searches.reserve(p);  // no reallocation once a thread runs
-      for (int j = 1; j < p; ++j) {
+      // Device searches leave this thread free: it trains the forest meanwhile
+      // (step 3, host work that does not depend on the hyperparameters).
+      for (int j = on_device ? 0 : 1; j < p; ++j) {
         try {
           searches.emplace_back(search, j);
         } catch (const std::system_error&) {
           search(j);  // no thread to spare: run it here
         }
       }
-      search(0);
+      if (!on_device) search(0);
+      // ---- 3. feasibility forest on every observation ---------------------
+      std::vector<double> label(n_obs);
+      for (int i = 0; i < n_obs; ++i) label[i] = valid[i] ? 1.0 : 0.0;
+      const int forest_rc = scoot_forest_train_create(X_obs, label.data(), n_obs, d, o.n_trees, o.max_depth,
+                                                      o.forest_seed, o.bootstrap, &h.forest);
+      const std::string forest_err = forest_rc != SCOOT_OK ? scoot_last_error() : "";
       for (auto& t : searches) t.join();
+      for (hipStream_t st : streams)
+        if (st) (void)hipStreamDestroy(st);
+      if (forest_rc != SCOOT_OK) return fail(forest_rc, forest_err);
       for (int j = 0; j < p; ++j)
         if (search_rc[j] != SCOOT_OK) return fail(search_rc[j], search_err[j]);
       for (int j = 0; j < p; ++j) {
@@ -262,13 +296,6 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
         h.gps.push_back(g);
       }
       if (theta_out) std::memcpy(theta_out, theta.data(), sizeof(double) * theta.size());
-
-      // ---- 3. feasibility forest on every observation ---------------------
-      std::vector<double> label(n_obs);
-      for (int i = 0; i < n_obs; ++i) label[i] = valid[i] ? 1.0 : 0.0;
-      rc = scoot_forest_train_create(X_obs, label.data(), n_obs, d, o.n_trees, o.max_depth, o.forest_seed,
-                                     o.bootstrap, &h.forest);
-      if (rc != SCOOT_OK) return rc;
 
       // ---- 5. score the pool and pick ----------------------------------
       void* mu = ws + o_mu;

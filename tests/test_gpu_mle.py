@@ -1,0 +1,165 @@
+"""The likelihood of the GP hyperparameters (Sec. 4.3) evaluated on the
+device, and the search driven by it, against the oracle (oracle/mle.py):
+NLL to 1e-10 relative, gradient to 1e-8, at sizes from one observation to the
+library's maximum (ragged against the 16-row blocks), both covariances, no /
+fixed / learned input warping; a singular K is reported as NOT_PD; the search
+ends at least as well as the oracle's."""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import paper_2408_04323_amd as S  # noqa: E402
+from oracle.mle import fit_hyperparameters, fit_hyperparameters_warp, nll_and_grad, nll_and_grad_warp  # noqa: E402
+from workloads import make_workload  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def _case(seed, m, d):
+    rng = np.random.default_rng(seed)
+    X = rng.random((m, d))
+    y = np.sin(3 * X[:, 0]) + 0.5 * np.cos(5 * X[:, min(1, d - 1)]) + 0.05 * rng.standard_normal(m)
+    return X, (y - y.mean()) / max(y.std(), 1e-12)
+
+
+def _theta(rng, d):
+    return np.concatenate([np.log(rng.uniform(0.1, 2.0, d)), [np.log(rng.uniform(0.3, 3)),
+                                                              np.log(rng.uniform(1e-4, 0.3))]])
+
+
+def _close(nll, g, nll_o, g_o):
+    assert nll == pytest.approx(nll_o, rel=1e-10, abs=1e-10)
+    np.testing.assert_allclose(g, g_o, rtol=1e-8, atol=1e-8)
+
+
+CASES = [  # (m, d, kernel, warp: None | "fixed")
+    (1, 1, "matern52", None),
+    (5, 2, "matern32", None),
+    (16, 3, "matern52", "fixed"),
+    (17, 2, "matern32", None),
+    (60, 5, "matern52", None),
+    (60, 5, "matern32", "fixed"),
+    (129, 16, "matern52", None),
+    (256, 10, "matern52", None),
+    (300, 4, "matern32", "fixed"),
+    (576, 12, "matern52", None),
+]
+
+
+@pytest.mark.parametrize("m,d,kernel,warp", CASES)
+def test_device_nll_matches_oracle(m, d, kernel, warp):
+    X, y = _case(m + d, m, d)
+    rng = np.random.default_rng(7 * m + d)
+    wp = (np.exp(0.4 * rng.standard_normal(d)), np.exp(0.4 * rng.standard_normal(d))) if warp else None
+    for trial in range(2):
+        theta = _theta(rng, d)
+        say("nll", m, d, kernel, warp, trial)
+        nll, g = S.gp_nll_device(X, y, theta, kernel=kernel, warp_a=None if wp is None else wp[0],
+                                 warp_b=None if wp is None else wp[1], prior_mean=0.05)
+        nll_o, g_o = nll_and_grad(theta, X, y, kernel, wp, prior_mean=0.05)
+        _close(nll, g, nll_o, g_o)
+
+
+@pytest.mark.parametrize("m,d,kernel", [(3, 1, "matern32"), (60, 5, "matern32"), (130, 3, "matern52")])
+def test_device_nll_learned_warp_matches_oracle(m, d, kernel):
+    X, y = _case(100 + m, m, d)
+    X[0, 0] = 0.0
+    X[1 % m, 0] = 1.0
+    X[2 % m, d - 1] = 1e-12
+    rng = np.random.default_rng(m)
+    for trial in range(2):
+        theta = np.concatenate([_theta(rng, d), 0.4 * rng.standard_normal(2 * d)])
+        say("nll warp", m, d, kernel, trial)
+        nll, g = S.gp_nll_device(X, y, theta, kernel=kernel, learn_warp=True, prior_mean=-0.1)
+        nll_o, g_o = nll_and_grad_warp(theta, X, y, kernel, prior_mean=-0.1)
+        _close(nll, g, nll_o, g_o)
+
+
+def test_device_nll_matches_host_on_the_workload():
+    """The two-objective workload's observations (m = 256, d = 10): device and
+    host evaluations agree to rounding."""
+    w = make_workload(3, n=16, with_forest=False)
+    X, Y = w["X"], w["Y"]
+    d = X.shape[1]
+    rng = np.random.default_rng(3)
+    for j in range(Y.shape[1]):
+        theta = _theta(rng, d)
+        say("workload objective", j)
+        nll, g = S.gp_nll_device(X, Y[:, j], theta)
+        nll_h, g_h = S.gp_nll(X, Y[:, j], theta)
+        assert nll == pytest.approx(nll_h, rel=1e-11, abs=1e-10)
+        np.testing.assert_allclose(g, g_h, rtol=1e-8, atol=1e-8)
+
+
+def test_device_nll_singular_and_argument_errors():
+    X, y = _case(4, 30, 2)
+    say("singular K")
+    with pytest.raises(S.ScootError) as e:  # duplicate inputs and no noise: K singular
+        S.gp_nll_device(np.vstack([X, X[:1]]), np.concatenate([y, y[:1]]), np.array([0.0, 0.0, 0.0, -60.0]))
+    assert e.value.status == -2
+    with pytest.raises(S.ScootError):
+        S.gp_nll_device(X, y, np.array([0.0, 0.0, 0.0, np.nan]))
+    with pytest.raises(S.ScootError):  # a learned warp takes no fixed warp
+        S.gp_nll_device(X, y, np.zeros(3 * 2 + 2), warp_a=np.ones(2), warp_b=np.ones(2), learn_warp=True)
+    # the same inputs still evaluate afterwards
+    nll, g = S.gp_nll_device(X, y, np.log(np.array([0.5, 0.5, 1.0, 0.01])))
+    nll_o, g_o = nll_and_grad(np.log(np.array([0.5, 0.5, 1.0, 0.01])), X, y)
+    _close(nll, g, nll_o, g_o)
+
+
+@pytest.mark.parametrize("kernel", ["matern52", "matern32"])
+def test_device_fit_reaches_the_oracle_optimum(kernel):
+    X, y = _case(3, 50, 3)
+    theta0 = np.log(np.array([0.5, 0.5, 0.5, 1.0, 0.05]))
+    lo = np.log(np.array([0.02] * 3 + [0.05, 1e-6]))
+    hi = np.log(np.array([10.0] * 3 + [20.0, 1.0]))
+    say("fit", kernel)
+    th, f, it = S.gp_mle_device(X, y, theta0, lo, hi, kernel=kernel)
+    th_o, f_o = fit_hyperparameters(X, y, theta0, lo, hi, kernel)
+    assert it > 0 and np.all(th >= lo) and np.all(th <= hi)
+    assert f == pytest.approx(nll_and_grad(th, X, y, kernel)[0], rel=1e-10, abs=1e-10)
+    assert f <= f_o + 1e-7 * max(1.0, abs(f_o))
+    _, g = nll_and_grad(th, X, y, kernel)
+    interior = (th > lo + 1e-3) & (th < hi - 1e-3)
+    assert np.all(np.abs(g[interior]) < 1e-4)
+
+
+def test_device_fit_with_the_warp_learned():
+    X, y = _case(9, 40, 2)
+    d = 2
+    theta0 = np.concatenate([np.log([0.5, 0.5]), [0.0, np.log(0.05)], np.zeros(2 * d)])
+    lo = np.concatenate([np.log([0.02, 0.02]), [np.log(0.05), np.log(1e-6)], np.full(2 * d, np.log(0.2))])
+    hi = np.concatenate([np.log([10.0, 10.0]), [np.log(20.0), 0.0], np.full(2 * d, np.log(5.0))])
+    say("fit warp")
+    th, f, it = S.gp_mle_device(X, y, theta0, lo, hi, kernel="matern32", learn_warp=True)
+    th_o, f_o = fit_hyperparameters_warp(X, y, theta0, lo, hi, "matern32")
+    assert it > 0 and np.all(th >= lo) and np.all(th <= hi)
+    assert f == pytest.approx(nll_and_grad_warp(th, X, y, "matern32")[0], rel=1e-10, abs=1e-10)
+    assert f <= f_o + 1e-6 * max(1.0, abs(f_o))
+
+
+def test_device_fit_matches_host_fit_on_the_workload():
+    """The search on the workload's first objective (m = 256, d = 10) ends at
+    the host search's optimum."""
+    w = make_workload(3, n=16, with_forest=False)
+    X, y = w["X"], w["Y"][:, 0]
+    d = X.shape[1]
+    theta0 = np.concatenate([np.log(np.full(d, 0.5)), [0.0, np.log(1e-2)]])
+    lo = np.concatenate([np.log(np.full(d, 0.01)), [np.log(0.05), np.log(1e-6)]])
+    hi = np.concatenate([np.log(np.full(d, 20.0)), [np.log(20.0), np.log(1.0)]])
+    say("workload fit")
+    th, f, it = S.gp_mle_device(X, y, theta0, lo, hi, max_iter=300)
+    th_h, f_h, it_h = S.gp_mle(X, y, theta0, lo, hi, max_iter=300)
+    print(f"[mle] device {it} iterations nll {f:.9f}; host {it_h} iterations nll {f_h:.9f}")
+    assert f <= f_h + 1e-7 * max(1.0, abs(f_h))
+    _, g = nll_and_grad(th, X, y)
+    interior = (th > lo + 1e-3) & (th < hi - 1e-3)
+    assert np.max(np.abs(g[interior])) < 1e-3
