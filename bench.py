@@ -460,7 +460,11 @@ def bench_suggest(args):
                       "config": {"workload": f"{c['name']}: {len(X_obs)} observations ({int(ok.sum())} valid) "
                                              f"d={d} p={p} pool={n} k={k} trees={c['trees']} depth={c['depth']}",
                                  "ms_per_step_host_search": ms_host, "parts_ms": parts,
-                                 "sources": src.tolist(), "sources_host_search": src_h.tolist()}}), flush=True)
+                                 "sources": src.tolist(), "sources_host_search": src_h.tolist(),
+                                 "picks_match_host_search": bool(np.array_equal(np.asarray(x), np.asarray(x_h))),
+                                 "theta_max_abs_diff_vs_host_search": float(np.max(np.abs(np.asarray(theta) -
+                                                                                         np.asarray(theta_h))))}}),
+          flush=True)
 
 
 def cpu_baseline(w, seconds):

@@ -16,11 +16,11 @@
 //   W. (warp learned) the warped inputs and their derivatives;
 //   K. K, one 16 x 16 block per workgroup;
 //   A. one workgroup (8 waves): the Cholesky factor L by 16-column block
-//      steps: the diagonal block by one wave in registers, the panel below it
-//      by forward substitution (a row per thread), the trailing update on
-//      v_mfma_f64_16x16x4f64; the next diagonal block is factored as soon as
-//      it is updated, by a wave whose SIMD the others leave free; then the
-//      inverses of the diagonal blocks;
+//      steps: the diagonal block factored and inverted by one wave in
+//      registers (a rank-1 update per column on v_mfma_f64_16x16x4f64), the
+//      panel below it as the product with that inverse and the trailing
+//      update, both on the matrix cores; the next diagonal block is factored
+//      as soon as it is updated, by a wave whose SIMD the others leave free;
 //   T. L^-1, one block column per workgroup (the columns are independent);
 //   U. K^-1 = L^-T L^-1, one block per workgroup;
 //   V. alpha = K^-1 r and the quadratic form, one block row per workgroup;
@@ -66,7 +66,8 @@ struct NllArgs {
   double* alpha;    // m_pad
   double* prod;     // nb: product of each diagonal block's pivots (real rows)
   double* qpart;    // nb: r^T alpha over each block of 16 rows
-  double* out;      // [0] NLL, [1] 1 when K is numerically positive definite else 0, [2 ..] gradient
+  double* out;      // [1] 1 when K is numerically positive definite, 0 when not, 2 when a wait ran out
+  double* hout;     // pinned host memory: [0] NLL, [1] the status of out[1], [2 ..] gradient
   double* part;     // kGradBlocks x P partial gradient sums
   int m, nb, d, m52, learn_warp;
   double theta[kMaxTheta];
@@ -142,6 +143,15 @@ __device__ inline void wave_lds_sync() {
   asm volatile("" ::: "memory");
 }
 
+// Workgroup barrier for waves that exchange data through LDS only: their LDS
+// accesses have completed, their global stores may still be in flight.
+__device__ inline void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Order-fixed sum over the 64 lanes.
 __device__ inline double wave_sum(double v) {
 #pragma unroll
@@ -181,6 +191,7 @@ __global__ __launch_bounds__(256) void nll_warp_kernel(NllArgs a) {
 
 // ---- kernel K: the covariance, one lower 16 x 16 block per workgroup --------
 // Diagonal blocks in full; padding rows and columns are those of the identity.
+// Each block is written transposed (column-major), the layout kernel A reads.
 __global__ __launch_bounds__(256) void nll_cov_kernel(NllArgs a) {
   __shared__ double sXi[16 * SCOOT_MAX_DIM], sXj[16 * SCOOT_MAX_DIM], sIl[SCOOT_MAX_DIM];
   const int nb = a.nb, m = a.m, d = a.d, t = threadIdx.x;
@@ -197,7 +208,8 @@ __global__ __launch_bounds__(256) void nll_cov_kernel(NllArgs a) {
   }
   if (t < d) sIl[t] = exp(-a.theta[t]);
   __syncthreads();
-  const int ii = t >> 4, jj = t & 15, i = 16 * I + ii, j = 16 * J + jj;
+  // block (I, J) is stored transposed: thread t holds element (ii, jj) at t = 16 jj + ii
+  const int jj = t >> 4, ii = t & 15, i = 16 * I + ii, j = 16 * J + jj;
   double v;
   if (i < m && j < m) {
     double r2 = 0.0;
@@ -221,25 +233,29 @@ __device__ inline double lane_bcast(double v, int src) {
   return __hiloint2double(hi, lo);
 }
 
-// Factors the 16 x 16 diagonal block kk in one wave: stores L_kk (row-major,
-// zero above the diagonal) to memory and to sL (16 x 17), 1 / L[c][c] to
-// sIc, the product of the pivots of real rows to sProd[kk]; raises sFlag when
-// such a pivot is not above floor (or a padding pivot is not positive).
-//
-// In: lane l holds column jl = l % 16 of the block, col[i] = A[i][jl] (each row
-// of 16 lanes a copy).  Step c takes the pivot from lane c; by the block's
-// symmetry lane j finds its entry of column c, L[j][c] = A[c][j] / L[c][c], in
-// its own registers, and the column goes to every lane entry by entry
-// (readlane) for the update of the columns right of c (lanes j <= c are
-// finished and their registers no longer read).
-__device__ inline void diag_step(const NllArgs& a, int kk, double (&col)[16], double* sL, double* sIc,
-                                 double* sProd, int* sFlag, double floor, int lane) {
-  const int jl = lane & 15, real = min(16, a.m - 16 * kk);
-  double row[16], prod = 1.0;
+// Factors the 16 x 16 diagonal block kk, held in C layout by one wave, and
+// inverts the factor on the way.  Column c: the pivot p = D[c][c] comes from
+// one lane; l = D[c][.] / sqrt(p) (row c, by symmetry column c of L) sits in
+// register c / 4 of row group c % 4, which is where v_mfma_f64_16x16x4f64 takes
+// both operands of its k = c % 4 slice, so one MFMA subtracts l l^T from the
+// whole block.  The same l against row c of Y (Y = I at the start) scaled by
+// 1 / L[c][c], which is row c of L^-1, carries out the forward substitution of
+// L Y = I a column at a time.  Stores L_kk column-major to memory, L_kk^-1
+// row-major to memory (Di) and as a row slot (sX), the product of the pivots of
+// real rows to sProd[kk]; raises sFlag[0] when such a pivot is not above floor
+// (or a padding pivot is not positive).
+__device__ inline void diag_factor(const NllArgs& a, int kk, d4_t D, double* sX, double* sProd, int* sFlag,
+                                   double floor, int lane) {
+  const int g = lane >> 4, j = lane & 15, real = min(16, a.m - 16 * kk);
+  d4_t Lt = zero4(), X = zero4(), Y;  // Lt: L^T in C layout (row c of Lt = column c of L)
+#pragma unroll
+  for (int r = 0; r < 4; ++r) Y[r] = g + 4 * r == j ? 1.0 : 0.0;
+  double prod = 1.0;
   bool bad = false;
 #pragma unroll
   for (int c = 0; c < 16; ++c) {
-    const double piv = lane_bcast(col[c], c);
+    const int cg = c & 3, cr = c >> 2;
+    const double piv = lane_bcast(D[cr], cg * 16 + c);
     const bool real_row = c < real;
     bad = bad || !(piv > (real_row ? floor : 0.0));
     prod *= real_row ? piv : 1.0;
@@ -250,222 +266,339 @@ __device__ inline void diag_step(const NllArgs& a, int kk, double (&col)[16], do
     const double h = 0.5 * piv;
     ic = ic * fma(-h * ic, ic, 1.5);
     ic = ic * fma(-h * ic, ic, 1.5);
-    const double lj = col[c] * ic;
-    row[c] = jl == c ? piv * ic : lj;
-    if (lane == c) sIc[c] = ic;
-#pragma unroll
-    for (int i = c + 1; i < 16; ++i) {
-      col[i] = fma(-lane_bcast(lj, i), lj, col[i]);
-      __builtin_amdgcn_sched_barrier(0);  // each broadcast used where it is made
+    const bool mine = g == cg;
+    const double l = mine && j >= c ? D[cr] * ic : 0.0;  // L[j][c], 0 above the diagonal
+    const double y = mine ? Y[cr] * ic : 0.0;            // (L^-1)[c][j]
+    if (mine) {
+      Lt[cr] = l;
+      X[cr] = y;
     }
+    D = __builtin_amdgcn_mfma_f64_16x16x4f64(-l, l, D, 0, 0, 0);
+    Y = __builtin_amdgcn_mfma_f64_16x16x4f64(-l, y, Y, 0, 0, 0);
   }
-  if (lane < 16) {
-    double* Lb = a.L + ((size_t)kk * a.nb + kk) * 256 + jl * 16;
-#pragma unroll
-    for (int c = 0; c < 16; ++c) {
-      const double v = c <= jl ? row[c] : 0.0;
-      Lb[c] = v;
-      sL[jl * 17 + c] = v;
-    }
-  }
+  st_c(a.L + ((size_t)kk * a.nb + kk) * 256, Lt, lane);  // L_kk column-major
+  st_c(a.Di + (size_t)kk * 256, X, lane);
+  st_row_slot(sX, X, lane);
   if (lane == 0) {
     sProd[kk] = prod;
     if (bad) sFlag[0] = 1;
   }
 }
 
-// ---- kernel A: L, K^-1, alpha, NLL --------------------------------------------
+// ---- kernel A: the Cholesky factor L and the inverses of its diagonal blocks --
+// Blocks are held transposed: the covariance kernel writes block (I, J)
+// column-major, the workers' registers hold A_ij^T in C layout (A_ij as an A
+// operand), and the factor goes to memory column-major too.  The worker blocks, (i, j) with 1 <= j <= i
+// but (1, 1), are listed by decreasing j (then increasing i) and dealt round
+// robin to the workers; at step k a worker's blocks with j >= k + 1 form a
+// prefix of its share, so each step's work is balanced and the first kRes
+// blocks of a share, the longest-lived, stay in registers for the whole
+// factorization (the others go through memory each step).
+constexpr int kRes = 8;
+
 __global__ __launch_bounds__(kNllThreads) void nll_factor_kernel(NllArgs a) {
   extern __shared__ __align__(16) double sm[];
-  const int nb = a.nb, m = a.m, d = a.d;
-  double* sPan = sm;                          // nb slots: the panel (row slots), a column of L (column slots)
-  double* sLkk = sPan + (size_t)nb * 256;     // 16 x 17: the current diagonal block's factor
-  double* sIc = sLkk + 16 * 17;               // 16: 1 / its pivots' roots
-  double* sScr = sIc + 16;                    // 256: wave 0's scratch, a block read by columns
-  double* sProd = sScr + 256;                 // per diagonal block: product of its pivots
-  double* sRed = sProd + SCOOT_MAX_OBS / 16;  // kNllWaves
-  int* sFlag = reinterpret_cast<int*>(sRed + kNllWaves);
+  const int nb = a.nb, d = a.d;
+  double* sPan = sm;                          // 2 x nb row slots: the panels of columns k and k + 1
+  double* sX = sPan + (size_t)2 * nb * 256;   // row slot: the inverse of the newest diagonal factor
+  double* sDiag = sX + 256;                   // 2 x 256: the next diagonal blocks as updated (C layout)
+  double* sProd = sDiag + 512;                // per diagonal block: product of its pivots
+  // [0] a pivot not above its floor, [1] the last diagonal block factored,
+  // [2] a wait for it ran out
+  int* sFlag = reinterpret_cast<int*>(sProd + SCOOT_MAX_OBS / 16);
   int* sSimd = sFlag + 4;                     // kNllWaves: the SIMD each wave runs on
+  int* sList = sSimd + kNllWaves;             // the worker blocks, (i << 8) | j
 
-  const int tid = threadIdx.x, lane = tid & 63, jl = lane & 15;
+  const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   if (lane == 0) sSimd[wave] = (int)((__builtin_amdgcn_s_getreg((31 << 11) | 4) >> 4) & 3);  // HW_ID.SIMD_ID
+  if (tid < 4) sFlag[tid] = 0;
+  const int n_list = nb > 1 ? nb * (nb - 1) / 2 - 1 : 0;
+  for (int n = tid; n < n_list; n += kNllThreads) {
+    int start = 0;
+    for (int j = nb - 1; j >= 1; --j) {
+      const int lo = j == 1 ? 2 : j, cnt = nb - lo;
+      if (n < start + cnt) {
+        sList[n] = ((lo + n - start) << 8) | j;
+        break;
+      }
+      start += cnt;
+    }
+  }
   const double s2 = exp(a.theta[d]), tau2 = exp(a.theta[d + 1]);
   // A pivot that is not above 1e-13 of its original diagonal entry (s2 + tau2)
   // means K is not numerically positive definite (the host factor's rule).
   const double floor = 1e-13 * (s2 + tau2);
-
-  // ---- Cholesky factor, 16 columns per step --------------------------------
-  // Step k: the panel L_ik = A_ik L_kk^-T (matrix cores), then the trailing
-  // update A_ij -= L_ik L_jk^T; the wave that updates block (k+1, k+1) factors
-  // it at once, while the others update the rest.
-  if (wave == 0) {
-    if (lane == 0) sFlag[0] = 0;
-    double col[16];
-    const double* blk = a.L;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) col[i] = blk[i * 16 + jl];
-    diag_step(a, 0, col, sLkk, sIc, sProd, sFlag, floor, lane);
-  }
-  __syncthreads();
+  lds_barrier();
   // The trailing update goes to the waves that do not share wave 0's SIMD:
-  // the vector ALU wave 0 factors with and the matrix unit are one datapath,
-  // so a neighbour's matrix instructions would stall the factorization.
-  int worker = -1, n_workers = 0;
+  // its vector ALU and the matrix unit are one datapath, so a neighbour's
+  // matrix instructions would stall the factorization.
+  int worker = -1, W = 0;
   for (int w = 1; w < kNllWaves; ++w)
     if (sSimd[w] != sSimd[0]) {
-      if (w == wave) worker = n_workers;
-      ++n_workers;
+      if (w == wave) worker = W;
+      ++W;
     }
-  bool failed = false;
-  for (int k = 0; k < nb; ++k) {
-    if (sFlag[0]) {
-      failed = true;
-      break;
-    }
-    // panel: L_ik = A_ik L_kk^-T, one row per thread (forward substitution)
-    const int rows = (nb - k - 1) * 16;
-    for (int ri = tid; ri < rows; ri += kNllThreads) {
-      const int ib = k + 1 + (ri >> 4), rr = ri & 15;
-      double* rowp = a.L + ((size_t)ib * nb + k) * 256 + rr * 16;
-      double x[16];
+  if (W == 0) {  // every wave on one SIMD: all but wave 0 work
+    worker = wave - 1;
+    W = kNllWaves - 1;
+  }
+  // a worker's blocks among the first S of the list; the blocks with j >= c
+  // are the first (nb - c)(nb - c + 1) / 2 (less (1, 1) when c = 1)
+  auto mine_below = [&](int S) { return S > worker ? (S - 1 - worker) / W + 1 : 0; };
+  auto from_col = [&](int c) { return (nb - c) * (nb - c + 1) / 2 - (c <= 1 ? 1 : 0); };
+
+  // ---- Cholesky factor, 16 columns per step --------------------------------
+  // Before step k the panel of column k, L_ik (i > k), is in row slots and
+  // L_kk^-1 in sX.  Step k: wave 0 updates block (k+1, k+1), factors and
+  // inverts it; the workers apply column k to their blocks with j >= k+1,
+  // A_ij^T -= L_jk L_ik^T (block (k+2, k+2) also to wave 0 through LDS), and
+  // once wave 0 has published the new inverse turn their blocks of column
+  // k+1 into the panel, L_i,k+1^T = L_k+1,k+1^-1 A_i,k+1^T.  The waves share
+  // data through LDS only (a worker reads back only blocks it wrote), so the
+  // one barrier per step does not wait for global stores.
+  constexpr int kCol0 = (SCOOT_MAX_OBS / 16 - 1 + kNllWaves - 2) / (kNllWaves - 1);  // column-0 blocks per wave
+  double c0[kCol0][4];
+  d4_t res[kRes];  // a worker's first kRes blocks (transposed, C layout)
+  int rij[kRes];
+  const int n_share = worker >= 0 ? mine_below(n_list) : 0;
 #pragma unroll
-      for (int c = 0; c < 16; c += 2) {
-        const d2_t v = *reinterpret_cast<const d2_t*>(rowp + c);
-        x[c] = v[0], x[c + 1] = v[1];
+  for (int s = 0; s < kRes; ++s) rij[s] = s < n_share ? __builtin_amdgcn_readfirstlane(sList[worker + W * s]) : 0;
+  if (wave == 0) {
+    diag_factor(a, 0, ld_c(a.L, lane), sX, sProd, sFlag, floor, lane);
+  } else {
+    // the blocks of column 0, while wave 0 factors block (0, 0)
+#pragma unroll
+    for (int t = 0; t < kCol0; ++t) {
+      const int i = wave + (kNllWaves - 1) * t;
+      if (i < nb) ld_cols(a.L + (size_t)i * nb * 256, lane, c0[t]);  // A_i0^T as a B operand
+    }
+  }
+  lds_barrier();
+  // the panel of column 0: L_i0^T = L_00^-1 A_i0^T (C layout, so column-major
+  // to memory and a row slot of L_i0 as it stands)
+  if (wave != 0) {
+    double xv[4];
+    ld_slot(sX, lane, xv);
+#pragma unroll
+    for (int t = 0; t < kCol0; ++t) {
+      const int i = wave + (kNllWaves - 1) * t;
+      if (i < nb) {
+        const d4_t v = mma16(zero4(), xv, c0[t]);
+        st_c(a.L + (size_t)i * nb * 256, v, lane);
+        st_col_slot(sPan + (size_t)i * 256, v, lane);
       }
-#pragma unroll
-      for (int c = 0; c < 16; ++c) {
-        x[c] *= sIc[c];
-#pragma unroll
-        for (int q = c + 1; q < 16; ++q) x[q] = fma(-x[c], sLkk[q * 17 + c], x[q]);
-      }
-      double* slot = sPan + (size_t)ib * 256;
-#pragma unroll
-      for (int c = 0; c < 16; c += 2) *reinterpret_cast<d2_t*>(rowp + c) = d2_t{x[c], x[c + 1]};
-#pragma unroll
-      for (int c = 0; c < 16; ++c) slot[row_slot_pos(rr, c)] = x[c];
     }
-    __syncthreads();
-    if (k == nb - 1) break;
+    // the worker's resident blocks
+#pragma unroll
+    for (int s = 0; s < kRes; ++s)
+      if (s < n_share) res[s] = ld_c(a.L + ((size_t)(rij[s] >> 8) * nb + (rij[s] & 255)) * 256, lane);
+  }
+  lds_barrier();
+  int cur = 0;
+  for (int k = 0; k + 1 < nb; ++k, cur ^= 1) {
+    if (sFlag[0] || sFlag[2]) break;
+    const double* pc = sPan + (size_t)cur * nb * 256;  // panel of column k
+    double* pn = sPan + (size_t)(cur ^ 1) * nb * 256;  // panel of column k + 1, being made
     if (wave == 0) {
       const int i = k + 1;
-      double* blk = a.L + ((size_t)i * nb + i) * 256;
-      d4_t acc = ld_c(blk, lane);
+      // block (k+1, k+1) as the previous step's update left it (from its
+      // worker through LDS, buffer k % 2; at k = 0 the covariance itself)
+      const double* dg = sDiag + (k & 1) * 256;
+      d4_t acc = k == 0 ? ld_c(a.L + ((size_t)i * nb + i) * 256, lane)
+                        : d4_t{dg[lane], dg[64 + lane], dg[128 + lane], dg[192 + lane]};
       double av[4], bv[4];
-      ld_slot(sPan + (size_t)i * 256, lane, bv);
+      ld_slot(pc + (size_t)i * 256, lane, bv);
 #pragma unroll
       for (int s = 0; s < 4; ++s) av[s] = -bv[s];
       acc = mma16(acc, av, bv);
-      st_c(sScr, acc, lane);  // row-major, to read by columns
-      wave_lds_sync();
-      double col[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) col[r] = sScr[r * 16 + jl];
-      diag_step(a, i, col, sLkk, sIc, sProd, sFlag, floor, lane);
+      diag_factor(a, i, acc, sX, sProd, sFlag, floor, lane);
+      wave_lds_sync();  // the inverse is in LDS
+      if (lane == 0) __hip_atomic_store(&sFlag[1], i, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     } else if (worker >= 0) {
-      // blocks 1, 2, ... of the trailing triangle (row by row) over the
-      // workers, four per wave at a time, their loads issued first
-      const int W = n_workers;
-      const int T = nb - k - 1, n_trail = T * (T + 1) / 2;
-      int I = 0, J = 0;
-      advance_lower(I, J, 1 + worker);
-      for (int b = 1 + worker; b < n_trail; b += 4 * W) {
+      const int n_trail = mine_below(from_col(k + 2));  // the share's blocks with j >= k+2
+      const int n_act = mine_below(from_col(k + 1));    // ... with j >= k+1
+      double* sNext = sDiag + ((k + 1) & 1) * 256;
+      // the inverse of block (k+1, k+1) from wave 0 (a bounded wait)
+      bool have_x = false;
+      double xv[4];
+      auto wait_x = [&]() {
+        if (have_x) return;
+        for (int spins = 0; __hip_atomic_load(&sFlag[1], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < k + 1;) {
+          if (++spins > (1 << 22)) {
+            if (lane == 0) sFlag[2] = 1;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(2);
+        }
+        wave_lds_sync();
+        ld_slot(sX, lane, xv);
+        have_x = true;
+      };
+      // resident blocks: the update
+#pragma unroll
+      for (int s = 0; s < kRes; ++s) {
+        const int i = rij[s] >> 8, j = rij[s] & 255;
+        if (s < n_act && !(i == k + 1 && j == k + 1)) {
+          double av[4], bv[4];
+          ld_slot(pc + (size_t)j * 256, lane, av);
+          ld_slot(pc + (size_t)i * 256, lane, bv);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) av[q] = -av[q];
+          res[s] = mma16(res[s], av, bv);
+          if (i == k + 2 && j == k + 2) st_c(sNext, res[s], lane);
+        }
+        __builtin_amdgcn_sched_barrier(0);  // a block's operands loaded where it is updated
+      }
+      // the others, four at a time, their loads first: the blocks with
+      // j >= k+2 back to memory, then those of column k+1 into the panel
+      for (int e0 = kRes; e0 < n_act; e0 += 4) {
         d4_t acc[4];
-        double* blk[4];
-        int bi[4], bj[4];
+        int ij[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          bi[u] = k + 1 + I;
-          bj[u] = k + 1 + J;
-          blk[u] = a.L + ((size_t)bi[u] * nb + bj[u]) * 256;
-          if (b + u * W < n_trail) acc[u] = ld_c(blk[u], lane);
-          advance_lower(I, J, W);
+          ij[u] = __builtin_amdgcn_readfirstlane(sList[worker + W * (e0 + u < n_act ? e0 + u : e0)]);
+          acc[u] = ld_c(a.L + ((size_t)(ij[u] >> 8) * nb + (ij[u] & 255)) * 256, lane);
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          if (b + u * W < n_trail) {
+          const int i = ij[u] >> 8, j = ij[u] & 255;
+          if (e0 + u < n_act && !(i == k + 1 && j == k + 1)) {
             double av[4], bv[4];
-            ld_slot(sPan + (size_t)bi[u] * 256, lane, av);
-            ld_slot(sPan + (size_t)bj[u] * 256, lane, bv);
+            ld_slot(pc + (size_t)j * 256, lane, av);
+            ld_slot(pc + (size_t)i * 256, lane, bv);
 #pragma unroll
-            for (int s = 0; s < 4; ++s) av[s] = -av[s];
-            st_c(blk[u], mma16(acc[u], av, bv), lane);
+            for (int q = 0; q < 4; ++q) av[q] = -av[q];
+            acc[u] = mma16(acc[u], av, bv);
+            if (e0 + u < n_trail) {
+              st_c(a.L + ((size_t)i * nb + j) * 256, acc[u], lane);
+              if (i == k + 2 && j == k + 2) st_c(sNext, acc[u], lane);
+            }
+          }
+        }
+        if (e0 + 3 >= n_trail) {  // a block of column k+1 among the four
+          wait_x();
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int i = ij[u] >> 8;
+            if (e0 + u >= n_trail && e0 + u < n_act && i != k + 1) {
+              const double tv[4] = {acc[u][0], acc[u][1], acc[u][2], acc[u][3]};
+              const d4_t v = mma16(zero4(), xv, tv);
+              st_c(a.L + ((size_t)i * nb + k + 1) * 256, v, lane);
+              st_col_slot(pn + (size_t)i * 256, v, lane);
+            }
           }
         }
       }
+      // resident blocks of column k+1: the panel
+      if (n_trail < kRes && n_trail < n_act) {
+        wait_x();
+#pragma unroll
+        for (int s = 0; s < kRes; ++s) {
+          const int i = rij[s] >> 8;
+          if (s >= n_trail && s < n_act && i != k + 1) {
+            const double tv[4] = {res[s][0], res[s][1], res[s][2], res[s][3]};
+            const d4_t v = mma16(zero4(), xv, tv);
+            st_c(a.L + ((size_t)i * nb + k + 1) * 256, v, lane);
+            st_col_slot(pn + (size_t)i * 256, v, lane);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
     }
-    __syncthreads();
+    lds_barrier();
   }
-
+  const bool failed = sFlag[0] || sFlag[2];
+  if (tid == 0 && sFlag[2]) {
+    a.out[1] = 2.0;  // a wait ran out: reported as a device failure
+    return;
+  }
   if (tid == 0) a.out[1] = failed ? 0.0 : 1.0;
   if (failed) return;
   if (tid < nb) a.prod[tid] = sProd[tid];
-  // inverses of the diagonal blocks, one column per lane of a group of 16
-  const int grp = tid >> 4, q = tid & 15;
-  for (int jb = grp; jb < nb; jb += kNllThreads / 16) {
-    const double* Lb = a.L + ((size_t)jb * nb + jb) * 256;
-    double x[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      double acc = i == q ? 1.0 : 0.0;
-#pragma unroll
-      for (int t = 0; t < i; ++t) acc = fma(-Lb[i * 16 + t], x[t], acc);
-      x[i] = acc / Lb[i * 16 + i];
-    }
-    double* Db = a.Di + (size_t)jb * 256;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) Db[i * 16 + q] = x[i];
-  }
 }
 
 // ---- kernel T: L^-1, one block column per workgroup ---------------------------
-// Column j: X_jj = Di_j, then for i = j+1 .. nb-1
-//   X_ij = -Di_i sum_{k=j}^{i-1} L_ik X_kj,
-// the sum split over the four waves (added in wave order), X's column kept in
-// LDS as column slots for the next rows.
-constexpr int kTriWaves = 4;
-__global__ __launch_bounds__(kTriWaves * 64) void nll_trtri_kernel(NllArgs a) {
-  extern __shared__ __align__(16) double sm[];
-  if (a.out[1] != 1.0) return;
-  const int nb = a.nb, j = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  double* sX = sm;                            // nb column slots: X_kj
-  double* sPart = sX + (size_t)nb * 256;      // kTriWaves column slots: partial sums
-  if (wave == 0) {
-    const d4_t v = ld_c(a.Di + (size_t)j * 256, lane);
-    st_col_slot(sX + (size_t)j * 256, v, lane);
-    st_c(a.Xi + ((size_t)j * nb + j) * 256, v, lane);
-  }
-  __syncthreads();
-  for (int i = j + 1; i < nb; ++i) {
-    d4_t S = zero4();
-    for (int k = j + wave; k < i; k += kTriWaves) {
-      double av[4], bv[4];
-      ld_rows(a.L + ((size_t)i * nb + k) * 256, lane, av);
-      ld_slot(sX + (size_t)k * 256, lane, bv);
-      S = mma16(S, av, bv);
-    }
-    st_col_slot(sPart + wave * 256, S, lane);
-    __syncthreads();
-    if (wave == 0) {
-      d4_t T = zero4();
-      for (int w = 0; w < kTriWaves; ++w) {
-        double pv[4];
-        ld_slot(sPart + w * 256, lane, pv);
+// Column j: X_jj = Di_j, and for i > j
+//   X_ij = -Di_i S_ij,   S_ij = sum_{k=j}^{i-1} L_ik X_kj.
+// Right-looking: as soon as X_kj is known every later row i adds its term
+// L_ik X_kj to S_ij, which the wave that finishes row i keeps in registers
+// (rows dealt round robin to the waves, R per wave at most); the owner of row
+// k+1 then finishes X_k+1,j into LDS, where the column stays until it is
+// written out at the end.  L was written by another compute unit, so its
+// blocks (column-major: an A operand is a contiguous read) are loaded
+// kTriAhead steps ahead into a ring of registers, and Di up front; every step
+// issues the same loads (a row with nothing to load reads block (0, 0)), so
+// each wait is for exactly the load it needs.
+constexpr int kTriWaves = 8;
+constexpr int kTriMaxRows = (SCOOT_MAX_OBS / 16 - 1 + kTriWaves - 1) / kTriWaves;
+constexpr int kTriAhead = 3;
+
+template <int R>
+struct TriState {
+  d4_t S[R];
+  double Lv[kTriAhead][R][4];  // ring: L_ik for steps k, k+1, k+2 in slot (k - j) % 3
+  double Dv[R][4];             // Di_i
+};
+
+// Step k of column j; ring slot B holds L_ik.  Steps past the column's end
+// only load and wait, so that every wave runs the same number of barriers.
+template <int R, int B>
+__device__ inline void tri_step(const NllArgs& a, TriState<R>& st, double* sXcol, int j, int k, int wave,
+                                int lane) {
+  const int nb = a.nb;
+  double xv[4];
+  ld_slot(sXcol + (size_t)(k < nb ? k : nb - 1) * 256, lane, xv);  // X_kj as a B operand
 #pragma unroll
-        for (int r = 0; r < 4; ++r) T[r] += pv[r];
+  for (int t = 0; t < R; ++t) {
+    const int i = j + 1 + wave + kTriWaves * t;
+    if (i > k && i < nb) {  // row k+1 (if this wave's) comes first
+      st.S[t] = mma16(st.S[t], st.Lv[B][t], xv);
+      if (i == k + 1) {
+        double nd[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) nd[s] = -st.Dv[t][s];
+        const double sv[4] = {st.S[t][0], st.S[t][1], st.S[t][2], st.S[t][3]};  // S as a B operand is its own C layout
+        st_col_slot(sXcol + (size_t)i * 256, mma16(zero4(), nd, sv), lane);
       }
-      double av[4];
-      ld_rows(a.Di + (size_t)i * 256, lane, av);
-#pragma unroll
-      for (int s = 0; s < 4; ++s) av[s] = -av[s];
-      const double tb[4] = {T[0], T[1], T[2], T[3]};  // T as a B operand is its own C layout
-      const d4_t v = mma16(zero4(), av, tb);
-      st_col_slot(sX + (size_t)i * 256, v, lane);
-      st_c(a.Xi + ((size_t)i * nb + j) * 256, v, lane);
     }
-    __syncthreads();
+    const bool next = i < nb && k + kTriAhead < i;
+    ld_cols(a.L + (next ? ((size_t)i * nb + k + kTriAhead) * 256 : 0), lane, st.Lv[B][t]);
+  }
+  lds_barrier();
+}
+
+template <int R>
+__global__ __launch_bounds__(kTriWaves * 64) void nll_trtri_kernel(NllArgs a) {
+  extern __shared__ __align__(16) double sXcol[];  // nb column slots: X_ij, i >= j
+  if (a.out[1] != 1.0) return;
+  const int nb = a.nb, j = blockIdx.x, lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  TriState<R> st;
+#pragma unroll
+  for (int t = 0; t < R; ++t) {
+    st.S[t] = zero4();
+    const int i = j + 1 + wave + kTriWaves * t;
+#pragma unroll
+    for (int b = 0; b < kTriAhead; ++b)
+      ld_cols(a.L + (i < nb && j + b < i ? ((size_t)i * nb + j + b) * 256 : 0), lane, st.Lv[b][t]);
+    ld_rows(a.Di + (i < nb ? (size_t)i * 256 : 0), lane, st.Dv[t]);
+  }
+  if (wave == 0) st_col_slot(sXcol + (size_t)j * 256, ld_c(a.Di + (size_t)j * 256, lane), lane);
+  // all of the above in registers before the loop, so that inside it a wait
+  // is only ever for the ring slot about to be used
+  __builtin_amdgcn_s_waitcnt(0);
+  lds_barrier();
+  for (int k = j; k + 1 < nb; k += kTriAhead) {
+    tri_step<R, 0>(a, st, sXcol, j, k, wave, lane);
+    tri_step<R, 1>(a, st, sXcol, j, k + 1, wave, lane);
+    tri_step<R, 2>(a, st, sXcol, j, k + 2, wave, lane);
+  }
+  // the column, row-major blocks
+  for (int i = j + wave; i < nb; i += kTriWaves) {
+    double x[4];
+    ld_slot(sXcol + (size_t)i * 256, lane, x);
+    st_c(a.Xi + ((size_t)i * nb + j) * 256, d4_t{x[0], x[1], x[2], x[3]}, lane);
   }
 }
 
@@ -603,19 +736,24 @@ __global__ __launch_bounds__(kGradThreads) void nll_grad_kernel(NllArgs a) {
 // a fixed butterfly); workgroup P forms the NLL from the quadratic form's
 // per-block parts and the pivots' products.
 __global__ __launch_bounds__(64) void nll_finish_kernel(NllArgs a, int P, int with_grad) {
-  if (a.out[1] != 1.0) return;
+  const double status = a.out[1];
   const int lane = threadIdx.x, p = blockIdx.x;
   if (p < P) {
-    if (!with_grad) return;
+    if (status != 1.0 || !with_grad) return;
     const double v = wave_sum(lane < kGradBlocks ? a.part[(size_t)lane * P + p] : 0.0);
-    if (lane == 0) a.out[2 + p] = v;
+    if (lane == 0) a.hout[2 + p] = v;
   } else if (lane == 0) {
-    double q = 0.0, logdet = 0.0;
-    for (int k = 0; k < a.nb; ++k) {
-      q += a.qpart[k];
-      logdet += log(a.prod[k]);
+    double nll = 0.0;
+    if (status == 1.0) {
+      double q = 0.0, logdet = 0.0;
+      for (int k = 0; k < a.nb; ++k) {
+        q += a.qpart[k];
+        logdet += log(a.prod[k]);
+      }
+      nll = 0.5 * q + 0.5 * logdet + 0.5 * a.m * kLog2PiD;
     }
-    a.out[0] = 0.5 * q + 0.5 * logdet + 0.5 * a.m * kLog2PiD;
+    a.hout[0] = nll;
+    a.hout[1] = status;
   }
 }
 
@@ -655,10 +793,17 @@ class DeviceNll {
       buf_ = nullptr;
       return fail(SCOOT_ERR_NO_MEMORY, "gp nll: device allocation failed");
     }
-    if (hipHostMalloc(&host_, (2 + P_) * sizeof(double), hipHostMallocDefault) != hipSuccess) {
+    // the results, written by the last kernel straight into coherent pinned
+    // host memory (no copy after it)
+    if (hipHostMalloc(&host_, (2 + P_) * sizeof(double), hipHostMallocMapped | hipHostMallocCoherent) !=
+        hipSuccess) {
       host_ = nullptr;
       return fail(SCOOT_ERR_NO_MEMORY, "gp nll: pinned allocation failed");
     }
+    void* hdev = nullptr;
+    if (hipHostGetDevicePointer(&hdev, host_, 0) != hipSuccess || hdev == nullptr)
+      return fail(SCOOT_ERR_DEVICE, "gp nll: pinned memory not visible to the device");
+    a_.hout = static_cast<double*>(hdev);
     double* p = buf_;
     double* Xd = p;
     p += up(md);
@@ -701,10 +846,16 @@ class DeviceNll {
         hipMemcpyAsync(rd, rp.data(), mp * sizeof(double), hipMemcpyHostToDevice, s) != hipSuccess ||
         hipStreamSynchronize(s) != hipSuccess)
       return fail(SCOOT_ERR_DEVICE, std::string("gp nll: upload failed: ") + hipGetErrorString(hipGetLastError()));
-    lds_ = ((size_t)nb_ * 256 + 16 * 17 + 16 + 256 + SCOOT_MAX_OBS / 16 + kNllWaves + 2 + kNllWaves) * sizeof(double);
-    lds_tri_ = ((size_t)nb_ + kTriWaves) * 256 * sizeof(double);
-    const int rc = allow_full_lds((const void*)nll_factor_kernel, "gp nll");
-    return rc != SCOOT_OK ? rc : allow_full_lds((const void*)nll_trtri_kernel, "gp nll");
+    lds_ = ((size_t)nb_ * 512 + 256 + 512 + SCOOT_MAX_OBS / 16) * sizeof(double) +
+           (4 + kNllWaves + (size_t)nb_ * (nb_ - 1) / 2) * sizeof(int);
+
+    int rc = allow_full_lds((const void*)nll_factor_kernel, "gp nll");
+    const void* tri[] = {(const void*)nll_trtri_kernel<1>, (const void*)nll_trtri_kernel<2>,
+                         (const void*)nll_trtri_kernel<3>, (const void*)nll_trtri_kernel<4>,
+                         (const void*)nll_trtri_kernel<kTriMaxRows>};
+    for (const void* f : tri)
+      if (rc == SCOOT_OK) rc = allow_full_lds(f, "gp nll");
+    return rc;
   }
   // false when K is not positive definite; a device failure is kept in error().
   bool eval(const double* theta, double* nll, double* grad) {
@@ -715,7 +866,15 @@ class DeviceNll {
       hipLaunchKernelGGL(nll_warp_kernel, dim3((unsigned)((m_ * d_ + 255) / 256)), dim3(256), 0, s_, a_);
     hipLaunchKernelGGL(nll_cov_kernel, dim3((unsigned)(nb_ * (nb_ + 1) / 2)), dim3(256), 0, s_, a_);
     hipLaunchKernelGGL(nll_factor_kernel, dim3(1), dim3(kNllThreads), lds_, s_, a_);
-    hipLaunchKernelGGL(nll_trtri_kernel, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri_, s_, a_);
+    const size_t lds_tri = (size_t)nb_ * 256 * sizeof(double);
+    switch ((nb_ - 1 + kTriWaves - 1) / kTriWaves) {
+      case 0:
+      case 1: hipLaunchKernelGGL(nll_trtri_kernel<1>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
+      case 2: hipLaunchKernelGGL(nll_trtri_kernel<2>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
+      case 3: hipLaunchKernelGGL(nll_trtri_kernel<3>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
+      case 4: hipLaunchKernelGGL(nll_trtri_kernel<4>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
+      default: hipLaunchKernelGGL(nll_trtri_kernel<kTriMaxRows>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_);
+    }
     hipLaunchKernelGGL(nll_lauum_kernel, dim3((unsigned)(nb_ * (nb_ + 1) / 2)), dim3(64), 0, s_, a_);
     hipLaunchKernelGGL(nll_alpha_kernel, dim3((unsigned)nb_), dim3(64), 0, s_, a_);
     if (grad) {
@@ -739,10 +898,13 @@ class DeviceNll {
       rc_ = fail(SCOOT_ERR_DEVICE, std::string("gp nll: launch failed: ") + hipGetErrorString(launched));
       return false;
     }
-    if (hipMemcpyAsync(host_, a_.out, (2 + P_) * sizeof(double), hipMemcpyDeviceToHost, s_) != hipSuccess ||
-        hipStreamSynchronize(s_) != hipSuccess) {
+    if (hipStreamSynchronize(s_) != hipSuccess) {
       rc_ = fail(SCOOT_ERR_DEVICE, std::string("gp nll: device evaluation failed: ") +
                                        hipGetErrorString(hipGetLastError()));
+      return false;
+    }
+    if (host_[1] == 2.0) {
+      rc_ = fail(SCOOT_ERR_DEVICE, "gp nll: the factorization's wait for its diagonal block ran out");
       return false;
     }
     if (host_[1] != 1.0) return false;
@@ -756,7 +918,7 @@ class DeviceNll {
   hipStream_t s_ = nullptr;
   int m_ = 0, d_ = 0, nb_ = 0, P_ = 0;
   bool lw_ = false;
-  size_t lds_ = 0, lds_tri_ = 0;
+  size_t lds_ = 0;
   double* buf_ = nullptr;
   double* host_ = nullptr;
   NllArgs a_{};

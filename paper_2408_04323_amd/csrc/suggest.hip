@@ -205,9 +205,10 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
       // so the objectives' kernels run side by side.
       const bool on_device = o.host_search == 0;
       int device = 0;
+      if (hipGetDevice(&device) != hipSuccess) return fail(SCOOT_ERR_DEVICE, "suggest: no current device");
       std::vector<hipStream_t> streams(p, nullptr);
+      h.gps.assign(p, nullptr);  // each search thread fits its objective's GP as soon as it has theta
       if (on_device) {
-        if (hipGetDevice(&device) != hipSuccess) return fail(SCOOT_ERR_DEVICE, "suggest: no current device");
         for (int j = 0; j < p; ++j)
           if (hipStreamCreateWithFlags(&streams[j], hipStreamNonBlocking) != hipSuccess) {
             for (int q = 0; q < j; ++q) (void)hipStreamDestroy(streams[q]);
@@ -226,12 +227,12 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
           const double* wa = o.warp_a ? o.warp_a + (size_t)j * d : nullptr;
           const double* wb = o.warp_b ? o.warp_b + (size_t)j * d : nullptr;
           const int iters = o.mle_max_iter > 0 ? o.mle_max_iter : kDefaultMleIter;
+          if (hipSetDevice(device) != hipSuccess) {
+            search_rc[j] = SCOOT_ERR_DEVICE;
+            search_err[j] = "suggest: cannot select the device";
+            return;
+          }
           if (!all_fixed && on_device) {
-            if (hipSetDevice(device) != hipSuccess) {
-              search_rc[j] = SCOOT_ERR_DEVICE;
-              search_err[j] = "suggest: cannot select the device";
-              return;
-            }
             search_rc[j] = scoot_gp_mle_device(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel,
                                                lw ? nullptr : wa, lw ? nullptr : wb, 0.0, lw ? 1 : 0, lo, hi, iters, th,
                                                nullptr, nullptr, streams[j]);
@@ -244,6 +245,22 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
             if (search_rc[j] != SCOOT_OK) search_err[j] = scoot_last_error();  // this thread's message
           }
           std::memcpy(&theta[(size_t)j * nt], th, sizeof(double) * nt);
+          if (search_rc[j] != SCOOT_OK) return;
+          // the GP at the hyperparameters found
+          double ell[SCOOT_MAX_DIM], la[SCOOT_MAX_DIM], lb[SCOOT_MAX_DIM];
+          for (int t = 0; t < d; ++t) ell[t] = std::exp(th[t]);
+          if (lw) {
+            for (int t = 0; t < d; ++t) {
+              la[t] = std::exp(th[d + 2 + t]);
+              lb[t] = std::exp(th[2 * d + 2 + t]);
+            }
+            wa = la;
+            wb = lb;
+          }
+          search_rc[j] = scoot_gp_fit_ex(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, ell, wa, wb,
+                                         std::exp(th[d]), std::exp(th[d + 1]), 0.0, (scoot_dtype)o.dtype, stream,
+                                         &h.gps[j]);
+          if (search_rc[j] != SCOOT_OK) search_err[j] = scoot_last_error();
         } catch (...) {
           search_rc[j] = SCOOT_ERR_NO_MEMORY;
           search_err[j] = "suggest: hyperparameter search ran out of memory";
@@ -273,28 +290,6 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
       if (forest_rc != SCOOT_OK) return fail(forest_rc, forest_err);
       for (int j = 0; j < p; ++j)
         if (search_rc[j] != SCOOT_OK) return fail(search_rc[j], search_err[j]);
-      for (int j = 0; j < p; ++j) {
-        const double* th = &theta[(size_t)j * nt];
-        std::vector<double> yj(m);
-        for (int r = 0; r < m; ++r) yj[r] = Yv[(size_t)r * p + j];
-        const double* wa = o.warp_a ? o.warp_a + (size_t)j * d : nullptr;
-        const double* wb = o.warp_b ? o.warp_b + (size_t)j * d : nullptr;
-        double ell[SCOOT_MAX_DIM], la[SCOOT_MAX_DIM], lb[SCOOT_MAX_DIM];
-        for (int t = 0; t < d; ++t) ell[t] = std::exp(th[t]);
-        if (lw) {
-          for (int t = 0; t < d; ++t) {
-            la[t] = std::exp(th[d + 2 + t]);
-            lb[t] = std::exp(th[2 * d + 2 + t]);
-          }
-          wa = la;
-          wb = lb;
-        }
-        scoot_gp g = nullptr;
-        rc = scoot_gp_fit_ex(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, ell, wa, wb, std::exp(th[d]),
-                             std::exp(th[d + 1]), 0.0, (scoot_dtype)o.dtype, stream, &g);
-        if (rc != SCOOT_OK) return rc;
-        h.gps.push_back(g);
-      }
       if (theta_out) std::memcpy(theta_out, theta.data(), sizeof(double) * theta.size());
 
       // ---- 5. score the pool and pick ----------------------------------
