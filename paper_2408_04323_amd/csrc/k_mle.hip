@@ -4,30 +4,34 @@
 // box-constrained L-BFGS of host_mle.cpp) stays on the host and calls this
 // once per trial point.
 //
-// With r = y - c, K = k_theta(X, X) + tau2 I (m x m) and W = alpha alpha^T - K^-1:
-//   NLL = 1/2 r^T alpha + 1/2 log det K + m/2 log(2 pi),   alpha = K^-1 r
+// With r = y - c, K = k_theta(X, X) + tau2 I (m x m), K = L L^T, u = L^-1 r and
+// W = alpha alpha^T - K^-1:
+//   NLL = 1/2 u^T u + 1/2 log det K + m/2 log(2 pi),   alpha = K^-1 r = L^-T u
 //   dNLL/dtheta_p = -1/2 sum_ij W_ij (dK/dtheta_p)_ij
 // with the derivatives of the covariance written out in host_mle.cpp.
 //
-// Matrices are 16 x 16 blocks (row-major inside a block), m padded to a
-// multiple of 16 with identity rows (their covariance with real rows is 0,
-// their diagonal 1, their r 0: log det, the quadratic form and the gradient do
-// not see them).  The kernels of one evaluation, on one stream:
+// Matrices are 16 x 16 blocks, m padded to a multiple of 16 with identity rows
+// (their covariance with real rows is 0, their diagonal 1, their r 0: log det,
+// the quadratic form and the gradient do not see them).  The kernels of one
+// evaluation, on one stream:
 //   W. (warp learned) the warped inputs and their derivatives;
 //   K. K, one 16 x 16 block per workgroup;
 //   A. one workgroup (8 waves): the Cholesky factor L by 16-column block
 //      steps: the diagonal block factored and inverted by one wave in
 //      registers (a rank-1 update per column on v_mfma_f64_16x16x4f64), the
 //      panel below it as the product with that inverse and the trailing
-//      update, both on the matrix cores; the next diagonal block is factored
-//      as soon as it is updated, by a wave whose SIMD the others leave free;
-//   T. L^-1, one block column per workgroup (the columns are independent);
+//      update, both on the matrix cores, and u = L^-1 r by forward
+//      substitution alongside; the next diagonal block is factored as soon
+//      as it is updated, by a wave whose SIMD the others leave free;
+// and, when the gradient is wanted,
+//   T. L^-1 and alpha = L^-T u, one block column per workgroup (the columns
+//      are independent);
 //   U. K^-1 = L^-T L^-1, one block per workgroup;
-//   V. alpha = K^-1 r and the quadratic form, one block row per workgroup;
 //   B. the gradient: one element of W per thread, the covariance and its
-//      derivatives recomputed, partial sums per workgroup;
-//   C. the NLL and the gradient's partial sums, added in a fixed order.
-// Every operation is in double and every sum has a fixed order, so an
+//      derivatives recomputed, partial sums per workgroup.
+// The kernels write their results (status, pivot products, |u|^2 per block,
+// partial gradient sums) straight into pinned host memory, and the host adds
+// them.  Every operation is in double and every sum has a fixed order, so an
 // evaluation is deterministic.
 #include <hip/hip_runtime.h>
 
@@ -63,12 +67,14 @@ struct NllArgs {
   double* Xw;       // m x d warped inputs (warp learned)
   double* Ga;       // m x d: d w / d log a (warp learned)
   double* Gb;       // m x d: d w / d log b (warp learned)
-  double* alpha;    // m_pad
-  double* prod;     // nb: product of each diagonal block's pivots (real rows)
-  double* qpart;    // nb: r^T alpha over each block of 16 rows
+  double* alpha;    // m_pad: K^-1 r
+  double* u;        // m_pad: L^-1 r
   double* out;      // [1] 1 when K is numerically positive definite, 0 when not, 2 when a wait ran out
-  double* hout;     // pinned host memory: [0] NLL, [1] the status of out[1], [2 ..] gradient
-  double* part;     // kGradBlocks x P partial gradient sums
+  // Pinned host memory the kernels write their results to: [0] the status of
+  // out[1], [1 .. nb] the product of each diagonal block's pivots (real rows),
+  // [nb + 1 ..] u (16 nb values), then kGradBlocks x P partial gradient sums;
+  // the host adds them in a fixed order.
+  double* hout;
   int m, nb, d, m52, learn_warp;
   double theta[kMaxTheta];
 };
@@ -285,6 +291,37 @@ __device__ inline void diag_factor(const NllArgs& a, int kk, d4_t D, double* sX,
   }
 }
 
+// Forward substitution for u = L^-1 r, the diagonal block's part: u_kk =
+// L_kk^-1 r_kk with L_kk^-1 from its row slot sX and r_kk (the residual) from
+// LDS, as one product C = R L_kk^-T where every row of R is r_kk, so that
+// every row of C is u_kk; to sU (16), to memory and to the host.
+__device__ inline void diag_solve(const NllArgs& a, int kk, const double* sX, const double* rk, double* sU,
+                                  int lane) {
+  const int g = lane >> 4, c = lane & 15;
+  double av[4], bv[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) av[s] = rk[4 * s + g];
+  ld_slot(sX, lane, bv);  // (L_kk^-1)^T as a B operand
+  const d4_t v = mma16(zero4(), av, bv);
+  if (lane < 16) {
+    sU[c] = v[0];
+    a.u[16 * kk + c] = v[0];
+    a.hout[1 + a.nb + 16 * kk + c] = v[0];
+  }
+}
+
+// The residual's update by a panel block: r_i -= L_ik u_k, with L_ik from its
+// row slot (lane (g, c) holds L_ik[c][4s + g]) and u_k in LDS.
+__device__ inline void resid_update(double* ri, const double* slot, const double* uk, int lane) {
+  const int g = lane >> 4;
+  double lv[4];
+  ld_slot(slot, lane, lv);
+  double s = lv[0] * uk[g] + lv[1] * uk[4 + g] + lv[2] * uk[8 + g] + lv[3] * uk[12 + g];
+  s += __shfl_xor(s, 16);
+  s += __shfl_xor(s, 32);
+  if (lane < 16) ri[lane] -= s;
+}
+
 // ---- kernel A: the Cholesky factor L and the inverses of its diagonal blocks --
 // Blocks are held transposed: the covariance kernel writes block (I, J)
 // column-major, the workers' registers hold A_ij^T in C layout (A_ij as an A
@@ -303,9 +340,11 @@ __global__ __launch_bounds__(kNllThreads) void nll_factor_kernel(NllArgs a) {
   double* sX = sPan + (size_t)2 * nb * 256;   // row slot: the inverse of the newest diagonal factor
   double* sDiag = sX + 256;                   // 2 x 256: the next diagonal blocks as updated (C layout)
   double* sProd = sDiag + 512;                // per diagonal block: product of its pivots
+  double* sR = sProd + SCOOT_MAX_OBS / 16;    // nb x 16: r, then the forward substitution's residual
+  double* sU = sR + (size_t)nb * 16;          // 2 x 16: u_k, by k % 2
   // [0] a pivot not above its floor, [1] the last diagonal block factored,
   // [2] a wait for it ran out
-  int* sFlag = reinterpret_cast<int*>(sProd + SCOOT_MAX_OBS / 16);
+  int* sFlag = reinterpret_cast<int*>(sU + 32);
   int* sSimd = sFlag + 4;                     // kNllWaves: the SIMD each wave runs on
   int* sList = sSimd + kNllWaves;             // the worker blocks, (i << 8) | j
 
@@ -313,6 +352,7 @@ __global__ __launch_bounds__(kNllThreads) void nll_factor_kernel(NllArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   if (lane == 0) sSimd[wave] = (int)((__builtin_amdgcn_s_getreg((31 << 11) | 4) >> 4) & 3);  // HW_ID.SIMD_ID
   if (tid < 4) sFlag[tid] = 0;
+  for (int i = tid; i < nb * 16; i += kNllThreads) sR[i] = a.r[i];
   const int n_list = nb > 1 ? nb * (nb - 1) / 2 - 1 : 0;
   for (int n = tid; n < n_list; n += kNllThreads) {
     int start = 0;
@@ -366,6 +406,8 @@ __global__ __launch_bounds__(kNllThreads) void nll_factor_kernel(NllArgs a) {
   for (int s = 0; s < kRes; ++s) rij[s] = s < n_share ? __builtin_amdgcn_readfirstlane(sList[worker + W * s]) : 0;
   if (wave == 0) {
     diag_factor(a, 0, ld_c(a.L, lane), sX, sProd, sFlag, floor, lane);
+    wave_lds_sync();
+    diag_solve(a, 0, sX, sR, sU, lane);
   } else {
     // the blocks of column 0, while wave 0 factors block (0, 0)
 #pragma unroll
@@ -415,6 +457,11 @@ __global__ __launch_bounds__(kNllThreads) void nll_factor_kernel(NllArgs a) {
       diag_factor(a, i, acc, sX, sProd, sFlag, floor, lane);
       wave_lds_sync();  // the inverse is in LDS
       if (lane == 0) __hip_atomic_store(&sFlag[1], i, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+      // while the workers make the panel: the residual of block k+1 takes
+      // column k's last term (the other blocks' come from the workers this
+      // step), then u_k+1
+      resid_update(sR + 16 * i, pc + (size_t)i * 256, sU + (k & 1) * 16, lane);
+      diag_solve(a, i, sX, sR + 16 * i, sU + (i & 1) * 16, lane);
     } else if (worker >= 0) {
       const int n_trail = mine_below(from_col(k + 2));  // the share's blocks with j >= k+2
       const int n_act = mine_below(from_col(k + 1));    // ... with j >= k+1
@@ -450,6 +497,9 @@ __global__ __launch_bounds__(kNllThreads) void nll_factor_kernel(NllArgs a) {
         }
         __builtin_amdgcn_sched_barrier(0);  // a block's operands loaded where it is updated
       }
+      // column k's term of the forward substitution for the blocks below k+1,
+      // r_i -= L_ik u_k, round robin over the workers
+      for (int i = k + 2 + worker; i < nb; i += W) resid_update(sR + 16 * i, pc + (size_t)i * 256, sU + (k & 1) * 16, lane);
       // the others, four at a time, their loads first: the blocks with
       // j >= k+2 back to memory, then those of column k+1 into the panel
       for (int e0 = kRes; e0 < n_act; e0 += 4) {
@@ -508,14 +558,14 @@ __global__ __launch_bounds__(kNllThreads) void nll_factor_kernel(NllArgs a) {
     }
     lds_barrier();
   }
-  const bool failed = sFlag[0] || sFlag[2];
-  if (tid == 0 && sFlag[2]) {
-    a.out[1] = 2.0;  // a wait ran out: reported as a device failure
-    return;
+  // status: 1 factored, 0 not positive definite, 2 a wait ran out (reported as
+  // a device failure)
+  const double status = sFlag[2] ? 2.0 : (sFlag[0] ? 0.0 : 1.0);
+  if (tid == 0) {
+    a.out[1] = status;
+    a.hout[0] = status;
   }
-  if (tid == 0) a.out[1] = failed ? 0.0 : 1.0;
-  if (failed) return;
-  if (tid < nb) a.prod[tid] = sProd[tid];
+  if (status == 1.0 && tid < nb) a.hout[1 + tid] = sProd[tid];
 }
 
 // ---- kernel T: L^-1, one block column per workgroup ---------------------------
@@ -572,9 +622,22 @@ template <int R>
 __global__ __launch_bounds__(kTriWaves * 64) void nll_trtri_kernel(NllArgs a) {
   extern __shared__ __align__(16) double sXcol[];  // nb column slots: X_ij, i >= j
   if (a.out[1] != 1.0) return;
-  const int nb = a.nb, j = blockIdx.x, lane = threadIdx.x & 63;
+  double* sAl = sXcol + (size_t)a.nb * 256;        // kTriWaves x 16: alpha's parts
+  const int nb = a.nb, j = blockIdx.x, lane = threadIdx.x & 63, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   TriState<R> st;
+  // u_i[4s + g] of the wave's rows and of row j (wave 0), loaded up front
+  // unless the registers are wanted for the ring
+  double uv[R + 1][4];
+  auto load_u = [&]() {
+#pragma unroll
+    for (int t = 0; t <= R; ++t) {
+      const int i = t < R ? j + 1 + wave + kTriWaves * t : j;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) uv[t][s] = i < nb ? a.u[16 * i + 4 * s + g] : 0.0;
+    }
+  };
+  if constexpr (R <= 4) load_u();
 #pragma unroll
   for (int t = 0; t < R; ++t) {
     st.S[t] = zero4();
@@ -599,6 +662,30 @@ __global__ __launch_bounds__(kTriWaves * 64) void nll_trtri_kernel(NllArgs a) {
     double x[4];
     ld_slot(sXcol + (size_t)i * 256, lane, x);
     st_c(a.Xi + ((size_t)i * nb + j) * 256, d4_t{x[0], x[1], x[2], x[3]}, lane);
+  }
+  // alpha_j = sum_{i >= j} X_ij^T u_i (alpha = L^-T L^-1 r): each wave its rows,
+  // then the waves in order
+  if constexpr (R > 4) load_u();
+  double acc = 0.0;
+#pragma unroll
+  for (int t = 0; t <= R; ++t) {
+    const int i = t < R ? j + 1 + wave + kTriWaves * t : j;
+    if (i < nb && (t < R || wave == 0)) {
+      double x[4];
+      ld_slot(sXcol + (size_t)i * 256, lane, x);  // X_ij[4s + g][c]
+#pragma unroll
+      for (int s = 0; s < 4; ++s) acc = fma(x[s], uv[t][s], acc);
+    }
+  }
+  acc += __shfl_xor(acc, 16);
+  acc += __shfl_xor(acc, 32);
+  if (lane < 16) sAl[wave * 16 + lane] = acc;
+  lds_barrier();
+  if (wave == 0 && lane < 16) {
+    double s = 0.0;
+#pragma unroll
+    for (int w = 0; w < kTriWaves; ++w) s += sAl[w * 16 + lane];
+    a.alpha[16 * j + lane] = s;
   }
 }
 
@@ -632,42 +719,6 @@ __global__ __launch_bounds__(64) void nll_lauum_kernel(NllArgs a) {
     for (int r = 0; r < 4; ++r) Zv[r] = 0.5 * (Zv[r] + sT[c * 16 + g + 4 * r]);
   }
   st_c(a.Z + ((size_t)I * nb + J) * 256, Zv, lane);
-}
-
-// ---- kernel V: alpha = K^-1 r and r^T alpha per block of 16 rows --------------
-__global__ __launch_bounds__(64) void nll_alpha_kernel(NllArgs a) {
-  if (a.out[1] != 1.0) return;
-  const int nb = a.nb, I = blockIdx.x, lane = threadIdx.x;
-  const int rowoff = (lane & 15) * 16 + (lane >> 4);
-  double acc = 0.0;
-  for (int J = 0; J < nb; J += 4) {
-    double av[4][4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int JJ = J + u;
-      if (JJ < nb) {
-        const bool below = JJ < I;  // Z_IJ stored, else Z_JI^T (Z_II is symmetric)
-        const double* p = a.Z + (below ? (size_t)I * nb + JJ : (size_t)JJ * nb + I) * 256 + (below ? rowoff : lane);
-        const int str = below ? 4 : 64;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) av[u][s] = p[s * str];
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (J + u < nb)
-#pragma unroll
-        for (int s = 0; s < 4; ++s) acc += av[u][s] * a.r[16 * (J + u) + 4 * s + (lane >> 4)];
-  }
-  acc += __shfl_xor(acc, 16);
-  acc += __shfl_xor(acc, 32);
-  double q = 0.0;
-  if (lane < 16) {
-    a.alpha[16 * I + lane] = acc;
-    q = acc * a.r[16 * I + lane];
-  }
-  q = wave_sum(q);
-  if (lane == 0) a.qpart[I] = q;
 }
 
 // ---- kernel B: gradient partial sums ----------------------------------------
@@ -727,33 +778,7 @@ __global__ __launch_bounds__(kGradThreads) void nll_grad_kernel(NllArgs a) {
     double s = 0.0;
 #pragma unroll
     for (int w = 0; w < kGradThreads / 64; ++w) s += sRed[w][t];
-    a.part[(size_t)blockIdx.x * P + t] = s;
-  }
-}
-
-// ---- kernel C: the NLL, and the gradient's partial sums in block order -------
-// Workgroup p < P adds parameter p's kGradBlocks partial sums (one per lane,
-// a fixed butterfly); workgroup P forms the NLL from the quadratic form's
-// per-block parts and the pivots' products.
-__global__ __launch_bounds__(64) void nll_finish_kernel(NllArgs a, int P, int with_grad) {
-  const double status = a.out[1];
-  const int lane = threadIdx.x, p = blockIdx.x;
-  if (p < P) {
-    if (status != 1.0 || !with_grad) return;
-    const double v = wave_sum(lane < kGradBlocks ? a.part[(size_t)lane * P + p] : 0.0);
-    if (lane == 0) a.hout[2 + p] = v;
-  } else if (lane == 0) {
-    double nll = 0.0;
-    if (status == 1.0) {
-      double q = 0.0, logdet = 0.0;
-      for (int k = 0; k < a.nb; ++k) {
-        q += a.qpart[k];
-        logdet += log(a.prod[k]);
-      }
-      nll = 0.5 * q + 0.5 * logdet + 0.5 * a.m * kLog2PiD;
-    }
-    a.hout[0] = nll;
-    a.hout[1] = status;
+    a.hout[1 + 17 * nb + (size_t)blockIdx.x * P + t] = s;
   }
 }
 
@@ -786,17 +811,17 @@ class DeviceNll {
     // every part 256-byte aligned (32 doubles)
     auto up = [](size_t n) { return (n + 31) / 32 * 32; };
     const size_t md = (size_t)m * d, mp = (size_t)nb_ * 16, blocks = (size_t)nb_ * nb_ * 256;
-    const size_t n = up(md) + up(mp) + 3 * blocks + (size_t)nb_ * 256 + (learn_warp ? 3 * up(md) : 0) + up(mp) +
-                     2 * up(nb_) +
-                     up(2 + P_) + up((size_t)kGradBlocks * P_);
+    const size_t n = up(md) + up(mp) + 3 * blocks + (size_t)nb_ * 256 + (learn_warp ? 3 * up(md) : 0) +
+                     2 * up(mp) + up(2);
     if (hipMalloc(&buf_, n * sizeof(double)) != hipSuccess) {
       buf_ = nullptr;
       return fail(SCOOT_ERR_NO_MEMORY, "gp nll: device allocation failed");
     }
-    // the results, written by the last kernel straight into coherent pinned
-    // host memory (no copy after it)
-    if (hipHostMalloc(&host_, (2 + P_) * sizeof(double), hipHostMallocMapped | hipHostMallocCoherent) !=
-        hipSuccess) {
+    // the results, written by the kernels straight into coherent pinned host
+    // memory (no copy after them): status, pivot products, u, partial gradient
+    // sums
+    if (hipHostMalloc(&host_, (1 + 17 * (size_t)nb_ + (size_t)kGradBlocks * P_) * sizeof(double),
+                      hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
       host_ = nullptr;
       return fail(SCOOT_ERR_NO_MEMORY, "gp nll: pinned allocation failed");
     }
@@ -826,13 +851,9 @@ class DeviceNll {
     }
     a_.alpha = p;
     p += up(mp);
-    a_.prod = p;
-    p += up(nb_);
-    a_.qpart = p;
-    p += up(nb_);
+    a_.u = p;
+    p += up(mp);
     a_.out = p;
-    p += up(2 + P_);
-    a_.part = p;
     a_.X = Xd;
     a_.r = rd;
     a_.m = m;
@@ -846,7 +867,7 @@ class DeviceNll {
         hipMemcpyAsync(rd, rp.data(), mp * sizeof(double), hipMemcpyHostToDevice, s) != hipSuccess ||
         hipStreamSynchronize(s) != hipSuccess)
       return fail(SCOOT_ERR_DEVICE, std::string("gp nll: upload failed: ") + hipGetErrorString(hipGetLastError()));
-    lds_ = ((size_t)nb_ * 512 + 256 + 512 + SCOOT_MAX_OBS / 16) * sizeof(double) +
+    lds_ = ((size_t)nb_ * 512 + 256 + 512 + SCOOT_MAX_OBS / 16 + (size_t)nb_ * 16 + 32) * sizeof(double) +
            (4 + kNllWaves + (size_t)nb_ * (nb_ - 1) / 2) * sizeof(int);
 
     int rc = allow_full_lds((const void*)nll_factor_kernel, "gp nll");
@@ -866,18 +887,17 @@ class DeviceNll {
       hipLaunchKernelGGL(nll_warp_kernel, dim3((unsigned)((m_ * d_ + 255) / 256)), dim3(256), 0, s_, a_);
     hipLaunchKernelGGL(nll_cov_kernel, dim3((unsigned)(nb_ * (nb_ + 1) / 2)), dim3(256), 0, s_, a_);
     hipLaunchKernelGGL(nll_factor_kernel, dim3(1), dim3(kNllThreads), lds_, s_, a_);
-    const size_t lds_tri = (size_t)nb_ * 256 * sizeof(double);
-    switch ((nb_ - 1 + kTriWaves - 1) / kTriWaves) {
-      case 0:
-      case 1: hipLaunchKernelGGL(nll_trtri_kernel<1>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
-      case 2: hipLaunchKernelGGL(nll_trtri_kernel<2>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
-      case 3: hipLaunchKernelGGL(nll_trtri_kernel<3>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
-      case 4: hipLaunchKernelGGL(nll_trtri_kernel<4>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
-      default: hipLaunchKernelGGL(nll_trtri_kernel<kTriMaxRows>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_);
-    }
-    hipLaunchKernelGGL(nll_lauum_kernel, dim3((unsigned)(nb_ * (nb_ + 1) / 2)), dim3(64), 0, s_, a_);
-    hipLaunchKernelGGL(nll_alpha_kernel, dim3((unsigned)nb_), dim3(64), 0, s_, a_);
-    if (grad) {
+    if (grad) {  // L^-1 and alpha, K^-1, the gradient's partial sums (the NLL needs none of them)
+      const size_t lds_tri = ((size_t)nb_ * 256 + kTriWaves * 16) * sizeof(double);
+      switch ((nb_ - 1 + kTriWaves - 1) / kTriWaves) {
+        case 0:
+        case 1: hipLaunchKernelGGL(nll_trtri_kernel<1>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
+        case 2: hipLaunchKernelGGL(nll_trtri_kernel<2>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
+        case 3: hipLaunchKernelGGL(nll_trtri_kernel<3>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
+        case 4: hipLaunchKernelGGL(nll_trtri_kernel<4>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
+        default: hipLaunchKernelGGL(nll_trtri_kernel<kTriMaxRows>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_);
+      }
+      hipLaunchKernelGGL(nll_lauum_kernel, dim3((unsigned)(nb_ * (nb_ + 1) / 2)), dim3(64), 0, s_, a_);
       const int rc = by_dim<1>(d_, [&](auto D) {
         if (lw_)
           hipLaunchKernelGGL((nll_grad_kernel<decltype(D)::value, true>), dim3(kGradBlocks), dim3(kGradThreads), 0,
@@ -892,7 +912,6 @@ class DeviceNll {
         return false;
       }
     }
-    hipLaunchKernelGGL(nll_finish_kernel, dim3((unsigned)(P_ + 1)), dim3(64), 0, s_, a_, P_, grad ? 1 : 0);
     const hipError_t launched = hipGetLastError();
     if (launched != hipSuccess) {
       rc_ = fail(SCOOT_ERR_DEVICE, std::string("gp nll: launch failed: ") + hipGetErrorString(launched));
@@ -903,13 +922,25 @@ class DeviceNll {
                                        hipGetErrorString(hipGetLastError()));
       return false;
     }
-    if (host_[1] == 2.0) {
+    if (host_[0] == 2.0) {
       rc_ = fail(SCOOT_ERR_DEVICE, "gp nll: the factorization's wait for its diagonal block ran out");
       return false;
     }
-    if (host_[1] != 1.0) return false;
-    *nll = host_[0];
-    if (grad) std::memcpy(grad, host_ + 2, sizeof(double) * P_);
+    if (host_[0] != 1.0) return false;
+    // NLL = 1/2 |L^-1 r|^2 + 1/2 log det K + m/2 log(2 pi), and the gradient's
+    // partial sums, each added in a fixed order
+    double q = 0.0, logdet = 0.0;
+    for (int k = 0; k < nb_; ++k) logdet += std::log(host_[1 + k]);
+    for (int i = 0; i < 16 * nb_; ++i) q += host_[1 + nb_ + i] * host_[1 + nb_ + i];
+    *nll = 0.5 * q + 0.5 * logdet + 0.5 * m_ * kLog2PiD;
+    if (grad) {
+      const double* part = host_ + 1 + 17 * nb_;
+      for (int p = 0; p < P_; ++p) {
+        double s = 0.0;
+        for (int b = 0; b < kGradBlocks; ++b) s += part[(size_t)b * P_ + p];
+        grad[p] = s;
+      }
+    }
     return true;
   }
   int error() const { return rc_; }
