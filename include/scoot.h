@@ -176,9 +176,10 @@ int scoot_gp_mle_warp(const double* X, const double* y, int m, int d, scoot_kern
  * theta [d + 2] with the fixed warp_a/warp_b (nullable); learn_warp = 1:
  * theta, lower, upper [3d + 2] as in scoot_gp_nll_warp, warp_a and warp_b
  * must be NULL.  The work of an evaluation runs on `stream` (NULL: the null
- * stream) and the call returns after it: K and its Cholesky factor by
- * 16 x 16 blocks (products on the fp64 matrix cores), K^-1 from the factor,
- * alpha, the NLL, then the gradient's trace terms.  Results agree with the
+ * stream) and the call returns after it: K, its Cholesky factor by 16 x 16
+ * blocks (products on the fp64 matrix cores) with u = L^-1 r alongside, the NLL
+ * from the pivots and u; with grad (nullable) also L^-1, alpha = L^-T u, K^-1
+ * and the gradient's trace terms.  Results agree with the
  * host calls to rounding (same definitions, other summation order).  The
  * search is the host's L-BFGS (same stopping rules) and allocates its device
  * work space (about 16 m^2 bytes) once per call.

@@ -200,9 +200,9 @@ def gp_mle_warp(X, y, theta0, lower, upper, kernel="matern32", prior_mean=0.0, m
 
 
 def gp_nll_device(X, y, theta, kernel="matern52", warp_a=None, warp_b=None, prior_mean=0.0, learn_warp=False,
-                  stream=None):
+                  stream=None, with_grad=True):
     """gp_nll (learn_warp=False) or gp_nll_warp (learn_warp=True) evaluated on
-    the current device."""
+    the current device; with_grad=False skips the gradient (returned as None)."""
     X, pX = _host(X, np.float64)
     y, py = _host(y, np.float64)
     m, d = X.shape
@@ -212,9 +212,10 @@ def gp_nll_device(X, y, theta, kernel="matern52", warp_a=None, warp_b=None, prio
     if th.size != P:
         raise ValueError(f"theta must have {P} entries")
     nll = C.c_double(0.0)
-    grad = np.zeros(P)
+    grad = np.zeros(P) if with_grad else None
     check(lib().scoot_gp_nll_device(pX, py, m, d, _kernel(kernel), pa, pb, prior_mean, int(bool(learn_warp)), pt,
-                                    C.byref(nll), grad.ctypes.data_as(C.POINTER(C.c_double)), _stream(stream)),
+                                    C.byref(nll), grad.ctypes.data_as(C.POINTER(C.c_double)) if with_grad else None,
+                                    _stream(stream)),
           "gp_nll_device")
     return nll.value, grad
 

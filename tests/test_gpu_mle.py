@@ -83,6 +83,20 @@ def test_device_nll_learned_warp_matches_oracle(m, d, kernel):
         _close(nll, g, nll_o, g_o)
 
 
+@pytest.mark.parametrize("m,d,kernel", [(1, 1, "matern32"), (37, 3, "matern52"), (256, 10, "matern52"),
+                                         (576, 12, "matern32")])
+def test_device_nll_without_gradient(m, d, kernel):
+    """The value alone (K and the factor only) is the same number as with the
+    gradient, and the oracle's to 1e-10."""
+    X, y = _case(500 + m, m, d)
+    theta = _theta(np.random.default_rng(m), d)
+    say("nll only", m, d, kernel)
+    nll, g = S.gp_nll_device(X, y, theta, kernel=kernel, prior_mean=0.02, with_grad=False)
+    nll_g, _ = S.gp_nll_device(X, y, theta, kernel=kernel, prior_mean=0.02)
+    assert g is None and nll == nll_g
+    assert nll == pytest.approx(nll_and_grad(theta, X, y, kernel, prior_mean=0.02)[0], rel=1e-10, abs=1e-10)
+
+
 def test_device_nll_matches_host_on_the_workload():
     """The two-objective workload's observations (m = 256, d = 10): device and
     host evaluations agree to rounding."""
