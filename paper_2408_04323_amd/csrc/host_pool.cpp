@@ -13,7 +13,9 @@
 // arrives after the last chunk was claimed finds the counter exhausted and
 // never calls the job's function, which may then no longer exist.  Up to
 // kSlots callers (say, the hyperparameter searches of several objectives) may
-// run jobs at the same time; idle threads take chunks from any of them.
+// run jobs at the same time; idle threads take chunks from any of them.  A
+// caller may cap the number of workers that join its jobs (PoolHelpers), to
+// leave cores to other threads of its own; the results do not change.
 #include <algorithm>
 #include <atomic>
 #include <chrono>
@@ -30,12 +32,15 @@
 
 namespace scoot {
 
+extern thread_local int t_max_helpers;  // this thread's cap on the workers that join its jobs
+
 namespace {
 
 struct Job {
   const std::function<void(int)>* fn;
   int n;
-  std::atomic<int> next{0}, done{0};
+  int max_helpers = -1;  // workers that may join, besides the caller (-1: any)
+  std::atomic<int> next{0}, done{0}, helpers{0};
   std::mutex err_mu;
   std::exception_ptr error;
 };
@@ -64,6 +69,8 @@ class Pool {
     for (auto& w : workers_) w.join();
   }
 
+  int threads() const { return (int)workers_.size() + 1; }
+
   void run(int n_chunks, const std::function<void(int)>& fn) {
     if (n_chunks <= 0) return;
     if (workers_.empty() || n_chunks == 1) {
@@ -73,6 +80,7 @@ class Pool {
     auto job = std::make_shared<Job>();
     job->fn = &fn;
     job->n = n_chunks;
+    job->max_helpers = t_max_helpers;
     int slot = -1;
     {
       std::unique_lock<std::mutex> lk(slots_mu_);
@@ -144,7 +152,8 @@ class Pool {
         any = false;
         for (int k = 0; k < kSlots; ++k) {
           std::shared_ptr<Job> job = std::atomic_load(&slots_[k]);
-          if (job && work(*job)) any = true;
+          if (job && (job->max_helpers < 0 || job->helpers.fetch_add(1) < job->max_helpers) && work(*job))
+            any = true;
         }
       }
     }
@@ -168,6 +177,13 @@ Pool& pool() {
 
 }  // namespace
 
+thread_local int t_max_helpers = -1;
+
 void parallel_chunks(int n_chunks, const std::function<void(int)>& fn) { pool().run(n_chunks, fn); }
+
+int pool_threads() { return pool().threads(); }
+
+PoolHelpers::PoolHelpers(int n) : prev_(t_max_helpers) { t_max_helpers = n < 0 ? -1 : n; }
+PoolHelpers::~PoolHelpers() { t_max_helpers = prev_; }
 
 }  // namespace scoot

@@ -149,6 +149,20 @@ inline int plan16_row(const RowPlan16& p, int e, int q) {
 // not call parallel_chunks itself.  Pool size: SCOOT_HOST_THREADS, else the
 // hardware threads up to 16.
 void parallel_chunks(int n_chunks, const std::function<void(int)>& fn);
+// Threads of the pool, the caller included.
+int pool_threads();
+// While it lives, the parallel steps this thread starts take at most n pool
+// workers besides itself (n < 0: no cap); results do not change.
+class PoolHelpers {
+ public:
+  explicit PoolHelpers(int n);
+  ~PoolHelpers();
+  PoolHelpers(const PoolHelpers&) = delete;
+  PoolHelpers& operator=(const PoolHelpers&) = delete;
+
+ private:
+  int prev_;
+};
 
 // In-place lower Cholesky factor of the m x m row-major A (the lower
 // triangle is read; the upper is zeroed); false when a pivot is not positive

@@ -257,6 +257,8 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
             wa = la;
             wb = lb;
           }
+          // the fit's host steps leave a core to each search still running
+          PoolHelpers cap(on_device ? std::max(0, (pool_threads() - p) / p - 1) : -1);
           search_rc[j] = scoot_gp_fit_ex(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, ell, wa, wb,
                                          std::exp(th[d]), std::exp(th[d + 1]), 0.0, (scoot_dtype)o.dtype, stream,
                                          &h.gps[j]);
@@ -281,8 +283,14 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
       // ---- 3. feasibility forest on every observation ---------------------
       std::vector<double> label(n_obs);
       for (int i = 0; i < n_obs; ++i) label[i] = valid[i] ? 1.0 : 0.0;
-      const int forest_rc = scoot_forest_train_create(X_obs, label.data(), n_obs, d, o.n_trees, o.max_depth,
-                                                      o.forest_seed, o.bootstrap, &h.forest);
+      int forest_rc;
+      {
+        // beside device searches, whose threads mostly launch and wait, the
+        // forest leaves them a core each
+        PoolHelpers cap(on_device ? std::max(0, pool_threads() - 1 - p) : -1);
+        forest_rc = scoot_forest_train_create(X_obs, label.data(), n_obs, d, o.n_trees, o.max_depth, o.forest_seed,
+                                              o.bootstrap, &h.forest);
+      }
       const std::string forest_err = forest_rc != SCOOT_OK ? scoot_last_error() : "";
       for (auto& t : searches) t.join();
       for (hipStream_t st : streams)
