@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define SCOOT_ABI_VERSION 4
+#define SCOOT_ABI_VERSION 5
 
 typedef enum scoot_dtype { SCOOT_F32 = 0, SCOOT_F64 = 1 } scoot_dtype;
 
@@ -120,6 +120,15 @@ int scoot_gp_factor_host_ex(const double* X, const double* y, int m, int d, scoo
 int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel kernel,
                     const double* lengthscale, const double* warp_a, const double* warp_b, double signal_var,
                     double noise_var, double prior_mean, scoot_dtype dt, void* stream, scoot_gp* out);
+/* scoot_gp_fit_device: scoot_gp_fit_ex with K, its Cholesky factor, L^-1 and
+ * alpha computed on the current device (fp64, the kernels of
+ * scoot_gp_nll_device, on `stream`), then packed and uploaded as there; the
+ * state agrees with scoot_gp_fit_ex's to rounding.  noise_var must be > 0.
+ * Errors: as scoot_gp_fit_ex; INVALID_ARG also for noise_var <= 0; DEVICE for
+ * a failed allocation or launch. */
+int scoot_gp_fit_device(const double* X, const double* y, int m, int d, scoot_kernel kernel,
+                        const double* lengthscale, const double* warp_a, const double* warp_b, double signal_var,
+                        double noise_var, double prior_mean, scoot_dtype dt, void* stream, scoot_gp* out);
 int scoot_gp_destroy(scoot_gp gp);
 
 /* ---------------------------------------------------------------------------

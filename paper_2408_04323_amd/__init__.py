@@ -133,6 +133,22 @@ def gp_fit(X, y, lengthscale, signal_var, noise_var, prior_mean=0.0, dtype="f32"
     return GP(h.value, m, d, dt)
 
 
+def gp_fit_device(X, y, lengthscale, signal_var, noise_var, prior_mean=0.0, dtype="f32", stream=None,
+                  kernel="matern52", warp_a=None, warp_b=None):
+    """gp_fit with the factorization, L^-1 and alpha on the current device
+    (noise_var > 0)."""
+    X, pX = _host(X, np.float64)
+    y, py = _host(y, np.float64)
+    ls, pl = _host(lengthscale, np.float64)
+    m, d = X.shape
+    a, b, pa, pb = _warp(warp_a, warp_b, d)
+    h = C.c_void_p(0)
+    dt = _dt(dtype)
+    check(lib().scoot_gp_fit_device(pX, py, m, d, _kernel(kernel), pl, pa, pb, signal_var, noise_var, prior_mean,
+                                    dt, _stream(stream), C.byref(h)), "gp_fit_device")
+    return GP(h.value, m, d, dt)
+
+
 # ---------------------------------------------------- maximum-likelihood fit
 def gp_nll(X, y, theta, kernel="matern52", warp_a=None, warp_b=None, prior_mean=0.0):
     """(nll, grad) at theta = (log l_1..d, log s2, log tau2)."""

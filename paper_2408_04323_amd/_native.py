@@ -25,6 +25,8 @@ SIGNATURES = {
                                 P_dbl, P_dbl],
     "scoot_gp_fit_ex": [P_dbl, P_dbl, c_int, c_int, c_int, P_dbl, P_dbl, P_dbl, c_dbl, c_dbl, c_dbl, c_int, c_vp,
                         C.POINTER(c_vp)],
+    "scoot_gp_fit_device": [P_dbl, P_dbl, c_int, c_int, c_int, P_dbl, P_dbl, P_dbl, c_dbl, c_dbl, c_dbl, c_int,
+                            c_vp, C.POINTER(c_vp)],
     "scoot_gp_destroy": [c_vp],
     "scoot_gp_nll": [P_dbl, P_dbl, c_int, c_int, c_int, P_dbl, P_dbl, c_dbl, P_dbl, P_dbl, P_dbl],
     "scoot_gp_mle": [P_dbl, P_dbl, c_int, c_int, c_int, P_dbl, P_dbl, c_dbl, P_dbl, P_dbl, c_int, P_dbl, P_dbl,

@@ -137,79 +137,10 @@ int upload_async(void* dst, const void* src, size_t bytes, int slot, void* strea
   return SCOOT_OK;
 }
 
-}  // namespace scoot
-
-using namespace scoot;
-
-namespace {
-constexpr double kLn2 = 0.69314718055994530942;
-
-bool check_dtype(scoot_dtype dt) { return dt == SCOOT_F32 || dt == SCOOT_F64; }
-
-int device_error(const char* what, hipError_t e) {
-  return fail(SCOOT_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
-}
-}  // namespace
-
-extern "C" {
-
-int scoot_abi_version(void) { return SCOOT_ABI_VERSION; }
-
-const char* scoot_status_string(int status) {
-  switch (status) {
-    case SCOOT_OK: return "ok";
-    case SCOOT_ERR_INVALID_ARG: return "invalid argument";
-    case SCOOT_ERR_NOT_PD: return "matrix not positive definite";
-    case SCOOT_ERR_DEVICE: return "device error";
-    case SCOOT_ERR_UNSUPPORTED: return "unsupported size";
-    case SCOOT_ERR_NO_MEMORY: return "out of memory";
-    default: return "unknown status";
-  }
-}
-
-const char* scoot_last_error(void) { return g_static_error ? g_static_error : g_last_error.c_str(); }
-
-int scoot_gp_factor_host_ex(const double* X, const double* y, int m, int d, scoot_kernel kernel,
-                            const double* lengthscale, const double* warp_a, const double* warp_b,
-                            double signal_var, double noise_var, double prior_mean, double* L, double* alpha) {
-  clear_error();
-  if (!L || !alpha) return fail(SCOOT_ERR_INVALID_ARG, "gp factor: null output");
+int gp_from_fit(const FitHost& f, const double* warp_a, const double* warp_b, scoot_dtype dt, scoot_gp* out) {
+  const int m = f.m, d = f.d;
+  const double signal_var = f.s2, noise_var = f.tau2, prior_mean = f.c;
   try {
-    FitHost f;
-    int rc = fit_host(X, y, m, d, kernel, lengthscale, warp_a, warp_b, signal_var, noise_var, prior_mean, f);
-    if (rc != SCOOT_OK) return rc;
-    std::memcpy(L, f.L.data(), sizeof(double) * (size_t)m * m);
-    std::memcpy(alpha, f.alpha.data(), sizeof(double) * (size_t)m);
-    return SCOOT_OK;
-  } catch (const std::bad_alloc&) {
-    return fail(SCOOT_ERR_NO_MEMORY, "gp factor: host allocation failed");
-  }
-}
-
-int scoot_gp_factor_host(const double* X, const double* y, int m, int d, const double* lengthscale,
-                         double signal_var, double noise_var, double prior_mean, double* L, double* alpha) {
-  return scoot_gp_factor_host_ex(X, y, m, d, SCOOT_MATERN52, lengthscale, nullptr, nullptr, signal_var, noise_var,
-                                 prior_mean, L, alpha);
-}
-
-int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* lengthscale, double signal_var,
-                 double noise_var, double prior_mean, scoot_dtype dt, void* stream, scoot_gp* out) {
-  return scoot_gp_fit_ex(X, y, m, d, SCOOT_MATERN52, lengthscale, nullptr, nullptr, signal_var, noise_var,
-                         prior_mean, dt, stream, out);
-}
-
-int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* lengthscale,
-                    const double* warp_a, const double* warp_b, double signal_var, double noise_var,
-                    double prior_mean, scoot_dtype dt, void* stream, scoot_gp* out) {
-  clear_error();
-  (void)stream;
-  if (!out) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: null output handle");
-  *out = nullptr;
-  if (!check_dtype(dt)) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: bad dtype");
-  try {
-    FitHost f;
-    int rc = fit_host(X, y, m, d, kernel, lengthscale, warp_a, warp_b, signal_var, noise_var, prior_mean, f);
-    if (rc != SCOOT_OK) return rc;
     GPDevice g;
     g.dt = dt;
     g.m = m;
@@ -284,7 +215,7 @@ int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel
     e = hipMemcpy(g.buf, img.data(), img.size(), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       hipFree(g.buf);
-      return device_error("gp fit: upload", e);
+      return fail(SCOOT_ERR_DEVICE, std::string("gp fit: upload: ") + hipGetErrorString(e));
     }
     g.linv = g.buf;
     g.xs = (unsigned char*)g.buf + linv_bytes;
@@ -295,6 +226,100 @@ int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel
     hipGetDevice(&h->device);
     *out = h;
     return SCOOT_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "gp fit: host allocation failed");
+  }
+}
+
+}  // namespace scoot
+
+using namespace scoot;
+
+namespace {
+constexpr double kLn2 = 0.69314718055994530942;
+
+bool check_dtype(scoot_dtype dt) { return dt == SCOOT_F32 || dt == SCOOT_F64; }
+
+int device_error(const char* what, hipError_t e) {
+  return fail(SCOOT_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+}  // namespace
+
+extern "C" {
+
+int scoot_abi_version(void) { return SCOOT_ABI_VERSION; }
+
+const char* scoot_status_string(int status) {
+  switch (status) {
+    case SCOOT_OK: return "ok";
+    case SCOOT_ERR_INVALID_ARG: return "invalid argument";
+    case SCOOT_ERR_NOT_PD: return "matrix not positive definite";
+    case SCOOT_ERR_DEVICE: return "device error";
+    case SCOOT_ERR_UNSUPPORTED: return "unsupported size";
+    case SCOOT_ERR_NO_MEMORY: return "out of memory";
+    default: return "unknown status";
+  }
+}
+
+const char* scoot_last_error(void) { return g_static_error ? g_static_error : g_last_error.c_str(); }
+
+int scoot_gp_factor_host_ex(const double* X, const double* y, int m, int d, scoot_kernel kernel,
+                            const double* lengthscale, const double* warp_a, const double* warp_b,
+                            double signal_var, double noise_var, double prior_mean, double* L, double* alpha) {
+  clear_error();
+  if (!L || !alpha) return fail(SCOOT_ERR_INVALID_ARG, "gp factor: null output");
+  try {
+    FitHost f;
+    int rc = fit_host(X, y, m, d, kernel, lengthscale, warp_a, warp_b, signal_var, noise_var, prior_mean, f);
+    if (rc != SCOOT_OK) return rc;
+    std::memcpy(L, f.L.data(), sizeof(double) * (size_t)m * m);
+    std::memcpy(alpha, f.alpha.data(), sizeof(double) * (size_t)m);
+    return SCOOT_OK;
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "gp factor: host allocation failed");
+  }
+}
+
+int scoot_gp_factor_host(const double* X, const double* y, int m, int d, const double* lengthscale,
+                         double signal_var, double noise_var, double prior_mean, double* L, double* alpha) {
+  return scoot_gp_factor_host_ex(X, y, m, d, SCOOT_MATERN52, lengthscale, nullptr, nullptr, signal_var, noise_var,
+                                 prior_mean, L, alpha);
+}
+
+int scoot_gp_fit(const double* X, const double* y, int m, int d, const double* lengthscale, double signal_var,
+                 double noise_var, double prior_mean, scoot_dtype dt, void* stream, scoot_gp* out) {
+  return scoot_gp_fit_ex(X, y, m, d, SCOOT_MATERN52, lengthscale, nullptr, nullptr, signal_var, noise_var,
+                         prior_mean, dt, stream, out);
+}
+
+int scoot_gp_fit_ex(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* lengthscale,
+                    const double* warp_a, const double* warp_b, double signal_var, double noise_var,
+                    double prior_mean, scoot_dtype dt, void* stream, scoot_gp* out) {
+  clear_error();
+  (void)stream;
+  if (!out) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: null output handle");
+  *out = nullptr;
+  if (!check_dtype(dt)) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: bad dtype");
+  try {
+    FitHost f;
+    int rc = fit_host(X, y, m, d, kernel, lengthscale, warp_a, warp_b, signal_var, noise_var, prior_mean, f);
+    if (rc != SCOOT_OK) return rc;
+    return gp_from_fit(f, warp_a, warp_b, dt, out);
+  } catch (const std::bad_alloc&) {
+    return fail(SCOOT_ERR_NO_MEMORY, "gp fit: host allocation failed");
+  }
+}
+
+int scoot_gp_fit_device(const double* X, const double* y, int m, int d, scoot_kernel kernel,
+                        const double* lengthscale, const double* warp_a, const double* warp_b, double signal_var,
+                        double noise_var, double prior_mean, scoot_dtype dt, void* stream, scoot_gp* out) {
+  clear_error();
+  if (!out) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: null output handle");
+  *out = nullptr;
+  if (!check_dtype(dt)) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: bad dtype");
+  try {
+    return gp_fit_device(X, y, m, d, kernel, lengthscale, warp_a, warp_b, signal_var, noise_var, prior_mean, dt,
+                         stream, out);
   } catch (const std::bad_alloc&) {
     return fail(SCOOT_ERR_NO_MEMORY, "gp fit: host allocation failed");
   }

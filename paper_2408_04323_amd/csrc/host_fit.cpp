@@ -33,8 +33,8 @@ bool finite_all(const double* v, size_t n) {
 }
 }  // namespace
 
-int fit_host(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* ls,
-             const double* warp_a, const double* warp_b, double s2, double tau2, double c, FitHost& f) {
+int fit_setup(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* ls,
+              const double* warp_a, const double* warp_b, double s2, double tau2, double c, FitHost& f) {
   if (!X || !y || !ls) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: null pointer");
   if (kernel != SCOOT_MATERN52 && kernel != SCOOT_MATERN32) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: bad kernel");
   if ((warp_a == nullptr) != (warp_b == nullptr))
@@ -68,11 +68,7 @@ int fit_host(const double* X, const double* y, int m, int d, scoot_kernel kernel
   f.coef[1] = s2 * kLn2;
   f.coef[2] = kernel == SCOOT_MATERN52 ? s2 * kLn2 * kLn2 / 3.0 : 0.0;
   f.scale.assign(d, 0.0);
-  std::vector<double> inv_ls(d);
-  for (int k = 0; k < d; ++k) {
-    inv_ls[k] = 1.0 / ls[k];
-    f.scale[k] = root * kLog2e / ls[k];
-  }
+  for (int k = 0; k < d; ++k) f.scale[k] = root * kLog2e / ls[k];
   f.Xw.assign(X, X + (size_t)m * d);
   if (warp_a) {
     f.warp_a.assign(warp_a, warp_a + d);
@@ -80,6 +76,16 @@ int fit_host(const double* X, const double* y, int m, int d, scoot_kernel kernel
     for (int i = 0; i < m; ++i)
       for (int k = 0; k < d; ++k) f.Xw[(size_t)i * d + k] = kumaraswamy(X[(size_t)i * d + k], warp_a[k], warp_b[k]);
   }
+  return SCOOT_OK;
+}
+
+int fit_host(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* ls,
+             const double* warp_a, const double* warp_b, double s2, double tau2, double c, FitHost& f) {
+  const int rc = fit_setup(X, y, m, d, kernel, ls, warp_a, warp_b, s2, tau2, c, f);
+  if (rc != SCOOT_OK) return rc;
+  const double root = kernel == SCOOT_MATERN52 ? kSqrt5 : kSqrt3;  // sqrt(2 nu)
+  std::vector<double> inv_ls(d);
+  for (int k = 0; k < d; ++k) inv_ls[k] = 1.0 / ls[k];
 
   // K = k(X, X) + tau^2 I (lower triangle; rows in parallel), factored in place.
   f.L.assign((size_t)m * m, 0.0);

@@ -196,6 +196,21 @@ struct FitHost {
 // warp_a / warp_b: both null (no warping) or d positive values each.
 int fit_host(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* ls,
              const double* warp_a, const double* warp_b, double s2, double tau2, double c, FitHost& out);
+// fit_host's validation and everything but the factorization (L, Linv and
+// alpha left empty).
+int fit_setup(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* ls,
+              const double* warp_a, const double* warp_b, double s2, double tau2, double c, FitHost& out);
+// The device GP handle of a fit (its Linv and alpha filled): packing and upload.
+int gp_from_fit(const FitHost& f, const double* warp_a, const double* warp_b, scoot_dtype dt, scoot_gp* out);
+// mle_fit_device, then the GP at the optimum with L^-1 and alpha from the
+// search's own device factorization (no host refit).
+int mle_fit_device_gp(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+                      const double* warp_b, double c, bool learn_warp, const double* lower, const double* upper,
+                      int max_iter, double* theta, scoot_dtype dt, void* stream, scoot_gp* out);
+// The GP at fixed hyperparameters with the factorization on the device.
+int gp_fit_device(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* ls,
+                  const double* warp_a, const double* warp_b, double s2, double tau2, double c, scoot_dtype dt,
+                  void* stream, scoot_gp* out);
 
 // Kumaraswamy input warping of one coordinate, w = 1 - (1 - x^a)^b, x clamped
 // to [0, 1], without cancellation: ln x from log1p(x - 1) above 1/2,

@@ -888,15 +888,7 @@ class DeviceNll {
     hipLaunchKernelGGL(nll_cov_kernel, dim3((unsigned)(nb_ * (nb_ + 1) / 2)), dim3(256), 0, s_, a_);
     hipLaunchKernelGGL(nll_factor_kernel, dim3(1), dim3(kNllThreads), lds_, s_, a_);
     if (grad) {  // L^-1 and alpha, K^-1, the gradient's partial sums (the NLL needs none of them)
-      const size_t lds_tri = ((size_t)nb_ * 256 + kTriWaves * 16) * sizeof(double);
-      switch ((nb_ - 1 + kTriWaves - 1) / kTriWaves) {
-        case 0:
-        case 1: hipLaunchKernelGGL(nll_trtri_kernel<1>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
-        case 2: hipLaunchKernelGGL(nll_trtri_kernel<2>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
-        case 3: hipLaunchKernelGGL(nll_trtri_kernel<3>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
-        case 4: hipLaunchKernelGGL(nll_trtri_kernel<4>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
-        default: hipLaunchKernelGGL(nll_trtri_kernel<kTriMaxRows>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_);
-      }
+      launch_trtri();
       hipLaunchKernelGGL(nll_lauum_kernel, dim3((unsigned)(nb_ * (nb_ + 1) / 2)), dim3(64), 0, s_, a_);
       const int rc = by_dim<1>(d_, [&](auto D) {
         if (lw_)
@@ -943,9 +935,64 @@ class DeviceNll {
     }
     return true;
   }
+  // K, the factor and L^-1 at theta, then L^-1 (m x m row-major, lower) and
+  // alpha to the host; false when K is not positive definite or on a device
+  // failure (kept in error()).
+  bool inverse(const double* theta, std::vector<double>& Linv, std::vector<double>& alpha) {
+    if (rc_ != SCOOT_OK) return false;
+    std::memcpy(a_.theta, theta, sizeof(double) * P_);
+    (void)hipGetLastError();  // clear an earlier, unrelated error
+    if (lw_)
+      hipLaunchKernelGGL(nll_warp_kernel, dim3((unsigned)((m_ * d_ + 255) / 256)), dim3(256), 0, s_, a_);
+    hipLaunchKernelGGL(nll_cov_kernel, dim3((unsigned)(nb_ * (nb_ + 1) / 2)), dim3(256), 0, s_, a_);
+    hipLaunchKernelGGL(nll_factor_kernel, dim3(1), dim3(kNllThreads), lds_, s_, a_);
+    launch_trtri();
+    const hipError_t launched = hipGetLastError();
+    if (launched != hipSuccess) {
+      rc_ = fail(SCOOT_ERR_DEVICE, std::string("gp fit: launch failed: ") + hipGetErrorString(launched));
+      return false;
+    }
+    if (hipStreamSynchronize(s_) != hipSuccess) {
+      rc_ = fail(SCOOT_ERR_DEVICE, std::string("gp fit: device factorization failed: ") +
+                                       hipGetErrorString(hipGetLastError()));
+      return false;
+    }
+    if (host_[0] == 2.0) {
+      rc_ = fail(SCOOT_ERR_DEVICE, "gp fit: the factorization's wait for its diagonal block ran out");
+      return false;
+    }
+    if (host_[0] != 1.0) return false;
+    std::vector<double> xi((size_t)nb_ * nb_ * 256), al((size_t)nb_ * 16);
+    if (hipMemcpyAsync(xi.data(), a_.Xi, xi.size() * sizeof(double), hipMemcpyDeviceToHost, s_) != hipSuccess ||
+        hipMemcpyAsync(al.data(), a_.alpha, al.size() * sizeof(double), hipMemcpyDeviceToHost, s_) != hipSuccess ||
+        hipStreamSynchronize(s_) != hipSuccess) {
+      rc_ = fail(SCOOT_ERR_DEVICE, std::string("gp fit: read-back failed: ") + hipGetErrorString(hipGetLastError()));
+      return false;
+    }
+    const int m = m_;
+    Linv.assign((size_t)m * m, 0.0);
+    for (int row = 0; row < m; ++row)
+      for (int col = 0; col <= row; ++col) {
+        const int I = row >> 4, J = col >> 4;
+        Linv[(size_t)row * m + col] = xi[((size_t)I * nb_ + J) * 256 + (row & 15) * 16 + (col & 15)];
+      }
+    alpha.assign(al.begin(), al.begin() + m);
+    return true;
+  }
   int error() const { return rc_; }
 
  private:
+  void launch_trtri() {
+    const size_t lds_tri = ((size_t)nb_ * 256 + kTriWaves * 16) * sizeof(double);
+    switch ((nb_ - 1 + kTriWaves - 1) / kTriWaves) {
+      case 0:
+      case 1: hipLaunchKernelGGL(nll_trtri_kernel<1>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
+      case 2: hipLaunchKernelGGL(nll_trtri_kernel<2>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
+      case 3: hipLaunchKernelGGL(nll_trtri_kernel<3>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
+      case 4: hipLaunchKernelGGL(nll_trtri_kernel<4>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_); break;
+      default: hipLaunchKernelGGL(nll_trtri_kernel<kTriMaxRows>, dim3((unsigned)nb_), dim3(kTriWaves * 64), lds_tri, s_, a_);
+    }
+  }
   hipStream_t s_ = nullptr;
   int m_ = 0, d_ = 0, nb_ = 0, P_ = 0;
   bool lw_ = false;
@@ -997,6 +1044,73 @@ int mle_fit_device(const double* X, const double* y, int m, int d, scoot_kernel 
                  learn_warp ? 3 * d + 2 : d + 2, lower, upper, max_iter, theta, nll_out, iters_out);
   if (dev.error() != SCOOT_OK) return dev.error();
   return rc;
+}
+
+namespace {
+// The GP at theta from a factorization on dev: the host part of a fit, then
+// L^-1 and alpha from the device.
+int gp_from_device(DeviceNll& dev, const double* X, const double* y, int m, int d, scoot_kernel kernel,
+                   const double* warp_a, const double* warp_b, double c, bool learn_warp, const double* theta,
+                   scoot_dtype dt, scoot_gp* out) {
+  double ls[SCOOT_MAX_DIM], wa[SCOOT_MAX_DIM], wb[SCOOT_MAX_DIM];
+  for (int k = 0; k < d; ++k) ls[k] = std::exp(theta[k]);
+  const double* pa = warp_a;
+  const double* pb = warp_b;
+  if (learn_warp) {
+    for (int k = 0; k < d; ++k) {
+      wa[k] = std::exp(theta[d + 2 + k]);
+      wb[k] = std::exp(theta[2 * d + 2 + k]);
+    }
+    pa = wa;
+    pb = wb;
+  }
+  FitHost f;
+  int rc = fit_setup(X, y, m, d, kernel, ls, pa, pb, std::exp(theta[d]), std::exp(theta[d + 1]), c, f);
+  if (rc != SCOOT_OK) return rc;
+  if (!dev.inverse(theta, f.Linv, f.alpha))
+    return dev.error() != SCOOT_OK ? dev.error()
+                                   : fail(SCOOT_ERR_NOT_PD, "gp fit: K + tau^2 I is not positive definite");
+  return gp_from_fit(f, pa, pb, dt, out);
+}
+}  // namespace
+
+int mle_fit_device_gp(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* warp_a,
+                      const double* warp_b, double c, bool learn_warp, const double* lower, const double* upper,
+                      int max_iter, double* theta, scoot_dtype dt, void* stream, scoot_gp* out) {
+  std::vector<double> Xu, r;
+  int rc = device_inputs(X, y, m, d, kernel, warp_a, warp_b, c, learn_warp, Xu, r);
+  if (rc != SCOOT_OK) return rc;
+  DeviceNll dev;
+  rc = dev.init(Xu, r, m, d, kernel, learn_warp, (hipStream_t)stream);
+  if (rc != SCOOT_OK) return rc;
+  rc = lbfgs_box([&](const double* t, double* f, double* g) { return dev.eval(t, f, g); },
+                 learn_warp ? 3 * d + 2 : d + 2, lower, upper, max_iter, theta, nullptr, nullptr);
+  if (dev.error() != SCOOT_OK) return dev.error();
+  if (rc != SCOOT_OK) return rc;
+  return gp_from_device(dev, X, y, m, d, kernel, warp_a, warp_b, c, learn_warp, theta, dt, out);
+}
+
+int gp_fit_device(const double* X, const double* y, int m, int d, scoot_kernel kernel, const double* ls,
+                  const double* warp_a, const double* warp_b, double s2, double tau2, double c, scoot_dtype dt,
+                  void* stream, scoot_gp* out) {
+  if (!ls) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: null pointer");
+  if (d < 1 || d > SCOOT_MAX_DIM) return fail(SCOOT_ERR_INVALID_ARG, "gp fit: bad d");
+  for (int k = 0; k < d; ++k)
+    if (!(ls[k] > 0) || !std::isfinite(ls[k]))
+      return fail(SCOOT_ERR_INVALID_ARG, "gp fit: lengthscales must be finite and > 0");
+  if (!(s2 > 0) || !std::isfinite(s2) || !(tau2 > 0) || !std::isfinite(tau2))
+    return fail(SCOOT_ERR_INVALID_ARG, "gp fit (device): signal and noise variance must be finite and > 0");
+  double theta[SCOOT_MAX_DIM + 2];
+  for (int k = 0; k < d; ++k) theta[k] = std::log(ls[k]);
+  theta[d] = std::log(s2);
+  theta[d + 1] = std::log(tau2);
+  std::vector<double> Xu, r;
+  int rc = device_inputs(X, y, m, d, kernel, warp_a, warp_b, c, false, Xu, r);
+  if (rc != SCOOT_OK) return rc;
+  DeviceNll dev;
+  rc = dev.init(Xu, r, m, d, kernel, false, (hipStream_t)stream);
+  if (rc != SCOOT_OK) return rc;
+  return gp_from_device(dev, X, y, m, d, kernel, warp_a, warp_b, c, false, theta, dt, out);
 }
 
 }  // namespace scoot

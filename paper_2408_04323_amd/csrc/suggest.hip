@@ -233,10 +233,14 @@ int scoot_suggest(const double* X_obs, const double* Y_obs, const uint8_t* valid
             return;
           }
           if (!all_fixed && on_device) {
-            search_rc[j] = scoot_gp_mle_device(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel,
-                                               lw ? nullptr : wa, lw ? nullptr : wb, 0.0, lw ? 1 : 0, lo, hi, iters, th,
-                                               nullptr, nullptr, streams[j]);
+            // the search, then the GP at its optimum from the search's own
+            // device factorization (no host refit)
+            search_rc[j] = mle_fit_device_gp(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, lw ? nullptr : wa,
+                                             lw ? nullptr : wb, 0.0, lw, lo, hi, iters, th, (scoot_dtype)o.dtype,
+                                             streams[j], &h.gps[j]);
             if (search_rc[j] != SCOOT_OK) search_err[j] = scoot_last_error();  // this thread's message
+            std::memcpy(&theta[(size_t)j * nt], th, sizeof(double) * nt);
+            return;
           } else if (!all_fixed) {
             search_rc[j] = lw ? scoot_gp_mle_warp(Xv.data(), yj.data(), m, d, (scoot_kernel)o.kernel, 0.0, lo, hi,
                                                   iters, th, nullptr, nullptr)

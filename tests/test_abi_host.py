@@ -32,7 +32,7 @@ def test_every_declared_symbol_is_exported():
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(SIGNATURES)
-    assert S.abi_version() == 4
+    assert S.abi_version() == 5
 
 
 def test_factor_matches_oracle():

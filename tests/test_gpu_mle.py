@@ -177,3 +177,45 @@ def test_device_fit_matches_host_fit_on_the_workload():
     _, g = nll_and_grad(th, X, y)
     interior = (th > lo + 1e-3) & (th < hi - 1e-3)
     assert np.max(np.abs(g[interior])) < 1e-3
+
+
+@pytest.mark.parametrize("m,d,kernel,warp,dtype", [(40, 3, "matern52", None, "f32"), (256, 10, "matern52", None, "f32"),
+                                                   (300, 4, "matern32", "fixed", "f32"),
+                                                   (576, 12, "matern52", None, "f32"), (129, 5, "matern32", None, "f64")])
+def test_device_gp_fit_matches_host_fit(m, d, kernel, warp, dtype):
+    """The GP fitted on the device (K, the factor, L^-1 and alpha from the
+    likelihood's kernels) gives the host fit's posterior: to the last bits of
+    float in fp32, to 1e-9 in fp64, and the oracle's to the fp32 bars."""
+    from oracle.gp import gp_fit as o_fit, gp_posterior as o_post
+    X, y = _case(900 + m, m, d)
+    rng = np.random.default_rng(m + d)
+    ls = rng.uniform(0.2, 1.5, d)
+    s2, tau2 = 1.3, 2e-3
+    wp = (np.exp(0.3 * rng.standard_normal(d)), np.exp(0.3 * rng.standard_normal(d))) if warp else None
+    kw = dict(kernel=kernel, warp_a=None if wp is None else wp[0], warp_b=None if wp is None else wp[1],
+              prior_mean=0.1, dtype=dtype)
+    say("device gp fit", m, d, kernel, warp, dtype)
+    Xc = torch.from_numpy(rng.random((3000, d)).astype(np.float32)).cuda()
+    g_dev = S.gp_fit_device(X, y, ls, s2, tau2, **kw)
+    g_host = S.gp_fit(X, y, ls, s2, tau2, **kw)
+    mu_d, sd_d = [t.cpu().numpy().astype(np.float64) for t in S.posterior(g_dev, Xc)]
+    mu_h, sd_h = [t.cpu().numpy().astype(np.float64) for t in S.posterior(g_host, Xc)]
+    torch.cuda.synchronize()
+    tol = 2e-6 if dtype == "f32" else 1e-9
+    np.testing.assert_allclose(mu_d, mu_h, rtol=0, atol=tol * np.sqrt(s2) * 10)
+    np.testing.assert_allclose(sd_d, sd_h, rtol=0, atol=tol * np.sqrt(s2) * 10)
+    mu_o, sd_o = o_post(o_fit(X, y, ls, s2, tau2, 0.1, kernel, wp), Xc.cpu().numpy().astype(np.float64))
+    bar = 2e-3 if dtype == "f32" else 1e-9
+    np.testing.assert_allclose(mu_d, mu_o, rtol=0, atol=bar * np.sqrt(s2))
+    np.testing.assert_allclose(sd_d, sd_o, rtol=0, atol=bar * np.sqrt(s2))
+
+
+def test_device_gp_fit_argument_errors():
+    X, y = _case(5, 20, 2)
+    with pytest.raises(S.ScootError):  # the device fit needs a positive noise variance
+        S.gp_fit_device(X, y, np.ones(2), 1.0, 0.0)
+    with pytest.raises(S.ScootError):
+        S.gp_fit_device(X, y, np.array([1.0, -1.0]), 1.0, 1e-3)
+    with pytest.raises(S.ScootError) as e:  # duplicate inputs without noise to speak of: not positive definite
+        S.gp_fit_device(np.vstack([X, X[:1]]), np.concatenate([y, y[:1]]), np.ones(2), 1.0, 1e-30)
+    assert e.value.status == -2
