@@ -311,6 +311,113 @@ def test_forest_bitexact(cfg):
         np.testing.assert_array_equal(mask.cpu().numpy(), feasibility_mask(v_o, delta, len(fd["tree_offset"]) - 1))
 
 
+def _grid_forest(rng, depths, d, grids, full=False, p0=0.0):
+    """Random trees whose thresholds come from per-feature value grids (so
+    candidates can sit exactly on them), one tree per entry of depths; with
+    full=True each tree is complete to its depth; p0 is the share of splits
+    forced onto feature 0."""
+    feat, thr, left, right, q16, off = [], [], [], [], [], [0]
+    for depth in depths:
+        nodes = []
+
+        def grow(level):
+            me = len(nodes)
+            nodes.append(None)
+            if level == depth or (not full and level > 0 and rng.random() < 0.25):
+                nodes[me] = (-1, 0.0, -1, -1, int(rng.integers(0, 65537)))
+                return me
+            k = 0 if rng.random() < p0 else int(rng.integers(0, d))
+            t = grids[k][int(rng.integers(0, len(grids[k])))]
+            lo = grow(level + 1)
+            hi = grow(level + 1)
+            nodes[me] = (k, t, lo, hi, 0)
+            return me
+
+        grow(0)
+        for k, t, lo, hi, q in nodes:
+            feat.append(max(k, 0))
+            thr.append(t)
+            left.append(lo)
+            right.append(hi)
+            q16.append(q)
+        off.append(off[-1] + len(nodes))
+    return dict(feature=np.array(feat, np.int32), threshold=np.array(thr, np.float32),
+                left=np.array(left, np.int32), right=np.array(right, np.int32),
+                leaf_q16=np.array(q16, np.int32), tree_offset=np.array(off, np.int64))
+
+
+def _near_candidates(rng, n, d, grids):
+    """Candidates on the grid values, one float32 step either side of them,
+    at +-0, +-inf and NaN, and uniform ones."""
+    X = rng.uniform(-2, 2, (n, d)).astype(np.float32)
+    for k in range(d):
+        g = np.asarray(grids[k], np.float32)
+        pick = g[rng.integers(0, len(g), n)]
+        side = rng.integers(0, 4, n)
+        near = np.where(side == 0, pick, np.where(side == 1, np.nextafter(pick, np.float32(np.inf)),
+                                                  np.where(side == 2, np.nextafter(pick, np.float32(-np.inf)), X[:, k])))
+        X[:, k] = near
+    special = np.array([0.0, -0.0, np.inf, -np.inf, np.nan], np.float32)
+    sel = rng.random((n, d)) < 0.05
+    X[sel] = special[rng.integers(0, len(special), sel.sum())]
+    return X
+
+
+def _check_forest(fd, d, X, what):
+    f = _forest(fd, d)
+    T = len(fd["tree_offset"]) - 1
+    for delta in (0.3, 0.6):
+        say(what, "n", len(X), "trees", T, "nodes", fd["tree_offset"][-1], "delta", delta)
+        votes, mask, leaves = S.rf_feasibility(f, dev(X), delta, leaf_idx=True)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(leaves.cpu().numpy(), forest_apply(fd, X))
+        v_o = forest_votes(fd, X)
+        np.testing.assert_array_equal(votes.cpu().numpy(), v_o)
+        np.testing.assert_array_equal(mask.cpu().numpy(), feasibility_mask(v_o, delta, T))
+
+
+def _grids(rng, d, counts):
+    base = [0.0, -0.0, np.inf, -np.inf, -1.5, 1e-30, -1e-30]
+    out = []
+    for k in range(d):
+        extra = np.unique(rng.uniform(-2, 2, 4 * counts[k]).astype(np.float32))
+        vals = np.unique(np.concatenate([np.array(base, np.float32), extra]))  # -0.0 == 0.0: one entry
+        out.append(vals[: counts[k]] if counts[k] < len(vals) else vals)
+    return out
+
+
+@pytest.mark.parametrize("top", [254, 255])
+def test_forest_ties_and_special_values(top):
+    """Every branch matches the oracle's float32 comparison bit for bit with
+    candidates on the thresholds and one float32 step either side of them,
+    thresholds and candidates at +-0, +-inf, NaN candidates, all sixteen
+    feature slots, and one feature with a few hundred distinct thresholds."""
+    rng = np.random.default_rng(top)
+    d = 16
+    counts = [top] + [int(c) for c in rng.integers(1, 40, d - 1)]
+    grids = _grids(rng, d, counts)
+    fd = _grid_forest(rng, [9] * 40, d, grids, p0=0.5)
+    k = np.where((fd["left"] >= 0) & (fd["feature"] == 0))[0]
+    fd["threshold"][k[: len(grids[0])]] = grids[0]  # every value of feature 0's grid on some node
+    z = k[fd["threshold"][k] == 0]
+    fd["threshold"][z[::2]] = -0.0  # signed zeros: one threshold value
+    assert len(np.unique(fd["threshold"][(fd["left"] >= 0) & (fd["feature"] == 0)])) == top
+    assert fd["tree_offset"][-1] < 8192
+    _check_forest(fd, d, _near_candidates(rng, 20000 + 37, d, grids), f"forest {top} thresholds")
+
+
+def test_forest_largest_tree_and_two_chunks():
+    """A complete tree of 8191 nodes (the largest one chunk holds) and one of
+    4095 nodes land in two chunks of one forest, one launch each, with the
+    votes carried between them."""
+    rng = np.random.default_rng(7)
+    d = 5
+    grids = _grids(rng, d, [30, 20, 10, 5, 3])
+    fd = _grid_forest(rng, [12, 11], d, grids, full=True)
+    assert np.diff(fd["tree_offset"]).tolist() == [8191, 4095]
+    _check_forest(fd, d, _near_candidates(rng, 9000 + 5, d, grids), "forest 8191 + 4095 nodes")
+
+
 # --------------------------------------------------------------------------- top-q
 @pytest.mark.parametrize("dt", [S.F32, S.F64], ids=["f32", "f64"])
 def test_topq_bitexact_shared_scores(dt):
