@@ -70,9 +70,11 @@ def parse():
                     help="time the whole suggestion step (scoot_suggest: hyperparameter search, forest "
                          "training, Sobol pool with known constraints, scoring, pick) on the workload's "
                          "observations and print its own line")
-    ap.add_argument("--only", choices=["all", "posterior", "forest", "ehvi", "topq", "copy"], default="all",
+    ap.add_argument("--only", choices=["all", "posterior", "forest", "ehvi", "topq", "pass", "copy"], default="all",
                     help="posterior / forest / ehvi / topq: only that kernel's loop (for profiler "
-                         "counters); copy: a plain 1 GiB device copy (counter calibration)")
+                         "counters); pass: only the loop of whole scoring passes (every kernel the metric "
+                         "times, the fused EHVI and top-q stage 1 included); copy: a plain 1 GiB device copy "
+                         "(counter calibration)")
     return ap.parse_args()
 
 
@@ -158,6 +160,10 @@ def main():
     if args.only == "posterior":
         ms = time_loop(post, args.kernel_loops)
         print(json.dumps({"posterior_ms": ms}))
+        return
+    if args.only == "pass":
+        step()
+        print(json.dumps({"pass_ms": time_loop(step, args.kernel_loops)}))
         return
     if args.only in ("forest", "ehvi", "topq"):
         step()
