@@ -26,9 +26,10 @@
 // and, when the gradient is wanted,
 //   T. L^-1 and alpha = L^-T u, one block column per workgroup (the columns
 //      are independent);
-//   U. K^-1 = L^-T L^-1, one block per workgroup;
-//   B. the gradient: one element of W per thread, the covariance and its
-//      derivatives recomputed, partial sums per workgroup.
+//   B. the gradient, one lower block per workgroup: the block of
+//      K^-1 = L^-T L^-1 on the matrix cores, then one element of W per
+//      thread, the covariance and its derivatives recomputed, partial sums
+//      per workgroup.
 // The kernels write their results (status, pivot products, |u|^2 per block,
 // partial gradient sums) straight into pinned host memory, and the host adds
 // them.  Every operation is in double and every sum has a fixed order, so an
@@ -51,8 +52,8 @@ typedef double d4_t __attribute__((ext_vector_type(4)));
 constexpr int kNllWaves = 8;
 constexpr int kNllThreads = kNllWaves * 64;
 constexpr int kMaxTheta = 3 * SCOOT_MAX_DIM + 2;
-constexpr int kGradBlocks = 64;
 constexpr int kGradThreads = 256;
+constexpr int kGradWaves = kGradThreads / 64;
 constexpr double kRoot5 = 2.23606797749978969641;
 constexpr double kRoot3 = 1.73205080756887729353;
 constexpr double kLog2PiD = 1.83787706640934548356;
@@ -61,7 +62,6 @@ struct NllArgs {
   const double* X;  // m x d inputs as the covariance sees them (raw when the warp is learned)
   const double* r;  // m_pad: y - c, 0 beyond m
   double* L;        // nb x nb blocks: K, then its lower factor (blocks I >= J)
-  double* Z;        // nb x nb blocks: K^-1 (blocks I >= J)
   double* Xi;       // nb x nb blocks: L^-1 (blocks I >= J)
   double* Di;       // nb blocks: inverses of L's diagonal blocks
   double* Xw;       // m x d warped inputs (warp learned)
@@ -72,8 +72,8 @@ struct NllArgs {
   double* out;      // [1] 1 when K is numerically positive definite, 0 when not, 2 when a wait ran out
   // Pinned host memory the kernels write their results to: [0] the status of
   // out[1], [1 .. nb] the product of each diagonal block's pivots (real rows),
-  // [nb + 1 ..] u (16 nb values), then kGradBlocks x P partial gradient sums;
-  // the host adds them in a fixed order.
+  // [nb + 1 ..] u (16 nb values), then nb (nb + 1) / 2 x P partial gradient
+  // sums (one row per lower block); the host adds them in a fixed order.
   double* hout;
   int m, nb, d, m52, learn_warp;
   double theta[kMaxTheta];
@@ -689,66 +689,57 @@ __global__ __launch_bounds__(kTriWaves * 64) void nll_trtri_kernel(NllArgs a) {
   }
 }
 
-// ---- kernel U: K^-1 = L^-T L^-1, one lower block per workgroup ----------------
-// Z_ij = sum_{k >= i} X_ki^T X_kj (i >= j); diagonal blocks made exactly
-// symmetric.
-__global__ __launch_bounds__(64) void nll_lauum_kernel(NllArgs a) {
-  __shared__ double sT[256];
-  if (a.out[1] != 1.0) return;
-  const int nb = a.nb, lane = threadIdx.x;
-  int I = 0, J = 0;
-  advance_lower(I, J, blockIdx.x);
-  d4_t Zv = zero4();
-  for (int k = I; k < nb; k += 4) {
-    double av[4][4], bv[4][4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (k + u < nb) {
-        ld_cols(a.Xi + ((size_t)(k + u) * nb + I) * 256, lane, av[u]);  // X_ki^T as an A operand
-        ld_cols(a.Xi + ((size_t)(k + u) * nb + J) * 256, lane, bv[u]);  // X_kj as a B operand
-      }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (k + u < nb) Zv = mma16(Zv, av[u], bv[u]);
-  }
-  if (I == J) {
-    const int g = lane >> 4, c = lane & 15;
-    st_c(sT, Zv, lane);
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < 4; ++r) Zv[r] = 0.5 * (Zv[r] + sT[c * 16 + g + 4 * r]);
-  }
-  st_c(a.Z + ((size_t)I * nb + J) * 256, Zv, lane);
-}
-
-// ---- kernel B: gradient partial sums ----------------------------------------
+// ---- kernel B: the gradient's partial sums, one lower block per workgroup ---
+// Z_IJ = (K^-1)_IJ = sum_{k >= I} X_kI^T X_kJ on the matrix cores (wave w
+// takes k = I + w, I + w + 4, ...; the four sums are added in order through
+// LDS, and a diagonal block is made exactly symmetric), then one element of
+// W = alpha alpha^T - K^-1 per thread with the covariance and its
+// derivatives recomputed.
 template <int D, bool LW>
 __global__ __launch_bounds__(kGradThreads) void nll_grad_kernel(NllArgs a) {
   constexpr int P = LW ? 3 * D + 2 : D + 2;
-  __shared__ double sRed[kGradThreads / 64][P];
+  __shared__ double sZ[kGradWaves][256];
+  __shared__ double sRed[kGradWaves][P];
   if (a.out[1] != 1.0) return;  // K not positive definite: no gradient
   const int nb = a.nb, m = a.m, t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const bool m52 = a.m52 != 0;
-  const double s2 = exp(a.theta[D]), tau2 = exp(a.theta[D + 1]);
-  const double root = m52 ? kRoot5 : kRoot3;
-  double inv_ls[D];
+  int I = 0, J = 0;
+  advance_lower(I, J, blockIdx.x);
+  d4_t Zv = zero4();
+  for (int k0 = I + wave; k0 < nb; k0 += 4 * kGradWaves) {
+    double av[4][4], bv[4][4];
 #pragma unroll
-  for (int k = 0; k < D; ++k) inv_ls[k] = exp(-a.theta[k]);
-  const double* X = LW ? a.Xw : a.X;
+    for (int u = 0; u < 4; ++u) {
+      const int k = k0 + u * kGradWaves;
+      if (k < nb) {
+        ld_cols(a.Xi + ((size_t)k * nb + I) * 256, lane, av[u]);  // X_kI^T as an A operand
+        ld_cols(a.Xi + ((size_t)k * nb + J) * 256, lane, bv[u]);  // X_kJ as a B operand
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (k0 + u * kGradWaves < nb) Zv = mma16(Zv, av[u], bv[u]);
+  }
+  st_c(sZ[wave], Zv, lane);
+  __syncthreads();
+  const int ii = t >> 4, jj = t & 15, i = 16 * I + ii, j = 16 * J + jj;
+  double zij = ((sZ[0][t] + sZ[1][t]) + sZ[2][t]) + sZ[3][t];
+  if (I == J) {
+    const int tt = jj * 16 + ii;
+    zij = 0.5 * (zij + (((sZ[0][tt] + sZ[1][tt]) + sZ[2][tt]) + sZ[3][tt]));
+  }
   double g[P];
 #pragma unroll
   for (int p = 0; p < P; ++p) g[p] = 0.0;
-  const int n_lower = nb * (nb + 1) / 2;
-  int I = 0, J = 0;
-  advance_lower(I, J, blockIdx.x);
-  for (int b = blockIdx.x; b < n_lower; b += gridDim.x, advance_lower(I, J, gridDim.x)) {
-    const int ii = t >> 4, jj = t & 15, i = 16 * I + ii, j = 16 * J + jj;
-    if ((I == J && jj > ii) || i >= m || j >= m) continue;
-    const double zij = a.Z[((size_t)I * nb + J) * 256 + t];
+  if (!((I == J && jj > ii) || i >= m || j >= m)) {
+    const bool m52 = a.m52 != 0;
+    const double s2 = exp(a.theta[D]), tau2 = exp(a.theta[D + 1]);
+    const double root = m52 ? kRoot5 : kRoot3;
+    const double* X = LW ? a.Xw : a.X;
     const double w = 0.5 * (i == j ? 1.0 : 2.0) * (a.alpha[i] * a.alpha[j] - zij);  // W and dK are symmetric
-    double tk[D], r2 = 0.0;
+    double tk[D], inv_ls[D], r2 = 0.0;
 #pragma unroll
     for (int k = 0; k < D; ++k) {
+      inv_ls[k] = exp(-a.theta[k]);
       tk[k] = (X[(size_t)i * D + k] - X[(size_t)j * D + k]) * inv_ls[k];
       r2 += tk[k] * tk[k];
     }
@@ -777,7 +768,7 @@ __global__ __launch_bounds__(kGradThreads) void nll_grad_kernel(NllArgs a) {
   if (t < P) {
     double s = 0.0;
 #pragma unroll
-    for (int w = 0; w < kGradThreads / 64; ++w) s += sRed[w][t];
+    for (int w = 0; w < kGradWaves; ++w) s += sRed[w][t];
     a.hout[1 + 17 * nb + (size_t)blockIdx.x * P + t] = s;
   }
 }
@@ -811,7 +802,7 @@ class DeviceNll {
     // every part 256-byte aligned (32 doubles)
     auto up = [](size_t n) { return (n + 31) / 32 * 32; };
     const size_t md = (size_t)m * d, mp = (size_t)nb_ * 16, blocks = (size_t)nb_ * nb_ * 256;
-    const size_t n = up(md) + up(mp) + 3 * blocks + (size_t)nb_ * 256 + (learn_warp ? 3 * up(md) : 0) +
+    const size_t n = up(md) + up(mp) + 2 * blocks + (size_t)nb_ * 256 + (learn_warp ? 3 * up(md) : 0) +
                      2 * up(mp) + up(2);
     if (hipMalloc(&buf_, n * sizeof(double)) != hipSuccess) {
       buf_ = nullptr;
@@ -820,7 +811,8 @@ class DeviceNll {
     // the results, written by the kernels straight into coherent pinned host
     // memory (no copy after them): status, pivot products, u, partial gradient
     // sums
-    if (hipHostMalloc(&host_, (1 + 17 * (size_t)nb_ + (size_t)kGradBlocks * P_) * sizeof(double),
+    n_lower_ = nb_ * (nb_ + 1) / 2;
+    if (hipHostMalloc(&host_, (1 + 17 * (size_t)nb_ + (size_t)n_lower_ * P_) * sizeof(double),
                       hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess) {
       host_ = nullptr;
       return fail(SCOOT_ERR_NO_MEMORY, "gp nll: pinned allocation failed");
@@ -835,8 +827,6 @@ class DeviceNll {
     double* rd = p;
     p += up(mp);
     a_.L = p;
-    p += blocks;
-    a_.Z = p;
     p += blocks;
     a_.Xi = p;
     p += blocks;
@@ -887,15 +877,14 @@ class DeviceNll {
       hipLaunchKernelGGL(nll_warp_kernel, dim3((unsigned)((m_ * d_ + 255) / 256)), dim3(256), 0, s_, a_);
     hipLaunchKernelGGL(nll_cov_kernel, dim3((unsigned)(nb_ * (nb_ + 1) / 2)), dim3(256), 0, s_, a_);
     hipLaunchKernelGGL(nll_factor_kernel, dim3(1), dim3(kNllThreads), lds_, s_, a_);
-    if (grad) {  // L^-1 and alpha, K^-1, the gradient's partial sums (the NLL needs none of them)
+    if (grad) {  // L^-1 and alpha, then K^-1 and the gradient's partial sums (the NLL needs none of them)
       launch_trtri();
-      hipLaunchKernelGGL(nll_lauum_kernel, dim3((unsigned)(nb_ * (nb_ + 1) / 2)), dim3(64), 0, s_, a_);
       const int rc = by_dim<1>(d_, [&](auto D) {
         if (lw_)
-          hipLaunchKernelGGL((nll_grad_kernel<decltype(D)::value, true>), dim3(kGradBlocks), dim3(kGradThreads), 0,
+          hipLaunchKernelGGL((nll_grad_kernel<decltype(D)::value, true>), dim3((unsigned)n_lower_), dim3(kGradThreads), 0,
                              s_, a_);
         else
-          hipLaunchKernelGGL((nll_grad_kernel<decltype(D)::value, false>), dim3(kGradBlocks), dim3(kGradThreads), 0,
+          hipLaunchKernelGGL((nll_grad_kernel<decltype(D)::value, false>), dim3((unsigned)n_lower_), dim3(kGradThreads), 0,
                              s_, a_);
         return SCOOT_OK;
       });
@@ -929,7 +918,7 @@ class DeviceNll {
       const double* part = host_ + 1 + 17 * nb_;
       for (int p = 0; p < P_; ++p) {
         double s = 0.0;
-        for (int b = 0; b < kGradBlocks; ++b) s += part[(size_t)b * P_ + p];
+        for (int b = 0; b < n_lower_; ++b) s += part[(size_t)b * P_ + p];
         grad[p] = s;
       }
     }
@@ -994,7 +983,7 @@ class DeviceNll {
     }
   }
   hipStream_t s_ = nullptr;
-  int m_ = 0, d_ = 0, nb_ = 0, P_ = 0;
+  int m_ = 0, d_ = 0, nb_ = 0, n_lower_ = 0, P_ = 0;
   bool lw_ = false;
   size_t lds_ = 0;
   double* buf_ = nullptr;
