@@ -56,6 +56,9 @@ def parse():
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="default run only: skip the other workloads timed after the metric (the whole "
+                         "suggestion step, three objectives at m=512 n=2^20, the believer, MACE)")
     ap.add_argument("--kernel-loops", type=int, default=20)
     ap.add_argument("--kernel", choices=["matern52", "matern32"], default="matern52",
                     help="covariance of the GPs (matern32 = the paper's own)")
@@ -278,7 +281,54 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    if (not args.no_secondary and args.only == "all" and args.config == 3 and args.kernel == "matern52"
+            and not args.warp and args.dtype == "f32"):
+        out["secondary"] = secondary_workloads()
     print(json.dumps(out), flush=True)
+
+
+# The other workloads, each timed by this script in a child process of its own
+# after the metric (they are not part of the metric's timed region), so that
+# one run of the default command measures them too.
+SECONDARY = [
+    ("suggest_step", ["--suggest", "--steps", "5", "--warmup", "2"]),
+    ("three_objective_pass", ["--config", "4", "--steps", "10", "--warmup", "10", "--kernel-loops", "5",
+                              "--no-cpu-baseline", "--no-secondary"]),
+    ("believer", ["--config", "5", "--steps", "5", "--warmup", "2"]),
+    ("mace", ["--config", "2", "--mace", "--steps", "20", "--warmup", "10"]),
+]
+
+
+def secondary_workloads():
+    import subprocess
+    res = {}
+    for name, extra in SECONDARY:
+        print(f"[bench] secondary workload {name}", file=sys.stderr, flush=True)
+        t0 = time.perf_counter()
+        try:
+            r = subprocess.run([sys.executable, "-u", os.path.abspath(__file__)] + extra, stdout=subprocess.PIPE,
+                               text=True, timeout=300)
+            lines = [ln for ln in r.stdout.splitlines() if ln.startswith("{")]
+            if r.returncode != 0 or not lines:
+                res[name] = {"error": f"exit status {r.returncode}"}
+                continue
+            d = json.loads(lines[-1])
+            cfg = d.get("config", {})
+            e = {"metric": d["metric"], "value": d["value"], "unit": d["unit"], "ms_per_step": d["ms_per_step"],
+                 "steps": d["steps"], "warmup": d["warmup"], "workload": cfg.get("workload")}
+            if name == "suggest_step":
+                e["ms_per_step_host_search"] = cfg.get("ms_per_step_host_search")
+                e["picks_match_host_search"] = cfg.get("picks_match_host_search")
+            if name == "three_objective_pass":
+                e["roofline_frac"] = d.get("roofline", {}).get("frac")
+            res[name] = e
+        except subprocess.TimeoutExpired:
+            res[name] = {"error": "timed out after 300 s"}
+        print(f"[bench] secondary workload {name} done in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
+              flush=True)
+    res["note"] = "each from `python bench.py` with the listed options, run after the metric in a child process"
+    res["options"] = {name: " ".join(extra) for name, extra in SECONDARY}
+    return res
 
 
 def bench_believer(args):
