@@ -282,6 +282,12 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
     const int64_t next = tile + gridDim.x;
     if (next < n_tiles) load_tile(next);
 
+    // The K* generation runs at a raised wave priority and the product at
+    // the normal one: where the CU's two workgroups are in different phases,
+    // the one generating is served first and reaches its product sooner, so
+    // that the SIMDs less often wait with both in the same phase (measured:
+    // 2-3% less time per launch at m = 256).
+    __builtin_amdgcn_s_setprio(2);
     // ---- phase 1: K* of observation blocks J = wave, wave + WAVES, ... ---
     // The block's operands are loaded one block ahead; its four column
     // tiles' chains are issued interleaved (independent accumulators), then
@@ -322,6 +328,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f32_kernel(
     }
     __syncthreads();
 
+    __builtin_amdgcn_s_setprio(0);
     // ---- phase 2: this wave's row blocks of V = L^-1 K*^T -----------------
     float sq[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     if (count > 0) {
@@ -533,6 +540,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f64_kernel(
       for (int q = 0; q < D; ++q) xr[q] = Xc[min(next * 32 + cl, a.n - 1) * D + q];
     }
 
+    __builtin_amdgcn_s_setprio(2);  // K* at a raised priority, as in the fp32 kernel
     // ---- phase 1: group G = 4J + 2 s2 + kk covers rows
     // 16J + 8 s2 + 4t + 2kk + h = 4G - 2kk + h + 4t (t = 0, 1) of block J;
     // WAVES is even, so kk = wave & 1 for all of a wave's groups and each
@@ -570,6 +578,7 @@ __global__ __launch_bounds__(WAVES * 64, 8 / WAVES) void posterior_f64_kernel(
     }
     __syncthreads();
 
+    __builtin_amdgcn_s_setprio(0);
     // ---- phase 2 ----------------------------------------------------------
     double sq0 = 0.0, sq1 = 0.0;
     if (count > 0) wave_tile16(ap, ks, rows_lo, rows_hi, count, lane, ax, sq0, sq1);
