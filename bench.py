@@ -307,7 +307,7 @@ def secondary_workloads():
         t0 = time.perf_counter()
         try:
             r = subprocess.run([sys.executable, "-u", os.path.abspath(__file__)] + extra, stdout=subprocess.PIPE,
-                               text=True, timeout=300)
+                               text=True, timeout=120)
             lines = [ln for ln in r.stdout.splitlines() if ln.startswith("{")]
             if r.returncode != 0 or not lines:
                 res[name] = {"error": f"exit status {r.returncode}"}
@@ -323,7 +323,7 @@ def secondary_workloads():
                 e["roofline_frac"] = d.get("roofline", {}).get("frac")
             res[name] = e
         except subprocess.TimeoutExpired:
-            res[name] = {"error": "timed out after 300 s"}
+            res[name] = {"error": "timed out after 120 s"}
         print(f"[bench] secondary workload {name} done in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
               flush=True)
     res["note"] = "each from `python bench.py` with the listed options, run after the metric in a child process"
